@@ -1,0 +1,112 @@
+"""Planted mistakes in the oracle must fail its pins.
+
+Each case copies the oracle into a temporary directory, plants one plausible
+mistake (a dropped term, a wrong coefficient, sign or index, a swapped
+operand), and runs the pin suite against the copy in a subprocess.  The pin
+suite must fail for every mistake.  CPU only; the real oracle is untouched.
+"""
+import os
+import shutil
+import subprocess
+import sys
+import tempfile
+from concurrent.futures import ThreadPoolExecutor
+
+import pytest
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+
+# (file, original text, planted mistake, what it breaks)
+MUTATIONS = [
+    ("dsm_oracle.py", "m_new = beta1_ * m + one_minus_b1 * g",
+     "m_new = beta1_ * m + one_minus_b2 * g", "AdamW first-moment coefficient"),
+    ("dsm_oracle.py", "m_hat = m_new / bc1", "m_hat = m_new", "AdamW bias correction dropped"),
+    ("dsm_oracle.py", "np.sqrt(v_hat) + eps_", "np.sqrt(v_hat + eps_)", "AdamW epsilon placement"),
+    ("dsm_oracle.py", "x_new = x - lr_ * (m_hat", "x_new = x + lr_ * (m_hat", "AdamW step sign"),
+    ("dsm_oracle.py", "+ wd_ * x)", "+ wd_ * m_hat)", "AdamW decay operand"),
+    ("dsm_oracle.py", "m_new = mu * m + g", "m_new = mu * m + (1 - mu) * g",
+     "Polyak momentum dampened"),
+    ("dsm_oracle.py", "u = beta1_ * mp + c1 * delta", "u = beta2_ * mp + c1 * delta",
+     "u uses beta2"),
+    ("dsm_oracle.py", "m_new = beta2_ * mp + c2 * delta", "m_new = beta2_ * mp + c1 * delta",
+     "momentum uses (1-beta1)"),
+    ("dsm_oracle.py", "u = beta1_ * mp + c1 * delta",
+     "u = beta1_ * (beta2_ * mp + c2 * delta) + c1 * delta", "u from the new momentum"),
+    ("dsm_oracle.py", "x_new = xp - step * (S + lam_p * xp)", "x_new = xp - step * S",
+     "global weight decay dropped"),
+    ("dsm_oracle.py", "lam_p = lam_ if decay[p] else dt(0.0)", "lam_p = lam_",
+     "decay mask ignored"),
+    ("dsm_oracle.py", "for i in range(1, n):", "for i in range(1, n - 1):",
+     "last worker dropped from the average"),
+    ("dsm_oracle.py", "delta = acc / dt(n)", "delta = acc", "average not divided by n"),
+    ("dsm_oracle.py", "c1 = dt((1.0 - b1) / g_)", "c1 = dt((1.0 - b1) * g_)",
+     "1/gamma scaling inverted"),
+    ("dsm_oracle.py", "step = dt(f32(eta) * g_)", "step = dt(f32(eta))",
+     "global step not scaled by gamma"),
+    ("dsm_oracle.py", "return np.sign(u) + u.dtype.type(0.0)",
+     "return np.where(u >= 0, 1.0, -1.0).astype(u.dtype)", "sign(0) taken as +1"),
+    ("dsm_oracle.py", "keep = _exact_less(2 * k - (1 << 24), B, au)",
+     "keep = _exact_less(k, B, au)", "Eq. (9) threshold replaced by Eq. (10)'s"),
+    ("dsm_oracle.py", "return np.where(keep, s, dt(0.0) - s)",
+     "return np.where(keep, s, s)", "Eq. (9) never flips"),
+    ("dsm_oracle.py", "B = np.max(np.abs(u)) if u.size else dt(0.0)",
+     "B = np.max(u) if u.size else dt(0.0)", "bound without absolute value"),
+    ("dsm_oracle.py", "w = philox4x32_10(q, tensor_index, t, PHILOX_STREAM,",
+     "w = philox4x32_10(q, t, tensor_index, PHILOX_STREAM,", "Philox counter words swapped"),
+    ("philox.py", "n0 = (p1 >> sh) ^ c1 ^ np.uint64(k0)",
+     "n0 = (p1 >> sh) ^ c1 ^ np.uint64(k1)", "Philox key word swapped"),
+    ("philox.py", "        p0 = M0 * c0\n", "        p0 = M1 * c0\n", "Philox multiplier swapped"),
+    ("dsm_oracle.py", '    st["replicas"] = synchronize(st["x"], st["n"])',
+     '    st["replicas"] = synchronize(st["x"], st["n"]) if False else st["replicas"]',
+     "replicas not synchronised"),
+    ("dsm_oracle.py",
+     "    local_steps(st, grads, H=H, decay=decay, first_step=t * H + 1, prec=prec, **local)",
+     "    st['s1'] = [[a * 0 for a in w] for w in st['s1']]\n"
+     "    local_steps(st, grads, H=H, decay=decay, first_step=t * H + 1, prec=prec, **local)",
+     "worker momentum reset every round"),
+]
+
+
+def _run_mutant(case):
+    fname, orig, planted, _ = case
+    tmp = tempfile.mkdtemp(prefix="dsm_mut_")
+    try:
+        shutil.copytree(os.path.join(ROOT, "oracle"), os.path.join(tmp, "oracle"),
+                        ignore=shutil.ignore_patterns("__pycache__"))
+        tdir = os.path.join(tmp, "tests")
+        os.makedirs(tdir)
+        shutil.copy(os.path.join(HERE, "test_oracle_pins.py"), tdir)
+        shutil.copytree(os.path.join(HERE, "golden"), os.path.join(tdir, "golden"))
+        shutil.copytree(os.path.join(HERE, "native"), os.path.join(tdir, "native"),
+                        ignore=shutil.ignore_patterns("bin"))
+        with open(os.path.join(tdir, "conftest.py"), "w") as f:
+            f.write("import os, sys\nsys.path.insert(0, os.path.dirname(os.path.dirname("
+                    "os.path.abspath(__file__))))\n")
+        path = os.path.join(tmp, "oracle", fname)
+        src = open(path).read()
+        assert src.count(orig) == 1, f"mutation anchor not unique: {orig!r}"
+        open(path, "w").write(src.replace(orig, planted))
+        env = dict(os.environ, PYTHONDONTWRITEBYTECODE="1")
+        r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                            os.path.join(tdir, "test_oracle_pins.py")],
+                           cwd=tmp, env=env, capture_output=True, text=True, timeout=600)
+        return r.returncode, r.stdout[-2000:]
+    finally:
+        shutil.rmtree(tmp, ignore_errors=True)
+
+
+def test_every_planted_mistake_fails_a_pin():
+    with ThreadPoolExecutor(max_workers=4) as ex:
+        results = list(ex.map(_run_mutant, MUTATIONS))
+    survivors = [(case[3], out) for case, (rc, out) in zip(MUTATIONS, results) if rc == 0]
+    errors = [(case[3], out) for case, (rc, out) in zip(MUTATIONS, results)
+              if rc not in (0, 1)]
+    assert not errors, f"pin suite errored instead of failing: {errors}"
+    assert not survivors, "mutants not caught: " + ", ".join(s for s, _ in survivors)
+
+
+def test_unmutated_copy_passes():
+    """Control: the same harness with an unchanged oracle passes."""
+    rc, out = _run_mutant(("dsm_oracle.py", "PHILOX_STREAM = 1", "PHILOX_STREAM = 1", "none"))
+    assert rc == 0, out

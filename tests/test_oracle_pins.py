@@ -1,0 +1,527 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+Each test checks the oracle against something other than itself: a
+hand-worked example, a closed form, a special case that reduces to a
+textbook or library routine (signSGD, sign momentum, Lion, torch's AdamW and
+SGD), Lemma 1's moments, or an exactness property.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _sgd_round(st, grads_round, t, *, gamma, eta, beta1, beta2, lam, decay, prec,
+               momentum=0.0, mode=O.SIGN_DET, seed=0):
+    """Drive one Algorithm-1 round with the SGD base and one local step."""
+    def grads(i, k):
+        return grads_round[i]
+    return O.communication_round(
+        st, grads, t, H=1, local=dict(lr=gamma, beta1=momentum), decay=decay,
+        glob=dict(eta=eta, beta1=beta1, beta2=beta2, lam=lam, mode=mode, seed=seed),
+        prec=prec)
+
+
+# ---------------------------------------------------------------- worked example
+
+@pytest.mark.parametrize("prec", ["fp64", "fp32"])
+def test_worked_example_sgd_rounds(prec):
+    """Hand-worked Algorithm 1 example (golden/worked_sgd_rounds.json)."""
+    with open(os.path.join(GOLDEN, "worked_sgd_rounds.json")) as f:
+        gold = json.load(f)
+    s = gold["setup"]
+    x0 = [np.array([float(v) for v in s["x0"]], dtype=np.float32)]
+    st = O.init_state(x0, s["n_workers"], "sgd")
+    for t, (grads_r, exp) in enumerate(zip(s["grads_per_round"], gold["expected"])):
+        g = [[np.array([float(v) for v in w], dtype=np.float32)] for w in grads_r]
+        res = _sgd_round(st, g, t, gamma=float(s["gamma"]), eta=float(s["eta"]),
+                         beta1=float(s["beta1"]), beta2=float(s["beta2"]),
+                         lam=float(s["lambda"]), decay=[True], prec=prec)
+        ex_x = np.array([float(v) for v in exp["x"]])
+        ex_m = np.array([float(v) for v in exp["m"]])
+        ex_u = np.array([float(v) for v in exp["u"]])
+        np.testing.assert_array_equal(res["S"][0], np.array(exp["S"], dtype=float))
+        # The hyperparameters are fp32 numbers (0.1, 0.9, 0.99 are not exact),
+        # which moves the result by a few 1e-8 relative; fp32 arithmetic adds
+        # a few fp32 ulps per round.  A structural mistake moves it by 1e-3.
+        tol = 2e-8 * (t + 1) if prec == "fp64" else 4e-7 * (t + 1)
+        np.testing.assert_allclose(res["x"][0], ex_x, rtol=0, atol=tol)
+        np.testing.assert_allclose(res["m"][0], ex_m, rtol=0, atol=tol)
+        np.testing.assert_allclose(res["u"][0], ex_u, rtol=0, atol=tol * 10)
+        # Element 3 stays exactly zero; element 1 never moves off -(0.99)^t
+        # by more than rounding.
+        assert res["x"][0][3] == 0.0
+
+
+@pytest.mark.parametrize("prec", ["fp64", "fp32"])
+def test_worked_example_momentum_two_tensors_exact(prec):
+    """Hand-worked dyadic example (golden/worked_sgdm_dyadic.json): Polyak
+    base with momentum carried across rounds, two local steps, two workers,
+    a decayed and an undecayed tensor, and an element with u = 0.  Every
+    operation is exact, so both precisions must match bit for bit."""
+    with open(os.path.join(GOLDEN, "worked_sgdm_dyadic.json")) as f:
+        gold = json.load(f)
+    s = gold["setup"]
+    names = list(s["tensors"])
+    x0 = [np.array(s["tensors"][k]["x0"], dtype=np.float32) for k in names]
+    decay = [s["tensors"][k]["decay"] for k in names]
+    st = O.init_state(x0, s["n_workers"], "sgd")
+    for t, exp in enumerate(gold["expected"]):
+        gr = s["grads"][f"round{t}"]
+
+        def grads(i, k):
+            return [np.array(gr[f"worker{i}"][k][name], dtype=np.float32) for name in names]
+        res = O.communication_round(
+            st, grads, t, H=s["local_steps"],
+            local=dict(lr=s["gamma"], beta1=s["momentum"]), decay=decay,
+            glob=dict(eta=s["eta"], beta1=s["beta1"], beta2=s["beta2"], lam=s["lambda"],
+                      mode=O.SIGN_DET, seed=0), prec=prec)
+        for p, name in enumerate(names):
+            np.testing.assert_array_equal(res["u"][p], exp["u"][name])
+            np.testing.assert_array_equal(res["S"][p], exp["S"][name])
+            np.testing.assert_array_equal(st["x"][p], exp["x"][name])
+            np.testing.assert_array_equal(st["m"][p], exp["m"][name])
+            for i in range(s["n_workers"]):
+                np.testing.assert_array_equal(st["s1"][i][p],
+                                              exp["worker_momentum"][f"worker{i}"][name])
+                np.testing.assert_array_equal(st["replicas"][i][p], st["x"][p])
+
+
+# ---------------------------------------------------------------- special cases
+
+def _dyadic(rng, size, scale_bits):
+    """Random numbers with few significant bits, so fp32/fp64 ops are exact."""
+    return (rng.integers(-64, 65, size=size) * 2.0 ** -scale_bits).astype(np.float32)
+
+
+@pytest.mark.parametrize("prec", ["fp64", "fp32"])
+def test_reduces_to_signsgd(prec):
+    """n=1, tau=1, beta1=beta2=0, lambda=0, SGD base: signSGD, Eq. (2), lr eta*gamma."""
+    rng = np.random.default_rng(1)
+    x = _dyadic(rng, 257, 8)
+    st = O.init_state([x], 1, "sgd")
+    gamma, eta = 0.125, 2.0
+    for t in range(5):
+        g = _dyadic(rng, 257, 4)
+        g[::7] = 0.0
+        res = _sgd_round(st, [[g]], t, gamma=gamma, eta=eta, beta1=0.0, beta2=0.0,
+                         lam=0.0, decay=[True], prec=prec)
+        x_expect = x - np.float32(eta * gamma) * np.sign(g)
+        np.testing.assert_array_equal(st["x"][0], x_expect)
+        np.testing.assert_array_equal(res["S"][0], np.sign(g))
+        x = x_expect
+
+
+@pytest.mark.parametrize("prec", ["fp64", "fp32"])
+def test_reduces_to_sign_momentum(prec):
+    """beta1=beta2=beta, lambda=0, tau=1: signSGD with momentum, Eq. (3),
+    driven by the worker-average gradient (Section 2, algorithm instances)."""
+    rng = np.random.default_rng(2)
+    n, beta, gamma, eta = 4, 0.5, 0.25, 1.0
+    x = _dyadic(rng, 300, 6)
+    st = O.init_state([x], n, "sgd")
+    mom = np.zeros_like(x, dtype=np.float64)
+    xe = x.astype(np.float64)
+    for t in range(6):
+        gs = [_dyadic(rng, 300, 3) for _ in range(n)]
+        res = _sgd_round(st, [[g] for g in gs], t, gamma=gamma, eta=eta, beta1=beta,
+                         beta2=beta, lam=0.0, decay=[True], prec=prec)
+        gbar = np.mean(np.stack(gs).astype(np.float64), axis=0)
+        mom = beta * mom + (1 - beta) * gbar
+        xe = xe - eta * gamma * np.sign(mom)
+        np.testing.assert_array_equal(st["m"][0].astype(np.float64), mom)
+        np.testing.assert_array_equal(st["x"][0].astype(np.float64), xe)
+
+
+def _lion_step(x, m, g, lr, b1, b2, lam):
+    """Lion, Algorithm 4 (Appendix A)."""
+    u = b1 * m + (1 - b1) * g
+    x = x - lr * (np.sign(u) + lam * x)
+    m = b2 * m + (1 - b2) * g
+    return x, m
+
+
+@pytest.mark.parametrize("prec", ["fp64", "fp32"])
+def test_reduces_to_lion(prec):
+    """n=1, tau=1, SGD base: each round is one Lion step (Algorithm 4) with
+    lr eta*gamma, taken from the round's stored fp32 state.  The replica is
+    stored in fp32 after the local step, so agreement is to fp32 rounding;
+    the sign must agree exactly (the inputs keep |u| far from 0)."""
+    rng = np.random.default_rng(3)
+    gamma, eta, b1, b2, lam = 0.125, 0.5, 0.75, 0.875, 0.25
+    x = _dyadic(rng, 500, 6)
+    st = O.init_state([x], 1, "sgd")
+    for t in range(8):
+        g = _dyadic(rng, 500, 5)
+        g[g == 0] = 0.5
+        x_prev = st["x"][0].astype(np.float64)
+        m_prev = st["m"][0].astype(np.float64)
+        res = _sgd_round(st, [[g]], t, gamma=gamma, eta=eta, beta1=b1, beta2=b2, lam=lam,
+                         decay=[True], prec=prec)
+        xl, ml = _lion_step(x_prev, m_prev, g.astype(np.float64), eta * gamma, b1, b2, lam)
+        u_l = b1 * m_prev + (1 - b1) * g
+        np.testing.assert_array_equal(res["S"][0], np.sign(u_l))
+        # Rounding the replica to fp32 perturbs x - x_1 by half an ulp of x;
+        # m is a difference of terms of size ~|g|, so bound it absolutely.
+        scale_x = np.abs(x_prev) + eta * gamma * (1 + lam * np.abs(x_prev))
+        assert np.all(np.abs(st["x"][0] - xl) <= 2.5e-7 * scale_x)
+        np.testing.assert_allclose(st["m"][0], ml, rtol=0,
+                                   atol=4e-7 * (np.abs(b2 * m_prev) + np.abs(g)).max())
+
+
+@pytest.mark.parametrize("prec", ["fp64", "fp32"])
+def test_equal_betas_give_u_equal_m(prec):
+    """beta1 = beta2: Eqs. (6) and (8) coincide, so u_{t+1} == m_{t+1} exactly."""
+    rng = np.random.default_rng(4)
+    x = [rng.normal(0, 0.02, 1000).astype(np.float32)]
+    m = [rng.normal(0, 1, 1000).astype(np.float32)]
+    reps = [[(x[0] - rng.normal(0, 1e-3, 1000)).astype(np.float32)] for _ in range(3)]
+    res = O.global_step(x, m, reps, gamma=1e-3, eta=0.8, beta1=0.9, beta2=0.9,
+                        lam=0.1, decay=[True], prec=prec)
+    np.testing.assert_array_equal(res["u"][0], res["m"][0])
+
+
+@pytest.mark.parametrize("prec", ["fp64", "fp32"])
+def test_single_worker_difference_is_exact(prec):
+    """n = 1: the all-reduce is the identity, so the difference is x - x_1."""
+    rng = np.random.default_rng(5)
+    x = rng.normal(0, 0.02, 999).astype(np.float32)
+    xr = (x * (1 + rng.normal(0, 1e-3, 999))).astype(np.float32)
+    res = O.global_step([x], [np.zeros_like(x)], [[xr]], gamma=0.01, eta=1.0,
+                        beta1=0.9, beta2=0.99, lam=0.0, decay=[False], prec=prec)
+    # Sterbenz: xr within a factor 2 of x, so x - xr is exact in fp32 too.
+    np.testing.assert_array_equal(res["delta"][0], (x.astype(np.float64) - xr))
+
+
+def test_difference_form_equals_paper_average_form():
+    """Algorithm 1 subtracts the all-reduce average of the models; the oracle
+    averages the differences.  Equal up to fp64 rounding of the sum."""
+    rng = np.random.default_rng(6)
+    x = rng.normal(0, 0.02, 4096).astype(np.float32)
+    reps = [(x + rng.normal(0, 1e-3, 4096)).astype(np.float32) for _ in range(8)]
+    res = O.global_step([x], [np.zeros_like(x)], [[r] for r in reps], gamma=1e-3,
+                        eta=0.8, beta1=0.95, beta2=0.98, lam=0.1, decay=[True])
+    avg = np.mean(np.stack(reps).astype(np.float64), axis=0)
+    lit = x.astype(np.float64) - avg
+    np.testing.assert_allclose(res["delta"][0], lit, rtol=0, atol=1e-17)
+
+
+# ---------------------------------------------------------------- closed forms
+
+def test_closed_form_sgd_constant_gradient():
+    """Same constant gradient g on every worker and step, SGD base, m_0 = 0:
+    (x_{t,0}-x_{t,tau})/gamma = tau*g, m_t = (1-beta2^t) tau g,
+    sign(u) = sign(g), x_t = (1-c)^t x_0 - eta*gamma*sign(g)(1-(1-c)^t)/c,
+    c = eta*gamma*lambda."""
+    rng = np.random.default_rng(7)
+    n, H, gamma, eta, b1, b2, lam = 3, 5, 0.01, 0.7, 0.95, 0.98, 0.1
+    x0 = rng.normal(0, 0.02, 64).astype(np.float32)
+    g = rng.normal(0, 1, 64).astype(np.float32)
+    st = O.init_state([x0], n, "sgd")
+    gamma32, eta32 = O.f32(gamma), O.f32(eta)
+    c = eta32 * gamma32 * O.f32(lam)
+    x_prev = x0.astype(np.float64)
+    for t in range(6):
+        res = O.communication_round(
+            st, lambda i, k: [g], t, H=H, local=dict(lr=gamma, beta1=0.0),
+            glob=dict(eta=eta, beta1=b1, beta2=b2, lam=lam, mode=O.SIGN_DET, seed=0),
+            decay=[True])
+        # Each local step stores the replica in fp32 (half an ulp of x), and
+        # the difference is divided by gamma: bound the error absolutely.
+        atol = 2 * H * 2.0 ** -24 * np.abs(x_prev).max() / gamma32
+        np.testing.assert_allclose(res["delta"][0] / gamma32, H * g.astype(np.float64),
+                                   rtol=1e-12, atol=atol)
+        np.testing.assert_array_equal(res["S"][0], np.sign(g))
+        x_expect = (1 - c) * x_prev - eta32 * gamma32 * np.sign(g)
+        np.testing.assert_allclose(res["x"][0], x_expect, rtol=1e-6, atol=1e-9)
+        x_prev = st["x"][0].astype(np.float64)
+    m_expect = (1 - O.f32(b2) ** 6) * H * g.astype(np.float64)
+    np.testing.assert_allclose(st["m"][0], m_expect, rtol=1e-4)
+    # Closed form after T rounds of x from x_0.
+    T = 6
+    xt = (1 - c) ** T * x0 - eta32 * gamma32 * np.sign(g) * (1 - (1 - c) ** T) / c
+    np.testing.assert_allclose(st["x"][0], xt, rtol=1e-5, atol=1e-8)
+
+
+def test_closed_form_adamw_constant_gradient():
+    """AdamW with a constant gradient: the bias-corrected moments are exactly
+    g and g^2, so x_{k+1} = x_k - lr (g/(|g|+eps) + lambda x_k) (Algorithm 2)."""
+    rng = np.random.default_rng(8)
+    x = rng.normal(0, 0.02, 200).astype(np.float32)
+    g = rng.normal(0, 1e-2, 200).astype(np.float32)
+    m = np.zeros_like(x)
+    v = np.zeros_like(x)
+    lr, wd, eps = O.f32(1e-3), O.f32(0.1), O.f32(1e-8)
+    xe = x.astype(np.float64)
+    for s in range(1, 30):
+        xn, mn, vn = O.local_adamw_step(x, g, m, v, lr=1e-3, beta1=0.9, beta2=0.95,
+                                        eps=1e-8, weight_decay=0.1, step=s)
+        x_expect = x.astype(np.float64) - lr * (g / (np.abs(g.astype(np.float64)) + eps)
+                                                + wd * x)
+        # m and v are stored in fp32 between steps, which perturbs the
+        # bias-corrected ratio by ~1e-7 relative; a wrong bias correction
+        # would change it by O(1), i.e. x by O(lr).
+        np.testing.assert_allclose(xn, x_expect, rtol=1e-12, atol=1e-6 * lr)
+        x, m, v = (a.astype(np.float32) for a in (xn, mn, vn))
+        xe = xe - lr * (g / (np.abs(g.astype(np.float64)) + eps) + wd * xe)
+    # 29 fp32 stores of x, half an ulp each.
+    np.testing.assert_allclose(x, xe, rtol=1e-5, atol=29 * 2.0 ** -24 * 0.1)
+
+
+# ---------------------------------------------------------------- library routines
+
+def _torch_adamw_one_step(x, g, m, v, s, lr, b1, b2, eps, wd):
+    p = torch.nn.Parameter(torch.tensor(x, dtype=torch.float64))
+    o = torch.optim.AdamW([p], lr=lr, betas=(b1, b2), eps=eps, weight_decay=wd,
+                          foreach=False)
+    o.state[p] = {"step": torch.tensor(float(s - 1)),
+                  "exp_avg": torch.tensor(m, dtype=torch.float64),
+                  "exp_avg_sq": torch.tensor(v, dtype=torch.float64)}
+    p.grad = torch.tensor(g, dtype=torch.float64)
+    o.step()
+    return (p.detach().numpy(), o.state[p]["exp_avg"].numpy(),
+            o.state[p]["exp_avg_sq"].numpy())
+
+
+def test_adamw_matches_torch_adamw():
+    """Algorithm 2 against torch.optim.AdamW (fp64, CPU): one step from
+    identical inputs agrees to fp64 rounding at several bias-correction
+    counts, and a 25-step fp32-stored trajectory stays within fp32 accuracy
+    of torch's fp64 trajectory."""
+    rng = np.random.default_rng(9)
+    d = 4097
+    b1, b2, eps, lr, wd = (O.f32(v) for v in (0.9, 0.95, 1e-8, 1e-3, 0.1))
+    x = rng.normal(0, 0.02, d).astype(np.float32)
+    m = rng.normal(0, 1e-3, d).astype(np.float32)
+    v = (rng.normal(0, 1e-3, d) ** 2).astype(np.float32)
+    for s in (1, 2, 13, 500):
+        g = rng.normal(0, 1e-2, d).astype(np.float32)
+        xn, mn, vn = O.local_adamw_step(x, g, m, v, lr=lr, beta1=b1, beta2=b2, eps=eps,
+                                        weight_decay=wd, step=s)
+        xt, mt, vt = _torch_adamw_one_step(x, g, m, v, s, lr, b1, b2, eps, wd)
+        np.testing.assert_allclose(xn, xt, rtol=1e-14, atol=1e-16)
+        np.testing.assert_allclose(mn, mt, rtol=1e-14, atol=1e-19)
+        np.testing.assert_allclose(vn, vt, rtol=1e-14, atol=1e-24)
+    p = torch.nn.Parameter(torch.tensor(x, dtype=torch.float64))
+    opt = torch.optim.AdamW([p], lr=lr, betas=(b1, b2), eps=eps, weight_decay=wd,
+                            foreach=False)
+    xo, mo, vo = x, np.zeros(d, np.float32), np.zeros(d, np.float32)
+    for s in range(1, 26):
+        g = rng.normal(0, 1e-2, d).astype(np.float32)
+        p.grad = torch.tensor(g, dtype=torch.float64)
+        opt.step()
+        xo, mo, vo = (a.astype(np.float32) for a in O.local_adamw_step(
+            xo, g, mo, vo, lr=lr, beta1=b1, beta2=b2, eps=eps, weight_decay=wd, step=s))
+    np.testing.assert_allclose(xo, p.detach().numpy(), rtol=1e-5, atol=1e-9)
+
+
+def test_sgdm_matches_torch_sgd():
+    """Algorithm 3 against torch.optim.SGD(momentum, dampening 0): a 20-step
+    fp32-stored trajectory stays within fp32 accuracy of torch's fp64 run."""
+    rng = np.random.default_rng(10)
+    d = 1000
+    x = rng.normal(0, 0.02, d).astype(np.float32)
+    p = torch.nn.Parameter(torch.tensor(x, dtype=torch.float64))
+    opt = torch.optim.SGD([p], lr=O.f32(0.1), momentum=O.f32(0.9), dampening=0.0,
+                          nesterov=False)
+    xo, mo = x, np.zeros(d, np.float32)
+    for _ in range(20):
+        g = rng.normal(0, 1e-3, d).astype(np.float32)
+        p.grad = torch.tensor(g, dtype=torch.float64)
+        opt.step()
+        xo, mo = (a.astype(np.float32) for a in O.local_sgdm_step(xo, g, mo, lr=0.1,
+                                                                   momentum=0.9))
+    np.testing.assert_allclose(xo, p.detach().numpy(), rtol=1e-5, atol=1e-8)
+    np.testing.assert_allclose(mo, opt.state[p]["momentum_buffer"].numpy(), rtol=1e-5,
+                               atol=1e-9)
+
+
+def test_sgdm_single_step_matches_torch_exactly():
+    """One Polyak step from identical inputs agrees with torch to fp64 rounding."""
+    rng = np.random.default_rng(11)
+    d = 777
+    x = rng.normal(0, 0.02, d).astype(np.float32)
+    m = rng.normal(0, 1e-2, d).astype(np.float32)
+    g = rng.normal(0, 1e-3, d).astype(np.float32)
+    p = torch.nn.Parameter(torch.tensor(x, dtype=torch.float64))
+    o = torch.optim.SGD([p], lr=O.f32(0.1), momentum=O.f32(0.9))
+    o.state[p] = {"momentum_buffer": torch.tensor(m, dtype=torch.float64)}
+    p.grad = torch.tensor(g, dtype=torch.float64)
+    o.step()
+    xn, mn = O.local_sgdm_step(x, g, m, lr=0.1, momentum=0.9)
+    np.testing.assert_allclose(xn, p.detach().numpy(), rtol=1e-15, atol=1e-19)
+    np.testing.assert_allclose(mn, o.state[p]["momentum_buffer"].numpy(), rtol=1e-15)
+
+
+def test_bias_correction_power():
+    """beta_power is beta**s (checked against exact rationals)."""
+    from fractions import Fraction
+    for beta in (0.9, 0.95, 0.999):
+        b = O.f32(beta)
+        for s in (1, 2, 7, 100, 1000):
+            exact = Fraction(b) ** s
+            got = O.beta_power(b, s)
+            if exact < Fraction(2) ** -80:
+                assert 1.0 - got == 1.0
+            else:
+                assert abs(Fraction(got) - exact) <= exact * Fraction(s + 1, 2 ** 52)
+
+
+# ---------------------------------------------------------------- randomized sign
+
+def test_randomized_sign_deterministic_limits():
+    """|u| = B keeps sign(u) with probability 1; u = 0 or B = 0 gives 0."""
+    k = np.arange(0, 1 << 24, 4099, dtype=np.int64)
+    for variant in (O.SIGN_RAND_FLIP, O.SIGN_RAND_ZERO):
+        for B in (1.0, 3.5e-3):
+            u = np.full(k.size, B)
+            u[::2] = -B
+            np.testing.assert_array_equal(O.randomized_sign(u, B, k, variant), np.sign(u))
+            z = O.randomized_sign(np.zeros(k.size), B, k, variant)
+            assert np.all(z == 0) and not np.any(np.signbit(z))
+        z = O.randomized_sign(np.zeros(k.size), 0.0, k, variant)
+        assert np.all(z == 0)
+
+
+def test_randomized_sign_threshold_is_exact():
+    """U < p is decided exactly: at U = p the sign is not kept, just below it is."""
+    B = O.f32(0.37)
+    # Eq. (10): keep iff k 2^-24 < |u|/B.  Choose u = k0 2^-24 B exactly.
+    k0 = 5_000_000
+    u = np.array([k0 * 2.0 ** -24 * B])
+    assert O.randomized_sign(u, B, np.array([k0]), O.SIGN_RAND_ZERO)[0] == 0.0
+    assert O.randomized_sign(u, B, np.array([k0 - 1]), O.SIGN_RAND_ZERO)[0] == 1.0
+    # Eq. (9): keep iff (2k - 2^24) 2^-24 B < |u|.
+    k1 = (1 << 23) + k0 // 2
+    u1 = np.array([(2 * k1 - (1 << 24)) * 2.0 ** -24 * B])
+    assert O.randomized_sign(u1, B, np.array([k1]), O.SIGN_RAND_FLIP)[0] == -1.0
+    assert O.randomized_sign(u1, B, np.array([k1 - 1]), O.SIGN_RAND_FLIP)[0] == 1.0
+
+
+@pytest.mark.parametrize("variant", [O.SIGN_RAND_FLIP, O.SIGN_RAND_ZERO])
+def test_lemma1_monte_carlo(variant):
+    """Lemma 1: E[S_r(v)] = v/B, and per element Var = 1 - (v/B)^2 (Eq. (9))
+    or |v|/B - (v/B)^2 (Eq. (10)); the total is at most d.  Draws come from
+    the oracle's Philox stream over many outer iterations t."""
+    B = 2.0
+    vals = np.array([-2.0, -1.5, -0.7, -0.1, 0.0, 0.05, 0.3, 1.0, 1.9, 2.0])
+    reps = 256
+    u = np.tile(vals, reps)
+    T = 40
+    draws = np.stack([O.randomized_sign(u, B, O.randomized_sign_uniforms(u.size, 3, t, 1234),
+                                        variant) for t in range(T)])
+    draws = draws.reshape(T * 1, reps, vals.size).reshape(-1, vals.size)
+    N = draws.shape[0]
+    mean = draws.mean(axis=0)
+    q = vals / B
+    var = 1 - q ** 2 if variant == O.SIGN_RAND_FLIP else np.abs(q) - q ** 2
+    var = np.where(q == 0, 0.0, var)   # sign(0) = 0: both outcomes of Eq. (9) are 0
+    sigma = np.sqrt(np.maximum(var, 1e-12) / N)
+    assert np.all(np.abs(mean - q) <= 5 * sigma + 1e-12), (mean, q)
+    emp_var = draws.var(axis=0)
+    assert np.all(np.abs(emp_var - var) <= 6 * np.sqrt(2.0 / N) + 1e-12)
+    # E||S_r(v) - v/B||^2 <= d.
+    assert np.mean(np.sum((draws - q) ** 2, axis=1)) <= vals.size
+
+
+def test_randomized_global_step_bound_and_support():
+    """Randomized global step: B is max |u| per tensor, S_r takes values in
+    {-1, 0, 1} with the support Eq. (9)/(10) allow, and elements with
+    |u| = B keep their sign."""
+    rng = np.random.default_rng(12)
+    x = [rng.normal(0, 0.02, s).astype(np.float32) for s in (1, 5, 1000)]
+    m = [rng.normal(0, 1, a.size).astype(np.float32) for a in x]
+    reps = [[(a + rng.normal(0, 1e-3, a.size)).astype(np.float32) for a in x]
+            for _ in range(2)]
+    for variant in (O.SIGN_RAND_FLIP, O.SIGN_RAND_ZERO):
+        res = O.global_step(x, m, reps, gamma=1e-3, eta=0.8, beta1=0.95, beta2=0.98,
+                            lam=0.1, decay=[False, True, True], t=3, mode=variant,
+                            seed=99, prec="fp32")
+        for p in range(3):
+            u, S, B = res["u"][p], res["S"][p], res["B"][p]
+            assert B == np.max(np.abs(u))
+            assert set(np.unique(S)).issubset({-1.0, 0.0, 1.0})
+            at_b = np.abs(u) == B
+            np.testing.assert_array_equal(S[at_b], np.sign(u[at_b]))
+            if variant == O.SIGN_RAND_ZERO:
+                assert np.all((S == 0) | (S == np.sign(u)))
+            else:
+                assert np.all(np.abs(S) == (u != 0))
+
+
+def test_randomized_stream_depends_on_counter_words():
+    """Every counter word (element block, tensor, t) and the seed change the draw."""
+    base = O.randomized_sign_uniforms(64, 2, 5, 77)
+    assert not np.array_equal(base, O.randomized_sign_uniforms(64, 3, 5, 77))
+    assert not np.array_equal(base, O.randomized_sign_uniforms(64, 2, 6, 77))
+    assert not np.array_equal(base, O.randomized_sign_uniforms(64, 2, 5, 78))
+    assert not np.array_equal(base, O.randomized_sign_uniforms(64, 2, 5, 77 + (1 << 32)))
+    assert np.all((base >= 0) & (base < (1 << 24)))
+    # A prefix of a longer tensor draws the same numbers (stream per element).
+    np.testing.assert_array_equal(base[:10], O.randomized_sign_uniforms(10, 2, 5, 77))
+
+
+# ---------------------------------------------------------------- Philox
+
+def test_philox_vectorised_matches_scalar():
+    rng = np.random.default_rng(13)
+    ctr = rng.integers(0, 2 ** 32, size=(64, 4), dtype=np.uint64)
+    key = rng.integers(0, 2 ** 32, size=2)
+    vec = O.philox4x32_10(ctr[:, 0], ctr[:, 1], ctr[:, 2], ctr[:, 3], int(key[0]), int(key[1]))
+    for r in range(64):
+        s = O.philox4x32_10_scalar(tuple(int(c) for c in ctr[r]), tuple(int(k) for k in key))
+        assert tuple(int(v[r]) for v in vec) == s
+
+
+def _build_rocrand_kat():
+    import shutil
+    import subprocess
+    import tempfile
+    hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+    if not os.path.exists(hipcc):
+        pytest.skip("hipcc not available to build the rocRAND known-answer program")
+    src = os.path.join(os.path.dirname(__file__), "native", "philox_kat.cpp")
+    out = os.path.join(tempfile.mkdtemp(prefix="dsm_kat_"), "philox_kat")
+    subprocess.run([hipcc, "-x", "hip", "--offload-host-only", "-O1", "-o", out, src],
+                   check=True, capture_output=True)
+    return out
+
+
+def test_philox_matches_rocrand_engine():
+    """Known answers from ROCm's open-source rocRAND Philox4x32-10 engine
+    (built for the host from its header): engine(seed, subsequence, offset)
+    with offset = 4*q returns the block with counter (q lo, q hi, subsequence
+    lo, subsequence hi) under key (seed lo, seed hi)."""
+    import subprocess
+    exe = _build_rocrand_kat()
+    rng = np.random.default_rng(14)
+    cases = [(0, 0, 0), (2 ** 64 - 1, 2 ** 64 - 1, 4 * (2 ** 62 - 1)), (1, 0, 4)]
+    for _ in range(200):
+        seed = int(rng.integers(0, 2 ** 63)) * 2 + int(rng.integers(0, 2))
+        sub = int(rng.integers(0, 2 ** 40)) << int(rng.integers(0, 24))
+        q = int(rng.integers(0, 2 ** 62))
+        cases.append((seed, sub % 2 ** 64, 4 * q))
+    inp = "".join(f"{s} {b} {o}\n" for s, b, o in cases)
+    out = subprocess.run([exe], input=inp, capture_output=True, text=True, check=True).stdout
+    lines = out.strip().split("\n")
+    assert len(lines) == len(cases)
+    for (seed, sub, off), line in zip(cases, lines):
+        q = off // 4
+        ctr = (q & 0xFFFFFFFF, q >> 32, sub & 0xFFFFFFFF, sub >> 32)
+        key = (seed & 0xFFFFFFFF, seed >> 32)
+        want = tuple(int(w, 16) for w in line.split())
+        assert O.philox4x32_10_scalar(ctr, key) == want, (seed, sub, off)
+    # The element stream used by the randomized sign, through the same engine:
+    # subsequence = t + 2^32 (t, stream word 1), offset = 4 ((p << 32) + j div 4).
+    seed, p, t = 0x0123456789ABCDEF, 7, 11
+    k = O.randomized_sign_uniforms(40, p, t, seed)
+    inp = "".join(f"{seed} {t + (1 << 32)} {4 * ((p << 32) + q)}\n" for q in range(10))
+    out = subprocess.run([exe], input=inp, capture_output=True, text=True, check=True).stdout
+    words = [int(w, 16) for line in out.strip().split("\n") for w in line.split()]
+    np.testing.assert_array_equal(k, np.array(words, dtype=np.int64) >> 8)
