@@ -1,0 +1,254 @@
+"""Benchmark of the distributed sign momentum hot path on one MI355X.
+
+One step = one outer iteration of Algorithm 1 on the GPT-2 1.5B-shaped
+workload (580 fp32 tensors, d = 1,557,611,200), n = 4 worker replicas:
+H = 12 fused local AdamW steps over all replicas, then one fused global step
+(worker average, sign momentum, decoupled weight decay, broadcast).  Every
+input is resident in HBM before timing starts.  Prints one JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--workload xl] [--sign det|rand]
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+METRIC = "param-updates/s and achieved HBM GB/s (% peak) for local step + global sign step"
+BYTES_LOCAL_ADAMW = 28     # x, g, m, v read; x, m, v written (fp32)
+BYTES_LOCAL_SGDM = 20      # x, g, m read; x, m written
+
+
+def bytes_global(n, randomized):
+    # x, m, n replicas read; x, m, n replicas written; the randomized sign
+    # adds the u round trip (write in pass 1, read in pass 2) and reads x twice.
+    return 16 + 8 * n + (12 if randomized else 0)
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("dsm_kernels.hip", "philox_device.h", "dsm_internal.h"):
+        with open(os.path.join(ROOT, "paper_2411_17866_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic(kernel_hash, name):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+    None when the counters were taken on a different kernel source."""
+    path = os.path.join(ROOT, "profiles", "hbm_traffic_xl.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_source_hash") != kernel_hash:
+        return None
+    k = rec.get("kernels", {}).get(name)
+    return None if k is None else k.get("bytes_per_launch")
+
+
+def cpu_baseline(w, ar, sample_tensors):
+    """The oracle (as it stands, fp64, one thread) on a bounded sample of the
+    same workload: one round of Algorithm 1 over a subset of the tensors."""
+    import numpy as np
+    import torch
+
+    import oracle as O
+
+    idx = [i for i, (name, _) in enumerate(w.tensors) if name in sample_tensors]
+    torch.cuda.synchronize()
+
+    def take(flat):
+        h = [flat[ar.offsets[i]:ar.offsets[i] + ar.numel[i]].cpu().numpy() for i in idx]
+        return h
+    x0 = take(ar.x)
+    grads = [take(ar.g_rep[i]) for i in range(w.n_workers)]
+    d_s = int(sum(ar.numel[i] for i in idx))
+    decay = [w.decay[i] for i in idx]
+    st = O.init_state(x0, w.n_workers, "adamw")
+    t0 = time.perf_counter()
+    O.communication_round(st, lambda i, k: grads[i], 0, H=w.local_steps, local=w.local,
+                          glob=dict(w.glob, mode=O.SIGN_DET, seed=0), decay=decay)
+    dt = time.perf_counter() - t0
+    updates = w.n_workers * w.local_steps * d_s + d_s
+    return {"value": updates / dt, "unit": "param-updates/s", "cores": 1, "kind": "oracle",
+            "sample": (f"one round (n={w.n_workers}, H={w.local_steps} AdamW local steps + "
+                       f"deterministic global step) of the oracle in fp64 on {len(idx)} tensors "
+                       f"({', '.join(sample_tensors)}), {d_s} of {w.d} parameters; "
+                       f"{dt:.1f} s on one host thread"),
+            "seconds": dt, "host_threads_available": len(os.sched_getaffinity(0))}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="xl")
+    ap.add_argument("--sign", choices=("det", "rand"), default="det",
+                    help="global sign of the timed steps")
+    ap.add_argument("--rand-steps", type=int, default=2,
+                    help="extra rounds with the randomized sign, timed separately")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 4 GiB device copy (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the multi-GPU exchange is a design note, not built)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2411_17866_amd import arena as A
+    from paper_2411_17866_amd import dsm
+    from paper_2411_17866_amd import workloads as W
+
+    dsm.load_library()
+    torch.cuda.set_device(0)
+    w = W.get(args.workload)
+    n, H = w.n_workers, w.local_steps
+    randomized_any = args.sign == "rand" or args.rand_steps > 0
+    print(f"[bench] workload {w.name}: d={w.d} tensors={len(w.tensors)} n={n} H={H}",
+          file=sys.stderr, flush=True)
+    ar = A.Arenas(w.numel, n, H, w.base, decay=w.decay, randomized=randomized_any)
+    gen = torch.Generator(device="cuda").manual_seed(w.seed)
+    W.fill_params_(ar.x, w, gen)
+    for i in range(n):
+        W.fill_grads_(ar.g_rep[i], w, i, 0)
+    ar.init()
+    torch.cuda.synchronize()
+    print("[bench] arenas resident: %.1f GB" % (torch.cuda.memory_allocated() / 1e9),
+          file=sys.stderr, flush=True)
+
+    stream = torch.cuda.current_stream()
+    lr = w.local["lr"]
+    ev = {"local": [], "global_det": [], "global_rand": []}
+    s_count = [0]
+
+    def one_round(t, mode, record):
+        for k in range(H):
+            s_count[0] += 1
+            if record:
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+            dsm.dsm_local_step(ar.ctx, -1, s_count[0], **w.local)
+            if record:
+                e1.record(stream)
+                ev["local"].append((e0, e1))
+        if record:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+        dsm.dsm_global_step(ar.ctx, t, gamma=lr, mode=mode, seed=w.philox_seed, broadcast=True,
+                            **w.glob)
+        if record:
+            e1.record(stream)
+            ev["global_rand" if mode else "global_det"].append((e0, e1))
+
+    mode_main = dsm.DSM_SIGN_DET if args.sign == "det" else dsm.DSM_SIGN_RAND_FLIP
+    t = 0
+    for _ in range(args.warmup):
+        one_round(t, mode_main, False)
+        t += 1
+    torch.cuda.synchronize()
+    print("[bench] warmup done", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        one_round(t, mode_main, True)
+        t += 1
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    print("[bench] timed steps done", file=sys.stderr, flush=True)
+    for _ in range(args.rand_steps if args.sign == "det" else 0):
+        one_round(t, dsm.DSM_SIGN_RAND_FLIP, True)
+        t += 1
+    torch.cuda.synchronize()
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    def avg_ms(pairs):
+        if not pairs:
+            return None
+        return sum(a.elapsed_time(b) for a, b in pairs) / len(pairs)
+
+    ms_local = avg_ms(ev["local"])
+    ms_gdet = avg_ms(ev["global_det"])
+    ms_grand = avg_ms(ev["global_rand"])
+    d = w.d
+    local_bytes = BYTES_LOCAL_ADAMW * n * d
+    khash = kernel_source_hash()
+    ms_per_step = wall * 1e3 / args.steps
+    updates_per_step = n * H * d + d
+    value = updates_per_step / (ms_per_step / 1e3)
+
+    def kern(ms, nbytes, updates):
+        if ms is None:
+            return None
+        gbs = nbytes / (ms / 1e3) / 1e9
+        return {"ms": round(ms, 4), "GB_per_s": round(gbs, 1),
+                "pct_peak_hbm": round(100 * gbs / PEAK_HBM_GBS, 2),
+                "param_updates_per_s": updates / (ms / 1e3), "algorithmic_bytes": nbytes}
+
+    traffic = committed_traffic(khash, "local_adamw")
+    achieved = local_bytes / (ms_local / 1e3) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "param-updates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"GPT-2 {w.name}-shaped parameter set ({len(w.tensors)} fp32 tensors, "
+                         f"d={d}), n={n} worker replicas, H={H} local AdamW steps + one "
+                         f"{'deterministic' if args.sign == 'det' else 'randomized'}-sign "
+                         "global step per step"),
+            "d": d, "n_workers": n, "local_steps": H, "base": "adamw",
+            "sign": args.sign, "updates_per_step": updates_per_step,
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "k_local_adamw (dsm_local_step, all workers)",
+            "achieved": round(achieved, 1),
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": local_bytes,
+            "avg_launch_ms": round(ms_local, 4),
+        },
+        "breakdown": {
+            "local_adamw": kern(ms_local, local_bytes, n * d),
+            "global_det": kern(ms_gdet, bytes_global(n, False) * d, d),
+            "global_rand_flip": kern(ms_grand, bytes_global(n, True) * d, d),
+        },
+        "kernel_source_hash": khash,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(
+            w, ar, ("h0.ln_1.weight", "h0.ln_1.bias", "h0.attn.c_attn.bias",
+                    "h0.attn.c_proj.weight", "h0.attn.c_proj.bias", "h0.ln_2.weight",
+                    "h0.ln_2.bias"))
+    ar.destroy()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

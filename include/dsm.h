@@ -1,0 +1,224 @@
+/*
+ * dsm.h - distributed sign momentum with local steps on one MI355X (gfx950).
+ *
+ * The method (arXiv 2411.17866, Section 2, Algorithm 1) minimises
+ * f(x) = (1/n) sum_i f_i(x), x in R^d (Eq. (1)), with n workers.  Each outer
+ * iteration t, every worker i takes tau = H local steps of a base optimizer
+ * (Eq. (4)); then the replicas are averaged (the all-reduce step), a global
+ * sign-momentum step updates the model and the global momentum (Eqs. (6)-(8))
+ * and the new model is copied back to every replica (synchronisation step).
+ *
+ * On one GPU the n workers are n replicas resident in HBM, and the all-reduce
+ * is a per-element sum over the replicas in worker order.  x in R^d is a list
+ * of tensors; they live concatenated in one flat fp32 arena per buffer, each
+ * tensor starting at a multiple of 64 elements (256 bytes).  dsm_layout gives
+ * the arena length (d_pad) and every tensor's offset.
+ *
+ * Conventions for every entry point:
+ *  - All arithmetic state is fp32.  Hyperparameters are fp32 numbers.
+ *  - Device pointers are allocated and owned by the caller (for instance as
+ *    torch tensors), must be 256-byte aligned, and must stay allocated and
+ *    unmoved for the lifetime of the context.  The library never allocates
+ *    or frees device memory.
+ *  - Calls that touch the GPU only enqueue work on the caller's stream and
+ *    return; completion is observed with the caller's stream or event
+ *    synchronisation.  dsm_read_bounds and dsm_destroy synchronise the stream.
+ *  - A status is returned; no exception crosses the boundary.  Argument and
+ *    state errors are detected on the host before anything is enqueued, and
+ *    then nothing is modified.  dsm_last_error gives the message.
+ *  - A context is not thread-safe; use one context per thread or lock.
+ */
+#ifndef DSM_H
+#define DSM_H
+
+#include <stdint.h>
+
+#if defined(__GNUC__)
+#define DSM_API __attribute__((visibility("default")))
+#else
+#define DSM_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct dsm_ctx dsm_ctx; /* opaque, host-side */
+
+typedef enum dsm_status {
+    DSM_OK = 0,
+    DSM_ERR_INVALID_ARG = 1, /* bad pointer, size, alignment or hyperparameter */
+    DSM_ERR_STATE = 2,       /* call out of the order Algorithm 1 requires */
+    DSM_ERR_HIP = 3,         /* HIP runtime error (no device, launch, copy) */
+    DSM_ERR_UNSUPPORTED = 4  /* valid request this build does not implement */
+} dsm_status;
+
+/* Base optimizer of the local steps (Section 2, "any base optimizer"). */
+typedef enum dsm_base {
+    DSM_BASE_ADAMW = 0,        /* Algorithm 2 (Appendix A) */
+    DSM_BASE_SGD_MOMENTUM = 1  /* Algorithm 3 (Appendix A), Polyak momentum */
+} dsm_base;
+
+/* The sign applied in the global step (Eq. (7)). */
+typedef enum dsm_sign {
+    DSM_SIGN_DET = 0,       /* sign(u), with sign(0) = 0 */
+    DSM_SIGN_RAND_FLIP = 1, /* randomized sign of Eq. (9) (Section 3.1) */
+    DSM_SIGN_RAND_ZERO = 2  /* randomized sign of Eq. (10) (Section 3.1) */
+} dsm_sign;
+
+/* The problem of Eq. (1): x in R^d given as n_tensors tensors. */
+typedef struct dsm_problem {
+    int32_t n_workers;     /* n, 1..64 */
+    int32_t local_steps;   /* tau = H >= 1, local steps per outer iteration */
+    int32_t n_tensors;     /* >= 0 */
+    int32_t base;          /* dsm_base */
+    const int64_t* numel;  /* host array [n_tensors], each in [0, 2^34) */
+    const uint8_t* decay;  /* host array [n_tensors]: 1 = weight decay applies
+                              (local and global); NULL = every tensor decays */
+} dsm_problem;
+
+/* Device buffers, all fp32 arenas of d_pad elements per copy.  The replica
+ * buffers hold n copies back to back (copy i at element offset i * d_pad). */
+typedef struct dsm_buffers {
+    float* x;          /* [d_pad]      global model x_{t,0} (in/out) */
+    float* m;          /* [d_pad]      global momentum m_t (zeroed by init) */
+    float* x_rep;      /* [n * d_pad]  worker replicas x^(i)_{t,k} */
+    float* g_rep;      /* [n * d_pad]  worker direction inputs (gradients),
+                          written by the caller before each local step */
+    float* s1_rep;     /* [n * d_pad]  AdamW first moment / Polyak momentum */
+    float* s2_rep;     /* [n * d_pad]  AdamW second moment; NULL for SGD */
+    float* u_scratch;  /* [d_pad]      u_{t+1} staging for the randomized
+                          sign; may be NULL if it is never used */
+    void* workspace;   /* device, >= workspace_bytes from dsm_layout */
+    int64_t workspace_bytes;
+    void* stream;      /* hipStream_t all work is enqueued on (NULL = default) */
+} dsm_buffers;
+
+/* Local hyperparameters (Algorithm 2 / Algorithm 3). */
+typedef struct dsm_local_hparams {
+    float lr;            /* gamma_t of Eq. (4), > 0 */
+    float beta1;         /* AdamW beta1, or the Polyak momentum coefficient */
+    float beta2;         /* AdamW beta2 (unused for SGD) */
+    float eps;           /* AdamW epsilon (unused for SGD) */
+    float weight_decay;  /* AdamW decoupled lambda on decayed tensors */
+} dsm_local_hparams;
+
+/* Global hyperparameters (Eqs. (6)-(8)). */
+typedef struct dsm_global_hparams {
+    float gamma;     /* gamma_t, the local learning rate of this round, > 0 */
+    float eta;       /* global learning rate eta >= 0 */
+    float beta1;     /* beta1 in [0, 1], Eq. (6) */
+    float beta2;     /* beta2 in [0, 1], Eq. (8) */
+    float lambda;    /* decoupled weight decay lambda >= 0, Eq. (7) */
+    int32_t mode;    /* dsm_sign */
+    uint64_t seed;   /* Philox key of the randomized sign */
+} dsm_global_hparams;
+
+/*
+ * dsm_layout - host only; enqueues nothing.
+ * Computes the arena layout for a problem: *arena_elems = d_pad, the length
+ * of one arena copy; tensor_offsets[p] = element offset of tensor p (the
+ * caller provides an array of n_tensors entries, or NULL); and
+ * *workspace_bytes = device workspace the context needs (tensor chunk table
+ * and the per-tensor bounds of the randomized sign).  Any output may be NULL.
+ * Errors: DSM_ERR_INVALID_ARG for an invalid problem.
+ */
+DSM_API dsm_status dsm_layout(const dsm_problem* problem, int64_t* arena_elems,
+                      int64_t* tensor_offsets, int64_t* workspace_bytes);
+
+/*
+ * dsm_init - Algorithm 1 initialisation: m_0 = 0, every replica x^(i)_{0,0} =
+ * x_{0,0} (the caller has written x), and the base-optimizer state of every
+ * worker is zero (Algorithms 2 and 3 start from m_0 = v_0 = 0).
+ * Creates *out (host memory only), uploads the chunk table into the caller's
+ * workspace and enqueues the initialisation kernel on buffers->stream.
+ * Errors: DSM_ERR_INVALID_ARG (problem, NULL or misaligned pointers, small
+ * workspace); DSM_ERR_HIP (no device, copy or launch failure).
+ */
+DSM_API dsm_status dsm_init(const dsm_problem* problem, const dsm_buffers* buffers,
+                    dsm_ctx** out);
+
+/*
+ * dsm_local_step - one local step of Eq. (4), x^(i) <- x^(i) - gamma_t d^(i),
+ * with d^(i) from the base optimizer (Algorithm 2 or 3) applied to the
+ * direction input g_rep of worker `worker` (0..n-1), or of every worker in
+ * one launch when worker == -1.  `step` is the AdamW bias-correction count
+ * s >= 1 (ignored for SGD); the caller passes it so that restarts are exact.
+ * Per element, in fp32 with one rounding per operation:
+ *   AdamW: m = b1*m + (1-b1)*g; v = b2*v + (1-b2)*(g*g);
+ *          x = x - lr*((m/(1-b1^s)) / (sqrt(v/(1-b2^s)) + eps) + wd_p*x)
+ *   SGD:   m = b1*m + g;  x = x - lr*m
+ * with wd_p = weight_decay on decayed tensors, else 0.
+ * Errors: DSM_ERR_INVALID_ARG (worker, step, hyperparameters);
+ * DSM_ERR_STATE (replicas not synchronised since the last global step with
+ * broadcast = 0, or the worker already took H local steps this round);
+ * DSM_ERR_HIP.
+ */
+DSM_API dsm_status dsm_local_step(dsm_ctx* ctx, int32_t worker, int64_t step,
+                          const dsm_local_hparams* hp);
+
+/*
+ * dsm_global_step - Algorithm 1 all-reduce and global step of outer
+ * iteration t, fused in one pass (two for the randomized sign):
+ *   delta = (1/n) sum_{i=0}^{n-1} (x - x^(i))        (worker order)
+ *   u     = b1*m + ((1-b1)/gamma)*delta               Eq. (6)
+ *   x     = x - (eta*gamma)*(S(u) + lambda_p*x)       Eq. (7)
+ *   m     = b2*m + ((1-b2)/gamma)*delta               Eq. (8), old m
+ * S = sign (sign(0) = 0), or the randomized sign of Eq. (9) / Eq. (10) with
+ * bound B_p = max_j |u_j| over tensor p and uniforms U = (w >> 8) 2^-24 from
+ * Philox4x32-10 keyed by `seed` with counter (j div 4, p, t, 1), word j mod 4
+ * (j = index inside the tensor); S keeps sign(u) exactly when U < the
+ * equation's probability.  When broadcast != 0 every replica is set to the
+ * new x (synchronisation step); otherwise call dsm_sync before the next
+ * local step.  The randomized modes need buffers->u_scratch.
+ * Errors: DSM_ERR_INVALID_ARG (t outside [0, 2^32), hyperparameters, mode,
+ * missing u_scratch); DSM_ERR_STATE (some worker has not taken exactly H
+ * local steps since the last synchronisation); DSM_ERR_HIP.
+ */
+DSM_API dsm_status dsm_global_step(dsm_ctx* ctx, int64_t t, const dsm_global_hparams* hp,
+                           int32_t broadcast);
+
+/*
+ * dsm_sync - the synchronisation step of Algorithm 1 on its own: every
+ * replica is set to x (bit-identical copies), and the local step counts of
+ * the round restart at zero.  Errors: DSM_ERR_INVALID_ARG, DSM_ERR_HIP.
+ */
+DSM_API dsm_status dsm_sync(dsm_ctx* ctx);
+
+/*
+ * dsm_read_bounds - copies the per-tensor bounds B_p of the last randomized
+ * global step into host_B[n_tensors] (host memory, caller-owned) and
+ * synchronises the stream.  Errors: DSM_ERR_STATE if the last global step was
+ * not randomized; DSM_ERR_INVALID_ARG; DSM_ERR_HIP.
+ */
+DSM_API dsm_status dsm_read_bounds(dsm_ctx* ctx, float* host_B);
+
+/*
+ * dsm_test_philox - diagnostic: writes Philox4x32-10 blocks for counters
+ * (q0 + b, tensor, t, 1), b = 0..count-1, under key `seed`, as 4*count
+ * uint32 words to device memory dev_out (caller-owned, 4-byte aligned), on
+ * `stream`.  The same generator the randomized sign uses.
+ * Errors: DSM_ERR_INVALID_ARG (NULL output, count < 0, q0 + count > 2^32,
+ * t outside [0, 2^32)); DSM_ERR_HIP.
+ */
+DSM_API dsm_status dsm_test_philox(uint64_t seed, uint32_t tensor, int64_t t, int64_t q0,
+                           int64_t count, uint32_t* dev_out, void* stream);
+
+/*
+ * dsm_destroy - synchronises the context's stream and frees the context's
+ * host memory.  The caller's device buffers are untouched.  NULL is a no-op.
+ */
+DSM_API dsm_status dsm_destroy(dsm_ctx* ctx);
+
+/*
+ * dsm_last_error - message of the last failed call on ctx, or, for ctx ==
+ * NULL, of the last failed call on this thread.  Empty string if none.  The
+ * pointer stays valid until the next call on the same context or thread.
+ */
+DSM_API const char* dsm_last_error(const dsm_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DSM_H */

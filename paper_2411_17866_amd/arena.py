@@ -1,0 +1,71 @@
+"""Device memory for the library: torch tensors as the caller-owned arenas.
+
+PyTorch only allocates device memory and supplies the stream; every step of
+the method runs in libdsm.so through the binding in ``dsm``.
+"""
+import torch
+
+from . import dsm
+
+
+class Arenas:
+    """The arenas and workspace of one problem, allocated with torch, plus the
+    dsm_buffers struct that points at them.
+
+    numel: per-tensor element counts; n_workers, local_steps, base: the
+    problem (dsm_problem); decay: per-tensor weight-decay flags or None;
+    randomized: allocate u_scratch for the randomized sign.
+    """
+
+    def __init__(self, numel, n_workers, local_steps, base, decay=None, randomized=True,
+                 device="cuda"):
+        self.numel = [int(v) for v in numel]
+        self.n = int(n_workers)
+        self.H = int(local_steps)
+        self.base = int(base)
+        self.decay = None if decay is None else [bool(v) for v in decay]
+        self.problem = dsm.make_problem(self.numel, self.n, self.H, self.base, self.decay)
+        self.arena_elems, self.offsets, self.workspace_bytes = dsm.dsm_layout(self.problem)
+        a = max(self.arena_elems, 64)
+        f32 = torch.float32
+        self.x = torch.zeros(a, dtype=f32, device=device)
+        self.m = torch.zeros(a, dtype=f32, device=device)
+        self.x_rep = torch.zeros(self.n, a, dtype=f32, device=device)
+        self.g_rep = torch.zeros(self.n, a, dtype=f32, device=device)
+        self.s1_rep = torch.zeros(self.n, a, dtype=f32, device=device)
+        self.s2_rep = (torch.zeros(self.n, a, dtype=f32, device=device)
+                       if self.base == dsm.DSM_BASE_ADAMW else None)
+        self.u = torch.zeros(a, dtype=f32, device=device) if randomized else None
+        self.workspace = torch.zeros(max(self.workspace_bytes, 256), dtype=torch.uint8,
+                                     device=device)
+        self.ctx = None
+
+    def buffers(self, stream=None):
+        if stream is None:
+            stream = torch.cuda.current_stream()
+
+        def ptr(t):
+            return None if t is None else t.data_ptr()
+        return dsm.dsm_buffers(ptr(self.x), ptr(self.m), ptr(self.x_rep), ptr(self.g_rep),
+                               ptr(self.s1_rep), ptr(self.s2_rep), ptr(self.u),
+                               ptr(self.workspace), self.workspace.numel(), stream.cuda_stream)
+
+    def init(self, stream=None):
+        """dsm_init on the current contents of x."""
+        self.ctx = dsm.dsm_init(self.problem, self.buffers(stream))
+        return self.ctx
+
+    def views(self, flat):
+        """Per-tensor views of one arena copy (a 1-D tensor of arena_elems)."""
+        return [flat[o:o + n] for o, n in zip(self.offsets, self.numel)]
+
+    def destroy(self):
+        if self.ctx is not None:
+            dsm.dsm_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass

@@ -1,0 +1,79 @@
+// Internal interface between the host runtime (dsm_runtime.cpp) and the
+// gfx950 kernels (dsm_kernels.hip).  Not part of the public C ABI.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace dsm {
+
+// Elements per work-group chunk.  A chunk never crosses a tensor boundary,
+// so the per-tensor facts a kernel needs (decay flag, tensor index for the
+// randomized sign's bound and Philox counter) are uniform per work-group and
+// read once.  Multiple of 4 (float4) and of 256 threads x 4.
+constexpr int kChunkElems = 16384;
+constexpr int kBlockThreads = 256;
+// Arena alignment of every tensor, in elements (256 bytes).
+constexpr int64_t kTensorAlign = 64;
+constexpr int kMaxWorkers = 64;
+
+// One chunk of one tensor inside an arena copy.  32 bytes.
+struct Chunk {
+    int64_t off;      // element offset of the chunk in the arena
+    int64_t j0;       // index of the chunk's first element inside its tensor
+    int32_t len;      // elements in the chunk, 1..kChunkElems
+    uint32_t tensor;  // tensor index p
+    uint32_t decay;   // 1 if weight decay applies to the tensor
+    uint32_t pad;
+};
+static_assert(sizeof(Chunk) == 32, "chunk descriptor is 32 bytes");
+
+// fp32 coefficients of one AdamW local step, formed on the host in fp64 and
+// rounded once.
+struct AdamScalars {
+    float beta1, one_minus_beta1, beta2, one_minus_beta2;
+    float bc1, bc2;   // 1 - beta1^s, 1 - beta2^s
+    float lr, eps, wd;
+};
+
+struct SgdScalars {
+    float mu, lr;
+};
+
+// fp32 coefficients of one global step.
+struct GlobalScalars {
+    float beta1, beta2;
+    float c1, c2;      // (1 - beta1)/gamma, (1 - beta2)/gamma
+    float step;        // eta * gamma
+    float lam;         // lambda (decayed tensors)
+    float inv_n;       // 1/n, used only when n is a power of two (then exact)
+    float n_f;         // n as float
+    int32_t n;
+    int32_t n_pow2;    // 1 if n is a power of two
+    uint32_t key0, key1;  // Philox key (seed low, seed high)
+    uint32_t t;           // outer iteration (Philox counter word 2)
+    int32_t mode;         // dsm_sign
+};
+
+// Kernel launchers (dsm_kernels.hip).  All return the launch status.
+hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float* m, float* x_rep,
+                       float* s1, float* s2, int64_t stride, int n, hipStream_t st);
+hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_rep,
+                              const float* g_rep, float* s1, float* s2, int64_t stride,
+                              int worker0, int n_workers, const AdamScalars& sc, hipStream_t st);
+hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep,
+                             const float* g_rep, float* s1, int64_t stride, int worker0,
+                             int n_workers, const SgdScalars& sc, hipStream_t st);
+hipError_t launch_global_det(const Chunk* chunks, int64_t n_chunks, float* x, float* m,
+                             float* x_rep, int64_t stride, const GlobalScalars& sc,
+                             bool broadcast, hipStream_t st);
+hipError_t launch_global_rand(const Chunk* chunks, int64_t n_chunks, int n_tensors, float* x,
+                              float* m, float* x_rep, float* u, uint32_t* bound_bits,
+                              int64_t stride, const GlobalScalars& sc, bool broadcast,
+                              hipStream_t st);
+hipError_t launch_broadcast(const Chunk* chunks, int64_t n_chunks, const float* x, float* x_rep,
+                            int64_t stride, int n, hipStream_t st);
+hipError_t launch_test_philox(uint32_t key0, uint32_t key1, uint32_t tensor, uint32_t t,
+                              uint32_t q0, int64_t count, uint32_t* out, hipStream_t st);
+
+}  // namespace dsm

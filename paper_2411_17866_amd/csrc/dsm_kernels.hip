@@ -1,0 +1,551 @@
+// gfx950 kernels of distributed sign momentum with local steps
+// (arXiv 2411.17866, Algorithm 1).
+//
+// Every kernel streams fp32 arenas: each work-group takes one chunk of one
+// tensor (Chunk), each thread moves 128-bit (float4) groups with nontemporal
+// loads and stores, consecutive threads touch consecutive 16-byte groups,
+// and every element is read and written once per pass.  Nothing here is a
+// dense contraction, so there is no MFMA; the bound is HBM bandwidth.
+//
+// Arithmetic: fp32, one IEEE round-to-nearest operation per written
+// operation, in the order the formulas are written; no contraction into FMA
+// (-ffp-contract=off and the pragma below), correctly rounded division and
+// square root, denormals kept.
+#include <hip/hip_runtime.h>
+
+#include "dsm_internal.h"
+#include "philox_device.h"
+
+#pragma clang fp contract(off)
+
+namespace dsm {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+constexpr int kUnroll = 2;
+
+__device__ __forceinline__ f4 ntload(const f4* p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ void ntstore(f4 v, f4* p) { __builtin_nontemporal_store(v, p); }
+
+// Stores the first k (1..3) lanes of v: the ragged end of a tensor.
+__device__ __forceinline__ void store_head(f4 v, float* p, int k) {
+    p[0] = v.x;
+    if (k > 1) p[1] = v.y;
+    if (k > 2) p[2] = v.z;
+}
+
+// Stores v at group q of p: whole group, or only the lanes inside the chunk.
+__device__ __forceinline__ void store_group(f4 v, f4* p, int q, int nfull, int len) {
+    if (q < nfull)
+        ntstore(v, p + q);
+    else
+        store_head(v, reinterpret_cast<float*>(p + q), len - 4 * q);
+}
+
+// ---------------------------------------------------------------- AdamW
+
+// Correctly rounded square root (the build asks for correctly rounded fp32
+// division and square root).
+__device__ __forceinline__ f4 sqrt_rn(f4 a) {
+    return f4{__builtin_sqrtf(a.x), __builtin_sqrtf(a.y), __builtin_sqrtf(a.z), __builtin_sqrtf(a.w)};
+}
+
+// Algorithm 2 on four elements (lane-wise); x, m, v updated in place.
+__device__ __forceinline__ void adamw4(f4& x, f4 g, f4& m, f4& v, float lam, const AdamScalars& s) {
+    const f4 m1 = s.beta1 * m;
+    const f4 m2 = s.one_minus_beta1 * g;
+    m = m1 + m2;
+    const f4 gg = g * g;
+    const f4 v1 = s.beta2 * v;
+    const f4 v2 = s.one_minus_beta2 * gg;
+    v = v1 + v2;
+    const f4 m_hat = m / s.bc1;
+    const f4 v_hat = v / s.bc2;
+    const f4 den = sqrt_rn(v_hat) + s.eps;
+    const f4 r = m_hat / den;
+    const f4 wx = lam * x;
+    const f4 d = r + wx;
+    const f4 st = s.lr * d;
+    x = x - st;
+}
+
+__global__ __launch_bounds__(kBlockThreads) void k_local_adamw(
+    const Chunk* __restrict__ chunks, float* __restrict__ x_rep, const float* __restrict__ g_rep,
+    float* __restrict__ s1, float* __restrict__ s2, int64_t stride, int worker0, AdamScalars sc) {
+    const Chunk c = chunks[blockIdx.x];
+    const int64_t base = static_cast<int64_t>(worker0 + static_cast<int>(blockIdx.y)) * stride + c.off;
+    f4* __restrict__ xp = reinterpret_cast<f4*>(x_rep + base);
+    const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + base);
+    f4* __restrict__ mp = reinterpret_cast<f4*>(s1 + base);
+    f4* __restrict__ vp = reinterpret_cast<f4*>(s2 + base);
+    const float lam = c.decay ? sc.wd : 0.0f;
+    const int nvec = (c.len + 3) >> 2;
+    const int nfull = c.len >> 2;
+    for (int q0 = threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+        f4 xv[kUnroll], gv[kUnroll], mv[kUnroll], vv[kUnroll];
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) {
+            const int q = q0 + k * kBlockThreads;
+            if (q < nvec) {
+                xv[k] = ntload(xp + q);
+                gv[k] = ntload(gp + q);
+                mv[k] = ntload(mp + q);
+                vv[k] = ntload(vp + q);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) {
+            const int q = q0 + k * kBlockThreads;
+            if (q < nvec) {
+                adamw4(xv[k], gv[k], mv[k], vv[k], lam, sc);
+                store_group(xv[k], xp, q, nfull, c.len);
+                store_group(mv[k], mp, q, nfull, c.len);
+                store_group(vv[k], vp, q, nfull, c.len);
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------- SGD + momentum
+
+// Algorithm 3 on four elements (lane-wise).
+__device__ __forceinline__ void sgdm4(f4& x, f4 g, f4& m, const SgdScalars& s) {
+    const f4 m1 = s.mu * m;
+    m = m1 + g;
+    const f4 st = s.lr * m;
+    x = x - st;
+}
+
+__global__ __launch_bounds__(kBlockThreads) void k_local_sgdm(
+    const Chunk* __restrict__ chunks, float* __restrict__ x_rep, const float* __restrict__ g_rep,
+    float* __restrict__ s1, int64_t stride, int worker0, SgdScalars sc) {
+    const Chunk c = chunks[blockIdx.x];
+    const int64_t base = static_cast<int64_t>(worker0 + static_cast<int>(blockIdx.y)) * stride + c.off;
+    f4* __restrict__ xp = reinterpret_cast<f4*>(x_rep + base);
+    const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + base);
+    f4* __restrict__ mp = reinterpret_cast<f4*>(s1 + base);
+    const int nvec = (c.len + 3) >> 2;
+    const int nfull = c.len >> 2;
+    for (int q0 = threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+        f4 xv[kUnroll], gv[kUnroll], mv[kUnroll];
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) {
+            const int q = q0 + k * kBlockThreads;
+            if (q < nvec) {
+                xv[k] = ntload(xp + q);
+                gv[k] = ntload(gp + q);
+                mv[k] = ntload(mp + q);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) {
+            const int q = q0 + k * kBlockThreads;
+            if (q < nvec) {
+                sgdm4(xv[k], gv[k], mv[k], sc);
+                store_group(xv[k], xp, q, nfull, c.len);
+                store_group(mv[k], mp, q, nfull, c.len);
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------- global step
+
+// sign with sign(+-0) = +0 and sign(NaN) = NaN.
+__device__ __forceinline__ float sign_of(float u) {
+    return u > 0.0f ? 1.0f : (u < 0.0f ? -1.0f : (u == u ? 0.0f : u));
+}
+
+// Worker sum of (x - x_i) over the n replicas of group q, in worker order,
+// divided by n.  N > 0: compile-time worker count (a power of two, so the
+// division is the exact multiplication by 1/n); N == 0: runtime count.
+template <int N>
+__device__ __forceinline__ f4 worker_mean_diff(f4 xv, const float* __restrict__ rbase,
+                                               int64_t stride, int q, const GlobalScalars& s) {
+    if constexpr (N > 0) {
+        f4 r[N];
+#pragma unroll
+        for (int i = 0; i < N; ++i) r[i] = ntload(reinterpret_cast<const f4*>(rbase + i * stride) + q);
+        f4 acc = xv - r[0];
+#pragma unroll
+        for (int i = 1; i < N; ++i) acc = acc + (xv - r[i]);
+        return acc * s.inv_n;
+    } else {
+        f4 acc = xv - ntload(reinterpret_cast<const f4*>(rbase) + q);
+        for (int i = 1; i < s.n; ++i)
+            acc = acc + (xv - ntload(reinterpret_cast<const f4*>(rbase + i * stride) + q));
+        if (s.n_pow2) return acc * s.inv_n;
+        return acc / s.n_f;
+    }
+}
+
+__device__ __forceinline__ f4 sign4(f4 u) {
+    return f4{sign_of(u.x), sign_of(u.y), sign_of(u.z), sign_of(u.w)};
+}
+
+// Eqs. (6) and (8) from the old m, lane-wise; returns u, updates m.
+__device__ __forceinline__ f4 momentum4(f4& m, f4 delta, const GlobalScalars& s) {
+    const f4 u1 = s.beta1 * m;
+    const f4 u2 = s.c1 * delta;
+    const f4 u = u1 + u2;
+    const f4 m1 = s.beta2 * m;
+    const f4 m2 = s.c2 * delta;
+    m = m1 + m2;
+    return u;
+}
+
+// Eq. (7) with the applied sign S, lane-wise.
+__device__ __forceinline__ f4 model4(f4 x, f4 S, float lam, const GlobalScalars& s) {
+    const f4 wx = lam * x;
+    const f4 a = S + wx;
+    const f4 st = s.step * a;
+    return x - st;
+}
+
+template <int N, bool BCAST>
+__global__ __launch_bounds__(kBlockThreads) void k_global_det(
+    const Chunk* __restrict__ chunks, float* __restrict__ x, float* __restrict__ m,
+    float* __restrict__ x_rep, int64_t stride, GlobalScalars sc) {
+    const Chunk c = chunks[blockIdx.x];
+    const int n = N > 0 ? N : sc.n;
+    f4* __restrict__ xp = reinterpret_cast<f4*>(x + c.off);
+    f4* __restrict__ mp = reinterpret_cast<f4*>(m + c.off);
+    float* __restrict__ rbase = x_rep + c.off;
+    const float lam = c.decay ? sc.lam : 0.0f;
+    const int nvec = (c.len + 3) >> 2;
+    const int nfull = c.len >> 2;
+    for (int q0 = threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+        f4 xv[kUnroll], mv[kUnroll], dv[kUnroll];
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) {
+            const int q = q0 + k * kBlockThreads;
+            if (q < nvec) {
+                xv[k] = ntload(xp + q);
+                mv[k] = ntload(mp + q);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) {
+            const int q = q0 + k * kBlockThreads;
+            if (q < nvec) dv[k] = worker_mean_diff<N>(xv[k], rbase, stride, q, sc);
+        }
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) {
+            const int q = q0 + k * kBlockThreads;
+            if (q < nvec) {
+                const f4 u = momentum4(mv[k], dv[k], sc);
+                const f4 xn = model4(xv[k], sign4(u), lam, sc);
+                store_group(xn, xp, q, nfull, c.len);
+                store_group(mv[k], mp, q, nfull, c.len);
+                if (BCAST) {
+                    for (int i = 0; i < n; ++i)
+                        store_group(xn, reinterpret_cast<f4*>(rbase + i * stride), q, nfull, c.len);
+                }
+            }
+        }
+    }
+}
+
+// Largest of the bit patterns of non-negative floats of a work-group, then
+// one atomic max per work-group into the tensor's bound.  For non-negative
+// IEEE floats the unsigned order of the bit patterns is the numeric order.
+__device__ __forceinline__ void block_max_to(uint32_t bits, uint32_t* wave_max, uint32_t* dst) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const uint32_t o = __shfl_xor(bits, off, 64);
+        bits = o > bits ? o : bits;
+    }
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    if (lane == 0) wave_max[wave] = bits;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t b = wave_max[0];
+#pragma unroll
+        for (int w = 1; w < kBlockThreads / 64; ++w) b = wave_max[w] > b ? wave_max[w] : b;
+        atomicMax(dst, b);
+    }
+}
+
+// Randomized sign, pass 1: the all-reduce difference, u_{t+1} (staged to u)
+// and m_{t+1} (Eqs. (6), (8)), and the tensor bound B_p = max |u|.
+template <int N>
+__global__ __launch_bounds__(kBlockThreads) void k_global_rand_pass1(
+    const Chunk* __restrict__ chunks, const float* __restrict__ x, float* __restrict__ m,
+    const float* __restrict__ x_rep, float* __restrict__ u_out, uint32_t* __restrict__ bound_bits,
+    int64_t stride, GlobalScalars sc) {
+    const Chunk c = chunks[blockIdx.x];
+    const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + c.off);
+    f4* __restrict__ mp = reinterpret_cast<f4*>(m + c.off);
+    f4* __restrict__ up = reinterpret_cast<f4*>(u_out + c.off);
+    const float* __restrict__ rbase = x_rep + c.off;
+    const int nvec = (c.len + 3) >> 2;
+    const int nfull = c.len >> 2;
+    __shared__ uint32_t wave_max[kBlockThreads / 64];
+    uint32_t maxbits = 0;
+    for (int q0 = threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+        f4 xv[kUnroll], mv[kUnroll], dv[kUnroll];
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) {
+            const int q = q0 + k * kBlockThreads;
+            if (q < nvec) {
+                xv[k] = ntload(xp + q);
+                mv[k] = ntload(mp + q);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) {
+            const int q = q0 + k * kBlockThreads;
+            if (q < nvec) dv[k] = worker_mean_diff<N>(xv[k], rbase, stride, q, sc);
+        }
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) {
+            const int q = q0 + k * kBlockThreads;
+            if (q < nvec) {
+                const f4 uv = momentum4(mv[k], dv[k], sc);
+                store_group(uv, up, q, nfull, c.len);
+                store_group(mv[k], mp, q, nfull, c.len);
+                const int valid = c.len - 4 * q;  // lanes inside the tensor
+                uint32_t b = __float_as_uint(fabsf(uv.x));
+                if (valid > 1) b = max(b, __float_as_uint(fabsf(uv.y)));
+                if (valid > 2) b = max(b, __float_as_uint(fabsf(uv.z)));
+                if (valid > 3) b = max(b, __float_as_uint(fabsf(uv.w)));
+                maxbits = max(maxbits, b);
+            }
+        }
+    }
+    block_max_to(maxbits, wave_max, bound_bits + c.tensor);
+}
+
+// S_r(u) of Eq. (9) (MODE 1) or Eq. (10) (MODE 2) for one element, given the
+// Philox word w (U = (w >> 8) 2^-24) and the bound B (as double).  "sign(u)
+// with probability p" is decided by the exact comparison U < p, evaluated in
+// fp64 where both sides are exact: (2k - 2^24) B < |u| 2^24 for Eq. (9),
+// k B < |u| 2^24 for Eq. (10).
+template <int MODE>
+__device__ __forceinline__ float rand_sign(float u, uint32_t w, double B) {
+    const float sgn = sign_of(u);
+    const double au = static_cast<double>(fabsf(u)) * 16777216.0;
+    const int32_t k = static_cast<int32_t>(w >> 8);
+    if constexpr (MODE == 1) {
+        const double a = static_cast<double>(2 * k - (1 << 24));
+        return (a * B < au) ? sgn : 0.0f - sgn;
+    } else {
+        return (static_cast<double>(k) * B < au) ? sgn : 0.0f;
+    }
+}
+
+// Randomized sign, pass 2: S_r, Eq. (7) and the synchronisation step.
+template <int MODE, bool BCAST>
+__global__ __launch_bounds__(kBlockThreads) void k_global_rand_pass2(
+    const Chunk* __restrict__ chunks, float* __restrict__ x, float* __restrict__ x_rep,
+    const float* __restrict__ u_in, const uint32_t* __restrict__ bound_bits, int64_t stride,
+    GlobalScalars sc) {
+    const Chunk c = chunks[blockIdx.x];
+    f4* __restrict__ xp = reinterpret_cast<f4*>(x + c.off);
+    const f4* __restrict__ up = reinterpret_cast<const f4*>(u_in + c.off);
+    float* __restrict__ rbase = x_rep + c.off;
+    const float lam = c.decay ? sc.lam : 0.0f;
+    const double B = static_cast<double>(__uint_as_float(bound_bits[c.tensor]));
+    const uint32_t blk0 = static_cast<uint32_t>(c.j0 >> 2);
+    const int nvec = (c.len + 3) >> 2;
+    const int nfull = c.len >> 2;
+    for (int q0 = threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+        f4 xv[kUnroll], uv[kUnroll];
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) {
+            const int q = q0 + k * kBlockThreads;
+            if (q < nvec) {
+                xv[k] = ntload(xp + q);
+                uv[k] = ntload(up + q);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) {
+            const int q = q0 + k * kBlockThreads;
+            if (q < nvec) {
+                uint32_t w0 = blk0 + static_cast<uint32_t>(q), w1 = c.tensor, w2 = sc.t,
+                         w3 = kSignStream;
+                philox4x32_10(w0, w1, w2, w3, sc.key0, sc.key1);
+                const f4 S = {rand_sign<MODE>(uv[k].x, w0, B), rand_sign<MODE>(uv[k].y, w1, B),
+                              rand_sign<MODE>(uv[k].z, w2, B), rand_sign<MODE>(uv[k].w, w3, B)};
+                const f4 xn = model4(xv[k], S, lam, sc);
+                store_group(xn, xp, q, nfull, c.len);
+                if (BCAST) {
+                    for (int i = 0; i < sc.n; ++i)
+                        store_group(xn, reinterpret_cast<f4*>(rbase + i * stride), q, nfull, c.len);
+                }
+            }
+        }
+    }
+}
+
+__global__ __launch_bounds__(kBlockThreads) void k_fill_u32(uint32_t* __restrict__ p, int count,
+                                                           uint32_t value) {
+    const int i = blockIdx.x * kBlockThreads + threadIdx.x;
+    if (i < count) p[i] = value;
+}
+
+// ---------------------------------------------------------------- sync / init
+
+// Synchronisation step: x_rep[i] <- x for every replica.
+__global__ __launch_bounds__(kBlockThreads) void k_broadcast(
+    const Chunk* __restrict__ chunks, const float* __restrict__ x, float* __restrict__ x_rep,
+    int64_t stride, int n) {
+    const Chunk c = chunks[blockIdx.x];
+    const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + c.off);
+    float* __restrict__ rbase = x_rep + c.off;
+    const int nvec = (c.len + 3) >> 2;
+    const int nfull = c.len >> 2;
+    for (int q = threadIdx.x; q < nvec; q += kBlockThreads) {
+        const f4 v = ntload(xp + q);
+        for (int i = 0; i < n; ++i)
+            store_group(v, reinterpret_cast<f4*>(rbase + i * stride), q, nfull, c.len);
+    }
+}
+
+// Algorithm 1 initialisation: m = 0, replicas = x, base state = 0.
+__global__ __launch_bounds__(kBlockThreads) void k_init(
+    const Chunk* __restrict__ chunks, const float* __restrict__ x, float* __restrict__ m,
+    float* __restrict__ x_rep, float* __restrict__ s1, float* __restrict__ s2, int64_t stride,
+    int n) {
+    const Chunk c = chunks[blockIdx.x];
+    const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + c.off);
+    const int nvec = (c.len + 3) >> 2;
+    const int nfull = c.len >> 2;
+    const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int q = threadIdx.x; q < nvec; q += kBlockThreads) {
+        const f4 v = ntload(xp + q);
+        store_group(zero, reinterpret_cast<f4*>(m + c.off), q, nfull, c.len);
+        for (int i = 0; i < n; ++i) {
+            const int64_t o = i * stride + c.off;
+            store_group(v, reinterpret_cast<f4*>(x_rep + o), q, nfull, c.len);
+            store_group(zero, reinterpret_cast<f4*>(s1 + o), q, nfull, c.len);
+            if (s2 != nullptr) store_group(zero, reinterpret_cast<f4*>(s2 + o), q, nfull, c.len);
+        }
+    }
+}
+
+__global__ __launch_bounds__(kBlockThreads) void k_test_philox(uint32_t key0, uint32_t key1,
+                                                              uint32_t tensor, uint32_t t,
+                                                              uint32_t q0, int64_t count,
+                                                              uint32_t* __restrict__ out) {
+    const int64_t b = static_cast<int64_t>(blockIdx.x) * kBlockThreads + threadIdx.x;
+    if (b >= count) return;
+    uint32_t w0 = q0 + static_cast<uint32_t>(b), w1 = tensor, w2 = t, w3 = kSignStream;
+    philox4x32_10(w0, w1, w2, w3, key0, key1);
+    out[4 * b + 0] = w0;
+    out[4 * b + 1] = w1;
+    out[4 * b + 2] = w2;
+    out[4 * b + 3] = w3;
+}
+
+dim3 chunk_grid(int64_t n_chunks, int n_workers) {
+    return dim3(static_cast<unsigned>(n_chunks), static_cast<unsigned>(n_workers), 1);
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- launchers
+
+hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float* m, float* x_rep,
+                       float* s1, float* s2, int64_t stride, int n, hipStream_t st) {
+    if (n_chunks == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_init, chunk_grid(n_chunks, 1), dim3(kBlockThreads), 0, st, chunks, x, m,
+                       x_rep, s1, s2, stride, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_rep,
+                              const float* g_rep, float* s1, float* s2, int64_t stride,
+                              int worker0, int n_workers, const AdamScalars& sc, hipStream_t st) {
+    if (n_chunks == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_local_adamw, chunk_grid(n_chunks, n_workers), dim3(kBlockThreads), 0, st,
+                       chunks, x_rep, g_rep, s1, s2, stride, worker0, sc);
+    return hipGetLastError();
+}
+
+hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep,
+                             const float* g_rep, float* s1, int64_t stride, int worker0,
+                             int n_workers, const SgdScalars& sc, hipStream_t st) {
+    if (n_chunks == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_local_sgdm, chunk_grid(n_chunks, n_workers), dim3(kBlockThreads), 0, st,
+                       chunks, x_rep, g_rep, s1, stride, worker0, sc);
+    return hipGetLastError();
+}
+
+template <bool BCAST>
+static void launch_global_det_n(const Chunk* chunks, int64_t n_chunks, float* x, float* m,
+                                float* x_rep, int64_t stride, const GlobalScalars& sc,
+                                hipStream_t st) {
+    const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
+    switch (sc.n) {
+        case 1: hipLaunchKernelGGL((k_global_det<1, BCAST>), grid, block, 0, st, chunks, x, m, x_rep, stride, sc); break;
+        case 2: hipLaunchKernelGGL((k_global_det<2, BCAST>), grid, block, 0, st, chunks, x, m, x_rep, stride, sc); break;
+        case 4: hipLaunchKernelGGL((k_global_det<4, BCAST>), grid, block, 0, st, chunks, x, m, x_rep, stride, sc); break;
+        case 8: hipLaunchKernelGGL((k_global_det<8, BCAST>), grid, block, 0, st, chunks, x, m, x_rep, stride, sc); break;
+        default: hipLaunchKernelGGL((k_global_det<0, BCAST>), grid, block, 0, st, chunks, x, m, x_rep, stride, sc); break;
+    }
+}
+
+hipError_t launch_global_det(const Chunk* chunks, int64_t n_chunks, float* x, float* m,
+                             float* x_rep, int64_t stride, const GlobalScalars& sc,
+                             bool broadcast, hipStream_t st) {
+    if (n_chunks == 0) return hipSuccess;
+    if (broadcast)
+        launch_global_det_n<true>(chunks, n_chunks, x, m, x_rep, stride, sc, st);
+    else
+        launch_global_det_n<false>(chunks, n_chunks, x, m, x_rep, stride, sc, st);
+    return hipGetLastError();
+}
+
+hipError_t launch_global_rand(const Chunk* chunks, int64_t n_chunks, int n_tensors, float* x,
+                              float* m, float* x_rep, float* u, uint32_t* bound_bits,
+                              int64_t stride, const GlobalScalars& sc, bool broadcast,
+                              hipStream_t st) {
+    if (n_tensors > 0) {
+        hipLaunchKernelGGL(k_fill_u32, dim3((n_tensors + kBlockThreads - 1) / kBlockThreads),
+                           dim3(kBlockThreads), 0, st, bound_bits, n_tensors, 0u);
+    }
+    if (n_chunks == 0) return hipGetLastError();
+    const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
+    switch (sc.n) {
+        case 1: hipLaunchKernelGGL(k_global_rand_pass1<1>, grid, block, 0, st, chunks, x, m, x_rep, u, bound_bits, stride, sc); break;
+        case 2: hipLaunchKernelGGL(k_global_rand_pass1<2>, grid, block, 0, st, chunks, x, m, x_rep, u, bound_bits, stride, sc); break;
+        case 4: hipLaunchKernelGGL(k_global_rand_pass1<4>, grid, block, 0, st, chunks, x, m, x_rep, u, bound_bits, stride, sc); break;
+        case 8: hipLaunchKernelGGL(k_global_rand_pass1<8>, grid, block, 0, st, chunks, x, m, x_rep, u, bound_bits, stride, sc); break;
+        default: hipLaunchKernelGGL(k_global_rand_pass1<0>, grid, block, 0, st, chunks, x, m, x_rep, u, bound_bits, stride, sc); break;
+    }
+    if (sc.mode == 1) {
+        if (broadcast)
+            hipLaunchKernelGGL((k_global_rand_pass2<1, true>), grid, block, 0, st, chunks, x, x_rep, u, bound_bits, stride, sc);
+        else
+            hipLaunchKernelGGL((k_global_rand_pass2<1, false>), grid, block, 0, st, chunks, x, x_rep, u, bound_bits, stride, sc);
+    } else {
+        if (broadcast)
+            hipLaunchKernelGGL((k_global_rand_pass2<2, true>), grid, block, 0, st, chunks, x, x_rep, u, bound_bits, stride, sc);
+        else
+            hipLaunchKernelGGL((k_global_rand_pass2<2, false>), grid, block, 0, st, chunks, x, x_rep, u, bound_bits, stride, sc);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_broadcast(const Chunk* chunks, int64_t n_chunks, const float* x, float* x_rep,
+                            int64_t stride, int n, hipStream_t st) {
+    if (n_chunks == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_broadcast, chunk_grid(n_chunks, 1), dim3(kBlockThreads), 0, st, chunks, x,
+                       x_rep, stride, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_test_philox(uint32_t key0, uint32_t key1, uint32_t tensor, uint32_t t,
+                              uint32_t q0, int64_t count, uint32_t* out, hipStream_t st) {
+    if (count == 0) return hipSuccess;
+    const int64_t blocks = (count + kBlockThreads - 1) / kBlockThreads;
+    hipLaunchKernelGGL(k_test_philox, dim3(static_cast<unsigned>(blocks)), dim3(kBlockThreads), 0,
+                       st, key0, key1, tensor, t, q0, count, out);
+    return hipGetLastError();
+}
+
+}  // namespace dsm

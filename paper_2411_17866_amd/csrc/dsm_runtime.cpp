@@ -1,0 +1,433 @@
+// Host runtime of the C ABI in include/dsm.h: argument validation, the arena
+// and chunk layout, the per-context state machine of Algorithm 1, the fp64
+// precomputation of the fp32 scalar coefficients, and kernel launches.
+// The runtime owns only host memory; every device buffer is the caller's.
+#include "dsm.h"
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "dsm_internal.h"
+
+struct dsm_ctx {
+    int n = 0, H = 0, n_tensors = 0, base = 0;
+    std::vector<int64_t> numel, offsets;
+    std::vector<uint8_t> decay;
+    int64_t arena_elems = 0;
+    std::vector<dsm::Chunk> chunks;  // host copy; the device copy lives in the workspace
+    dsm_buffers buf{};
+    dsm::Chunk* d_chunks = nullptr;
+    uint32_t* d_bounds = nullptr;
+    hipStream_t stream = nullptr;
+    std::vector<int> local_count;  // local steps per worker since the last synchronisation
+    bool synced = true;            // every replica equals x
+    bool bounds_valid = false;     // the last global step was randomized
+    std::string last_error;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+constexpr int64_t kMaxNumel = int64_t(1) << 34;
+constexpr int64_t kMaxChunks = (int64_t(1) << 24) - 1;
+
+dsm_status fail(dsm_ctx* ctx, dsm_status st, const char* fmt, ...) {
+    char msg[512];
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(msg, sizeof msg, fmt, ap);
+    va_end(ap);
+    g_last_error = msg;
+    if (ctx) ctx->last_error = msg;
+    return st;
+}
+
+dsm_status hip_fail(dsm_ctx* ctx, const char* what, hipError_t e) {
+    return fail(ctx, DSM_ERR_HIP, "%s: %s (%d)", what, hipGetErrorString(e), static_cast<int>(e));
+}
+
+int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
+
+bool aligned256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
+
+bool finite_in(float v, float lo, float hi) { return std::isfinite(v) && v >= lo && v <= hi; }
+
+struct Layout {
+    std::vector<int64_t> offsets;
+    int64_t arena_elems = 0;
+    int64_t n_chunks = 0;
+    int64_t chunk_bytes = 0;
+    int64_t bounds_off = 0;
+    int64_t workspace_bytes = 0;
+};
+
+dsm_status check_problem(const dsm_problem* p) {
+    if (!p) return fail(nullptr, DSM_ERR_INVALID_ARG, "problem is NULL");
+    if (p->n_workers < 1 || p->n_workers > dsm::kMaxWorkers)
+        return fail(nullptr, DSM_ERR_INVALID_ARG, "n_workers must be in [1, %d], got %d",
+                    dsm::kMaxWorkers, p->n_workers);
+    if (p->local_steps < 1)
+        return fail(nullptr, DSM_ERR_INVALID_ARG, "local_steps must be >= 1, got %d", p->local_steps);
+    if (p->n_tensors < 0)
+        return fail(nullptr, DSM_ERR_INVALID_ARG, "n_tensors must be >= 0, got %d", p->n_tensors);
+    if (p->base != DSM_BASE_ADAMW && p->base != DSM_BASE_SGD_MOMENTUM)
+        return fail(nullptr, DSM_ERR_INVALID_ARG, "unknown base optimizer %d", p->base);
+    if (p->n_tensors > 0 && !p->numel)
+        return fail(nullptr, DSM_ERR_INVALID_ARG, "numel is NULL");
+    for (int i = 0; i < p->n_tensors; ++i) {
+        if (p->numel[i] < 0 || p->numel[i] >= kMaxNumel)
+            return fail(nullptr, DSM_ERR_INVALID_ARG, "numel[%d] = %lld outside [0, 2^34)", i,
+                        static_cast<long long>(p->numel[i]));
+    }
+    return DSM_OK;
+}
+
+// Tensors back to back, each starting at a multiple of 64 elements; the
+// chunk table (kChunkElems elements per chunk, never crossing a tensor)
+// followed by the per-tensor bound words, each at a 256-byte boundary.
+dsm_status make_layout(const dsm_problem* p, Layout* L, std::vector<dsm::Chunk>* chunks) {
+    L->offsets.resize(p->n_tensors);
+    int64_t off = 0, n_chunks = 0;
+    for (int i = 0; i < p->n_tensors; ++i) {
+        L->offsets[i] = off;
+        off += round_up(p->numel[i], dsm::kTensorAlign);
+        n_chunks += (p->numel[i] + dsm::kChunkElems - 1) / dsm::kChunkElems;
+    }
+    if (n_chunks > kMaxChunks)
+        return fail(nullptr, DSM_ERR_UNSUPPORTED, "problem needs %lld chunks, limit %lld",
+                    static_cast<long long>(n_chunks), static_cast<long long>(kMaxChunks));
+    L->arena_elems = off;
+    L->n_chunks = n_chunks;
+    L->chunk_bytes = round_up(n_chunks * static_cast<int64_t>(sizeof(dsm::Chunk)), 256);
+    L->bounds_off = L->chunk_bytes;
+    L->workspace_bytes = L->chunk_bytes + round_up(int64_t(p->n_tensors) * 4, 256);
+    if (chunks) {
+        chunks->clear();
+        chunks->reserve(n_chunks);
+        for (int i = 0; i < p->n_tensors; ++i) {
+            const uint32_t dec = p->decay ? (p->decay[i] ? 1u : 0u) : 1u;
+            for (int64_t j = 0; j < p->numel[i]; j += dsm::kChunkElems) {
+                dsm::Chunk c{};
+                c.off = L->offsets[i] + j;
+                c.j0 = j;
+                c.len = static_cast<int32_t>(std::min<int64_t>(dsm::kChunkElems, p->numel[i] - j));
+                c.tensor = static_cast<uint32_t>(i);
+                c.decay = dec;
+                chunks->push_back(c);
+            }
+        }
+    }
+    return DSM_OK;
+}
+
+// beta^s in fp64 by s successive multiplications; once the product is below
+// 2^-80, 1 - beta^s is 1 in fp64 and no longer changes.
+double beta_power(double beta, int64_t s) {
+    double p = 1.0;
+    for (int64_t k = 0; k < s; ++k) {
+        p *= beta;
+        if (p < 0x1p-80) return 0.0;
+    }
+    return p;
+}
+
+dsm_status check_ctx(dsm_ctx* ctx) {
+    if (!ctx) return fail(nullptr, DSM_ERR_INVALID_ARG, "context is NULL");
+    return DSM_OK;
+}
+
+dsm_status check_device(dsm_ctx* ctx) {
+    int count = 0;
+    hipError_t e = hipGetDeviceCount(&count);
+    if (e != hipSuccess || count == 0)
+        return fail(ctx, DSM_ERR_HIP, "no HIP device available (%s)",
+                    e == hipSuccess ? "0 devices" : hipGetErrorString(e));
+    return DSM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+dsm_status dsm_layout(const dsm_problem* problem, int64_t* arena_elems, int64_t* tensor_offsets,
+                      int64_t* workspace_bytes) {
+    dsm_status st = check_problem(problem);
+    if (st != DSM_OK) return st;
+    Layout L;
+    st = make_layout(problem, &L, nullptr);
+    if (st != DSM_OK) return st;
+    if (arena_elems) *arena_elems = L.arena_elems;
+    if (tensor_offsets && problem->n_tensors > 0)
+        std::memcpy(tensor_offsets, L.offsets.data(), sizeof(int64_t) * problem->n_tensors);
+    if (workspace_bytes) *workspace_bytes = L.workspace_bytes;
+    return DSM_OK;
+}
+
+dsm_status dsm_init(const dsm_problem* problem, const dsm_buffers* b, dsm_ctx** out) {
+    if (!out) return fail(nullptr, DSM_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    dsm_status st = check_problem(problem);
+    if (st != DSM_OK) return st;
+    if (!b) return fail(nullptr, DSM_ERR_INVALID_ARG, "buffers is NULL");
+    Layout L;
+    std::vector<dsm::Chunk> chunks;
+    st = make_layout(problem, &L, &chunks);
+    if (st != DSM_OK) return st;
+    const bool adamw = problem->base == DSM_BASE_ADAMW;
+    if (L.arena_elems > 0) {
+        struct {
+            const void* p;
+            const char* name;
+            bool required;
+        } ptrs[] = {{b->x, "x", true},           {b->m, "m", true},
+                    {b->x_rep, "x_rep", true},   {b->g_rep, "g_rep", true},
+                    {b->s1_rep, "s1_rep", true}, {b->s2_rep, "s2_rep", adamw},
+                    {b->u_scratch, "u_scratch", false}};
+        for (const auto& q : ptrs) {
+            if (q.required && !q.p)
+                return fail(nullptr, DSM_ERR_INVALID_ARG, "buffer %s is NULL", q.name);
+            if (q.p && !aligned256(q.p))
+                return fail(nullptr, DSM_ERR_INVALID_ARG, "buffer %s is not 256-byte aligned", q.name);
+        }
+    }
+    if (L.workspace_bytes > 0) {
+        if (!b->workspace) return fail(nullptr, DSM_ERR_INVALID_ARG, "workspace is NULL");
+        if (!aligned256(b->workspace))
+            return fail(nullptr, DSM_ERR_INVALID_ARG, "workspace is not 256-byte aligned");
+        if (b->workspace_bytes < L.workspace_bytes)
+            return fail(nullptr, DSM_ERR_INVALID_ARG, "workspace has %lld bytes, needs %lld",
+                        static_cast<long long>(b->workspace_bytes),
+                        static_cast<long long>(L.workspace_bytes));
+    }
+    st = check_device(nullptr);
+    if (st != DSM_OK) return st;
+
+    dsm_ctx* ctx = new (std::nothrow) dsm_ctx();
+    if (!ctx) return fail(nullptr, DSM_ERR_INVALID_ARG, "out of host memory");
+    ctx->n = problem->n_workers;
+    ctx->H = problem->local_steps;
+    ctx->n_tensors = problem->n_tensors;
+    ctx->base = problem->base;
+    ctx->numel.assign(problem->numel, problem->numel + problem->n_tensors);
+    ctx->decay.resize(problem->n_tensors);
+    for (int i = 0; i < problem->n_tensors; ++i)
+        ctx->decay[i] = problem->decay ? (problem->decay[i] ? 1 : 0) : 1;
+    ctx->offsets = L.offsets;
+    ctx->arena_elems = L.arena_elems;
+    ctx->chunks = std::move(chunks);
+    ctx->buf = *b;
+    ctx->stream = static_cast<hipStream_t>(b->stream);
+    ctx->d_chunks = static_cast<dsm::Chunk*>(b->workspace);
+    ctx->d_bounds = reinterpret_cast<uint32_t*>(static_cast<char*>(b->workspace) + L.bounds_off);
+    ctx->local_count.assign(ctx->n, 0);
+
+    if (!ctx->chunks.empty()) {
+        hipError_t e = hipMemcpyAsync(ctx->d_chunks, ctx->chunks.data(),
+                                      ctx->chunks.size() * sizeof(dsm::Chunk),
+                                      hipMemcpyHostToDevice, ctx->stream);
+        if (e != hipSuccess) {
+            dsm_status r = hip_fail(nullptr, "uploading the chunk table", e);
+            delete ctx;
+            return r;
+        }
+        e = dsm::launch_init(ctx->d_chunks, static_cast<int64_t>(ctx->chunks.size()), b->x, b->m,
+                             b->x_rep, b->s1_rep, adamw ? b->s2_rep : nullptr, ctx->arena_elems,
+                             ctx->n, ctx->stream);
+        if (e != hipSuccess) {
+            dsm_status r = hip_fail(nullptr, "launching the initialisation kernel", e);
+            delete ctx;
+            return r;
+        }
+    }
+    *out = ctx;
+    return DSM_OK;
+}
+
+dsm_status dsm_local_step(dsm_ctx* ctx, int32_t worker, int64_t step, const dsm_local_hparams* hp) {
+    dsm_status st = check_ctx(ctx);
+    if (st != DSM_OK) return st;
+    if (!hp) return fail(ctx, DSM_ERR_INVALID_ARG, "hyperparameters are NULL");
+    if (worker < -1 || worker >= ctx->n)
+        return fail(ctx, DSM_ERR_INVALID_ARG, "worker must be -1 or in [0, %d), got %d", ctx->n, worker);
+    if (!(std::isfinite(hp->lr) && hp->lr > 0.0f))
+        return fail(ctx, DSM_ERR_INVALID_ARG, "lr must be finite and > 0");
+    if (!finite_in(hp->beta1, 0.0f, 1.0f))
+        return fail(ctx, DSM_ERR_INVALID_ARG, "beta1 must be in [0, 1]");
+    const bool adamw = ctx->base == DSM_BASE_ADAMW;
+    if (adamw) {
+        if (step < 1) return fail(ctx, DSM_ERR_INVALID_ARG, "step must be >= 1, got %lld",
+                                  static_cast<long long>(step));
+        if (!finite_in(hp->beta2, 0.0f, 1.0f))
+            return fail(ctx, DSM_ERR_INVALID_ARG, "beta2 must be in [0, 1]");
+        if (!(std::isfinite(hp->eps) && hp->eps >= 0.0f))
+            return fail(ctx, DSM_ERR_INVALID_ARG, "eps must be finite and >= 0");
+        if (!(std::isfinite(hp->weight_decay) && hp->weight_decay >= 0.0f))
+            return fail(ctx, DSM_ERR_INVALID_ARG, "weight_decay must be finite and >= 0");
+        if (hp->beta1 == 1.0f || hp->beta2 == 1.0f)
+            return fail(ctx, DSM_ERR_INVALID_ARG, "AdamW needs beta1, beta2 < 1 (bias correction)");
+    }
+    if (!ctx->synced)
+        return fail(ctx, DSM_ERR_STATE,
+                    "replicas are not synchronised: the last global step had broadcast = 0; "
+                    "call dsm_sync first");
+    const int w0 = worker < 0 ? 0 : worker;
+    const int nw = worker < 0 ? ctx->n : 1;
+    for (int i = w0; i < w0 + nw; ++i) {
+        if (ctx->local_count[i] >= ctx->H)
+            return fail(ctx, DSM_ERR_STATE,
+                        "worker %d already took H = %d local steps this round; take the global step",
+                        i, ctx->H);
+    }
+    const int64_t n_chunks = static_cast<int64_t>(ctx->chunks.size());
+    hipError_t e;
+    if (adamw) {
+        dsm::AdamScalars sc{};
+        const double b1 = hp->beta1, b2 = hp->beta2;
+        sc.beta1 = hp->beta1;
+        sc.beta2 = hp->beta2;
+        sc.one_minus_beta1 = static_cast<float>(1.0 - b1);
+        sc.one_minus_beta2 = static_cast<float>(1.0 - b2);
+        sc.bc1 = static_cast<float>(1.0 - beta_power(b1, step));
+        sc.bc2 = static_cast<float>(1.0 - beta_power(b2, step));
+        sc.lr = hp->lr;
+        sc.eps = hp->eps;
+        sc.wd = hp->weight_decay;
+        e = dsm::launch_local_adamw(ctx->d_chunks, n_chunks, ctx->buf.x_rep, ctx->buf.g_rep,
+                                    ctx->buf.s1_rep, ctx->buf.s2_rep, ctx->arena_elems, w0, nw, sc,
+                                    ctx->stream);
+    } else {
+        dsm::SgdScalars sc{hp->beta1, hp->lr};
+        e = dsm::launch_local_sgdm(ctx->d_chunks, n_chunks, ctx->buf.x_rep, ctx->buf.g_rep,
+                                   ctx->buf.s1_rep, ctx->arena_elems, w0, nw, sc, ctx->stream);
+    }
+    if (e != hipSuccess) return hip_fail(ctx, "launching the local step", e);
+    for (int i = w0; i < w0 + nw; ++i) ctx->local_count[i] += 1;
+    return DSM_OK;
+}
+
+dsm_status dsm_global_step(dsm_ctx* ctx, int64_t t, const dsm_global_hparams* hp, int32_t broadcast) {
+    dsm_status st = check_ctx(ctx);
+    if (st != DSM_OK) return st;
+    if (!hp) return fail(ctx, DSM_ERR_INVALID_ARG, "hyperparameters are NULL");
+    if (t < 0 || t >= (int64_t(1) << 32))
+        return fail(ctx, DSM_ERR_INVALID_ARG, "t must be in [0, 2^32), got %lld", static_cast<long long>(t));
+    if (!(std::isfinite(hp->gamma) && hp->gamma > 0.0f))
+        return fail(ctx, DSM_ERR_INVALID_ARG, "gamma must be finite and > 0");
+    if (!(std::isfinite(hp->eta) && hp->eta >= 0.0f))
+        return fail(ctx, DSM_ERR_INVALID_ARG, "eta must be finite and >= 0");
+    if (!finite_in(hp->beta1, 0.0f, 1.0f) || !finite_in(hp->beta2, 0.0f, 1.0f))
+        return fail(ctx, DSM_ERR_INVALID_ARG, "beta1 and beta2 must be in [0, 1]");
+    if (!(std::isfinite(hp->lambda) && hp->lambda >= 0.0f))
+        return fail(ctx, DSM_ERR_INVALID_ARG, "lambda must be finite and >= 0");
+    if (hp->mode != DSM_SIGN_DET && hp->mode != DSM_SIGN_RAND_FLIP && hp->mode != DSM_SIGN_RAND_ZERO)
+        return fail(ctx, DSM_ERR_INVALID_ARG, "unknown sign mode %d", hp->mode);
+    const bool randomized = hp->mode != DSM_SIGN_DET;
+    if (randomized && ctx->arena_elems > 0 && !ctx->buf.u_scratch)
+        return fail(ctx, DSM_ERR_INVALID_ARG, "the randomized sign needs buffers.u_scratch");
+    if (!ctx->synced)
+        return fail(ctx, DSM_ERR_STATE, "replicas are not synchronised; call dsm_sync first");
+    for (int i = 0; i < ctx->n; ++i) {
+        if (ctx->local_count[i] != ctx->H)
+            return fail(ctx, DSM_ERR_STATE,
+                        "worker %d took %d of H = %d local steps; the global step needs all H",
+                        i, ctx->local_count[i], ctx->H);
+    }
+    dsm::GlobalScalars sc{};
+    const double gamma = hp->gamma;
+    sc.beta1 = hp->beta1;
+    sc.beta2 = hp->beta2;
+    sc.c1 = static_cast<float>((1.0 - static_cast<double>(hp->beta1)) / gamma);
+    sc.c2 = static_cast<float>((1.0 - static_cast<double>(hp->beta2)) / gamma);
+    sc.step = static_cast<float>(static_cast<double>(hp->eta) * gamma);
+    sc.lam = hp->lambda;
+    sc.n = ctx->n;
+    sc.n_pow2 = (ctx->n & (ctx->n - 1)) == 0 ? 1 : 0;
+    sc.inv_n = static_cast<float>(1.0 / ctx->n);
+    sc.n_f = static_cast<float>(ctx->n);
+    sc.key0 = static_cast<uint32_t>(hp->seed & 0xFFFFFFFFu);
+    sc.key1 = static_cast<uint32_t>(hp->seed >> 32);
+    sc.t = static_cast<uint32_t>(t);
+    sc.mode = hp->mode;
+    const int64_t n_chunks = static_cast<int64_t>(ctx->chunks.size());
+    hipError_t e;
+    if (!randomized) {
+        e = dsm::launch_global_det(ctx->d_chunks, n_chunks, ctx->buf.x, ctx->buf.m, ctx->buf.x_rep,
+                                   ctx->arena_elems, sc, broadcast != 0, ctx->stream);
+    } else {
+        e = dsm::launch_global_rand(ctx->d_chunks, n_chunks, ctx->n_tensors, ctx->buf.x, ctx->buf.m,
+                                    ctx->buf.x_rep, ctx->buf.u_scratch, ctx->d_bounds,
+                                    ctx->arena_elems, sc, broadcast != 0, ctx->stream);
+    }
+    if (e != hipSuccess) return hip_fail(ctx, "launching the global step", e);
+    for (int i = 0; i < ctx->n; ++i) ctx->local_count[i] = 0;
+    ctx->synced = broadcast != 0;
+    ctx->bounds_valid = randomized;
+    return DSM_OK;
+}
+
+dsm_status dsm_sync(dsm_ctx* ctx) {
+    dsm_status st = check_ctx(ctx);
+    if (st != DSM_OK) return st;
+    hipError_t e = dsm::launch_broadcast(ctx->d_chunks, static_cast<int64_t>(ctx->chunks.size()),
+                                         ctx->buf.x, ctx->buf.x_rep, ctx->arena_elems, ctx->n,
+                                         ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, "launching the synchronisation", e);
+    for (int i = 0; i < ctx->n; ++i) ctx->local_count[i] = 0;
+    ctx->synced = true;
+    return DSM_OK;
+}
+
+dsm_status dsm_read_bounds(dsm_ctx* ctx, float* host_B) {
+    dsm_status st = check_ctx(ctx);
+    if (st != DSM_OK) return st;
+    if (!ctx->bounds_valid)
+        return fail(ctx, DSM_ERR_STATE, "the last global step did not use the randomized sign");
+    if (ctx->n_tensors == 0) return DSM_OK;
+    if (!host_B) return fail(ctx, DSM_ERR_INVALID_ARG, "host_B is NULL");
+    hipError_t e = hipMemcpyAsync(host_B, ctx->d_bounds, sizeof(uint32_t) * ctx->n_tensors,
+                                  hipMemcpyDeviceToHost, ctx->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, "reading the bounds", e);
+    return DSM_OK;
+}
+
+dsm_status dsm_test_philox(uint64_t seed, uint32_t tensor, int64_t t, int64_t q0, int64_t count,
+                           uint32_t* dev_out, void* stream) {
+    if (!dev_out) return fail(nullptr, DSM_ERR_INVALID_ARG, "dev_out is NULL");
+    if (count < 0 || q0 < 0 || q0 + count > (int64_t(1) << 32))
+        return fail(nullptr, DSM_ERR_INVALID_ARG, "need count >= 0, q0 >= 0, q0 + count <= 2^32");
+    if (count > (int64_t(1) << 30))
+        return fail(nullptr, DSM_ERR_INVALID_ARG, "count must be <= 2^30");
+    if (t < 0 || t >= (int64_t(1) << 32))
+        return fail(nullptr, DSM_ERR_INVALID_ARG, "t must be in [0, 2^32)");
+    if ((reinterpret_cast<uintptr_t>(dev_out) & 3u) != 0)
+        return fail(nullptr, DSM_ERR_INVALID_ARG, "dev_out is not 4-byte aligned");
+    dsm_status st = check_device(nullptr);
+    if (st != DSM_OK) return st;
+    hipError_t e = dsm::launch_test_philox(static_cast<uint32_t>(seed & 0xFFFFFFFFu),
+                                           static_cast<uint32_t>(seed >> 32), tensor,
+                                           static_cast<uint32_t>(t), static_cast<uint32_t>(q0),
+                                           count, dev_out, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(nullptr, "launching the Philox test kernel", e);
+    return DSM_OK;
+}
+
+dsm_status dsm_destroy(dsm_ctx* ctx) {
+    if (!ctx) return DSM_OK;
+    hipError_t e = hipStreamSynchronize(ctx->stream);
+    delete ctx;
+    if (e != hipSuccess) return hip_fail(nullptr, "synchronising the stream at destroy", e);
+    return DSM_OK;
+}
+
+const char* dsm_last_error(const dsm_ctx* ctx) {
+    return ctx ? ctx->last_error.c_str() : g_last_error.c_str();
+}
+
+}  // extern "C"

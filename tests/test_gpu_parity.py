@@ -1,0 +1,329 @@
+"""GPU path (libdsm.so through the C ABI) against the CPU oracle.
+
+Seeded synthetic inputs at sizes the oracle finishes in seconds, spanning
+several 16384-element chunks, ragged tensor ends (numel not a multiple of 4)
+and an empty tensor.  Each call is compared element by element against the
+oracle run from the same device state (copied to the host before the call),
+to the bars described in tests/parity.py.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2411_17866_amd import arena as A
+from paper_2411_17866_amd import dsm
+
+from parity import (adamw_scales, global_scales, rel_check, rms, scaled_check, sgdm_scales)
+
+pytestmark = pytest.mark.gpu
+
+RAGGED = [1, 3, 4, 5, 63, 64, 65, 0, 1000, 16383, 16384, 16385, 40003]
+DECAY = [i % 3 != 1 for i in range(len(RAGGED))]
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.detach().cpu().numpy().copy()
+
+
+def make(numel, n, H, base, decay=None, seed=0, randomized=True):
+    ar = A.Arenas(numel, n, H, base, decay=decay, randomized=randomized)
+    gen = torch.Generator(device="cuda").manual_seed(seed)
+    ar.x.normal_(0.0, 0.02, generator=gen)
+    ar.init()
+    return ar, gen
+
+
+def per_tensor(ar, flat):
+    """Host per-tensor arrays of one arena copy."""
+    h = host(flat)
+    return [h[o:o + n].copy() for o, n in zip(ar.offsets, ar.numel)]
+
+
+def padding_mask(ar):
+    mask = np.ones(ar.x.numel(), dtype=bool)
+    for o, n in zip(ar.offsets, ar.numel):
+        mask[o:o + n] = False
+    return mask
+
+
+# ---------------------------------------------------------------- Philox
+
+@pytest.mark.parametrize("seed,tensor,t,q0,count", [
+    (0, 0, 0, 0, 1000), (0x0123456789ABCDEF, 579, 12345, 77, 4099),
+    ((1 << 64) - 1, 3, (1 << 32) - 1, (1 << 32) - 300, 300)])
+def test_device_philox_matches_oracle(seed, tensor, t, q0, count):
+    out = torch.zeros(4 * count, dtype=torch.int32, device="cuda")
+    dsm.dsm_test_philox(seed, tensor, t, q0, count, out.data_ptr(),
+                        torch.cuda.current_stream().cuda_stream)
+    got = host(out).view(np.uint32).reshape(count, 4)
+    q = np.arange(q0, q0 + count, dtype=np.uint64)
+    want = np.stack(O.philox4x32_10(q, tensor, t, O.PHILOX_STREAM, seed & 0xFFFFFFFF, seed >> 32),
+                    axis=1)
+    np.testing.assert_array_equal(got, want)
+
+
+# ---------------------------------------------------------------- local steps
+
+def _randomize_state(ar, gen, adamw):
+    """Arbitrary (non-zero) replica and base-optimizer state."""
+    ar.x_rep.normal_(0.0, 0.02, generator=gen)
+    ar.g_rep.normal_(0.0, 0.01, generator=gen)
+    ar.s1_rep.normal_(0.0, 1e-3, generator=gen)
+    if adamw:
+        ar.s2_rep.normal_(0.0, 1e-3, generator=gen).square_()
+
+
+@pytest.mark.parametrize("n,worker,step", [(3, -1, 1), (4, -1, 7), (4, 2, 3), (1, 0, 1000)])
+def test_local_adamw_parity(n, worker, step):
+    hp = dict(lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1)
+    ar, gen = make(RAGGED, n, 4, dsm.DSM_BASE_ADAMW, decay=DECAY, seed=n + step)
+    _randomize_state(ar, gen, True)
+    pad = padding_mask(ar)
+    before = {k: [per_tensor(ar, getattr(ar, k)[i]) for i in range(n)]
+              for k in ("x_rep", "g_rep", "s1_rep", "s2_rep")}
+    pad_before = host(ar.x_rep)[:, pad]
+    dsm.dsm_local_step(ar.ctx, worker, step, **hp)
+    after = {k: [per_tensor(ar, getattr(ar, k)[i]) for i in range(n)]
+             for k in ("x_rep", "s1_rep", "s2_rep")}
+    np.testing.assert_array_equal(host(ar.x_rep)[:, pad], pad_before)
+    nonbit = 0
+    for i in range(n):
+        for p in range(len(RAGGED)):
+            x, g, m, v = (before[k][i][p] for k in ("x_rep", "g_rep", "s1_rep", "s2_rep"))
+            gx, gm, gv = (after[k][i][p] for k in ("x_rep", "s1_rep", "s2_rep"))
+            if worker not in (-1, i):
+                for a, b in ((gx, x), (gm, m), (gv, v)):
+                    np.testing.assert_array_equal(a, b)
+                continue
+            wd = hp["weight_decay"] if DECAY[p] else 0.0
+            kw = dict(hp, weight_decay=wd, step=step)
+            o32 = O.local_adamw_step(x, g, m, v, prec="fp32", **kw)
+            o64 = O.local_adamw_step(x, g, m, v, prec="fp64", **kw)
+            for name, gg, oo in (("x", gx, o32[0]), ("m", gm, o32[1]), ("v", gv, o32[2])):
+                nonbit += rel_check(gg, oo, f"worker {i} tensor {p} {name}")
+            s_m, s_v, s_x = adamw_scales(x, g, m, v, o64=o64, **kw)
+            scaled_check(gx, o64[0], s_x, f"x vs fp64, worker {i} tensor {p}")
+            scaled_check(gm, o64[1], s_m, f"m vs fp64, worker {i} tensor {p}")
+            scaled_check(gv, o64[2], s_v, f"v vs fp64, worker {i} tensor {p}")
+    print(f"adamw n={n} worker={worker}: {nonbit} elements not bit-identical to the fp32 oracle")
+    ar.destroy()
+
+
+@pytest.mark.parametrize("n,worker", [(2, -1), (5, -1), (3, 0)])
+def test_local_sgdm_parity(n, worker):
+    hp = dict(lr=0.1, beta1=0.9)
+    ar, gen = make(RAGGED, n, 2, dsm.DSM_BASE_SGD_MOMENTUM, seed=100 + n)
+    _randomize_state(ar, gen, False)
+    before = {k: [per_tensor(ar, getattr(ar, k)[i]) for i in range(n)]
+              for k in ("x_rep", "g_rep", "s1_rep")}
+    dsm.dsm_local_step(ar.ctx, worker, 1, **hp)
+    after = {k: [per_tensor(ar, getattr(ar, k)[i]) for i in range(n)] for k in ("x_rep", "s1_rep")}
+    nonbit = 0
+    for i in range(n):
+        for p in range(len(RAGGED)):
+            x, g, m = (before[k][i][p] for k in ("x_rep", "g_rep", "s1_rep"))
+            gx, gm = after["x_rep"][i][p], after["s1_rep"][i][p]
+            if worker not in (-1, i):
+                np.testing.assert_array_equal(gx, x)
+                np.testing.assert_array_equal(gm, m)
+                continue
+            o32 = O.local_sgdm_step(x, g, m, lr=hp["lr"], momentum=hp["beta1"], prec="fp32")
+            o64 = O.local_sgdm_step(x, g, m, lr=hp["lr"], momentum=hp["beta1"], prec="fp64")
+            nonbit += rel_check(gx, o32[0], f"sgd x worker {i} tensor {p}")
+            nonbit += rel_check(gm, o32[1], f"sgd m worker {i} tensor {p}")
+            s_m, s_x = sgdm_scales(x, g, m, lr=hp["lr"], momentum=hp["beta1"])
+            scaled_check(gx, o64[0], s_x, "sgd x vs fp64")
+            scaled_check(gm, o64[1], s_m, "sgd m vs fp64")
+    print(f"sgdm n={n}: {nonbit} elements not bit-identical to the fp32 oracle")
+    ar.destroy()
+
+
+# ---------------------------------------------------------------- global step
+
+def _ready_for_global(ar, gen, H, n):
+    """H local SGD steps on every worker from perturbed replicas, then a
+    random momentum, so the global step sees non-trivial x - x_i and m."""
+    for _ in range(H):
+        ar.g_rep.normal_(0.0, 1e-3, generator=gen)
+        dsm.dsm_local_step(ar.ctx, -1, 1, lr=0.05, beta1=0.5)
+    ar.m.normal_(0.0, 1.0, generator=gen)
+
+
+GLOB = dict(gamma=1e-3, eta=0.8, beta1=0.95, beta2=0.98, lam=0.1)
+
+
+@pytest.mark.parametrize("n,broadcast", [(1, True), (2, True), (3, True), (4, True), (4, False),
+                                          (5, True), (8, True)])
+def test_global_det_parity(n, broadcast):
+    H = 2
+    ar, gen = make(RAGGED, n, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, seed=200 + n)
+    _ready_for_global(ar, gen, H, n)
+    x0, m0 = per_tensor(ar, ar.x), per_tensor(ar, ar.m)
+    reps = [per_tensor(ar, ar.x_rep[i]) for i in range(n)]
+    rep_before = host(ar.x_rep)
+    dsm.dsm_global_step(ar.ctx, 5, mode=dsm.DSM_SIGN_DET, broadcast=broadcast, **GLOB)
+    gx, gm = per_tensor(ar, ar.x), per_tensor(ar, ar.m)
+    o32 = O.global_step(x0, m0, reps, decay=DECAY, prec="fp32", **GLOB)
+    o64 = O.global_step(x0, m0, reps, decay=DECAY, prec="fp64", **GLOB)
+    nonbit, flips = 0, 0
+    for p in range(len(RAGGED)):
+        nonbit += rel_check(gx[p], o32["x"][p], f"x tensor {p}")
+        nonbit += rel_check(gm[p], o32["m"][p], f"m tensor {p}")
+        lam_p = GLOB["lam"] if DECAY[p] else 0.0
+        s_u, s_m, s_x = global_scales(x0[p], m0[p], [r[p] for r in reps], o64["S"][p],
+                                      lam_p=lam_p, **{k: v for k, v in GLOB.items() if k != "lam"})
+        scaled_check(gm[p], o64["m"][p], s_m, f"m vs fp64 tensor {p}")
+        # Sign decisions vs fp64: only where |u| is tiny.
+        flip = o32["S"][p] != o64["S"][p]
+        if flip.any():
+            assert np.all(np.abs(o64["u"][p][flip]) < 1e-6 * rms(o64["u"][p])), f"tensor {p}"
+        flips += int(flip.sum())
+        scaled_check(gx[p], o64["x"][p], s_x, f"x vs fp64 tensor {p}", mask=~flip)
+    rep_after = host(ar.x_rep)
+    if broadcast:
+        xa = host(ar.x)
+        for i in range(n):
+            for o, k in zip(ar.offsets, ar.numel):
+                assert np.array_equal(rep_after[i, o:o + k].view(np.uint32),
+                                      xa[o:o + k].view(np.uint32))
+    else:
+        np.testing.assert_array_equal(rep_after, rep_before)
+        with pytest.raises(dsm.DsmError) as e:
+            dsm.dsm_local_step(ar.ctx, -1, 1, lr=0.05, beta1=0.5)
+        assert e.value.status == dsm.DSM_ERR_STATE
+        dsm.dsm_sync(ar.ctx)
+        xa, ra = host(ar.x), host(ar.x_rep)
+        for i in range(n):
+            for o, k in zip(ar.offsets, ar.numel):
+                assert np.array_equal(ra[i, o:o + k].view(np.uint32), xa[o:o + k].view(np.uint32))
+    print(f"global det n={n}: {nonbit} non-bit-identical vs fp32 oracle, {flips} sign flips vs fp64")
+    ar.destroy()
+
+
+@pytest.mark.parametrize("n,mode,seed", [(2, dsm.DSM_SIGN_RAND_FLIP, 1),
+                                         (4, dsm.DSM_SIGN_RAND_ZERO, (1 << 63) + 12345),
+                                         (3, dsm.DSM_SIGN_RAND_FLIP, 2 ** 40 + 7),
+                                         (8, dsm.DSM_SIGN_RAND_ZERO, 99)])
+def test_global_randomized_parity(n, mode, seed):
+    H = 1
+    ar, gen = make(RAGGED, n, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, seed=300 + n)
+    _ready_for_global(ar, gen, H, n)
+    x0, m0 = per_tensor(ar, ar.x), per_tensor(ar, ar.m)
+    reps = [per_tensor(ar, ar.x_rep[i]) for i in range(n)]
+    t = 77
+    dsm.dsm_global_step(ar.ctx, t, mode=mode, seed=seed, broadcast=True, **GLOB)
+    gx, gm, gu = per_tensor(ar, ar.x), per_tensor(ar, ar.m), per_tensor(ar, ar.u)
+    B = dsm.dsm_read_bounds(ar.ctx, len(RAGGED))
+    o32 = O.global_step(x0, m0, reps, decay=DECAY, prec="fp32", t=t, mode=mode, seed=seed, **GLOB)
+    nonbit = 0
+    for p in range(len(RAGGED)):
+        assert B[p].view(np.uint32) == np.float32(o32["B"][p]).view(np.uint32), f"B tensor {p}"
+        np.testing.assert_array_equal(gu[p].view(np.uint32), o32["u"][p].view(np.uint32))
+        nonbit += rel_check(gm[p], o32["m"][p], f"m tensor {p}")
+        nonbit += rel_check(gx[p], o32["x"][p], f"x tensor {p}")
+    ra, xa = host(ar.x_rep), host(ar.x)
+    for i in range(n):
+        for o, k in zip(ar.offsets, ar.numel):
+            assert np.array_equal(ra[i, o:o + k].view(np.uint32), xa[o:o + k].view(np.uint32))
+    print(f"global rand n={n} mode={mode}: {nonbit} non-bit-identical vs fp32 oracle")
+    ar.destroy()
+
+
+# ---------------------------------------------------------------- whole rounds
+
+def test_tiny_rounds_free_running_bit_identical():
+    """The tiny workload (8 x 2^17, n=4, H=4 AdamW, deterministic sign): three
+    free-running rounds of Algorithm 1 on the GPU and in the fp32 oracle from
+    the same inputs end bit-identical (no re-seeding between rounds)."""
+    from paper_2411_17866_amd import workloads as W
+    w = W.get("tiny")
+    ar, gen = make(w.numel, w.n_workers, w.local_steps, w.base, decay=w.decay, seed=w.seed,
+                   randomized=False)
+    st = O.init_state(per_tensor(ar, ar.x), w.n_workers, "adamw")
+    glob = dict(w.glob, mode=O.SIGN_DET, seed=0)
+    for t in range(3):
+        grads = {}
+        for k in range(w.local_steps):
+            for i in range(w.n_workers):
+                W.fill_grads_(ar.g_rep[i], w, i, t * w.local_steps + k)
+                grads[(i, k)] = per_tensor(ar, ar.g_rep[i])
+            dsm.dsm_local_step(ar.ctx, -1, t * w.local_steps + k + 1, **w.local)
+        dsm.dsm_global_step(ar.ctx, t, gamma=w.local["lr"], mode=dsm.DSM_SIGN_DET,
+                            broadcast=True, **w.glob)
+        O.communication_round(st, lambda i, k: grads[(i, k)], t, H=w.local_steps, local=w.local,
+                              glob=glob, decay=w.decay, prec="fp32")
+        for p in range(len(w.numel)):
+            for name, gpu, ora in (("x", per_tensor(ar, ar.x)[p], st["x"][p]),
+                                   ("m", per_tensor(ar, ar.m)[p], st["m"][p])):
+                assert np.array_equal(gpu.view(np.uint32), ora.view(np.uint32)), (t, name, p)
+            for i in range(w.n_workers):
+                assert np.array_equal(per_tensor(ar, ar.s1_rep[i])[p], st["s1"][i][p])
+                assert np.array_equal(per_tensor(ar, ar.s2_rep[i])[p], st["s2"][i][p])
+                assert np.array_equal(per_tensor(ar, ar.x_rep[i])[p], st["replicas"][i][p])
+    ar.destroy()
+
+
+def test_rerun_is_bitwise_deterministic():
+    """Two identical runs (local steps, randomized global step) agree bit for bit."""
+    outs = []
+    for _ in range(2):
+        ar, gen = make(RAGGED, 3, 2, dsm.DSM_BASE_ADAMW, decay=DECAY, seed=5)
+        for k in range(2):
+            ar.g_rep.normal_(0.0, 0.01, generator=gen)
+            dsm.dsm_local_step(ar.ctx, -1, k + 1, lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8,
+                               weight_decay=0.1)
+        dsm.dsm_global_step(ar.ctx, 3, mode=dsm.DSM_SIGN_RAND_FLIP, seed=42, **GLOB)
+        outs.append([host(t) for t in (ar.x, ar.m, ar.x_rep, ar.s1_rep, ar.s2_rep, ar.u)])
+        ar.destroy()
+    for a, b in zip(*outs):
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def test_state_machine_on_gpu():
+    ar, gen = make([100, 5000], 2, 2, dsm.DSM_BASE_ADAMW, seed=9, randomized=False)
+    hp = dict(lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.0)
+    with pytest.raises(dsm.DsmError) as e:
+        dsm.dsm_global_step(ar.ctx, 0, **GLOB)
+    assert e.value.status == dsm.DSM_ERR_STATE
+    dsm.dsm_local_step(ar.ctx, 0, 1, **hp)
+    dsm.dsm_local_step(ar.ctx, 0, 2, **hp)
+    with pytest.raises(dsm.DsmError) as e:
+        dsm.dsm_local_step(ar.ctx, 0, 3, **hp)     # worker 0 past H
+    assert e.value.status == dsm.DSM_ERR_STATE
+    with pytest.raises(dsm.DsmError) as e:
+        dsm.dsm_global_step(ar.ctx, 0, **GLOB)     # worker 1 has 0 steps
+    assert e.value.status == dsm.DSM_ERR_STATE
+    with pytest.raises(dsm.DsmError) as e:
+        dsm.dsm_global_step(ar.ctx, 0, mode=dsm.DSM_SIGN_RAND_FLIP, **GLOB)  # no u_scratch
+    assert e.value.status == dsm.DSM_ERR_INVALID_ARG
+    dsm.dsm_local_step(ar.ctx, 1, 1, **hp)
+    dsm.dsm_local_step(ar.ctx, 1, 2, **hp)
+    with pytest.raises(dsm.DsmError) as e:
+        dsm.dsm_read_bounds(ar.ctx, 2)
+    assert e.value.status == dsm.DSM_ERR_STATE
+    for bad in (dict(GLOB, gamma=0.0), dict(GLOB, beta1=1.5), dict(GLOB, lam=-1.0)):
+        with pytest.raises(dsm.DsmError) as e:
+            dsm.dsm_global_step(ar.ctx, 0, **bad)
+        assert e.value.status == dsm.DSM_ERR_INVALID_ARG
+    with pytest.raises(dsm.DsmError):
+        dsm.dsm_global_step(ar.ctx, 1 << 32, **GLOB)
+    dsm.dsm_global_step(ar.ctx, 0, **GLOB)
+    # dsm_sync restarts the round: local counts back to zero.
+    dsm.dsm_local_step(ar.ctx, -1, 3, **hp)
+    dsm.dsm_sync(ar.ctx)
+    dsm.dsm_local_step(ar.ctx, -1, 3, **hp)
+    dsm.dsm_local_step(ar.ctx, -1, 4, **hp)
+    dsm.dsm_global_step(ar.ctx, 1, **GLOB)
+    ar.destroy()
+
+
+def test_empty_problem_is_a_no_op():
+    ar = A.Arenas([], 2, 1, dsm.DSM_BASE_ADAMW)
+    ar.init()
+    dsm.dsm_local_step(ar.ctx, -1, 1, lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8)
+    dsm.dsm_global_step(ar.ctx, 0, mode=dsm.DSM_SIGN_RAND_FLIP, **GLOB)
+    assert dsm.dsm_read_bounds(ar.ctx, 0).size == 0
+    dsm.dsm_sync(ar.ctx)
+    ar.destroy()
