@@ -54,22 +54,28 @@ def _run(cmd, verbose):
     return r
 
 
-def build(verbose=False):
-    """Compiles the kernels and the host runtime and links libdsm.so."""
-    os.makedirs(LIBDIR, exist_ok=True)
-    os.makedirs(OBJDIR, exist_ok=True)
+def build(verbose=False, out=LIBPATH, defines=()):
+    """Compiles the kernels and the host runtime and links libdsm.so.
+
+    defines: extra -D settings of the build-time tuning knobs (DSM_UNROLL,
+    DSM_NT, DSM_CHUNK_ELEMS); the defaults are the tuned values.
+    """
+    os.makedirs(os.path.dirname(out), exist_ok=True)
+    objdir = os.path.join(OBJDIR, "_".join(d.replace("=", "") for d in defines) or "default")
+    os.makedirs(objdir, exist_ok=True)
+    dflags = [f"-D{d}" for d in defines]
     cc = hipcc()
-    k_obj = os.path.join(OBJDIR, "dsm_kernels.o")
-    r_obj = os.path.join(OBJDIR, "dsm_runtime.o")
-    _run([cc, "-x", "hip", *COMMON_FLAGS, *DEVICE_FLAGS, "-c",
+    k_obj = os.path.join(objdir, "dsm_kernels.o")
+    r_obj = os.path.join(objdir, "dsm_runtime.o")
+    _run([cc, "-x", "hip", *COMMON_FLAGS, *DEVICE_FLAGS, *dflags, "-c",
           os.path.join(CSRC, "dsm_kernels.hip"), "-o", k_obj], verbose)
-    _run([cc, "-x", "c++", "-D__HIP_PLATFORM_AMD__", f"-I{ROCM}/include", *COMMON_FLAGS, "-c",
-          os.path.join(CSRC, "dsm_runtime.cpp"), "-o", r_obj], verbose)
-    tmp = LIBPATH + ".tmp"
+    _run([cc, "-x", "c++", "-D__HIP_PLATFORM_AMD__", f"-I{ROCM}/include", *COMMON_FLAGS,
+          *dflags, "-c", os.path.join(CSRC, "dsm_runtime.cpp"), "-o", r_obj], verbose)
+    tmp = out + ".tmp"
     _run([cc, "-shared", f"--offload-arch={ARCH}", "-o", tmp, k_obj, r_obj,
           "-Wl,--no-undefined", "-Wl,-soname,libdsm.so"], verbose)
-    os.replace(tmp, LIBPATH)
-    return LIBPATH
+    os.replace(tmp, out)
+    return out
 
 
 def kernel_isa(path=None):

@@ -11,7 +11,11 @@ namespace dsm {
 // so the per-tensor facts a kernel needs (decay flag, tensor index for the
 // randomized sign's bound and Philox counter) are uniform per work-group and
 // read once.  Multiple of 4 (float4) and of 256 threads x 4.
-constexpr int kChunkElems = 16384;
+#ifndef DSM_CHUNK_ELEMS
+#define DSM_CHUNK_ELEMS 16384
+#endif
+constexpr int kChunkElems = DSM_CHUNK_ELEMS;
+static_assert(kChunkElems % 1024 == 0, "chunk must be a multiple of 256 threads x 4");
 constexpr int kBlockThreads = 256;
 // Arena alignment of every tensor, in elements (256 bytes).
 constexpr int64_t kTensorAlign = 64;

@@ -23,10 +23,30 @@ namespace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-constexpr int kUnroll = 2;
+// float4 groups per stream in flight per thread, and whether the streams use
+// nontemporal loads and stores (build-time tuning knobs).
+#ifndef DSM_UNROLL
+#define DSM_UNROLL 2
+#endif
+#ifndef DSM_NT
+#define DSM_NT 1
+#endif
+constexpr int kUnroll = DSM_UNROLL;
 
-__device__ __forceinline__ f4 ntload(const f4* p) { return __builtin_nontemporal_load(p); }
-__device__ __forceinline__ void ntstore(f4 v, f4* p) { __builtin_nontemporal_store(v, p); }
+__device__ __forceinline__ f4 ntload(const f4* p) {
+#if DSM_NT
+    return __builtin_nontemporal_load(p);
+#else
+    return *p;
+#endif
+}
+__device__ __forceinline__ void ntstore(f4 v, f4* p) {
+#if DSM_NT
+    __builtin_nontemporal_store(v, p);
+#else
+    *p = v;
+#endif
+}
 
 // Stores the first k (1..3) lanes of v: the ragged end of a tensor.
 __device__ __forceinline__ void store_head(f4 v, float* p, int k) {
