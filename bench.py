@@ -78,8 +78,8 @@ def cpu_baseline(w, ar, sample_tensors):
     updates = w.n_workers * w.local_steps * d_s + d_s
     return {"value": updates / dt, "unit": "param-updates/s", "cores": 1, "kind": "oracle",
             "sample": (f"one round (n={w.n_workers}, H={w.local_steps} AdamW local steps + "
-                       f"deterministic global step) of the oracle in fp64 on {len(idx)} tensors "
-                       f"({', '.join(sample_tensors)}), {d_s} of {w.d} parameters; "
+                       f"deterministic global step) of the oracle in fp64 on the {len(idx)} "
+                       f"tensors of transformer layer 0 ({d_s} of {w.d} parameters); "
                        f"{dt:.1f} s on one host thread"),
             "seconds": dt, "host_threads_available": len(os.sched_getaffinity(0))}
 
@@ -168,6 +168,31 @@ def main():
         one_round(t, dsm.DSM_SIGN_RAND_FLIP, True)
         t += 1
     torch.cuda.synchronize()
+    # Row a2 (local SGD + Polyak momentum, Algorithm 3) and row a6 on its own
+    # (dsm_sync) at the same scale: a second context, SGD base, over the same
+    # arenas, after the timed steps.
+    ar.destroy()
+    sgd_problem = dsm.make_problem(w.numel, n, H, dsm.DSM_BASE_SGD_MOMENTUM, w.decay)
+    bufs = ar.buffers()
+    bufs.s2_rep = None
+    ctx2 = dsm.dsm_init(sgd_problem, bufs)
+    ev_sgd, ev_sync = [], []
+    for k in range(min(H, 6)):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        dsm.dsm_local_step(ctx2, -1, k + 1, lr=0.1, beta1=0.9)
+        e1.record(stream)
+        if k > 0:
+            ev_sgd.append((e0, e1))
+    for k in range(4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        dsm.dsm_sync(ctx2)
+        e1.record(stream)
+        if k > 0:
+            ev_sync.append((e0, e1))
+    torch.cuda.synchronize()
+    dsm.dsm_destroy(ctx2)
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
@@ -184,6 +209,8 @@ def main():
     ms_local = avg_ms(ev["local"])
     ms_gdet = avg_ms(ev["global_det"])
     ms_grand = avg_ms(ev["global_rand"])
+    ms_sgd = avg_ms(ev_sgd)
+    ms_sync = avg_ms(ev_sync)
     d = w.d
     local_bytes = BYTES_LOCAL_ADAMW * n * d
     khash = kernel_source_hash()
@@ -237,16 +264,15 @@ def main():
             "local_adamw": kern(ms_local, local_bytes, n * d),
             "global_det": kern(ms_gdet, bytes_global(n, False) * d, d),
             "global_rand_flip": kern(ms_grand, bytes_global(n, True) * d, d),
+            "local_sgdm": kern(ms_sgd, BYTES_LOCAL_SGDM * n * d, n * d),
+            "sync": kern(ms_sync, (4 + 4 * n) * d, n * d),
         },
         "kernel_source_hash": khash,
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(
-            w, ar, ("h0.ln_1.weight", "h0.ln_1.bias", "h0.attn.c_attn.bias",
-                    "h0.attn.c_proj.weight", "h0.attn.c_proj.bias", "h0.ln_2.weight",
-                    "h0.ln_2.bias"))
-    ar.destroy()
+            w, ar, tuple(name for name, _ in w.tensors if name.startswith("h0.")))
     print(json.dumps(out), flush=True)
 
 

@@ -8,6 +8,6 @@ from .dsm_oracle import (  # noqa: F401
     PRECISIONS, SIGN_DET, SIGN_RAND_FLIP, SIGN_RAND_ZERO, PHILOX_STREAM,
     beta_power, communication_round, f32, global_step, init_state,
     local_adamw_step, local_sgdm_step, local_steps, randomized_sign,
-    randomized_sign_uniforms, sign, synchronize,
+    randomized_sign_uniforms, randomized_sign_uniforms_at, sign, synchronize,
 )
 from .philox import philox4x32_10, philox4x32_10_scalar  # noqa: F401

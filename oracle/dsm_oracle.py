@@ -173,6 +173,19 @@ def randomized_sign_uniforms(numel, tensor_index, t, seed):
     return (words >> np.uint32(8)).astype(np.int64)
 
 
+def randomized_sign_uniforms_at(j, tensor_index, t, seed):
+    """k = w >> 8 for chosen element indices j of a tensor (same stream as
+    randomized_sign_uniforms, evaluated only where asked)."""
+    if not (0 <= t < 2 ** 32):
+        raise ValueError("t must be in [0, 2^32)")
+    j = np.asarray(j, dtype=np.uint64)
+    w = philox4x32_10(j >> np.uint64(2), tensor_index, t, PHILOX_STREAM,
+                      seed & 0xFFFFFFFF, (seed >> 32) & 0xFFFFFFFF)
+    words = np.stack(w, axis=1)
+    pick = words[np.arange(j.size), (j & np.uint64(3)).astype(np.int64)]
+    return (pick >> np.uint32(8)).astype(np.int64)
+
+
 def _exact_less(a_int, B, au):
     """Elementwise exact test  a_int * B < au * 2^24  for integers a_int.
 
@@ -214,7 +227,8 @@ def randomized_sign(u, B, k, variant):
 
 
 def global_step(x, m, replicas, *, gamma, eta, beta1, beta2, lam, decay,
-                t=0, mode=SIGN_DET, seed=0, prec="fp64"):
+                t=0, mode=SIGN_DET, seed=0, prec="fp64", tensor_ids=None,
+                element_ids=None, bounds=None):
     """Algorithm 1 global step for a model given as a list of tensors.
 
     x:        list of arrays, x_{t,0} per tensor.
@@ -223,6 +237,12 @@ def global_step(x, m, replicas, *, gamma, eta, beta1, beta2, lam, decay,
     decay:    list of bools, whether lambda applies to each tensor.
     mode:     SIGN_DET, SIGN_RAND_FLIP (Eq. (9)) or SIGN_RAND_ZERO (Eq. (10)).
     t, seed:  outer iteration and 64-bit seed keying the randomized sign.
+    Evaluating samples of tensors (every update is elementwise given B_p):
+    tensor_ids:  tensor index p of each entry (default: its list position);
+    element_ids: per entry, the in-tensor indices j of its elements (default:
+                 the entry is the whole tensor, j = 0..numel-1);
+    bounds:      per entry, B_p of the whole tensor (default: max |u| over
+                 the entry, which is B_p when the entry is the whole tensor).
 
     Returns a dict of per-tensor lists: x (x_{t+1,0}), m (m_{t+1}), u
     (u_{t+1}), S (the sign actually applied), delta ((x_{t,0}-x_{t,tau})),
@@ -255,8 +275,15 @@ def global_step(x, m, replicas, *, gamma, eta, beta1, beta2, lam, decay,
         if mode == SIGN_DET:
             S = sign(u)
         else:
-            B = np.max(np.abs(u)) if u.size else dt(0.0)
-            k = randomized_sign_uniforms(u.size, p, t, seed)
+            pid = p if tensor_ids is None else int(tensor_ids[p])
+            if bounds is not None:
+                B = dt(bounds[p])
+            else:
+                B = np.max(np.abs(u)) if u.size else dt(0.0)
+            if element_ids is None:
+                k = randomized_sign_uniforms(u.size, pid, t, seed)
+            else:
+                k = randomized_sign_uniforms_at(element_ids[p], pid, t, seed)
             S = randomized_sign(u, B, k, mode)
             out["B"].append(dt(B))
         lam_p = lam_ if decay[p] else dt(0.0)

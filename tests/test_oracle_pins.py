@@ -465,6 +465,9 @@ def test_randomized_stream_depends_on_counter_words():
     assert np.all((base >= 0) & (base < (1 << 24)))
     # A prefix of a longer tensor draws the same numbers (stream per element).
     np.testing.assert_array_equal(base[:10], O.randomized_sign_uniforms(10, 2, 5, 77))
+    # Pointwise evaluation gives the same draws.
+    j = np.array([0, 1, 2, 3, 4, 17, 63])
+    np.testing.assert_array_equal(O.randomized_sign_uniforms_at(j, 2, 5, 77), base[j])
 
 
 # ---------------------------------------------------------------- Philox
@@ -525,3 +528,21 @@ def test_philox_matches_rocrand_engine():
     out = subprocess.run([exe], input=inp, capture_output=True, text=True, check=True).stdout
     words = [int(w, 16) for line in out.strip().split("\n") for w in line.split()]
     np.testing.assert_array_equal(k, np.array(words, dtype=np.int64) >> 8)
+
+
+def test_sampled_global_step_matches_whole_tensor():
+    """Evaluating chosen elements (with their tensor index, in-tensor indices
+    and the whole tensor's bound) gives the whole-tensor result there."""
+    rng = np.random.default_rng(15)
+    x = [rng.normal(0, 0.02, s).astype(np.float32) for s in (37, 1000)]
+    m = [rng.normal(0, 1, a.size).astype(np.float32) for a in x]
+    reps = [[(a + rng.normal(0, 1e-3, a.size)).astype(np.float32) for a in x] for _ in range(3)]
+    kw = dict(gamma=1e-3, eta=0.8, beta1=0.95, beta2=0.98, lam=0.1, t=4, seed=5, prec="fp32")
+    for mode in (O.SIGN_RAND_FLIP, O.SIGN_RAND_ZERO):
+        full = O.global_step(x, m, reps, decay=[True, False], mode=mode, **kw)
+        j = rng.choice(1000, 50, replace=False)
+        part = O.global_step([x[1][j]], [m[1][j]], [[r[1][j]] for r in reps], decay=[False],
+                             mode=mode, tensor_ids=[1], element_ids=[j], bounds=[full["B"][1]],
+                             **kw)
+        np.testing.assert_array_equal(part["x"][0], full["x"][1][j])
+        np.testing.assert_array_equal(part["S"][0], full["S"][1][j])
