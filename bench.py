@@ -70,14 +70,15 @@ def cpu_baseline(w, ar, sample_tensors):
     grads = [take(ar.g_rep[i]) for i in range(w.n_workers)]
     d_s = int(sum(ar.numel[i] for i in idx))
     decay = [w.decay[i] for i in idx]
-    st = O.init_state(x0, w.n_workers, "adamw")
+    base = "adamw" if w.base == 0 else "sgd"
+    st = O.init_state(x0, w.n_workers, base)
     t0 = time.perf_counter()
     O.communication_round(st, lambda i, k: grads[i], 0, H=w.local_steps, local=w.local,
                           glob=dict(w.glob, mode=O.SIGN_DET, seed=0), decay=decay)
     dt = time.perf_counter() - t0
     updates = w.n_workers * w.local_steps * d_s + d_s
     return {"value": updates / dt, "unit": "param-updates/s", "cores": 1, "kind": "oracle",
-            "sample": (f"one round (n={w.n_workers}, H={w.local_steps} AdamW local steps + "
+            "sample": (f"one round (n={w.n_workers}, H={w.local_steps} {base} local steps + "
                        f"deterministic global step) of the oracle in fp64 on the {len(idx)} "
                        f"tensors of transformer layer 0 ({d_s} of {w.d} parameters); "
                        f"{dt:.1f} s on one host thread"),
@@ -92,11 +93,15 @@ def main():
     ap.add_argument("--workload", default="xl")
     ap.add_argument("--sign", choices=("det", "rand"), default="det",
                     help="global sign of the timed steps")
-    ap.add_argument("--rand-steps", type=int, default=2,
-                    help="extra rounds with the randomized sign, timed separately")
+    ap.add_argument("--path", choices=("fused", "split"), default="fused",
+                    help="fused: H-1 local steps + dsm_round_end with the lazy broadcast; "
+                         "split: H local steps + dsm_global_step with broadcast")
+    ap.add_argument("--extra-steps", type=int, default=2,
+                    help="rounds of each other path/sign combination, timed separately")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
-                    help="also run a plain 4 GiB device copy (counter calibration)")
+                    help="accepted for the counter runs; the plain 4 GiB device copy that "
+                         "calibrates the byte counters always runs")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -113,10 +118,10 @@ def main():
     torch.cuda.set_device(0)
     w = W.get(args.workload)
     n, H = w.n_workers, w.local_steps
-    randomized_any = args.sign == "rand" or args.rand_steps > 0
+    adamw = w.base == W.BASE_ADAMW
     print(f"[bench] workload {w.name}: d={w.d} tensors={len(w.tensors)} n={n} H={H}",
           file=sys.stderr, flush=True)
-    ar = A.Arenas(w.numel, n, H, w.base, decay=w.decay, randomized=randomized_any)
+    ar = A.Arenas(w.numel, n, H, w.base, decay=w.decay, randomized=True)
     gen = torch.Generator(device="cuda").manual_seed(w.seed)
     W.fill_params_(ar.x, w, gen)
     for i in range(n):
@@ -128,46 +133,57 @@ def main():
 
     stream = torch.cuda.current_stream()
     lr = w.local["lr"]
-    ev = {"local": [], "global_det": [], "global_rand": []}
+    ev = {"local": [], "split_det": [], "split_rand": [], "fused_det": [], "fused_rand": []}
     s_count = [0]
 
-    def one_round(t, mode, record):
+    def timed(key, fn):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        if key is not None:
+            ev[key].append((e0, e1))
+
+    def one_round(t, mode, path, record):
+        sign = "rand" if mode else "det"
         for k in range(H):
             s_count[0] += 1
-            if record:
-                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                e0.record(stream)
-            dsm.dsm_local_step(ar.ctx, -1, s_count[0], **w.local)
-            if record:
-                e1.record(stream)
-                ev["local"].append((e0, e1))
-        if record:
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-        dsm.dsm_global_step(ar.ctx, t, gamma=lr, mode=mode, seed=w.philox_seed, broadcast=True,
-                            **w.glob)
-        if record:
-            e1.record(stream)
-            ev["global_rand" if mode else "global_det"].append((e0, e1))
+            s = s_count[0]
+            if path == "fused" and k == H - 1:
+                timed(f"fused_{sign}" if record else None,
+                      lambda: dsm.dsm_round_end(ar.ctx, s, w.local, t, gamma=lr, mode=mode,
+                                                seed=w.philox_seed, broadcast=False, **w.glob))
+            else:
+                timed("local" if record else None,
+                      lambda: dsm.dsm_local_step(ar.ctx, -1, s, **w.local))
+        if path == "split":
+            timed(f"split_{sign}" if record else None,
+                  lambda: dsm.dsm_global_step(ar.ctx, t, gamma=lr, mode=mode, seed=w.philox_seed,
+                                              broadcast=True, **w.glob))
 
     mode_main = dsm.DSM_SIGN_DET if args.sign == "det" else dsm.DSM_SIGN_RAND_FLIP
     t = 0
     for _ in range(args.warmup):
-        one_round(t, mode_main, False)
+        one_round(t, mode_main, args.path, False)
         t += 1
     torch.cuda.synchronize()
     print("[bench] warmup done", file=sys.stderr, flush=True)
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        one_round(t, mode_main, True)
+        one_round(t, mode_main, args.path, True)
         t += 1
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     print("[bench] timed steps done", file=sys.stderr, flush=True)
-    for _ in range(args.rand_steps if args.sign == "det" else 0):
-        one_round(t, dsm.DSM_SIGN_RAND_FLIP, True)
-        t += 1
+    for path in ("fused", "split"):
+        for mode in (dsm.DSM_SIGN_DET, dsm.DSM_SIGN_RAND_FLIP):
+            if (path, mode) == (args.path, mode_main):
+                continue
+            for _ in range(args.extra_steps):
+                one_round(t, mode, path, True)
+                t += 1
     torch.cuda.synchronize()
+
     # Row a2 (local SGD + Polyak momentum, Algorithm 3) and row a6 on its own
     # (dsm_sync) at the same scale: a second context, SGD base, over the same
     # arenas, after the timed steps.
@@ -193,41 +209,51 @@ def main():
             ev_sync.append((e0, e1))
     torch.cuda.synchronize()
     dsm.dsm_destroy(ctx2)
-    if args.copy_calibration:
-        src = torch.empty(1 << 30, dtype=torch.float32, device="cuda")
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+
+    # Practical ceiling of this device: a plain 4 GiB copy and fill (torch).
+    src = torch.empty(1 << 30, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    dst.fill_(1.0)
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    e[0].record(stream)
+    for _ in range(3):
+        dst.copy_(src)
+    e[1].record(stream)
+    for _ in range(3):
+        dst.fill_(2.0)
+    e[2].record(stream)
+    torch.cuda.synchronize()
+    copy_gbs = 3 * 8 * (1 << 30) / (e[0].elapsed_time(e[1]) / 1e3) / 1e9
+    fill_gbs = 3 * 4 * (1 << 30) / (e[1].elapsed_time(e[2]) / 1e3) / 1e9
+    del src, dst
 
     def avg_ms(pairs):
         if not pairs:
             return None
         return sum(a.elapsed_time(b) for a, b in pairs) / len(pairs)
 
-    ms_local = avg_ms(ev["local"])
-    ms_gdet = avg_ms(ev["global_det"])
-    ms_grand = avg_ms(ev["global_rand"])
-    ms_sgd = avg_ms(ev_sgd)
-    ms_sync = avg_ms(ev_sync)
     d = w.d
-    local_bytes = BYTES_LOCAL_ADAMW * n * d
     khash = kernel_source_hash()
     ms_per_step = wall * 1e3 / args.steps
     updates_per_step = n * H * d + d
     value = updates_per_step / (ms_per_step / 1e3)
 
-    def kern(ms, nbytes, updates):
+    def kern(pairs, nbytes, updates):
+        ms = avg_ms(pairs)
         if ms is None:
             return None
         gbs = nbytes / (ms / 1e3) / 1e9
         return {"ms": round(ms, 4), "GB_per_s": round(gbs, 1),
                 "pct_peak_hbm": round(100 * gbs / PEAK_HBM_GBS, 2),
-                "param_updates_per_s": updates / (ms / 1e3), "algorithmic_bytes": nbytes}
+                "param_updates_per_s": updates / (ms / 1e3), "algorithmic_bytes": nbytes,
+                "launches": len(pairs)}
 
+    local_bytes = (BYTES_LOCAL_ADAMW if adamw else BYTES_LOCAL_SGDM) * n * d
+    ms_local = avg_ms(ev["local"])
     traffic = committed_traffic(khash, "local_adamw")
     achieved = local_bytes / (ms_local / 1e3) / 1e9
+    local_state = 16 if adamw else 12        # x, g, s1 (, s2) read per worker
     out = {
         "metric": METRIC,
         "value": value,
@@ -243,15 +269,17 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": (f"GPT-2 {w.name}-shaped parameter set ({len(w.tensors)} fp32 tensors, "
-                         f"d={d}), n={n} worker replicas, H={H} local AdamW steps + one "
-                         f"{'deterministic' if args.sign == 'det' else 'randomized'}-sign "
-                         "global step per step"),
-            "d": d, "n_workers": n, "local_steps": H, "base": "adamw",
-            "sign": args.sign, "updates_per_step": updates_per_step,
+                         f"d={d}), n={n} worker replicas; one step = one outer iteration of "
+                         f"Algorithm 1: H={H} local {'AdamW' if adamw else 'SGD-momentum'} steps "
+                         f"on every replica + the "
+                         f"{'deterministic' if args.sign == 'det' else 'randomized'}-sign global "
+                         f"step ({args.path} path)"),
+            "d": d, "n_workers": n, "local_steps": H, "base": "adamw" if adamw else "sgd_momentum",
+            "sign": args.sign, "path": args.path, "updates_per_step": updates_per_step,
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "k_local_adamw (dsm_local_step, all workers)",
+            "kernel": f"k_local_{'adamw' if adamw else 'sgdm'} (dsm_local_step, all workers)",
             "achieved": round(achieved, 1),
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",
@@ -261,12 +289,18 @@ def main():
             "avg_launch_ms": round(ms_local, 4),
         },
         "breakdown": {
-            "local_adamw": kern(ms_local, local_bytes, n * d),
-            "global_det": kern(ms_gdet, bytes_global(n, False) * d, d),
-            "global_rand_flip": kern(ms_grand, bytes_global(n, True) * d, d),
-            "local_sgdm": kern(ms_sgd, BYTES_LOCAL_SGDM * n * d, n * d),
-            "sync": kern(ms_sync, (4 + 4 * n) * d, n * d),
+            "local_step": kern(ev["local"], local_bytes, n * d),
+            "round_end_fused_det": kern(ev["fused_det"], (16 + (local_state + 8) * n) * d,
+                                        n * d + d),
+            "round_end_fused_rand_flip": kern(ev["fused_rand"],
+                                              (28 + (local_state + 8) * n) * d, n * d + d),
+            "global_det": kern(ev["split_det"], bytes_global(n, False) * d, d),
+            "global_rand_flip": kern(ev["split_rand"], bytes_global(n, True) * d, d),
+            "local_sgdm": kern(ev_sgd, BYTES_LOCAL_SGDM * n * d, n * d),
+            "sync": kern(ev_sync, (4 + 4 * n) * d, n * d),
         },
+        "device_ceiling": {"torch_copy_GB_per_s": round(copy_gbs, 1),
+                           "torch_fill_GB_per_s": round(fill_gbs, 1)},
         "kernel_source_hash": khash,
     }
     if not args.no_cpu_baseline:

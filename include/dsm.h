@@ -149,9 +149,12 @@ DSM_API dsm_status dsm_init(const dsm_problem* problem, const dsm_buffers* buffe
  *          x = x - lr*((m/(1-b1^s)) / (sqrt(v/(1-b2^s)) + eps) + wd_p*x)
  *   SGD:   m = b1*m + g;  x = x - lr*m
  * with wd_p = weight_decay on decayed tensors, else 0.
+ * After a global step with broadcast = 0 a worker's replica is stale: its
+ * next local step reads the new global model x in place of the replica (the
+ * synchronisation step of Algorithm 1 folded into this step) and writes the
+ * replica, which saves the broadcast's n replica writes.
  * Errors: DSM_ERR_INVALID_ARG (worker, step, hyperparameters);
- * DSM_ERR_STATE (replicas not synchronised since the last global step with
- * broadcast = 0, or the worker already took H local steps this round);
+ * DSM_ERR_STATE (the worker already took H local steps this round);
  * DSM_ERR_HIP.
  */
 DSM_API dsm_status dsm_local_step(dsm_ctx* ctx, int32_t worker, int64_t step,
@@ -169,14 +172,32 @@ DSM_API dsm_status dsm_local_step(dsm_ctx* ctx, int32_t worker, int64_t step,
  * Philox4x32-10 keyed by `seed` with counter (j div 4, p, t, 1), word j mod 4
  * (j = index inside the tensor); S keeps sign(u) exactly when U < the
  * equation's probability.  When broadcast != 0 every replica is set to the
- * new x (synchronisation step); otherwise call dsm_sync before the next
- * local step.  The randomized modes need buffers->u_scratch.
+ * new x (synchronisation step); otherwise the replicas are left stale and
+ * each worker's next local step reads x (see dsm_local_step), or dsm_sync
+ * copies x into them.  The randomized modes need buffers->u_scratch.
  * Errors: DSM_ERR_INVALID_ARG (t outside [0, 2^32), hyperparameters, mode,
  * missing u_scratch); DSM_ERR_STATE (some worker has not taken exactly H
  * local steps since the last synchronisation); DSM_ERR_HIP.
  */
 DSM_API dsm_status dsm_global_step(dsm_ctx* ctx, int64_t t, const dsm_global_hparams* hp,
                            int32_t broadcast);
+
+/*
+ * dsm_round_end - the end of outer iteration t of Algorithm 1 in one pass:
+ * local step H of every worker (as dsm_local_step(ctx, -1, step, local_hp))
+ * fused with the all-reduce and global step (as dsm_global_step(ctx, t,
+ * global_hp, broadcast)).  Each worker's step-H replica value is folded into
+ * the worker-order sum of Eq. (6)'s difference in registers and is never
+ * stored or read back; the base-optimizer state of step H is stored.  The
+ * results are bit-identical to the two separate calls.  With broadcast = 0
+ * the replicas are left stale (read as x by the next local step), which
+ * with the fusion saves 4n + 4n bytes per element per round.
+ * Errors: as dsm_local_step and dsm_global_step; DSM_ERR_STATE unless every
+ * worker has taken exactly H - 1 local steps this round.
+ */
+DSM_API dsm_status dsm_round_end(dsm_ctx* ctx, int64_t step, const dsm_local_hparams* local_hp,
+                                 int64_t t, const dsm_global_hparams* global_hp,
+                                 int32_t broadcast);
 
 /*
  * dsm_sync - the synchronisation step of Algorithm 1 on its own: every

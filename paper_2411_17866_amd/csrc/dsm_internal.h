@@ -62,12 +62,33 @@ struct GlobalScalars {
 // Kernel launchers (dsm_kernels.hip).  All return the launch status.
 hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float* m, float* x_rep,
                        float* s1, float* s2, int64_t stride, int n, hipStream_t st);
+// Local steps: worker w reads its replica from x_src + w * src_stride (the
+// replica, or the shared global model with src_stride = 0) and writes it to
+// x_rep + w * stride.
 hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_rep,
-                              const float* g_rep, float* s1, float* s2, int64_t stride,
-                              int worker0, int n_workers, const AdamScalars& sc, hipStream_t st);
+                              const float* x_src, int64_t src_stride, const float* g_rep,
+                              float* s1, float* s2, int64_t stride, int worker0, int n_workers,
+                              const AdamScalars& sc, hipStream_t st);
 hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep,
-                             const float* g_rep, float* s1, int64_t stride, int worker0,
-                             int n_workers, const SgdScalars& sc, hipStream_t st);
+                             const float* x_src, int64_t src_stride, const float* g_rep,
+                             float* s1, int64_t stride, int worker0, int n_workers,
+                             const SgdScalars& sc, hipStream_t st);
+
+// Arguments of the fused last-local-step + global-step launch.
+struct RoundEndArgs {
+    float *x, *m, *x_rep;
+    const float* x_src;
+    int64_t src_stride;
+    const float* g_rep;
+    float *s1, *s2, *u;
+    uint32_t* bound_bits;
+    int64_t stride;
+    AdamScalars as;
+    SgdScalars ss;
+    GlobalScalars gs;
+};
+hipError_t launch_round_end(const Chunk* chunks, int64_t n_chunks, int n_tensors, bool adamw,
+                            const RoundEndArgs& a, bool broadcast, hipStream_t st);
 hipError_t launch_global_det(const Chunk* chunks, int64_t n_chunks, float* x, float* m,
                              float* x_rep, int64_t stride, const GlobalScalars& sc,
                              bool broadcast, hipStream_t st);

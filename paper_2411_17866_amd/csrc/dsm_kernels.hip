@@ -90,12 +90,19 @@ __device__ __forceinline__ void adamw4(f4& x, f4 g, f4& m, f4& v, float lam, con
     x = x - st;
 }
 
+// x_src/src_stride: where worker w reads its replica, x_src + w * src_stride
+// (the replica itself, or with src_stride = 0 the global model x when the
+// replicas are stale after a global step without broadcast); the result is
+// written to the replica x_rep + w * stride.
 __global__ __launch_bounds__(kBlockThreads) void k_local_adamw(
-    const Chunk* __restrict__ chunks, float* __restrict__ x_rep, const float* __restrict__ g_rep,
-    float* __restrict__ s1, float* __restrict__ s2, int64_t stride, int worker0, AdamScalars sc) {
+    const Chunk* __restrict__ chunks, float* __restrict__ x_rep, const float* __restrict__ x_src,
+    int64_t src_stride, const float* __restrict__ g_rep, float* __restrict__ s1,
+    float* __restrict__ s2, int64_t stride, int worker0, AdamScalars sc) {
     const Chunk c = chunks[blockIdx.x];
-    const int64_t base = static_cast<int64_t>(worker0 + static_cast<int>(blockIdx.y)) * stride + c.off;
+    const int64_t w = worker0 + static_cast<int>(blockIdx.y);
+    const int64_t base = w * stride + c.off;
     f4* __restrict__ xp = reinterpret_cast<f4*>(x_rep + base);
+    const f4* __restrict__ xs = reinterpret_cast<const f4*>(x_src + w * src_stride + c.off);
     const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + base);
     f4* __restrict__ mp = reinterpret_cast<f4*>(s1 + base);
     f4* __restrict__ vp = reinterpret_cast<f4*>(s2 + base);
@@ -108,7 +115,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_local_adamw(
         for (int k = 0; k < kUnroll; ++k) {
             const int q = q0 + k * kBlockThreads;
             if (q < nvec) {
-                xv[k] = ntload(xp + q);
+                xv[k] = ntload(xs + q);
                 gv[k] = ntload(gp + q);
                 mv[k] = ntload(mp + q);
                 vv[k] = ntload(vp + q);
@@ -138,11 +145,14 @@ __device__ __forceinline__ void sgdm4(f4& x, f4 g, f4& m, const SgdScalars& s) {
 }
 
 __global__ __launch_bounds__(kBlockThreads) void k_local_sgdm(
-    const Chunk* __restrict__ chunks, float* __restrict__ x_rep, const float* __restrict__ g_rep,
-    float* __restrict__ s1, int64_t stride, int worker0, SgdScalars sc) {
+    const Chunk* __restrict__ chunks, float* __restrict__ x_rep, const float* __restrict__ x_src,
+    int64_t src_stride, const float* __restrict__ g_rep, float* __restrict__ s1, int64_t stride,
+    int worker0, SgdScalars sc) {
     const Chunk c = chunks[blockIdx.x];
-    const int64_t base = static_cast<int64_t>(worker0 + static_cast<int>(blockIdx.y)) * stride + c.off;
+    const int64_t w = worker0 + static_cast<int>(blockIdx.y);
+    const int64_t base = w * stride + c.off;
     f4* __restrict__ xp = reinterpret_cast<f4*>(x_rep + base);
+    const f4* __restrict__ xs = reinterpret_cast<const f4*>(x_src + w * src_stride + c.off);
     const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + base);
     f4* __restrict__ mp = reinterpret_cast<f4*>(s1 + base);
     const int nvec = (c.len + 3) >> 2;
@@ -153,7 +163,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_local_sgdm(
         for (int k = 0; k < kUnroll; ++k) {
             const int q = q0 + k * kBlockThreads;
             if (q < nvec) {
-                xv[k] = ntload(xp + q);
+                xv[k] = ntload(xs + q);
                 gv[k] = ntload(gp + q);
                 mv[k] = ntload(mp + q);
             }
@@ -401,6 +411,115 @@ __global__ __launch_bounds__(kBlockThreads) void k_global_rand_pass2(
     }
 }
 
+// ---------------------------------------------------------------- fused round end
+
+// The last local step of every worker (Algorithm 2 or 3, Eq. (4)) fused with
+// the global step (all-reduce, Eqs. (6)-(8)): each worker's step-H replica
+// value stays in registers and is folded into the worker-order sum
+// sum_i (x - x_i) as it is produced, so the replicas are neither stored after
+// step H nor read back.  Per element the operations and their order are those
+// of k_local_* followed by k_global_det / k_global_rand_pass1, so the results
+// are bit-identical.  KIND: 0 deterministic sign, 1 deterministic sign with
+// broadcast, 2 randomized pass 1 (u, m and the bound; pass 2 follows).
+constexpr int kBaseAdamW = 0;
+constexpr int kBaseSgd = 1;
+
+template <int N, int BASE, int KIND>
+__global__ __launch_bounds__(kBlockThreads) void k_round_end(
+    const Chunk* __restrict__ chunks, float* __restrict__ x, float* __restrict__ m,
+    float* __restrict__ x_rep, const float* __restrict__ x_src, int64_t src_stride,
+    const float* __restrict__ g_rep, float* __restrict__ s1, float* __restrict__ s2,
+    float* __restrict__ u_out, uint32_t* __restrict__ bound_bits, int64_t stride,
+    AdamScalars as, SgdScalars ss, GlobalScalars gs) {
+    __shared__ uint32_t wave_max[kBlockThreads / 64];
+    const Chunk c = chunks[blockIdx.x];
+    const int n = N > 0 ? N : gs.n;
+    f4* __restrict__ xp = reinterpret_cast<f4*>(x + c.off);
+    f4* __restrict__ mp = reinterpret_cast<f4*>(m + c.off);
+    const float lam_local = c.decay ? as.wd : 0.0f;
+    const float lam = c.decay ? gs.lam : 0.0f;
+    const int nvec = (c.len + 3) >> 2;
+    const int nfull = c.len >> 2;
+    uint32_t maxbits = 0;
+    for (int q0 = threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+        f4 xv[kUnroll], mv[kUnroll], acc[kUnroll];
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) {
+            const int q = q0 + k * kBlockThreads;
+            if (q < nvec) {
+                xv[k] = ntload(xp + q);
+                mv[k] = ntload(mp + q);
+            }
+        }
+        // Worker loop: fully unrolled for a compile-time worker count.
+#pragma unroll
+        for (int i = 0; i < (N > 0 ? N : n); ++i) {
+            const int64_t wo = i * stride + c.off;
+            const f4* __restrict__ xs = reinterpret_cast<const f4*>(x_src + i * src_stride + c.off);
+            const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + wo);
+            f4* __restrict__ s1p = reinterpret_cast<f4*>(s1 + wo);
+            f4* __restrict__ s2p = reinterpret_cast<f4*>(s2 + wo);
+            f4 xi[kUnroll], gi[kUnroll], mi[kUnroll], vi[kUnroll];
+#pragma unroll
+            for (int k = 0; k < kUnroll; ++k) {
+                const int q = q0 + k * kBlockThreads;
+                if (q < nvec) {
+                    xi[k] = ntload(xs + q);
+                    gi[k] = ntload(gp + q);
+                    mi[k] = ntload(s1p + q);
+                    if (BASE == kBaseAdamW) vi[k] = ntload(s2p + q);
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < kUnroll; ++k) {
+                const int q = q0 + k * kBlockThreads;
+                if (q < nvec) {
+                    if (BASE == kBaseAdamW) {
+                        adamw4(xi[k], gi[k], mi[k], vi[k], lam_local, as);
+                        store_group(vi[k], s2p, q, nfull, c.len);
+                    } else {
+                        sgdm4(xi[k], gi[k], mi[k], ss);
+                    }
+                    store_group(mi[k], s1p, q, nfull, c.len);
+                    const f4 d = xv[k] - xi[k];
+                    acc[k] = (i == 0) ? d : acc[k] + d;
+                }
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) {
+            const int q = q0 + k * kBlockThreads;
+            if (q < nvec) {
+                f4 delta;
+                if (N > 0 || gs.n_pow2)
+                    delta = acc[k] * gs.inv_n;
+                else
+                    delta = acc[k] / gs.n_f;
+                const f4 u = momentum4(mv[k], delta, gs);
+                store_group(mv[k], mp, q, nfull, c.len);
+                if (KIND == 2) {
+                    store_group(u, reinterpret_cast<f4*>(u_out + c.off), q, nfull, c.len);
+                    const int valid = c.len - 4 * q;
+                    uint32_t b = __float_as_uint(fabsf(u.x));
+                    if (valid > 1) b = max(b, __float_as_uint(fabsf(u.y)));
+                    if (valid > 2) b = max(b, __float_as_uint(fabsf(u.z)));
+                    if (valid > 3) b = max(b, __float_as_uint(fabsf(u.w)));
+                    maxbits = max(maxbits, b);
+                } else {
+                    const f4 xn = model4(xv[k], sign4(u), lam, gs);
+                    store_group(xn, xp, q, nfull, c.len);
+                    if (KIND == 1) {
+                        for (int i = 0; i < n; ++i)
+                            store_group(xn, reinterpret_cast<f4*>(x_rep + i * stride + c.off), q,
+                                        nfull, c.len);
+                    }
+                }
+            }
+        }
+    }
+    if (KIND == 2) block_max_to(maxbits, wave_max, bound_bits + c.tensor);
+}
+
 __global__ __launch_bounds__(kBlockThreads) void k_fill_u32(uint32_t* __restrict__ p, int count,
                                                            uint32_t value) {
     const int i = blockIdx.x * kBlockThreads + threadIdx.x;
@@ -478,20 +597,81 @@ hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float* m
 }
 
 hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_rep,
-                              const float* g_rep, float* s1, float* s2, int64_t stride,
-                              int worker0, int n_workers, const AdamScalars& sc, hipStream_t st) {
+                              const float* x_src, int64_t src_stride, const float* g_rep,
+                              float* s1, float* s2, int64_t stride, int worker0, int n_workers,
+                              const AdamScalars& sc, hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_local_adamw, chunk_grid(n_chunks, n_workers), dim3(kBlockThreads), 0, st,
-                       chunks, x_rep, g_rep, s1, s2, stride, worker0, sc);
+                       chunks, x_rep, x_src, src_stride, g_rep, s1, s2, stride, worker0, sc);
     return hipGetLastError();
 }
 
 hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep,
-                             const float* g_rep, float* s1, int64_t stride, int worker0,
-                             int n_workers, const SgdScalars& sc, hipStream_t st) {
+                             const float* x_src, int64_t src_stride, const float* g_rep,
+                             float* s1, int64_t stride, int worker0, int n_workers,
+                             const SgdScalars& sc, hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_local_sgdm, chunk_grid(n_chunks, n_workers), dim3(kBlockThreads), 0, st,
-                       chunks, x_rep, g_rep, s1, stride, worker0, sc);
+                       chunks, x_rep, x_src, src_stride, g_rep, s1, stride, worker0, sc);
+    return hipGetLastError();
+}
+
+template <int BASE, int KIND>
+static void launch_round_end_n(const Chunk* chunks, int64_t n_chunks, const RoundEndArgs& a,
+                               hipStream_t st) {
+    const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
+#define DSM_ROUND_END(NW)                                                                        \
+    hipLaunchKernelGGL((k_round_end<NW, BASE, KIND>), grid, block, 0, st, chunks, a.x, a.m,      \
+                       a.x_rep, a.x_src, a.src_stride, a.g_rep, a.s1, a.s2, a.u, a.bound_bits,  \
+                       a.stride, a.as, a.ss, a.gs)
+    switch (a.gs.n) {
+        case 1: DSM_ROUND_END(1); break;
+        case 2: DSM_ROUND_END(2); break;
+        case 4: DSM_ROUND_END(4); break;
+        case 8: DSM_ROUND_END(8); break;
+        default: DSM_ROUND_END(0); break;
+    }
+#undef DSM_ROUND_END
+}
+
+template <int BASE>
+static void launch_round_end_base(const Chunk* chunks, int64_t n_chunks, const RoundEndArgs& a,
+                                  int kind, hipStream_t st) {
+    if (kind == 0)
+        launch_round_end_n<BASE, 0>(chunks, n_chunks, a, st);
+    else if (kind == 1)
+        launch_round_end_n<BASE, 1>(chunks, n_chunks, a, st);
+    else
+        launch_round_end_n<BASE, 2>(chunks, n_chunks, a, st);
+}
+
+hipError_t launch_round_end(const Chunk* chunks, int64_t n_chunks, int n_tensors, bool adamw,
+                            const RoundEndArgs& a, bool broadcast, hipStream_t st) {
+    const bool randomized = a.gs.mode != 0;
+    if (randomized && n_tensors > 0) {
+        hipLaunchKernelGGL(k_fill_u32, dim3((n_tensors + kBlockThreads - 1) / kBlockThreads),
+                           dim3(kBlockThreads), 0, st, a.bound_bits, n_tensors, 0u);
+    }
+    if (n_chunks == 0) return hipGetLastError();
+    const int kind = randomized ? 2 : (broadcast ? 1 : 0);
+    if (adamw)
+        launch_round_end_base<kBaseAdamW>(chunks, n_chunks, a, kind, st);
+    else
+        launch_round_end_base<kBaseSgd>(chunks, n_chunks, a, kind, st);
+    if (randomized) {
+        const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
+        if (a.gs.mode == 1) {
+            if (broadcast)
+                hipLaunchKernelGGL((k_global_rand_pass2<1, true>), grid, block, 0, st, chunks, a.x, a.x_rep, a.u, a.bound_bits, a.stride, a.gs);
+            else
+                hipLaunchKernelGGL((k_global_rand_pass2<1, false>), grid, block, 0, st, chunks, a.x, a.x_rep, a.u, a.bound_bits, a.stride, a.gs);
+        } else {
+            if (broadcast)
+                hipLaunchKernelGGL((k_global_rand_pass2<2, true>), grid, block, 0, st, chunks, a.x, a.x_rep, a.u, a.bound_bits, a.stride, a.gs);
+            else
+                hipLaunchKernelGGL((k_global_rand_pass2<2, false>), grid, block, 0, st, chunks, a.x, a.x_rep, a.u, a.bound_bits, a.stride, a.gs);
+        }
+    }
     return hipGetLastError();
 }
 

@@ -25,7 +25,8 @@ struct dsm_ctx {
     uint32_t* d_bounds = nullptr;
     hipStream_t stream = nullptr;
     std::vector<int> local_count;  // local steps per worker since the last synchronisation
-    bool synced = true;            // every replica equals x
+    std::vector<uint8_t> stale;    // replica not yet reset to x after a global step
+                                   // without broadcast: its next local step reads x
     bool bounds_valid = false;     // the last global step was randomized
     std::string last_error;
 };
@@ -151,6 +152,107 @@ dsm_status check_device(dsm_ctx* ctx) {
     return DSM_OK;
 }
 
+struct LocalCoefs {
+    dsm::AdamScalars adam{};
+    dsm::SgdScalars sgd{};
+};
+
+// Validates the local hyperparameters and forms the fp32 coefficients of one
+// local step (fp64, rounded once).
+dsm_status local_coefs(dsm_ctx* ctx, const dsm_local_hparams* hp, int64_t step, LocalCoefs* out) {
+    if (!hp) return fail(ctx, DSM_ERR_INVALID_ARG, "local hyperparameters are NULL");
+    if (!(std::isfinite(hp->lr) && hp->lr > 0.0f))
+        return fail(ctx, DSM_ERR_INVALID_ARG, "lr must be finite and > 0");
+    if (!finite_in(hp->beta1, 0.0f, 1.0f))
+        return fail(ctx, DSM_ERR_INVALID_ARG, "beta1 must be in [0, 1]");
+    if (ctx->base == DSM_BASE_ADAMW) {
+        if (step < 1) return fail(ctx, DSM_ERR_INVALID_ARG, "step must be >= 1, got %lld",
+                                  static_cast<long long>(step));
+        if (!finite_in(hp->beta2, 0.0f, 1.0f))
+            return fail(ctx, DSM_ERR_INVALID_ARG, "beta2 must be in [0, 1]");
+        if (!(std::isfinite(hp->eps) && hp->eps >= 0.0f))
+            return fail(ctx, DSM_ERR_INVALID_ARG, "eps must be finite and >= 0");
+        if (!(std::isfinite(hp->weight_decay) && hp->weight_decay >= 0.0f))
+            return fail(ctx, DSM_ERR_INVALID_ARG, "weight_decay must be finite and >= 0");
+        if (hp->beta1 == 1.0f || hp->beta2 == 1.0f)
+            return fail(ctx, DSM_ERR_INVALID_ARG, "AdamW needs beta1, beta2 < 1 (bias correction)");
+        const double b1 = hp->beta1, b2 = hp->beta2;
+        dsm::AdamScalars& sc = out->adam;
+        sc.beta1 = hp->beta1;
+        sc.beta2 = hp->beta2;
+        sc.one_minus_beta1 = static_cast<float>(1.0 - b1);
+        sc.one_minus_beta2 = static_cast<float>(1.0 - b2);
+        sc.bc1 = static_cast<float>(1.0 - beta_power(b1, step));
+        sc.bc2 = static_cast<float>(1.0 - beta_power(b2, step));
+        sc.lr = hp->lr;
+        sc.eps = hp->eps;
+        sc.wd = hp->weight_decay;
+    } else {
+        out->sgd = dsm::SgdScalars{hp->beta1, hp->lr};
+    }
+    return DSM_OK;
+}
+
+// Validates the global hyperparameters and forms the fp32 coefficients of
+// Eqs. (6)-(8) (fp64, rounded once).
+dsm_status global_coefs(dsm_ctx* ctx, int64_t t, const dsm_global_hparams* hp,
+                        dsm::GlobalScalars* out) {
+    if (!hp) return fail(ctx, DSM_ERR_INVALID_ARG, "global hyperparameters are NULL");
+    if (t < 0 || t >= (int64_t(1) << 32))
+        return fail(ctx, DSM_ERR_INVALID_ARG, "t must be in [0, 2^32), got %lld", static_cast<long long>(t));
+    if (!(std::isfinite(hp->gamma) && hp->gamma > 0.0f))
+        return fail(ctx, DSM_ERR_INVALID_ARG, "gamma must be finite and > 0");
+    if (!(std::isfinite(hp->eta) && hp->eta >= 0.0f))
+        return fail(ctx, DSM_ERR_INVALID_ARG, "eta must be finite and >= 0");
+    if (!finite_in(hp->beta1, 0.0f, 1.0f) || !finite_in(hp->beta2, 0.0f, 1.0f))
+        return fail(ctx, DSM_ERR_INVALID_ARG, "beta1 and beta2 must be in [0, 1]");
+    if (!(std::isfinite(hp->lambda) && hp->lambda >= 0.0f))
+        return fail(ctx, DSM_ERR_INVALID_ARG, "lambda must be finite and >= 0");
+    if (hp->mode != DSM_SIGN_DET && hp->mode != DSM_SIGN_RAND_FLIP && hp->mode != DSM_SIGN_RAND_ZERO)
+        return fail(ctx, DSM_ERR_INVALID_ARG, "unknown sign mode %d", hp->mode);
+    if (hp->mode != DSM_SIGN_DET && ctx->arena_elems > 0 && !ctx->buf.u_scratch)
+        return fail(ctx, DSM_ERR_INVALID_ARG, "the randomized sign needs buffers.u_scratch");
+    dsm::GlobalScalars& sc = *out;
+    const double gamma = hp->gamma;
+    sc.beta1 = hp->beta1;
+    sc.beta2 = hp->beta2;
+    sc.c1 = static_cast<float>((1.0 - static_cast<double>(hp->beta1)) / gamma);
+    sc.c2 = static_cast<float>((1.0 - static_cast<double>(hp->beta2)) / gamma);
+    sc.step = static_cast<float>(static_cast<double>(hp->eta) * gamma);
+    sc.lam = hp->lambda;
+    sc.n = ctx->n;
+    sc.n_pow2 = (ctx->n & (ctx->n - 1)) == 0 ? 1 : 0;
+    sc.inv_n = static_cast<float>(1.0 / ctx->n);
+    sc.n_f = static_cast<float>(ctx->n);
+    sc.key0 = static_cast<uint32_t>(hp->seed & 0xFFFFFFFFu);
+    sc.key1 = static_cast<uint32_t>(hp->seed >> 32);
+    sc.t = static_cast<uint32_t>(t);
+    sc.mode = hp->mode;
+    return DSM_OK;
+}
+
+hipError_t launch_local(dsm_ctx* ctx, const LocalCoefs& lc, const float* src, int64_t src_stride,
+                        int w0, int nw) {
+    const int64_t n_chunks = static_cast<int64_t>(ctx->chunks.size());
+    if (ctx->base == DSM_BASE_ADAMW)
+        return dsm::launch_local_adamw(ctx->d_chunks, n_chunks, ctx->buf.x_rep, src, src_stride,
+                                       ctx->buf.g_rep, ctx->buf.s1_rep, ctx->buf.s2_rep,
+                                       ctx->arena_elems, w0, nw, lc.adam, ctx->stream);
+    return dsm::launch_local_sgdm(ctx->d_chunks, n_chunks, ctx->buf.x_rep, src, src_stride,
+                                  ctx->buf.g_rep, ctx->buf.s1_rep, ctx->arena_elems, w0, nw, lc.sgd,
+                                  ctx->stream);
+}
+
+// After a global step: the round's local counts restart; without broadcast
+// every replica is stale until its worker's next local step.
+void end_round(dsm_ctx* ctx, bool broadcast, bool randomized) {
+    for (int i = 0; i < ctx->n; ++i) {
+        ctx->local_count[i] = 0;
+        ctx->stale[i] = broadcast ? 0 : 1;
+    }
+    ctx->bounds_valid = randomized;
+}
+
 }  // namespace
 
 extern "C" {
@@ -226,6 +328,7 @@ dsm_status dsm_init(const dsm_problem* problem, const dsm_buffers* b, dsm_ctx** 
     ctx->d_chunks = static_cast<dsm::Chunk*>(b->workspace);
     ctx->d_bounds = reinterpret_cast<uint32_t*>(static_cast<char*>(b->workspace) + L.bounds_off);
     ctx->local_count.assign(ctx->n, 0);
+    ctx->stale.assign(ctx->n, 0);
 
     if (!ctx->chunks.empty()) {
         hipError_t e = hipMemcpyAsync(ctx->d_chunks, ctx->chunks.data(),
@@ -252,30 +355,11 @@ dsm_status dsm_init(const dsm_problem* problem, const dsm_buffers* b, dsm_ctx** 
 dsm_status dsm_local_step(dsm_ctx* ctx, int32_t worker, int64_t step, const dsm_local_hparams* hp) {
     dsm_status st = check_ctx(ctx);
     if (st != DSM_OK) return st;
-    if (!hp) return fail(ctx, DSM_ERR_INVALID_ARG, "hyperparameters are NULL");
     if (worker < -1 || worker >= ctx->n)
         return fail(ctx, DSM_ERR_INVALID_ARG, "worker must be -1 or in [0, %d), got %d", ctx->n, worker);
-    if (!(std::isfinite(hp->lr) && hp->lr > 0.0f))
-        return fail(ctx, DSM_ERR_INVALID_ARG, "lr must be finite and > 0");
-    if (!finite_in(hp->beta1, 0.0f, 1.0f))
-        return fail(ctx, DSM_ERR_INVALID_ARG, "beta1 must be in [0, 1]");
-    const bool adamw = ctx->base == DSM_BASE_ADAMW;
-    if (adamw) {
-        if (step < 1) return fail(ctx, DSM_ERR_INVALID_ARG, "step must be >= 1, got %lld",
-                                  static_cast<long long>(step));
-        if (!finite_in(hp->beta2, 0.0f, 1.0f))
-            return fail(ctx, DSM_ERR_INVALID_ARG, "beta2 must be in [0, 1]");
-        if (!(std::isfinite(hp->eps) && hp->eps >= 0.0f))
-            return fail(ctx, DSM_ERR_INVALID_ARG, "eps must be finite and >= 0");
-        if (!(std::isfinite(hp->weight_decay) && hp->weight_decay >= 0.0f))
-            return fail(ctx, DSM_ERR_INVALID_ARG, "weight_decay must be finite and >= 0");
-        if (hp->beta1 == 1.0f || hp->beta2 == 1.0f)
-            return fail(ctx, DSM_ERR_INVALID_ARG, "AdamW needs beta1, beta2 < 1 (bias correction)");
-    }
-    if (!ctx->synced)
-        return fail(ctx, DSM_ERR_STATE,
-                    "replicas are not synchronised: the last global step had broadcast = 0; "
-                    "call dsm_sync first");
+    LocalCoefs lc;
+    st = local_coefs(ctx, hp, step, &lc);
+    if (st != DSM_OK) return st;
     const int w0 = worker < 0 ? 0 : worker;
     const int nw = worker < 0 ? ctx->n : 1;
     for (int i = w0; i < w0 + nw; ++i) {
@@ -284,76 +368,39 @@ dsm_status dsm_local_step(dsm_ctx* ctx, int32_t worker, int64_t step, const dsm_
                         "worker %d already took H = %d local steps this round; take the global step",
                         i, ctx->H);
     }
-    const int64_t n_chunks = static_cast<int64_t>(ctx->chunks.size());
-    hipError_t e;
-    if (adamw) {
-        dsm::AdamScalars sc{};
-        const double b1 = hp->beta1, b2 = hp->beta2;
-        sc.beta1 = hp->beta1;
-        sc.beta2 = hp->beta2;
-        sc.one_minus_beta1 = static_cast<float>(1.0 - b1);
-        sc.one_minus_beta2 = static_cast<float>(1.0 - b2);
-        sc.bc1 = static_cast<float>(1.0 - beta_power(b1, step));
-        sc.bc2 = static_cast<float>(1.0 - beta_power(b2, step));
-        sc.lr = hp->lr;
-        sc.eps = hp->eps;
-        sc.wd = hp->weight_decay;
-        e = dsm::launch_local_adamw(ctx->d_chunks, n_chunks, ctx->buf.x_rep, ctx->buf.g_rep,
-                                    ctx->buf.s1_rep, ctx->buf.s2_rep, ctx->arena_elems, w0, nw, sc,
-                                    ctx->stream);
-    } else {
-        dsm::SgdScalars sc{hp->beta1, hp->lr};
-        e = dsm::launch_local_sgdm(ctx->d_chunks, n_chunks, ctx->buf.x_rep, ctx->buf.g_rep,
-                                   ctx->buf.s1_rep, ctx->arena_elems, w0, nw, sc, ctx->stream);
+    // Workers whose replica is stale read the global model (the
+    // synchronisation step folded into their first local step).  One launch
+    // per run of consecutive workers with the same source.
+    for (int a = w0; a < w0 + nw;) {
+        int b = a + 1;
+        while (b < w0 + nw && ctx->stale[b] == ctx->stale[a]) ++b;
+        const bool from_x = ctx->stale[a] != 0;
+        const float* src = from_x ? ctx->buf.x : ctx->buf.x_rep;
+        const int64_t src_stride = from_x ? 0 : ctx->arena_elems;
+        hipError_t e = launch_local(ctx, lc, src, src_stride, a, b - a);
+        if (e != hipSuccess) return hip_fail(ctx, "launching the local step", e);
+        a = b;
     }
-    if (e != hipSuccess) return hip_fail(ctx, "launching the local step", e);
-    for (int i = w0; i < w0 + nw; ++i) ctx->local_count[i] += 1;
+    for (int i = w0; i < w0 + nw; ++i) {
+        ctx->local_count[i] += 1;
+        ctx->stale[i] = 0;
+    }
     return DSM_OK;
 }
 
 dsm_status dsm_global_step(dsm_ctx* ctx, int64_t t, const dsm_global_hparams* hp, int32_t broadcast) {
     dsm_status st = check_ctx(ctx);
     if (st != DSM_OK) return st;
-    if (!hp) return fail(ctx, DSM_ERR_INVALID_ARG, "hyperparameters are NULL");
-    if (t < 0 || t >= (int64_t(1) << 32))
-        return fail(ctx, DSM_ERR_INVALID_ARG, "t must be in [0, 2^32), got %lld", static_cast<long long>(t));
-    if (!(std::isfinite(hp->gamma) && hp->gamma > 0.0f))
-        return fail(ctx, DSM_ERR_INVALID_ARG, "gamma must be finite and > 0");
-    if (!(std::isfinite(hp->eta) && hp->eta >= 0.0f))
-        return fail(ctx, DSM_ERR_INVALID_ARG, "eta must be finite and >= 0");
-    if (!finite_in(hp->beta1, 0.0f, 1.0f) || !finite_in(hp->beta2, 0.0f, 1.0f))
-        return fail(ctx, DSM_ERR_INVALID_ARG, "beta1 and beta2 must be in [0, 1]");
-    if (!(std::isfinite(hp->lambda) && hp->lambda >= 0.0f))
-        return fail(ctx, DSM_ERR_INVALID_ARG, "lambda must be finite and >= 0");
-    if (hp->mode != DSM_SIGN_DET && hp->mode != DSM_SIGN_RAND_FLIP && hp->mode != DSM_SIGN_RAND_ZERO)
-        return fail(ctx, DSM_ERR_INVALID_ARG, "unknown sign mode %d", hp->mode);
-    const bool randomized = hp->mode != DSM_SIGN_DET;
-    if (randomized && ctx->arena_elems > 0 && !ctx->buf.u_scratch)
-        return fail(ctx, DSM_ERR_INVALID_ARG, "the randomized sign needs buffers.u_scratch");
-    if (!ctx->synced)
-        return fail(ctx, DSM_ERR_STATE, "replicas are not synchronised; call dsm_sync first");
+    dsm::GlobalScalars sc{};
+    st = global_coefs(ctx, t, hp, &sc);
+    if (st != DSM_OK) return st;
     for (int i = 0; i < ctx->n; ++i) {
         if (ctx->local_count[i] != ctx->H)
             return fail(ctx, DSM_ERR_STATE,
                         "worker %d took %d of H = %d local steps; the global step needs all H",
                         i, ctx->local_count[i], ctx->H);
     }
-    dsm::GlobalScalars sc{};
-    const double gamma = hp->gamma;
-    sc.beta1 = hp->beta1;
-    sc.beta2 = hp->beta2;
-    sc.c1 = static_cast<float>((1.0 - static_cast<double>(hp->beta1)) / gamma);
-    sc.c2 = static_cast<float>((1.0 - static_cast<double>(hp->beta2)) / gamma);
-    sc.step = static_cast<float>(static_cast<double>(hp->eta) * gamma);
-    sc.lam = hp->lambda;
-    sc.n = ctx->n;
-    sc.n_pow2 = (ctx->n & (ctx->n - 1)) == 0 ? 1 : 0;
-    sc.inv_n = static_cast<float>(1.0 / ctx->n);
-    sc.n_f = static_cast<float>(ctx->n);
-    sc.key0 = static_cast<uint32_t>(hp->seed & 0xFFFFFFFFu);
-    sc.key1 = static_cast<uint32_t>(hp->seed >> 32);
-    sc.t = static_cast<uint32_t>(t);
-    sc.mode = hp->mode;
+    const bool randomized = hp->mode != DSM_SIGN_DET;
     const int64_t n_chunks = static_cast<int64_t>(ctx->chunks.size());
     hipError_t e;
     if (!randomized) {
@@ -365,9 +412,51 @@ dsm_status dsm_global_step(dsm_ctx* ctx, int64_t t, const dsm_global_hparams* hp
                                     ctx->arena_elems, sc, broadcast != 0, ctx->stream);
     }
     if (e != hipSuccess) return hip_fail(ctx, "launching the global step", e);
-    for (int i = 0; i < ctx->n; ++i) ctx->local_count[i] = 0;
-    ctx->synced = broadcast != 0;
-    ctx->bounds_valid = randomized;
+    end_round(ctx, broadcast != 0, randomized);
+    return DSM_OK;
+}
+
+dsm_status dsm_round_end(dsm_ctx* ctx, int64_t step, const dsm_local_hparams* local_hp, int64_t t,
+                         const dsm_global_hparams* global_hp, int32_t broadcast) {
+    dsm_status st = check_ctx(ctx);
+    if (st != DSM_OK) return st;
+    LocalCoefs lc;
+    st = local_coefs(ctx, local_hp, step, &lc);
+    if (st != DSM_OK) return st;
+    dsm::GlobalScalars gs{};
+    st = global_coefs(ctx, t, global_hp, &gs);
+    if (st != DSM_OK) return st;
+    for (int i = 0; i < ctx->n; ++i) {
+        if (ctx->local_count[i] != ctx->H - 1)
+            return fail(ctx, DSM_ERR_STATE,
+                        "worker %d took %d local steps; dsm_round_end takes step H = %d and needs "
+                        "H - 1 taken", i, ctx->local_count[i], ctx->H);
+    }
+    // With H - 1 >= 1 steps taken every replica is fresh; with H = 1 the
+    // replicas are all stale or all fresh (no local step since the last
+    // global step or synchronisation).
+    const bool from_x = ctx->stale[0] != 0;
+    dsm::RoundEndArgs a{};
+    a.x = ctx->buf.x;
+    a.m = ctx->buf.m;
+    a.x_rep = ctx->buf.x_rep;
+    a.x_src = from_x ? ctx->buf.x : ctx->buf.x_rep;
+    a.src_stride = from_x ? 0 : ctx->arena_elems;
+    a.g_rep = ctx->buf.g_rep;
+    a.s1 = ctx->buf.s1_rep;
+    a.s2 = ctx->buf.s2_rep;
+    a.u = ctx->buf.u_scratch;
+    a.bound_bits = ctx->d_bounds;
+    a.stride = ctx->arena_elems;
+    a.as = lc.adam;
+    a.ss = lc.sgd;
+    a.gs = gs;
+    const bool randomized = global_hp->mode != DSM_SIGN_DET;
+    hipError_t e = dsm::launch_round_end(ctx->d_chunks, static_cast<int64_t>(ctx->chunks.size()),
+                                         ctx->n_tensors, ctx->base == DSM_BASE_ADAMW, a,
+                                         broadcast != 0, ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, "launching the fused round end", e);
+    end_round(ctx, broadcast != 0, randomized);
     return DSM_OK;
 }
 
@@ -378,8 +467,10 @@ dsm_status dsm_sync(dsm_ctx* ctx) {
                                          ctx->buf.x, ctx->buf.x_rep, ctx->arena_elems, ctx->n,
                                          ctx->stream);
     if (e != hipSuccess) return hip_fail(ctx, "launching the synchronisation", e);
-    for (int i = 0; i < ctx->n; ++i) ctx->local_count[i] = 0;
-    ctx->synced = true;
+    for (int i = 0; i < ctx->n; ++i) {
+        ctx->local_count[i] = 0;
+        ctx->stale[i] = 0;
+    }
     return DSM_OK;
 }
 

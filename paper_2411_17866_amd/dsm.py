@@ -28,7 +28,8 @@ DSM_SIGN_DET = 0
 DSM_SIGN_RAND_FLIP = 1
 DSM_SIGN_RAND_ZERO = 2
 
-EXPORTED = ("dsm_layout", "dsm_init", "dsm_local_step", "dsm_global_step", "dsm_sync",
+EXPORTED = ("dsm_layout", "dsm_init", "dsm_local_step", "dsm_global_step", "dsm_round_end",
+            "dsm_sync",
             "dsm_read_bounds", "dsm_test_philox", "dsm_destroy", "dsm_last_error")
 
 
@@ -85,6 +86,9 @@ def load_library(path=LIBPATH):
                                    ctypes.POINTER(dsm_local_hparams)]
     lib.dsm_global_step.argtypes = [ctypes.c_void_p, ctypes.c_int64,
                                     ctypes.POINTER(dsm_global_hparams), ctypes.c_int32]
+    lib.dsm_round_end.argtypes = [ctypes.c_void_p, ctypes.c_int64,
+                                  ctypes.POINTER(dsm_local_hparams), ctypes.c_int64,
+                                  ctypes.POINTER(dsm_global_hparams), ctypes.c_int32]
     lib.dsm_sync.argtypes = [ctypes.c_void_p]
     lib.dsm_read_bounds.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_float)]
     lib.dsm_test_philox.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int64,
@@ -151,6 +155,16 @@ def dsm_global_step(ctx, t, gamma, eta, beta1, beta2, lam, mode=DSM_SIGN_DET, se
                     broadcast=True):
     hp = dsm_global_hparams(gamma, eta, beta1, beta2, lam, mode, seed)
     _check(load_library().dsm_global_step(ctx, t, ctypes.byref(hp), 1 if broadcast else 0), ctx)
+
+
+def dsm_round_end(ctx, step, local, t, gamma, eta, beta1, beta2, lam, mode=DSM_SIGN_DET, seed=0,
+                  broadcast=True):
+    """local: dict of dsm_local_hparams fields (lr, beta1, beta2, eps, weight_decay)."""
+    lhp = dsm_local_hparams(local["lr"], local["beta1"], local.get("beta2", 0.0),
+                            local.get("eps", 0.0), local.get("weight_decay", 0.0))
+    ghp = dsm_global_hparams(gamma, eta, beta1, beta2, lam, mode, seed)
+    _check(load_library().dsm_round_end(ctx, step, ctypes.byref(lhp), t, ctypes.byref(ghp),
+                                        1 if broadcast else 0), ctx)
 
 
 def dsm_sync(ctx):
