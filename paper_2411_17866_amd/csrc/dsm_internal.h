@@ -17,6 +17,21 @@ namespace dsm {
 constexpr int kChunkElems = DSM_CHUNK_ELEMS;
 static_assert(kChunkElems % 1024 == 0, "chunk must be a multiple of 256 threads x 4");
 constexpr int kBlockThreads = 256;
+// float4 groups per stream in flight per thread, and loop iterations per
+// work-group: a work-group takes one piece of kBlockThreads * kUnroll *
+// kIters float4 groups of a chunk (build-time tuning knobs).
+#ifndef DSM_UNROLL
+#define DSM_UNROLL 1
+#endif
+#ifndef DSM_ITERS
+#define DSM_ITERS 2
+#endif
+constexpr int kUnroll = DSM_UNROLL;
+constexpr int kIters = DSM_ITERS;
+constexpr int kPieceVec = kBlockThreads * kUnroll * kIters;
+static_assert((kChunkElems / 4) % kPieceVec == 0, "a chunk must split into whole pieces");
+// Work-groups per chunk.
+constexpr int kSplit = (kChunkElems / 4) / kPieceVec;
 // Arena alignment of every tensor, in elements (256 bytes).
 constexpr int64_t kTensorAlign = 64;
 constexpr int kMaxWorkers = 64;

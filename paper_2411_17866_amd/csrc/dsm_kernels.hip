@@ -23,15 +23,10 @@ namespace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-// float4 groups per stream in flight per thread, and whether the streams use
-// nontemporal loads and stores (build-time tuning knobs).
-#ifndef DSM_UNROLL
-#define DSM_UNROLL 2
-#endif
+// Whether the streams use nontemporal loads and stores (build-time knob).
 #ifndef DSM_NT
 #define DSM_NT 1
 #endif
-constexpr int kUnroll = DSM_UNROLL;
 
 __device__ __forceinline__ f4 ntload(const f4* p) {
 #if DSM_NT
@@ -61,6 +56,26 @@ __device__ __forceinline__ void store_group(f4 v, f4* p, int q, int nfull, int l
         ntstore(v, p + q);
     else
         store_head(v, reinterpret_cast<float*>(p + q), len - 4 * q);
+}
+
+// The piece of a chunk this work-group processes: work-group b takes piece
+// b % kSplit of chunk b / kSplit, float4 groups [q_lo, q_hi).  Work-groups
+// are short-lived and dispatched in address order, so the addresses in
+// flight form one compact front across the arena.
+struct Piece {
+    Chunk c;
+    int q_lo, q_hi;  // float4 groups of the chunk handled here
+    int nfull;       // groups of four valid lanes in the chunk
+};
+
+__device__ __forceinline__ Piece piece_of(const Chunk* __restrict__ chunks) {
+    Piece pc;
+    pc.c = chunks[blockIdx.x / kSplit];
+    const int nvec = (pc.c.len + 3) >> 2;
+    pc.q_lo = static_cast<int>(blockIdx.x % kSplit) * kPieceVec;
+    pc.q_hi = min(nvec, pc.q_lo + kPieceVec);
+    pc.nfull = pc.c.len >> 2;
+    return pc;
 }
 
 // ---------------------------------------------------------------- AdamW
@@ -98,7 +113,8 @@ __global__ __launch_bounds__(kBlockThreads) void k_local_adamw(
     const Chunk* __restrict__ chunks, float* __restrict__ x_rep, const float* __restrict__ x_src,
     int64_t src_stride, const float* __restrict__ g_rep, float* __restrict__ s1,
     float* __restrict__ s2, int64_t stride, int worker0, AdamScalars sc) {
-    const Chunk c = chunks[blockIdx.x];
+    const Piece pc = piece_of(chunks);
+    const Chunk& c = pc.c;
     const int64_t w = worker0 + static_cast<int>(blockIdx.y);
     const int64_t base = w * stride + c.off;
     f4* __restrict__ xp = reinterpret_cast<f4*>(x_rep + base);
@@ -107,9 +123,9 @@ __global__ __launch_bounds__(kBlockThreads) void k_local_adamw(
     f4* __restrict__ mp = reinterpret_cast<f4*>(s1 + base);
     f4* __restrict__ vp = reinterpret_cast<f4*>(s2 + base);
     const float lam = c.decay ? sc.wd : 0.0f;
-    const int nvec = (c.len + 3) >> 2;
-    const int nfull = c.len >> 2;
-    for (int q0 = threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+    const int nvec = pc.q_hi;
+    const int nfull = pc.nfull;
+    for (int q0 = pc.q_lo + threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
         f4 xv[kUnroll], gv[kUnroll], mv[kUnroll], vv[kUnroll];
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
@@ -148,16 +164,17 @@ __global__ __launch_bounds__(kBlockThreads) void k_local_sgdm(
     const Chunk* __restrict__ chunks, float* __restrict__ x_rep, const float* __restrict__ x_src,
     int64_t src_stride, const float* __restrict__ g_rep, float* __restrict__ s1, int64_t stride,
     int worker0, SgdScalars sc) {
-    const Chunk c = chunks[blockIdx.x];
+    const Piece pc = piece_of(chunks);
+    const Chunk& c = pc.c;
     const int64_t w = worker0 + static_cast<int>(blockIdx.y);
     const int64_t base = w * stride + c.off;
     f4* __restrict__ xp = reinterpret_cast<f4*>(x_rep + base);
     const f4* __restrict__ xs = reinterpret_cast<const f4*>(x_src + w * src_stride + c.off);
     const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + base);
     f4* __restrict__ mp = reinterpret_cast<f4*>(s1 + base);
-    const int nvec = (c.len + 3) >> 2;
-    const int nfull = c.len >> 2;
-    for (int q0 = threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+    const int nvec = pc.q_hi;
+    const int nfull = pc.nfull;
+    for (int q0 = pc.q_lo + threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
         f4 xv[kUnroll], gv[kUnroll], mv[kUnroll];
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
@@ -237,15 +254,16 @@ template <int N, bool BCAST>
 __global__ __launch_bounds__(kBlockThreads) void k_global_det(
     const Chunk* __restrict__ chunks, float* __restrict__ x, float* __restrict__ m,
     float* __restrict__ x_rep, int64_t stride, GlobalScalars sc) {
-    const Chunk c = chunks[blockIdx.x];
+    const Piece pc = piece_of(chunks);
+    const Chunk& c = pc.c;
     const int n = N > 0 ? N : sc.n;
     f4* __restrict__ xp = reinterpret_cast<f4*>(x + c.off);
     f4* __restrict__ mp = reinterpret_cast<f4*>(m + c.off);
     float* __restrict__ rbase = x_rep + c.off;
     const float lam = c.decay ? sc.lam : 0.0f;
-    const int nvec = (c.len + 3) >> 2;
-    const int nfull = c.len >> 2;
-    for (int q0 = threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+    const int nvec = pc.q_hi;
+    const int nfull = pc.nfull;
+    for (int q0 = pc.q_lo + threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
         f4 xv[kUnroll], mv[kUnroll], dv[kUnroll];
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
@@ -294,7 +312,11 @@ __device__ __forceinline__ void block_max_to(uint32_t bits, uint32_t* wave_max, 
         uint32_t b = wave_max[0];
 #pragma unroll
         for (int w = 1; w < kBlockThreads / 64; ++w) b = wave_max[w] > b ? wave_max[w] : b;
-        atomicMax(dst, b);
+        // The bound only grows, so a work-group whose maximum does not exceed
+        // the value already stored has nothing to add; skipping its atomic
+        // keeps the many work-groups of a large tensor off one address.
+        const uint32_t cur = __hip_atomic_load(dst, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (b > cur) atomicMax(dst, b);
     }
 }
 
@@ -305,16 +327,17 @@ __global__ __launch_bounds__(kBlockThreads) void k_global_rand_pass1(
     const Chunk* __restrict__ chunks, const float* __restrict__ x, float* __restrict__ m,
     const float* __restrict__ x_rep, float* __restrict__ u_out, uint32_t* __restrict__ bound_bits,
     int64_t stride, GlobalScalars sc) {
-    const Chunk c = chunks[blockIdx.x];
+    const Piece pc = piece_of(chunks);
+    const Chunk& c = pc.c;
     const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + c.off);
     f4* __restrict__ mp = reinterpret_cast<f4*>(m + c.off);
     f4* __restrict__ up = reinterpret_cast<f4*>(u_out + c.off);
     const float* __restrict__ rbase = x_rep + c.off;
-    const int nvec = (c.len + 3) >> 2;
-    const int nfull = c.len >> 2;
+    const int nvec = pc.q_hi;
+    const int nfull = pc.nfull;
     __shared__ uint32_t wave_max[kBlockThreads / 64];
     uint32_t maxbits = 0;
-    for (int q0 = threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+    for (int q0 = pc.q_lo + threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
         f4 xv[kUnroll], mv[kUnroll], dv[kUnroll];
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
@@ -372,16 +395,17 @@ __global__ __launch_bounds__(kBlockThreads) void k_global_rand_pass2(
     const Chunk* __restrict__ chunks, float* __restrict__ x, float* __restrict__ x_rep,
     const float* __restrict__ u_in, const uint32_t* __restrict__ bound_bits, int64_t stride,
     GlobalScalars sc) {
-    const Chunk c = chunks[blockIdx.x];
+    const Piece pc = piece_of(chunks);
+    const Chunk& c = pc.c;
     f4* __restrict__ xp = reinterpret_cast<f4*>(x + c.off);
     const f4* __restrict__ up = reinterpret_cast<const f4*>(u_in + c.off);
     float* __restrict__ rbase = x_rep + c.off;
     const float lam = c.decay ? sc.lam : 0.0f;
     const double B = static_cast<double>(__uint_as_float(bound_bits[c.tensor]));
     const uint32_t blk0 = static_cast<uint32_t>(c.j0 >> 2);
-    const int nvec = (c.len + 3) >> 2;
-    const int nfull = c.len >> 2;
-    for (int q0 = threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+    const int nvec = pc.q_hi;
+    const int nfull = pc.nfull;
+    for (int q0 = pc.q_lo + threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
         f4 xv[kUnroll], uv[kUnroll];
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
@@ -432,16 +456,17 @@ __global__ __launch_bounds__(kBlockThreads) void k_round_end(
     float* __restrict__ u_out, uint32_t* __restrict__ bound_bits, int64_t stride,
     AdamScalars as, SgdScalars ss, GlobalScalars gs) {
     __shared__ uint32_t wave_max[kBlockThreads / 64];
-    const Chunk c = chunks[blockIdx.x];
+    const Piece pc = piece_of(chunks);
+    const Chunk& c = pc.c;
     const int n = N > 0 ? N : gs.n;
     f4* __restrict__ xp = reinterpret_cast<f4*>(x + c.off);
     f4* __restrict__ mp = reinterpret_cast<f4*>(m + c.off);
     const float lam_local = c.decay ? as.wd : 0.0f;
     const float lam = c.decay ? gs.lam : 0.0f;
-    const int nvec = (c.len + 3) >> 2;
-    const int nfull = c.len >> 2;
+    const int nvec = pc.q_hi;
+    const int nfull = pc.nfull;
     uint32_t maxbits = 0;
-    for (int q0 = threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+    for (int q0 = pc.q_lo + threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
         f4 xv[kUnroll], mv[kUnroll], acc[kUnroll];
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
@@ -532,12 +557,13 @@ __global__ __launch_bounds__(kBlockThreads) void k_fill_u32(uint32_t* __restrict
 __global__ __launch_bounds__(kBlockThreads) void k_broadcast(
     const Chunk* __restrict__ chunks, const float* __restrict__ x, float* __restrict__ x_rep,
     int64_t stride, int n) {
-    const Chunk c = chunks[blockIdx.x];
+    const Piece pc = piece_of(chunks);
+    const Chunk& c = pc.c;
     const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + c.off);
     float* __restrict__ rbase = x_rep + c.off;
-    const int nvec = (c.len + 3) >> 2;
-    const int nfull = c.len >> 2;
-    for (int q = threadIdx.x; q < nvec; q += kBlockThreads) {
+    const int nvec = pc.q_hi;
+    const int nfull = pc.nfull;
+    for (int q = pc.q_lo + threadIdx.x; q < nvec; q += kBlockThreads) {
         const f4 v = ntload(xp + q);
         for (int i = 0; i < n; ++i)
             store_group(v, reinterpret_cast<f4*>(rbase + i * stride), q, nfull, c.len);
@@ -549,12 +575,13 @@ __global__ __launch_bounds__(kBlockThreads) void k_init(
     const Chunk* __restrict__ chunks, const float* __restrict__ x, float* __restrict__ m,
     float* __restrict__ x_rep, float* __restrict__ s1, float* __restrict__ s2, int64_t stride,
     int n) {
-    const Chunk c = chunks[blockIdx.x];
+    const Piece pc = piece_of(chunks);
+    const Chunk& c = pc.c;
     const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + c.off);
-    const int nvec = (c.len + 3) >> 2;
-    const int nfull = c.len >> 2;
+    const int nvec = pc.q_hi;
+    const int nfull = pc.nfull;
     const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
-    for (int q = threadIdx.x; q < nvec; q += kBlockThreads) {
+    for (int q = pc.q_lo + threadIdx.x; q < nvec; q += kBlockThreads) {
         const f4 v = ntload(xp + q);
         store_group(zero, reinterpret_cast<f4*>(m + c.off), q, nfull, c.len);
         for (int i = 0; i < n; ++i) {
@@ -581,7 +608,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_test_philox(uint32_t key0, ui
 }
 
 dim3 chunk_grid(int64_t n_chunks, int n_workers) {
-    return dim3(static_cast<unsigned>(n_chunks), static_cast<unsigned>(n_workers), 1);
+    return dim3(static_cast<unsigned>(n_chunks * kSplit), static_cast<unsigned>(n_workers), 1);
 }
 
 }  // namespace

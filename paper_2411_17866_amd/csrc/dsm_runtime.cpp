@@ -36,7 +36,9 @@ namespace {
 thread_local std::string g_last_error;
 
 constexpr int64_t kMaxNumel = int64_t(1) << 34;
-constexpr int64_t kMaxChunks = (int64_t(1) << 24) - 1;
+// A launch has n_chunks * kSplit work-groups of kBlockThreads threads per
+// grid row, and a grid dimension holds fewer than 2^32 threads.
+constexpr int64_t kMaxChunks = ((int64_t(1) << 32) / dsm::kBlockThreads - 1) / dsm::kSplit;
 
 dsm_status fail(dsm_ctx* ctx, dsm_status st, const char* fmt, ...) {
     char msg[512];
