@@ -6,6 +6,7 @@ library and never imports it.
 """
 from .dsm_oracle import (  # noqa: F401
     PRECISIONS, SIGN_DET, SIGN_RAND_FLIP, SIGN_RAND_ZERO, PHILOX_STREAM,
+    RULE_SIGN_MOMENTUM, RULE_LOOKAHEAD, RULE_SIGNED_SLOWMO, RULE_GLOBAL_ADAMW,
     beta_power, communication_round, f32, global_step, init_state,
     local_adamw_step, local_sgdm_step, local_steps, randomized_sign,
     randomized_sign_uniforms, randomized_sign_uniforms_at, sign, synchronize,

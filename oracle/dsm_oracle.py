@@ -66,6 +66,13 @@ SIGN_RAND_FLIP = 1   # Eq. (9): -sign w.p. 1/2 - |v|/2B, sign w.p. 1/2 + |v|/2B
 SIGN_RAND_ZERO = 2   # Eq. (10): 0 w.p. 1 - |v|/B, sign w.p. |v|/B
 
 PHILOX_STREAM = 1    # fourth counter word of the randomized-sign stream
+
+# Global-step rules: the method's sign momentum and the ablation variants of
+# Section 4.1 and Appendix C.
+RULE_SIGN_MOMENTUM = 0   # Eqs. (6)-(8)
+RULE_LOOKAHEAD = 1       # Eq. (7) replaced by x - eta gamma u (Section 4.1)
+RULE_SIGNED_SLOWMO = 2   # Eqs. (6), (7) with sign on the difference (Section 4.1)
+RULE_GLOBAL_ADAMW = 3    # Algorithm 7 (Appendix C)
 _TWO24 = 16777216.0
 
 
@@ -228,7 +235,7 @@ def randomized_sign(u, B, k, variant):
 
 def global_step(x, m, replicas, *, gamma, eta, beta1, beta2, lam, decay,
                 t=0, mode=SIGN_DET, seed=0, prec="fp64", tensor_ids=None,
-                element_ids=None, bounds=None):
+                element_ids=None, bounds=None, rule=RULE_SIGN_MOMENTUM, v=None, eps=1e-8):
     """Algorithm 1 global step for a model given as a list of tensors.
 
     x:        list of arrays, x_{t,0} per tensor.
@@ -244,9 +251,24 @@ def global_step(x, m, replicas, *, gamma, eta, beta1, beta2, lam, decay,
     bounds:      per entry, B_p of the whole tensor (default: max |u| over
                  the entry, which is B_p when the entry is the whole tensor).
 
+    rule:     the global update (deterministic sign only for the variants):
+      RULE_SIGN_MOMENTUM  Eqs. (6)-(8).
+      RULE_LOOKAHEAD      Section 4.1: Eq. (7) replaced by
+                          x_{t+1,0} = x_{t,0} - eta gamma_t (u_{t+1} + lambda x_{t,0});
+                          lambda = 0 is the paper's Lookahead.
+      RULE_SIGNED_SLOWMO  Section 4.1: u_{t+1} = beta1 m_t + (1-beta1)/gamma_t
+                          sign(x_{t,0} - x_{t,tau}); x_{t+1,0} = x_{t,0} - eta gamma_t
+                          (u_{t+1} + lambda x_{t,0}); Eq. (8) unchanged.
+      RULE_GLOBAL_ADAMW   Algorithm 7: AdamW on the pseudo-gradient
+                          g_t = (1/gamma_t)(x_{t,0} - x_{t,tau}) with bias
+                          corrections 1 - beta^(t+1), learning rate eta (not
+                          scaled by gamma), epsilon eps and second moment v.
+
     Returns a dict of per-tensor lists: x (x_{t+1,0}), m (m_{t+1}), u
-    (u_{t+1}), S (the sign actually applied), delta ((x_{t,0}-x_{t,tau})),
-    and B (per-tensor bound, randomized modes only, else None).
+    (u_{t+1}; for Global AdamW the pseudo-gradient g_t), S (the sign actually
+    applied; None for Lookahead and Global AdamW), delta ((x_{t,0}-x_{t,tau})),
+    B (per-tensor bound, randomized modes only, else None) and v (Global AdamW
+    only).
     """
     dt = _dtype(prec)
     n = len(replicas)
@@ -258,6 +280,11 @@ def global_step(x, m, replicas, *, gamma, eta, beta1, beta2, lam, decay,
     c2 = dt((1.0 - b2) / g_)           # (1 - beta2) / gamma_t
     step = dt(f32(eta) * g_)           # eta * gamma_t
     lam_ = dt(f32(lam))
+    if rule != RULE_SIGN_MOMENTUM and mode != SIGN_DET:
+        raise ValueError("the randomized sign applies to the sign-momentum rule only")
+    if rule == RULE_GLOBAL_ADAMW:
+        return _global_adamw(x, m, v, replicas, gamma=gamma, eta=eta, beta1=beta1, beta2=beta2,
+                             lam=lam, eps=eps, decay=decay, t=t, dt=dt)
     out = {"x": [], "m": [], "u": [], "S": [], "delta": [], "B": None}
     if mode != SIGN_DET:
         out["B"] = []
@@ -270,8 +297,20 @@ def global_step(x, m, replicas, *, gamma, eta, beta1, beta2, lam, decay,
             acc = acc + (xp - np.asarray(replicas[i][p], dtype=np.float32).astype(dt))
         delta = acc / dt(n)
         # Eq. (6) and Eq. (8), both from the old m_t.
-        u = beta1_ * mp + c1 * delta
+        if rule == RULE_SIGNED_SLOWMO:
+            u = beta1_ * mp + c1 * sign(delta)
+        else:
+            u = beta1_ * mp + c1 * delta
         m_new = beta2_ * mp + c2 * delta
+        if rule in (RULE_LOOKAHEAD, RULE_SIGNED_SLOWMO):
+            # The variants step along u itself (no sign).
+            lam_p = lam_ if decay[p] else dt(0.0)
+            out["x"].append(xp - step * (u + lam_p * xp))
+            out["m"].append(m_new)
+            out["u"].append(u)
+            out["S"].append(None)
+            out["delta"].append(delta)
+            continue
         if mode == SIGN_DET:
             S = sign(u)
         else:
@@ -293,6 +332,48 @@ def global_step(x, m, replicas, *, gamma, eta, beta1, beta2, lam, decay,
         out["m"].append(m_new)
         out["u"].append(u)
         out["S"].append(S)
+        out["delta"].append(delta)
+    return out
+
+
+def _worker_mean_difference(xp, reps_p, dt):
+    """(1/n) sum_i (x - x_i) in worker order (the all-reduce, reading above)."""
+    acc = xp - np.asarray(reps_p[0], dtype=np.float32).astype(dt)
+    for r in reps_p[1:]:
+        acc = acc + (xp - np.asarray(r, dtype=np.float32).astype(dt))
+    return acc / dt(len(reps_p))
+
+
+def _global_adamw(x, m, v, replicas, *, gamma, eta, beta1, beta2, lam, eps, decay, t, dt):
+    """Algorithm 7 (Appendix C): AdamW on the pseudo-gradient of round t."""
+    if v is None:
+        raise ValueError("Global AdamW needs the second-moment buffer v")
+    b1, b2 = f32(beta1), f32(beta2)
+    beta1_, beta2_ = dt(b1), dt(b2)
+    one_minus_b1, one_minus_b2 = dt(1.0 - b1), dt(1.0 - b2)
+    inv_gamma = dt(1.0 / f32(gamma))
+    bc1 = dt(1.0 - beta_power(b1, t + 1))
+    bc2 = dt(1.0 - beta_power(b2, t + 1))
+    eta_, eps_, lam_ = dt(f32(eta)), dt(f32(eps)), dt(f32(lam))
+    out = {"x": [], "m": [], "v": [], "u": [], "S": [], "delta": [], "B": None}
+    for p in range(len(x)):
+        xp = np.asarray(x[p], dtype=np.float32).astype(dt)
+        mp = np.asarray(m[p], dtype=np.float32).astype(dt)
+        vp = np.asarray(v[p], dtype=np.float32).astype(dt)
+        delta = _worker_mean_difference(xp, [r[p] for r in replicas], dt)
+        # Pseudo-gradient, momentum updates, bias corrections, parameter update.
+        g = inv_gamma * delta
+        m_new = beta1_ * mp + one_minus_b1 * g
+        v_new = beta2_ * vp + one_minus_b2 * (g * g)
+        m_hat = m_new / bc1
+        v_hat = v_new / bc2
+        lam_p = lam_ if decay[p] else dt(0.0)
+        x_new = xp - eta_ * (m_hat / (np.sqrt(v_hat) + eps_) + lam_p * xp)
+        out["x"].append(x_new)
+        out["m"].append(m_new)
+        out["v"].append(v_new)
+        out["u"].append(g)
+        out["S"].append(None)
         out["delta"].append(delta)
     return out
 
@@ -364,9 +445,14 @@ def communication_round(st, grads, t, *, H, local, glob, decay, prec="fp64"):
     Returns the global-step output dict.
     """
     local_steps(st, grads, H=H, decay=decay, first_step=t * H + 1, prec=prec, **local)
+    extra = {}
+    if glob.get("rule", RULE_SIGN_MOMENTUM) == RULE_GLOBAL_ADAMW:
+        extra["v"] = st.setdefault("v", [np.zeros_like(a) for a in st["x"]])
     res = global_step(st["x"], st["m"], st["replicas"], gamma=local["lr"], decay=decay,
-                      t=t, prec=prec, **glob)
+                      t=t, prec=prec, **glob, **extra)
     st["x"] = [_store(a) for a in res["x"]]
     st["m"] = [_store(a) for a in res["m"]]
+    if "v" in res:
+        st["v"] = [_store(a) for a in res["v"]]
     st["replicas"] = synchronize(st["x"], st["n"])
     return res

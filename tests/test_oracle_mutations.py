@@ -16,13 +16,15 @@ import pytest
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
+PIN_FILES = ("test_oracle_pins.py", "test_oracle_variants.py")
 
 # (file, original text, planted mistake, what it breaks)
 MUTATIONS = [
     ("dsm_oracle.py", "m_new = beta1_ * m + one_minus_b1 * g",
      "m_new = beta1_ * m + one_minus_b2 * g", "AdamW first-moment coefficient"),
-    ("dsm_oracle.py", "m_hat = m_new / bc1", "m_hat = m_new", "AdamW bias correction dropped"),
-    ("dsm_oracle.py", "np.sqrt(v_hat) + eps_", "np.sqrt(v_hat + eps_)", "AdamW epsilon placement"),
+    ("dsm_oracle.py", "\n    m_hat = m_new / bc1", "\n    m_hat = m_new", "AdamW bias correction dropped"),
+    ("dsm_oracle.py", "(m_hat / (np.sqrt(v_hat) + eps_) + wd_ * x)",
+     "(m_hat / np.sqrt(v_hat + eps_) + wd_ * x)", "AdamW epsilon placement"),
     ("dsm_oracle.py", "x_new = x - lr_ * (m_hat", "x_new = x + lr_ * (m_hat", "AdamW step sign"),
     ("dsm_oracle.py", "+ wd_ * x)", "+ wd_ * m_hat)", "AdamW decay operand"),
     ("dsm_oracle.py", "m_new = mu * m + g", "m_new = mu * m + (1 - mu) * g",
@@ -35,8 +37,10 @@ MUTATIONS = [
      "u = beta1_ * (beta2_ * mp + c2 * delta) + c1 * delta", "u from the new momentum"),
     ("dsm_oracle.py", "x_new = xp - step * (S + lam_p * xp)", "x_new = xp - step * S",
      "global weight decay dropped"),
-    ("dsm_oracle.py", "lam_p = lam_ if decay[p] else dt(0.0)", "lam_p = lam_",
-     "decay mask ignored"),
+    ("dsm_oracle.py", "lam_p = lam_ if decay[p] else dt(0.0)\n        # Eq. (7)",
+     "lam_p = lam_\n        # Eq. (7)", "decay mask ignored"),
+    ("dsm_oracle.py", "\n        m_hat = m_new / bc1", "\n        m_hat = m_new",
+     "Global AdamW bias correction dropped"),
     ("dsm_oracle.py", "for i in range(1, n):", "for i in range(1, n - 1):",
      "last worker dropped from the average"),
     ("dsm_oracle.py", "delta = acc / dt(n)", "delta = acc", "average not divided by n"),
@@ -60,6 +64,15 @@ MUTATIONS = [
     ("dsm_oracle.py", '    st["replicas"] = synchronize(st["x"], st["n"])',
      '    st["replicas"] = synchronize(st["x"], st["n"]) if False else st["replicas"]',
      "replicas not synchronised"),
+    ("dsm_oracle.py", "u = beta1_ * mp + c1 * sign(delta)", "u = beta1_ * mp + c1 * delta",
+     "signed SlowMo without the sign"),
+    ("dsm_oracle.py", "out[\"x\"].append(xp - step * (u + lam_p * xp))",
+     "out[\"x\"].append(xp - step * (sign(u) + lam_p * xp))", "Lookahead keeps the sign"),
+    ("dsm_oracle.py", "g = inv_gamma * delta", "g = delta", "Global AdamW without 1/gamma"),
+    ("dsm_oracle.py", "bc1 = dt(1.0 - beta_power(b1, t + 1))", "bc1 = dt(1.0 - beta_power(b1, t + 2))",
+     "Global AdamW bias correction off by one"),
+    ("dsm_oracle.py", "x_new = xp - eta_ * (m_hat", "x_new = xp - eta_ * inv_gamma * (m_hat",
+     "Global AdamW step scaled by 1/gamma"),
     ("dsm_oracle.py",
      "    local_steps(st, grads, H=H, decay=decay, first_step=t * H + 1, prec=prec, **local)",
      "    st['s1'] = [[a * 0 for a in w] for w in st['s1']]\n"
@@ -76,7 +89,8 @@ def _run_mutant(case):
                         ignore=shutil.ignore_patterns("__pycache__"))
         tdir = os.path.join(tmp, "tests")
         os.makedirs(tdir)
-        shutil.copy(os.path.join(HERE, "test_oracle_pins.py"), tdir)
+        for f in PIN_FILES:
+            shutil.copy(os.path.join(HERE, f), tdir)
         shutil.copytree(os.path.join(HERE, "golden"), os.path.join(tdir, "golden"))
         shutil.copytree(os.path.join(HERE, "native"), os.path.join(tdir, "native"),
                         ignore=shutil.ignore_patterns("bin"))
@@ -89,7 +103,7 @@ def _run_mutant(case):
         open(path, "w").write(src.replace(orig, planted))
         env = dict(os.environ, PYTHONDONTWRITEBYTECODE="1")
         r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-                            os.path.join(tdir, "test_oracle_pins.py")],
+                            *[os.path.join(tdir, f) for f in PIN_FILES]],
                            cwd=tmp, env=env, capture_output=True, text=True, timeout=600)
         return r.returncode, r.stdout[-2000:]
     finally:
