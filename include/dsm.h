@@ -66,6 +66,20 @@ typedef enum dsm_sign {
     DSM_SIGN_RAND_ZERO = 2  /* randomized sign of Eq. (10) (Section 3.1) */
 } dsm_sign;
 
+/* The global update (dsm_global_hparams.rule): the method's sign momentum,
+ * or one of the ablation variants of its global step. */
+typedef enum dsm_global_rule {
+    DSM_RULE_SIGN_MOMENTUM = 0, /* Eqs. (6)-(8) */
+    DSM_RULE_LOOKAHEAD = 1,     /* Section 4.1: Eq. (7) with u in place of sign(u):
+                                   x <- x - eta gamma (u + lambda x); lambda = 0 is the
+                                   paper's Lookahead */
+    DSM_RULE_SIGNED_SLOWMO = 2, /* Section 4.1: u = b1 m + ((1-b1)/gamma) sign(delta),
+                                   x <- x - eta gamma (u + lambda x), Eq. (8) unchanged */
+    DSM_RULE_GLOBAL_ADAMW = 3   /* Algorithm 7 (Appendix C): AdamW with learning rate
+                                   eta on g = delta/gamma, bias corrections 1 - b^(t+1);
+                                   needs buffers.v */
+} dsm_global_rule;
+
 /* The problem of Eq. (1): x in R^d given as n_tensors tensors. */
 typedef struct dsm_problem {
     int32_t n_workers;     /* n, 1..64 */
@@ -92,6 +106,8 @@ typedef struct dsm_buffers {
     void* workspace;   /* device, >= workspace_bytes from dsm_layout */
     int64_t workspace_bytes;
     void* stream;      /* hipStream_t all work is enqueued on (NULL = default) */
+    float* v;          /* [d_pad]      global second moment of DSM_RULE_GLOBAL_ADAMW
+                          (zeroed by init); may be NULL if that rule is never used */
 } dsm_buffers;
 
 /* Local hyperparameters (Algorithm 2 / Algorithm 3). */
@@ -110,8 +126,10 @@ typedef struct dsm_global_hparams {
     float beta1;     /* beta1 in [0, 1], Eq. (6) */
     float beta2;     /* beta2 in [0, 1], Eq. (8) */
     float lambda;    /* decoupled weight decay lambda >= 0, Eq. (7) */
-    int32_t mode;    /* dsm_sign */
+    int32_t mode;    /* dsm_sign; the variants take DSM_SIGN_DET only */
     uint64_t seed;   /* Philox key of the randomized sign */
+    int32_t rule;    /* dsm_global_rule */
+    float eps;       /* epsilon of DSM_RULE_GLOBAL_ADAMW (Algorithm 7), >= 0 */
 } dsm_global_hparams;
 
 /*
@@ -175,8 +193,12 @@ DSM_API dsm_status dsm_local_step(dsm_ctx* ctx, int32_t worker, int64_t step,
  * new x (synchronisation step); otherwise the replicas are left stale and
  * each worker's next local step reads x (see dsm_local_step), or dsm_sync
  * copies x into them.  The randomized modes need buffers->u_scratch.
+ * hp->rule selects an ablation variant of the global update instead
+ * (deterministic, same fused pass; Global AdamW also reads and writes
+ * buffers->v).
  * Errors: DSM_ERR_INVALID_ARG (t outside [0, 2^32), hyperparameters, mode,
- * missing u_scratch); DSM_ERR_STATE (some worker has not taken exactly H
+ * unknown rule, a randomized mode with a variant rule, missing u_scratch or
+ * v); DSM_ERR_STATE (some worker has not taken exactly H
  * local steps since the last synchronisation); DSM_ERR_HIP.
  */
 DSM_API dsm_status dsm_global_step(dsm_ctx* ctx, int64_t t, const dsm_global_hparams* hp,
@@ -193,7 +215,8 @@ DSM_API dsm_status dsm_global_step(dsm_ctx* ctx, int64_t t, const dsm_global_hpa
  * the replicas are left stale (read as x by the next local step), which
  * with the fusion saves 4n + 4n bytes per element per round.
  * Errors: as dsm_local_step and dsm_global_step; DSM_ERR_STATE unless every
- * worker has taken exactly H - 1 local steps this round.
+ * worker has taken exactly H - 1 local steps this round; DSM_ERR_UNSUPPORTED
+ * for a rule other than DSM_RULE_SIGN_MOMENTUM (use the two separate calls).
  */
 DSM_API dsm_status dsm_round_end(dsm_ctx* ctx, int64_t step, const dsm_local_hparams* local_hp,
                                  int64_t t, const dsm_global_hparams* global_hp,

@@ -14,11 +14,12 @@ class Arenas:
 
     numel: per-tensor element counts; n_workers, local_steps, base: the
     problem (dsm_problem); decay: per-tensor weight-decay flags or None;
-    randomized: allocate u_scratch for the randomized sign.
+    randomized: allocate u_scratch for the randomized sign; global_adamw:
+    allocate the global second moment v of the Global AdamW rule.
     """
 
     def __init__(self, numel, n_workers, local_steps, base, decay=None, randomized=True,
-                 device="cuda"):
+                 global_adamw=False, device="cuda"):
         self.numel = [int(v) for v in numel]
         self.n = int(n_workers)
         self.H = int(local_steps)
@@ -36,6 +37,7 @@ class Arenas:
         self.s2_rep = (torch.zeros(self.n, a, dtype=f32, device=device)
                        if self.base == dsm.DSM_BASE_ADAMW else None)
         self.u = torch.zeros(a, dtype=f32, device=device) if randomized else None
+        self.v = torch.zeros(a, dtype=f32, device=device) if global_adamw else None
         self.workspace = torch.zeros(max(self.workspace_bytes, 256), dtype=torch.uint8,
                                      device=device)
         self.ctx = None
@@ -48,7 +50,8 @@ class Arenas:
             return None if t is None else t.data_ptr()
         return dsm.dsm_buffers(ptr(self.x), ptr(self.m), ptr(self.x_rep), ptr(self.g_rep),
                                ptr(self.s1_rep), ptr(self.s2_rep), ptr(self.u),
-                               ptr(self.workspace), self.workspace.numel(), stream.cuda_stream)
+                               ptr(self.workspace), self.workspace.numel(), stream.cuda_stream,
+                               ptr(self.v))
 
     def init(self, stream=None):
         """dsm_init on the current contents of x."""

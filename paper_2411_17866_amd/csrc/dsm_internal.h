@@ -72,11 +72,17 @@ struct GlobalScalars {
     uint32_t key0, key1;  // Philox key (seed low, seed high)
     uint32_t t;           // outer iteration (Philox counter word 2)
     int32_t mode;         // dsm_sign
+    int32_t rule;         // dsm_global_rule
+    // Global AdamW (Algorithm 7) only.
+    float inv_gamma;      // 1/gamma
+    float one_minus_beta1, one_minus_beta2;
+    float bc1, bc2;       // 1 - beta^(t+1)
+    float eta, eps;
 };
 
 // Kernel launchers (dsm_kernels.hip).  All return the launch status.
-hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float* m, float* x_rep,
-                       float* s1, float* s2, int64_t stride, int n, hipStream_t st);
+hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float* m, float* v,
+                       float* x_rep, float* s1, float* s2, int64_t stride, int n, hipStream_t st);
 // Local steps: worker w reads its replica from x_src + w * src_stride (the
 // replica, or the shared global model with src_stride = 0) and writes it to
 // x_rep + w * stride.
@@ -104,8 +110,9 @@ struct RoundEndArgs {
 };
 hipError_t launch_round_end(const Chunk* chunks, int64_t n_chunks, int n_tensors, bool adamw,
                             const RoundEndArgs& a, bool broadcast, hipStream_t st);
+// Deterministic global step of any rule; v is the Global AdamW second moment.
 hipError_t launch_global_det(const Chunk* chunks, int64_t n_chunks, float* x, float* m,
-                             float* x_rep, int64_t stride, const GlobalScalars& sc,
+                             float* v, float* x_rep, int64_t stride, const GlobalScalars& sc,
                              bool broadcast, hipStream_t st);
 hipError_t launch_global_rand(const Chunk* chunks, int64_t n_chunks, int n_tensors, float* x,
                               float* m, float* x_rep, float* u, uint32_t* bound_bits,

@@ -250,27 +250,57 @@ __device__ __forceinline__ f4 model4(f4 x, f4 S, float lam, const GlobalScalars&
     return x - st;
 }
 
-template <int N, bool BCAST>
+// Global-step rules (dsm_global_rule).
+constexpr int kRuleSignMomentum = 0;  // Eqs. (6)-(8)
+constexpr int kRuleLookahead = 1;     // Section 4.1: x - eta gamma (u + lambda x)
+constexpr int kRuleSignedSlowMo = 2;  // Section 4.1: sign on the averaged difference
+constexpr int kRuleGlobalAdamW = 3;   // Algorithm 7
+
+// Algorithm 7 on four elements: AdamW on the pseudo-gradient
+// g = (1/gamma) delta; m and v updated in place; returns the new x.
+__device__ __forceinline__ f4 global_adamw4(f4 x, f4 delta, f4& m, f4& v, float lam,
+                                           const GlobalScalars& s) {
+    const f4 g = s.inv_gamma * delta;
+    const f4 m1 = s.beta1 * m;
+    const f4 m2 = s.one_minus_beta1 * g;
+    m = m1 + m2;
+    const f4 gg = g * g;
+    const f4 v1 = s.beta2 * v;
+    const f4 v2 = s.one_minus_beta2 * gg;
+    v = v1 + v2;
+    const f4 m_hat = m / s.bc1;
+    const f4 v_hat = v / s.bc2;
+    const f4 den = sqrt_rn(v_hat) + s.eps;
+    const f4 r = m_hat / den;
+    const f4 wx = lam * x;
+    const f4 d = r + wx;
+    const f4 st = s.eta * d;
+    return x - st;
+}
+
+template <int N, int RULE, bool BCAST>
 __global__ __launch_bounds__(kBlockThreads) void k_global_det(
     const Chunk* __restrict__ chunks, float* __restrict__ x, float* __restrict__ m,
-    float* __restrict__ x_rep, int64_t stride, GlobalScalars sc) {
+    float* __restrict__ v, float* __restrict__ x_rep, int64_t stride, GlobalScalars sc) {
     const Piece pc = piece_of(chunks);
     const Chunk& c = pc.c;
     const int n = N > 0 ? N : sc.n;
     f4* __restrict__ xp = reinterpret_cast<f4*>(x + c.off);
     f4* __restrict__ mp = reinterpret_cast<f4*>(m + c.off);
+    f4* __restrict__ vp = reinterpret_cast<f4*>(v + c.off);
     float* __restrict__ rbase = x_rep + c.off;
     const float lam = c.decay ? sc.lam : 0.0f;
     const int nvec = pc.q_hi;
     const int nfull = pc.nfull;
     for (int q0 = pc.q_lo + threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
-        f4 xv[kUnroll], mv[kUnroll], dv[kUnroll];
+        f4 xv[kUnroll], mv[kUnroll], vv[kUnroll], dv[kUnroll];
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = q0 + k * kBlockThreads;
             if (q < nvec) {
                 xv[k] = ntload(xp + q);
                 mv[k] = ntload(mp + q);
+                if (RULE == kRuleGlobalAdamW) vv[k] = ntload(vp + q);
             }
         }
 #pragma unroll
@@ -282,8 +312,26 @@ __global__ __launch_bounds__(kBlockThreads) void k_global_det(
         for (int k = 0; k < kUnroll; ++k) {
             const int q = q0 + k * kBlockThreads;
             if (q < nvec) {
-                const f4 u = momentum4(mv[k], dv[k], sc);
-                const f4 xn = model4(xv[k], sign4(u), lam, sc);
+                f4 xn;
+                if constexpr (RULE == kRuleSignMomentum) {
+                    const f4 u = momentum4(mv[k], dv[k], sc);
+                    xn = model4(xv[k], sign4(u), lam, sc);
+                } else if constexpr (RULE == kRuleLookahead) {
+                    const f4 u = momentum4(mv[k], dv[k], sc);
+                    xn = model4(xv[k], u, lam, sc);
+                } else if constexpr (RULE == kRuleSignedSlowMo) {
+                    // u from the old m and the sign of the difference; m by Eq. (8).
+                    const f4 u1 = sc.beta1 * mv[k];
+                    const f4 u2 = sc.c1 * sign4(dv[k]);
+                    const f4 u = u1 + u2;
+                    const f4 m1 = sc.beta2 * mv[k];
+                    const f4 m2 = sc.c2 * dv[k];
+                    mv[k] = m1 + m2;
+                    xn = model4(xv[k], u, lam, sc);
+                } else {
+                    xn = global_adamw4(xv[k], dv[k], mv[k], vv[k], lam, sc);
+                    store_group(vv[k], vp, q, nfull, c.len);
+                }
                 store_group(xn, xp, q, nfull, c.len);
                 store_group(mv[k], mp, q, nfull, c.len);
                 if (BCAST) {
@@ -573,8 +621,8 @@ __global__ __launch_bounds__(kBlockThreads) void k_broadcast(
 // Algorithm 1 initialisation: m = 0, replicas = x, base state = 0.
 __global__ __launch_bounds__(kBlockThreads) void k_init(
     const Chunk* __restrict__ chunks, const float* __restrict__ x, float* __restrict__ m,
-    float* __restrict__ x_rep, float* __restrict__ s1, float* __restrict__ s2, int64_t stride,
-    int n) {
+    float* __restrict__ v, float* __restrict__ x_rep, float* __restrict__ s1,
+    float* __restrict__ s2, int64_t stride, int n) {
     const Piece pc = piece_of(chunks);
     const Chunk& c = pc.c;
     const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + c.off);
@@ -582,11 +630,12 @@ __global__ __launch_bounds__(kBlockThreads) void k_init(
     const int nfull = pc.nfull;
     const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
     for (int q = pc.q_lo + threadIdx.x; q < nvec; q += kBlockThreads) {
-        const f4 v = ntload(xp + q);
+        const f4 xv = ntload(xp + q);
         store_group(zero, reinterpret_cast<f4*>(m + c.off), q, nfull, c.len);
+        if (v != nullptr) store_group(zero, reinterpret_cast<f4*>(v + c.off), q, nfull, c.len);
         for (int i = 0; i < n; ++i) {
             const int64_t o = i * stride + c.off;
-            store_group(v, reinterpret_cast<f4*>(x_rep + o), q, nfull, c.len);
+            store_group(xv, reinterpret_cast<f4*>(x_rep + o), q, nfull, c.len);
             store_group(zero, reinterpret_cast<f4*>(s1 + o), q, nfull, c.len);
             if (s2 != nullptr) store_group(zero, reinterpret_cast<f4*>(s2 + o), q, nfull, c.len);
         }
@@ -615,11 +664,11 @@ dim3 chunk_grid(int64_t n_chunks, int n_workers) {
 
 // ---------------------------------------------------------------- launchers
 
-hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float* m, float* x_rep,
-                       float* s1, float* s2, int64_t stride, int n, hipStream_t st) {
+hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float* m, float* v,
+                       float* x_rep, float* s1, float* s2, int64_t stride, int n, hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_init, chunk_grid(n_chunks, 1), dim3(kBlockThreads), 0, st, chunks, x, m,
-                       x_rep, s1, s2, stride, n);
+                       v, x_rep, s1, s2, stride, n);
     return hipGetLastError();
 }
 
@@ -702,28 +751,56 @@ hipError_t launch_round_end(const Chunk* chunks, int64_t n_chunks, int n_tensors
     return hipGetLastError();
 }
 
-template <bool BCAST>
+template <int RULE, bool BCAST>
 static void launch_global_det_n(const Chunk* chunks, int64_t n_chunks, float* x, float* m,
-                                float* x_rep, int64_t stride, const GlobalScalars& sc,
+                                float* v, float* x_rep, int64_t stride, const GlobalScalars& sc,
                                 hipStream_t st) {
     const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
+#define DSM_GLOBAL_DET(NW)                                                                     \
+    hipLaunchKernelGGL((k_global_det<NW, RULE, BCAST>), grid, block, 0, st, chunks, x, m, v,   \
+                       x_rep, stride, sc)
     switch (sc.n) {
-        case 1: hipLaunchKernelGGL((k_global_det<1, BCAST>), grid, block, 0, st, chunks, x, m, x_rep, stride, sc); break;
-        case 2: hipLaunchKernelGGL((k_global_det<2, BCAST>), grid, block, 0, st, chunks, x, m, x_rep, stride, sc); break;
-        case 4: hipLaunchKernelGGL((k_global_det<4, BCAST>), grid, block, 0, st, chunks, x, m, x_rep, stride, sc); break;
-        case 8: hipLaunchKernelGGL((k_global_det<8, BCAST>), grid, block, 0, st, chunks, x, m, x_rep, stride, sc); break;
-        default: hipLaunchKernelGGL((k_global_det<0, BCAST>), grid, block, 0, st, chunks, x, m, x_rep, stride, sc); break;
+        case 1: DSM_GLOBAL_DET(1); break;
+        case 2: DSM_GLOBAL_DET(2); break;
+        case 4: DSM_GLOBAL_DET(4); break;
+        case 8: DSM_GLOBAL_DET(8); break;
+        default: DSM_GLOBAL_DET(0); break;
     }
+#undef DSM_GLOBAL_DET
+}
+
+template <int RULE>
+static void launch_global_det_rule(const Chunk* chunks, int64_t n_chunks, float* x, float* m,
+                                   float* v, float* x_rep, int64_t stride,
+                                   const GlobalScalars& sc, bool broadcast, hipStream_t st) {
+    if (broadcast)
+        launch_global_det_n<RULE, true>(chunks, n_chunks, x, m, v, x_rep, stride, sc, st);
+    else
+        launch_global_det_n<RULE, false>(chunks, n_chunks, x, m, v, x_rep, stride, sc, st);
 }
 
 hipError_t launch_global_det(const Chunk* chunks, int64_t n_chunks, float* x, float* m,
-                             float* x_rep, int64_t stride, const GlobalScalars& sc,
+                             float* v, float* x_rep, int64_t stride, const GlobalScalars& sc,
                              bool broadcast, hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
-    if (broadcast)
-        launch_global_det_n<true>(chunks, n_chunks, x, m, x_rep, stride, sc, st);
-    else
-        launch_global_det_n<false>(chunks, n_chunks, x, m, x_rep, stride, sc, st);
+    switch (sc.rule) {
+        case kRuleLookahead:
+            launch_global_det_rule<kRuleLookahead>(chunks, n_chunks, x, m, v, x_rep, stride, sc,
+                                                   broadcast, st);
+            break;
+        case kRuleSignedSlowMo:
+            launch_global_det_rule<kRuleSignedSlowMo>(chunks, n_chunks, x, m, v, x_rep, stride,
+                                                      sc, broadcast, st);
+            break;
+        case kRuleGlobalAdamW:
+            launch_global_det_rule<kRuleGlobalAdamW>(chunks, n_chunks, x, m, v, x_rep, stride, sc,
+                                                     broadcast, st);
+            break;
+        default:
+            launch_global_det_rule<kRuleSignMomentum>(chunks, n_chunks, x, m, v, x_rep, stride,
+                                                      sc, broadcast, st);
+            break;
+    }
     return hipGetLastError();
 }
 

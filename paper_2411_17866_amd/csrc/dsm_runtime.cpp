@@ -214,6 +214,19 @@ dsm_status global_coefs(dsm_ctx* ctx, int64_t t, const dsm_global_hparams* hp,
         return fail(ctx, DSM_ERR_INVALID_ARG, "unknown sign mode %d", hp->mode);
     if (hp->mode != DSM_SIGN_DET && ctx->arena_elems > 0 && !ctx->buf.u_scratch)
         return fail(ctx, DSM_ERR_INVALID_ARG, "the randomized sign needs buffers.u_scratch");
+    if (hp->rule < DSM_RULE_SIGN_MOMENTUM || hp->rule > DSM_RULE_GLOBAL_ADAMW)
+        return fail(ctx, DSM_ERR_INVALID_ARG, "unknown global rule %d", hp->rule);
+    if (hp->rule != DSM_RULE_SIGN_MOMENTUM && hp->mode != DSM_SIGN_DET)
+        return fail(ctx, DSM_ERR_INVALID_ARG,
+                    "the randomized sign applies to the sign-momentum rule only");
+    if (hp->rule == DSM_RULE_GLOBAL_ADAMW) {
+        if (ctx->arena_elems > 0 && !ctx->buf.v)
+            return fail(ctx, DSM_ERR_INVALID_ARG, "Global AdamW needs buffers.v");
+        if (!(std::isfinite(hp->eps) && hp->eps >= 0.0f))
+            return fail(ctx, DSM_ERR_INVALID_ARG, "eps must be finite and >= 0");
+        if (hp->beta1 == 1.0f || hp->beta2 == 1.0f)
+            return fail(ctx, DSM_ERR_INVALID_ARG, "Global AdamW needs beta1, beta2 < 1");
+    }
     dsm::GlobalScalars& sc = *out;
     const double gamma = hp->gamma;
     sc.beta1 = hp->beta1;
@@ -230,6 +243,14 @@ dsm_status global_coefs(dsm_ctx* ctx, int64_t t, const dsm_global_hparams* hp,
     sc.key1 = static_cast<uint32_t>(hp->seed >> 32);
     sc.t = static_cast<uint32_t>(t);
     sc.mode = hp->mode;
+    sc.rule = hp->rule;
+    sc.inv_gamma = static_cast<float>(1.0 / gamma);
+    sc.one_minus_beta1 = static_cast<float>(1.0 - static_cast<double>(hp->beta1));
+    sc.one_minus_beta2 = static_cast<float>(1.0 - static_cast<double>(hp->beta2));
+    sc.bc1 = static_cast<float>(1.0 - beta_power(hp->beta1, t + 1));
+    sc.bc2 = static_cast<float>(1.0 - beta_power(hp->beta2, t + 1));
+    sc.eta = hp->eta;
+    sc.eps = hp->eps;
     return DSM_OK;
 }
 
@@ -292,7 +313,7 @@ dsm_status dsm_init(const dsm_problem* problem, const dsm_buffers* b, dsm_ctx** 
         } ptrs[] = {{b->x, "x", true},           {b->m, "m", true},
                     {b->x_rep, "x_rep", true},   {b->g_rep, "g_rep", true},
                     {b->s1_rep, "s1_rep", true}, {b->s2_rep, "s2_rep", adamw},
-                    {b->u_scratch, "u_scratch", false}};
+                    {b->u_scratch, "u_scratch", false}, {b->v, "v", false}};
         for (const auto& q : ptrs) {
             if (q.required && !q.p)
                 return fail(nullptr, DSM_ERR_INVALID_ARG, "buffer %s is NULL", q.name);
@@ -342,7 +363,7 @@ dsm_status dsm_init(const dsm_problem* problem, const dsm_buffers* b, dsm_ctx** 
             return r;
         }
         e = dsm::launch_init(ctx->d_chunks, static_cast<int64_t>(ctx->chunks.size()), b->x, b->m,
-                             b->x_rep, b->s1_rep, adamw ? b->s2_rep : nullptr, ctx->arena_elems,
+                             b->v, b->x_rep, b->s1_rep, adamw ? b->s2_rep : nullptr, ctx->arena_elems,
                              ctx->n, ctx->stream);
         if (e != hipSuccess) {
             dsm_status r = hip_fail(nullptr, "launching the initialisation kernel", e);
@@ -406,8 +427,9 @@ dsm_status dsm_global_step(dsm_ctx* ctx, int64_t t, const dsm_global_hparams* hp
     const int64_t n_chunks = static_cast<int64_t>(ctx->chunks.size());
     hipError_t e;
     if (!randomized) {
-        e = dsm::launch_global_det(ctx->d_chunks, n_chunks, ctx->buf.x, ctx->buf.m, ctx->buf.x_rep,
-                                   ctx->arena_elems, sc, broadcast != 0, ctx->stream);
+        e = dsm::launch_global_det(ctx->d_chunks, n_chunks, ctx->buf.x, ctx->buf.m, ctx->buf.v,
+                                   ctx->buf.x_rep, ctx->arena_elems, sc, broadcast != 0,
+                                   ctx->stream);
     } else {
         e = dsm::launch_global_rand(ctx->d_chunks, n_chunks, ctx->n_tensors, ctx->buf.x, ctx->buf.m,
                                     ctx->buf.x_rep, ctx->buf.u_scratch, ctx->d_bounds,
@@ -428,6 +450,10 @@ dsm_status dsm_round_end(dsm_ctx* ctx, int64_t step, const dsm_local_hparams* lo
     dsm::GlobalScalars gs{};
     st = global_coefs(ctx, t, global_hp, &gs);
     if (st != DSM_OK) return st;
+    if (global_hp->rule != DSM_RULE_SIGN_MOMENTUM)
+        return fail(ctx, DSM_ERR_UNSUPPORTED,
+                    "dsm_round_end fuses the sign-momentum rule only; use dsm_local_step and "
+                    "dsm_global_step for the variants");
     for (int i = 0; i < ctx->n; ++i) {
         if (ctx->local_count[i] != ctx->H - 1)
             return fail(ctx, DSM_ERR_STATE,

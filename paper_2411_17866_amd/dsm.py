@@ -28,6 +28,11 @@ DSM_SIGN_DET = 0
 DSM_SIGN_RAND_FLIP = 1
 DSM_SIGN_RAND_ZERO = 2
 
+DSM_RULE_SIGN_MOMENTUM = 0
+DSM_RULE_LOOKAHEAD = 1
+DSM_RULE_SIGNED_SLOWMO = 2
+DSM_RULE_GLOBAL_ADAMW = 3
+
 EXPORTED = ("dsm_layout", "dsm_init", "dsm_local_step", "dsm_global_step", "dsm_round_end",
             "dsm_sync",
             "dsm_read_bounds", "dsm_test_philox", "dsm_destroy", "dsm_last_error")
@@ -52,7 +57,7 @@ class dsm_buffers(ctypes.Structure):
                 ("g_rep", ctypes.c_void_p), ("s1_rep", ctypes.c_void_p),
                 ("s2_rep", ctypes.c_void_p), ("u_scratch", ctypes.c_void_p),
                 ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_int64),
-                ("stream", ctypes.c_void_p)]
+                ("stream", ctypes.c_void_p), ("v", ctypes.c_void_p)]
 
 
 class dsm_local_hparams(ctypes.Structure):
@@ -63,7 +68,7 @@ class dsm_local_hparams(ctypes.Structure):
 class dsm_global_hparams(ctypes.Structure):
     _fields_ = [("gamma", ctypes.c_float), ("eta", ctypes.c_float), ("beta1", ctypes.c_float),
                 ("beta2", ctypes.c_float), ("lambda_", ctypes.c_float), ("mode", ctypes.c_int32),
-                ("seed", ctypes.c_uint64)]
+                ("seed", ctypes.c_uint64), ("rule", ctypes.c_int32), ("eps", ctypes.c_float)]
 
 
 _lib = None
@@ -152,17 +157,17 @@ def dsm_local_step(ctx, worker, step, lr, beta1, beta2=0.0, eps=0.0, weight_deca
 
 
 def dsm_global_step(ctx, t, gamma, eta, beta1, beta2, lam, mode=DSM_SIGN_DET, seed=0,
-                    broadcast=True):
-    hp = dsm_global_hparams(gamma, eta, beta1, beta2, lam, mode, seed)
+                    broadcast=True, rule=DSM_RULE_SIGN_MOMENTUM, eps=1e-8):
+    hp = dsm_global_hparams(gamma, eta, beta1, beta2, lam, mode, seed, rule, eps)
     _check(load_library().dsm_global_step(ctx, t, ctypes.byref(hp), 1 if broadcast else 0), ctx)
 
 
 def dsm_round_end(ctx, step, local, t, gamma, eta, beta1, beta2, lam, mode=DSM_SIGN_DET, seed=0,
-                  broadcast=True):
+                  broadcast=True, rule=DSM_RULE_SIGN_MOMENTUM, eps=1e-8):
     """local: dict of dsm_local_hparams fields (lr, beta1, beta2, eps, weight_decay)."""
     lhp = dsm_local_hparams(local["lr"], local["beta1"], local.get("beta2", 0.0),
                             local.get("eps", 0.0), local.get("weight_decay", 0.0))
-    ghp = dsm_global_hparams(gamma, eta, beta1, beta2, lam, mode, seed)
+    ghp = dsm_global_hparams(gamma, eta, beta1, beta2, lam, mode, seed, rule, eps)
     _check(load_library().dsm_round_end(ctx, step, ctypes.byref(lhp), t, ctypes.byref(ghp),
                                         1 if broadcast else 0), ctx)
 

@@ -97,7 +97,7 @@ def _fake_buffers(arena, n, ws, misalign=None, null=None, ws_bytes=None, adamw=T
         ptrs[null] = None
     return dsm.dsm_buffers(ptrs["x"], ptrs["m"], ptrs["x_rep"], ptrs["g_rep"], ptrs["s1_rep"],
                            ptrs["s2_rep"], ptrs["u_scratch"], ptrs["workspace"],
-                           ws if ws_bytes is None else ws_bytes, None)
+                           ws if ws_bytes is None else ws_bytes, None, None)
 
 
 @needs_no_gpu
@@ -153,10 +153,10 @@ def test_struct_layouts_match_header(lib):
     """ctypes mirrors of the header structs have the C sizes and offsets."""
     assert ctypes.sizeof(dsm.dsm_problem) == 32
     assert dsm.dsm_problem.numel.offset == 16
-    assert ctypes.sizeof(dsm.dsm_buffers) == 80
+    assert ctypes.sizeof(dsm.dsm_buffers) == 88
     assert dsm.dsm_buffers.stream.offset == 72
     assert ctypes.sizeof(dsm.dsm_local_hparams) == 20
-    assert ctypes.sizeof(dsm.dsm_global_hparams) == 32
+    assert ctypes.sizeof(dsm.dsm_global_hparams) == 40
     assert dsm.dsm_global_hparams.seed.offset == 24
 
 
@@ -177,7 +177,7 @@ def test_header_compiles_as_c_and_struct_sizes_agree(tmp_path):
     subprocess.run([cc, "-std=c99", "-Wall", "-Werror", "-I", os.path.join(ROOT, "include"),
                     str(src), "-o", str(exe)], check=True)
     out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split()
-    assert [int(v) for v in out] == [32, 80, 20, 32, 72, 24]
+    assert [int(v) for v in out] == [32, 88, 20, 40, 72, 24]
 
 
 def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
