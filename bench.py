@@ -121,7 +121,7 @@ def main():
     adamw = w.base == W.BASE_ADAMW
     print(f"[bench] workload {w.name}: d={w.d} tensors={len(w.tensors)} n={n} H={H}",
           file=sys.stderr, flush=True)
-    ar = A.Arenas(w.numel, n, H, w.base, decay=w.decay, randomized=True)
+    ar = A.Arenas(w.numel, n, H, w.base, decay=w.decay, randomized=True, global_adamw=True)
     gen = torch.Generator(device="cuda").manual_seed(w.seed)
     W.fill_params_(ar.x, w, gen)
     for i in range(n):
@@ -133,7 +133,8 @@ def main():
 
     stream = torch.cuda.current_stream()
     lr = w.local["lr"]
-    ev = {"local": [], "split_det": [], "split_rand": [], "fused_det": [], "fused_rand": []}
+    ev = {"local": [], "split_det": [], "split_rand": [], "fused_det": [], "fused_rand": [],
+          "lookahead": [], "signed_slowmo": [], "global_adamw": []}
     s_count = [0]
 
     def timed(key, fn):
@@ -182,6 +183,19 @@ def main():
             for _ in range(args.extra_steps):
                 one_round(t, mode, path, True)
                 t += 1
+    # The ablation variants of the global step (Section 4.1, Algorithm 7),
+    # one split round each.
+    variants = (("lookahead", dsm.DSM_RULE_LOOKAHEAD, w.glob),
+                ("signed_slowmo", dsm.DSM_RULE_SIGNED_SLOWMO, w.glob),
+                ("global_adamw", dsm.DSM_RULE_GLOBAL_ADAMW,
+                 dict(eta=1e-3, beta1=0.9, beta2=0.95, lam=w.glob["lam"], eps=1e-8)))
+    for key, rule, ghp in variants:
+        for k in range(H):
+            s_count[0] += 1
+            dsm.dsm_local_step(ar.ctx, -1, s_count[0], **w.local)
+        timed(key, lambda: dsm.dsm_global_step(ar.ctx, t, gamma=lr, rule=rule, broadcast=True,
+                                               **ghp))
+        t += 1
     torch.cuda.synchronize()
 
     # Row a2 (local SGD + Polyak momentum, Algorithm 3) and row a6 on its own
@@ -296,6 +310,9 @@ def main():
                                               (28 + (local_state + 8) * n) * d, n * d + d),
             "global_det": kern(ev["split_det"], bytes_global(n, False) * d, d),
             "global_rand_flip": kern(ev["split_rand"], bytes_global(n, True) * d, d),
+            "global_lookahead": kern(ev["lookahead"], bytes_global(n, False) * d, d),
+            "global_signed_slowmo": kern(ev["signed_slowmo"], bytes_global(n, False) * d, d),
+            "global_adamw": kern(ev["global_adamw"], (bytes_global(n, False) + 8) * d, d),
             "local_sgdm": kern(ev_sgd, BYTES_LOCAL_SGDM * n * d, n * d),
             "sync": kern(ev_sync, (4 + 4 * n) * d, n * d),
         },

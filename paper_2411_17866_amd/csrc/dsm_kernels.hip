@@ -23,9 +23,13 @@ namespace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-// Whether the streams use nontemporal loads and stores (build-time knob).
+// Whether the streams use nontemporal loads and stores, and how far the
+// fused round end unrolls its worker loop (build-time knobs).
 #ifndef DSM_NT
 #define DSM_NT 1
+#endif
+#ifndef DSM_ROUND_END_UNROLL
+#define DSM_ROUND_END_UNROLL 1
 #endif
 
 __device__ __forceinline__ f4 ntload(const f4* p) {
@@ -524,8 +528,15 @@ __global__ __launch_bounds__(kBlockThreads) void k_round_end(
                 mv[k] = ntload(mp + q);
             }
         }
-        // Worker loop: fully unrolled for a compile-time worker count.
+        // Worker loop: unrolled DSM_ROUND_END_UNROLL workers at a time (0: fully,
+        // for a compile-time worker count); fewer registers, higher occupancy.
+#if DSM_ROUND_END_UNROLL == 0
 #pragma unroll
+#elif DSM_ROUND_END_UNROLL == 1
+#pragma unroll 1
+#elif DSM_ROUND_END_UNROLL == 2
+#pragma unroll 2
+#endif
         for (int i = 0; i < (N > 0 ? N : n); ++i) {
             const int64_t wo = i * stride + c.off;
             const f4* __restrict__ xs = reinterpret_cast<const f4*>(x_src + i * src_stride + c.off);
