@@ -89,17 +89,15 @@ def f32(h):
 
 
 def beta_power(beta, s):
-    """beta**s in fp64 by s successive multiplications.
-
-    Stops once the product is below 2^-80: from there on 1 - beta**s equals
-    1 in fp64, so the result of 1 - beta**s no longer changes.
-    """
-    p = 1.0
-    for _ in range(int(s)):
-        p *= beta
-        if p < 2.0 ** -80:
-            return 0.0
-    return p
+    """beta**s in fp64 by binary exponentiation (square and multiply, lowest
+    bit of s first): O(log s) operations for any s and any beta in [0, 1]."""
+    result, base, e = 1.0, float(beta), int(s)
+    while e > 0:
+        if e & 1:
+            result *= base
+        base *= base
+        e >>= 1
+    return result
 
 
 # --------------------------------------------------------------------------

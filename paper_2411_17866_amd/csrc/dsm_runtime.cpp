@@ -129,15 +129,15 @@ dsm_status make_layout(const dsm_problem* p, Layout* L, std::vector<dsm::Chunk>*
     return DSM_OK;
 }
 
-// beta^s in fp64 by s successive multiplications; once the product is below
-// 2^-80, 1 - beta^s is 1 in fp64 and no longer changes.
+// beta^s in fp64 by binary exponentiation (square and multiply, lowest bit
+// of s first): O(log s) operations for any s and beta.
 double beta_power(double beta, int64_t s) {
-    double p = 1.0;
-    for (int64_t k = 0; k < s; ++k) {
-        p *= beta;
-        if (p < 0x1p-80) return 0.0;
+    double result = 1.0, base = beta;
+    for (uint64_t e = static_cast<uint64_t>(s); e > 0; e >>= 1) {
+        if (e & 1u) result *= base;
+        base *= base;
     }
-    return p;
+    return result;
 }
 
 dsm_status check_ctx(dsm_ctx* ctx) {

@@ -335,3 +335,63 @@ def test_empty_problem_is_a_no_op():
     assert dsm.dsm_read_bounds(ar.ctx, 0).size == 0
     dsm.dsm_sync(ar.ctx)
     ar.destroy()
+
+
+# ---------------------------------------------------------------- limits, degenerate cases
+
+def test_max_workers_every_entry_point():
+    """n = 64 (the largest worker count): local AdamW, deterministic and
+    randomized global steps and the fused round end, against the oracle."""
+    n, H = 64, 2
+    numel = [5, 1000, 16385]
+    decay = [False, True, True]
+    local = dict(lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1)
+    ar, gen = make(numel, n, H, dsm.DSM_BASE_ADAMW, decay=decay, seed=64)
+    st = O.init_state(per_tensor(ar, ar.x), n, "adamw")
+    for t, (mode, fused) in enumerate(((dsm.DSM_SIGN_DET, False), (dsm.DSM_SIGN_RAND_ZERO, False),
+                                       (dsm.DSM_SIGN_RAND_FLIP, True))):
+        grads = {}
+        for k in range(H):
+            ar.g_rep.normal_(0.0, 0.01, generator=gen)
+            for i in range(n):
+                grads[(i, k)] = per_tensor(ar, ar.g_rep[i])
+            s = t * H + k + 1
+            if fused and k == H - 1:
+                dsm.dsm_round_end(ar.ctx, s, local, t, mode=mode, seed=3, **GLOB)
+            else:
+                dsm.dsm_local_step(ar.ctx, -1, s, **local)
+        if not fused:
+            dsm.dsm_global_step(ar.ctx, t, mode=mode, seed=3, **GLOB)
+        O.communication_round(st, lambda i, k: grads[(i, k)], t, H=H, local=local,
+                              glob=dict({k: v for k, v in GLOB.items() if k != "gamma"},
+                                        mode=mode, seed=3),
+                              decay=decay, prec="fp32")
+        gx, gm = per_tensor(ar, ar.x), per_tensor(ar, ar.m)
+        for p in range(len(numel)):
+            assert np.array_equal(gx[p].view(np.uint32), st["x"][p].view(np.uint32)), (t, p)
+            assert np.array_equal(gm[p].view(np.uint32), st["m"][p].view(np.uint32)), (t, p)
+    ar.destroy()
+
+
+@pytest.mark.parametrize("hp", [dict(eta=0.0, beta1=0.95, beta2=0.98, lam=0.1),
+                                dict(eta=0.8, beta1=1.0, beta2=0.0, lam=0.0),
+                                dict(eta=0.8, beta1=0.0, beta2=1.0, lam=0.0)])
+def test_global_step_degenerate_hyperparameters(hp):
+    """eta = 0 leaves x fixed; beta1 = 1 makes u the old momentum; beta2 = 1
+    freezes the momentum; beta = 0 forgets it.  Against the oracle, bitwise."""
+    n, H = 3, 1
+    ar, gen = make(RAGGED, n, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, seed=77)
+    _ready_for_global(ar, gen, H, n)
+    x0, m0 = per_tensor(ar, ar.x), per_tensor(ar, ar.m)
+    reps = [per_tensor(ar, ar.x_rep[i]) for i in range(n)]
+    dsm.dsm_global_step(ar.ctx, 0, gamma=1e-3, **hp)
+    gx, gm = per_tensor(ar, ar.x), per_tensor(ar, ar.m)
+    o32 = O.global_step(x0, m0, reps, gamma=1e-3, decay=DECAY, prec="fp32", **hp)
+    for p in range(len(RAGGED)):
+        assert np.array_equal(gx[p].view(np.uint32), o32["x"][p].view(np.uint32)), p
+        assert np.array_equal(gm[p].view(np.uint32), o32["m"][p].view(np.uint32)), p
+        if hp["eta"] == 0.0:
+            assert np.array_equal(gx[p], x0[p])
+        if hp["beta2"] == 1.0:
+            assert np.array_equal(gm[p], m0[p])
+    ar.destroy()

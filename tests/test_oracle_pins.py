@@ -360,17 +360,24 @@ def test_sgdm_single_step_matches_torch_exactly():
 
 
 def test_bias_correction_power():
-    """beta_power is beta**s (checked against exact rationals)."""
+    """beta_power is beta**s (checked against exact rationals), and 1 - beta**s
+    rounds to the correctly rounded fp32 value of the exact 1 - beta**s."""
     from fractions import Fraction
-    for beta in (0.9, 0.95, 0.999):
+    for beta in (0.5, 0.9, 0.95, 0.999, 1.0 - 2 ** -24):
         b = O.f32(beta)
-        for s in (1, 2, 7, 100, 1000):
+        for s in (1, 2, 7, 100, 1000, 123457):
             exact = Fraction(b) ** s
             got = O.beta_power(b, s)
-            if exact < Fraction(2) ** -80:
-                assert 1.0 - got == 1.0
-            else:
-                assert abs(Fraction(got) - exact) <= exact * Fraction(s + 1, 2 ** 52)
+            if exact < Fraction(2) ** -1000:      # below fp64's normal range
+                assert got < 2.0 ** -1000 and 1.0 - got == 1.0
+                continue
+            # Squaring doubles the relative error already in the base, so the
+            # bound is about s + 2 log2(s) roundings of 2^-53.
+            assert abs(Fraction(got) - exact) <= exact * Fraction(s + 2 * s.bit_length() + 2, 2 ** 53)
+            ex32 = np.float32(float(1 - exact))
+            assert np.float32(1.0 - got) == ex32 or abs(float(1 - exact) - float(ex32)) < 1e-12
+    assert O.beta_power(1.0, 2 ** 40) == 1.0 and O.beta_power(0.0, 5) == 0.0
+    assert O.beta_power(0.9, 0) == 1.0
 
 
 # ---------------------------------------------------------------- randomized sign
