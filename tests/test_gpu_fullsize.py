@@ -1,14 +1,19 @@
-"""Parity at full size: the GPT-2 1.5B-shaped workload (580 tensors,
-d = 1,557,611,200, n = 4 replicas, H = 12 local AdamW steps) in the launch
-configuration the benchmark times.
+"""Parity at full size for every GPT-2-shaped workload, in the launch
+configuration the benchmark times:
+
+  small   124M parameters, n = 8, H = 12, AdamW, deterministic sign
+  medium  355M, n = 8, H = 12, SGD + Polyak momentum, randomized sign Eq. (9)
+  large   774M, n = 8, H = 24, AdamW, heavy-tailed gradients, deterministic
+  xl      1.56B, n = 4, H = 12, AdamW, deterministic and randomized sign
 
 Every update is elementwise given the per-tensor bound, so outputs are
-checked on sampled elements the oracle computes one by one (random elements
-plus the first and last elements of every tensor and the chunk seams of the
-largest one), against the oracle in fp32 and fp64 as in tests/parity.py.
-The randomized bound B_p is checked against the maximum of |u| over the
-whole tensor, computed independently on the GPU (exact), and against the
-oracle on whole tensors for the smaller tensors.
+checked on sampled elements the oracle computes one by one (random elements,
+the first and last elements of every tensor, chunk seams of the largest
+one), against the oracle in fp32 and fp64 as in tests/parity.py.  Each
+workload runs one local step (sampled), split rounds ending in
+dsm_global_step, and a fused round ending in dsm_round_end (sampled).  The
+randomized bound B_p is checked against the exact max |u| of every whole
+tensor on the GPU, and against the oracle on whole tensors for a subset.
 """
 import numpy as np
 import pytest
@@ -19,12 +24,12 @@ from paper_2411_17866_amd import arena as A
 from paper_2411_17866_amd import dsm
 from paper_2411_17866_amd import workloads as W
 
-from parity import adamw_scales, global_scales, rel_check, rms, scaled_check
+from parity import adamw_scales, global_scales, rel_check, rms, scaled_check, sgdm_scales
 
 pytestmark = pytest.mark.gpu
 
 
-def _sample_indices(ar, rng, n_random=200_000):
+def _sample_indices(ar, rng, n_random=150_000):
     """(tensor index p, element index j) pairs to check."""
     ps, js = [], []
     for p, k in enumerate(ar.numel):
@@ -41,162 +46,231 @@ def _sample_indices(ar, rng, n_random=200_000):
     rj = (rng.random(n_random) * np.asarray(ar.numel)[rp]).astype(np.int64)
     ps.append(rp)
     js.append(rj)
-    p = np.concatenate(ps).astype(np.int64)
-    j = np.concatenate(js).astype(np.int64)
-    return p, j
+    return np.concatenate(ps).astype(np.int64), np.concatenate(js).astype(np.int64)
 
 
 def _gather(flat, idx):
     return flat[idx].cpu().numpy().copy()
 
 
-@pytest.fixture(scope="module")
-def xl():
-    w = W.get("xl")
+class Run:
+    """One workload's arenas, initialised, plus the sampled elements."""
+
+    def __init__(self, name):
+        self.w = W.get(name)
+        w = self.w
+        self.adamw = w.base == W.BASE_ADAMW
+        self.mode = dsm.DSM_SIGN_RAND_FLIP if 1 in w.sign_modes else dsm.DSM_SIGN_DET
+        self.ar = A.Arenas(w.numel, w.n_workers, w.local_steps, w.base, decay=w.decay,
+                           randomized=True)
+        gen = torch.Generator(device="cuda").manual_seed(w.seed)
+        W.fill_params_(self.ar.x, w, gen)
+        self.ar.init()
+        rng = np.random.default_rng(2024)
+        self.p, self.j = _sample_indices(self.ar, rng)
+        self.idx = torch.as_tensor(np.asarray(self.ar.offsets)[self.p] + self.j, device="cuda")
+        self.decay = np.asarray(w.decay)[self.p]
+        self.state_keys = ("x_rep", "g_rep", "s1_rep") + (("s2_rep",) if self.adamw else ())
+
+    def grads(self, s):
+        for i in range(self.w.n_workers):
+            W.fill_grads_(self.ar.g_rep[i], self.w, i, s)
+
+    def local(self, s):
+        dsm.dsm_local_step(self.ar.ctx, -1, s, **self.w.local)
+
+    def sample_state(self, keys):
+        torch.cuda.synchronize()
+        return {k: [_gather(getattr(self.ar, k)[i], self.idx) for i in range(self.w.n_workers)]
+                for k in keys}
+
+    def glob_kw(self):
+        return dict(gamma=self.w.local["lr"], seed=self.w.philox_seed, **self.w.glob)
+
+
+@pytest.fixture(scope="module", params=["small", "medium", "large", "xl"])
+def run(request):
     if torch.cuda.get_device_properties(0).total_memory < 200e9:
         pytest.skip("needs the full HBM of one MI355X")
-    ar = A.Arenas(w.numel, w.n_workers, w.local_steps, w.base, decay=w.decay, randomized=True)
-    gen = torch.Generator(device="cuda").manual_seed(w.seed)
-    W.fill_params_(ar.x, w, gen)
-    for i in range(w.n_workers):
-        W.fill_grads_(ar.g_rep[i], w, i, 0)
-    ar.init()
-    rng = np.random.default_rng(2024)
-    p, j = _sample_indices(ar, rng)
-    idx = torch.as_tensor(np.asarray(ar.offsets)[p] + j, device="cuda")
-    yield w, ar, p, j, idx
-    ar.destroy()
-    del ar
+    r = Run(request.param)
+    yield r
+    r.ar.destroy()
+    del r
     torch.cuda.empty_cache()
 
 
-def test_fullsize_local_adamw_sampled(xl):
-    w, ar, p, j, idx = xl
-    n = w.n_workers
-    torch.cuda.synchronize()
-    before = {k: [_gather(getattr(ar, k)[i], idx) for i in range(n)]
-              for k in ("x_rep", "g_rep", "s1_rep", "s2_rep")}
-    dsm.dsm_local_step(ar.ctx, -1, 1, **w.local)
-    torch.cuda.synchronize()
-    after = {k: [_gather(getattr(ar, k)[i], idx) for i in range(n)]
-             for k in ("x_rep", "s1_rep", "s2_rep")}
-    decay = np.asarray(w.decay)[p]
+def _local_oracle(r, before, i, sel, s, dec, prec):
+    """Oracle local step of worker i on the sampled elements sel."""
+    w = r.w
+    if r.adamw:
+        kw = dict(w.local, weight_decay=w.local["weight_decay"] if dec else 0.0, step=s)
+        return O.local_adamw_step(*(before[k][i][sel] for k in ("x_rep", "g_rep", "s1_rep",
+                                                                "s2_rep")), prec=prec, **kw)
+    return O.local_sgdm_step(*(before[k][i][sel] for k in ("x_rep", "g_rep", "s1_rep")),
+                             lr=w.local["lr"], momentum=w.local["beta1"], prec=prec)
+
+
+def test_fullsize_local_step_sampled(run):
+    r = run
+    w = r.w
+    r.grads(1)
+    before = r.sample_state(r.state_keys)
+    r.local(1)
+    after = r.sample_state([k for k in r.state_keys if k != "g_rep"])
     nonbit = 0
-    for i in range(n):
+    for i in range(w.n_workers):
         for dec in (True, False):
-            sel = decay == dec
-            x, g, m, v = (before[k][i][sel] for k in ("x_rep", "g_rep", "s1_rep", "s2_rep"))
-            kw = dict(w.local, weight_decay=w.local["weight_decay"] if dec else 0.0, step=1)
-            o32 = O.local_adamw_step(x, g, m, v, prec="fp32", **kw)
-            o64 = O.local_adamw_step(x, g, m, v, prec="fp64", **kw)
-            got = [after[k][i][sel] for k in ("x_rep", "s1_rep", "s2_rep")]
-            for name, gg, oo in zip("xmv", got, o32):
-                nonbit += rel_check(gg, oo, f"xl worker {i} {name}")
-            s_m, s_v, s_x = adamw_scales(x, g, m, v, o64=o64, **kw)
-            for gg, oo, sc, name in zip(got, o64, (s_x, s_m, s_v), "xmv"):
-                scaled_check(gg, oo, sc, f"xl worker {i} {name} vs fp64")
-    print(f"xl local AdamW: {p.size} sampled elements x {n} workers, {nonbit} not bit-identical")
+            sel = r.decay == dec
+            if not sel.any():
+                continue
+            o32 = _local_oracle(r, before, i, sel, 1, dec, "fp32")
+            o64 = _local_oracle(r, before, i, sel, 1, dec, "fp64")
+            x, g, m = (before[k][i][sel] for k in ("x_rep", "g_rep", "s1_rep"))
+            if r.adamw:
+                kw = dict(w.local, weight_decay=w.local["weight_decay"] if dec else 0.0, step=1)
+                s_m, s_v, s_x = adamw_scales(x, g, m, before["s2_rep"][i][sel], o64=o64, **kw)
+                names, scales = ("x_rep", "s1_rep", "s2_rep"), (s_x, s_m, s_v)
+            else:
+                s_m, s_x = sgdm_scales(x, g, m, lr=w.local["lr"], momentum=w.local["beta1"])
+                names, scales = ("x_rep", "s1_rep"), (s_x, s_m)
+            for k, name in enumerate(names):
+                got = after[name][i][sel]
+                nonbit += rel_check(got, o32[k], f"{w.name} worker {i} {name}")
+                scaled_check(got, o64[k], scales[k], f"{w.name} worker {i} {name} vs fp64")
+    print(f"{w.name} local step: {r.p.size} sampled elements x {w.n_workers} workers, "
+          f"{nonbit} not bit-identical")
 
 
-def _local_round(w, ar, t):
-    """All H local steps of round t on every worker, fresh gradients per step,
-    after restarting the round from the synchronised model."""
-    dsm.dsm_sync(ar.ctx)
-    for k in range(w.local_steps):
-        s = t * w.local_steps + k + 1
-        for i in range(w.n_workers):
-            W.fill_grads_(ar.g_rep[i], w, i, s)
-        dsm.dsm_local_step(ar.ctx, -1, s, **w.local)
-
-
-def test_fullsize_global_det_sampled(xl):
-    w, ar, p, j, idx = xl
-    n = w.n_workers
-    # Round 0 with its global step, then the local steps of round 1, so that
-    # the global step under test sees a non-zero momentum.
-    _local_round(w, ar, 0)
-    dsm.dsm_global_step(ar.ctx, 0, gamma=w.local["lr"], **w.glob)
-    _local_round(w, ar, 1)
-    torch.cuda.synchronize()
-    x0, m0 = _gather(ar.x, idx), _gather(ar.m, idx)
-    reps = [_gather(ar.x_rep[i], idx) for i in range(n)]
-    dsm.dsm_global_step(ar.ctx, 1, gamma=w.local["lr"], **w.glob)
-    torch.cuda.synchronize()
-    gx, gm = _gather(ar.x, idx), _gather(ar.m, idx)
-    decay = np.asarray(w.decay)[p]
+def _check_global_sampled(r, x0, m0, reps, t, gx, gm, mode):
+    """Sampled x, m after a global step against the oracle (randomized: with
+    each tensor's bound from the GPU, checked separately)."""
+    w = r.w
+    kw = dict(gamma=w.local["lr"], t=t, seed=w.philox_seed, **w.glob)
     nonbit = flips = 0
-    for dec in (True, False):
-        sel = decay == dec
-        if not sel.any():
-            continue
-        args = dict(gamma=w.local["lr"], decay=[dec], **w.glob)
-        o32 = O.global_step([x0[sel]], [m0[sel]], [[r[sel]] for r in reps], prec="fp32", **args)
-        o64 = O.global_step([x0[sel]], [m0[sel]], [[r[sel]] for r in reps], prec="fp64", **args)
-        nonbit += rel_check(gx[sel], o32["x"][0], f"xl global x decay={dec}")
-        nonbit += rel_check(gm[sel], o32["m"][0], f"xl global m decay={dec}")
-        lam_p = w.glob["lam"] if dec else 0.0
-        s_u, s_m, s_x = global_scales(x0[sel], m0[sel], [r[sel] for r in reps], o64["S"][0],
-                                      gamma=w.local["lr"], eta=w.glob["eta"],
-                                      beta1=w.glob["beta1"], beta2=w.glob["beta2"], lam_p=lam_p)
-        scaled_check(gm[sel], o64["m"][0], s_m, "xl global m vs fp64")
-        flip = o32["S"][0] != o64["S"][0]
-        if flip.any():
-            assert np.all(np.abs(o64["u"][0][flip]) < 1e-6 * rms(o64["u"][0]))
-        flips += int(flip.sum())
-        scaled_check(gx[sel], o64["x"][0], s_x, "xl global x vs fp64", mask=~flip)
-    # Broadcast: every replica equals x, checked on the GPU for the whole arena.
-    for i in range(n):
-        assert torch.equal(ar.x_rep[i].view(torch.int32), ar.x.view(torch.int32))
-    print(f"xl global det: {p.size} sampled elements, {nonbit} not bit-identical, {flips} flips vs fp64")
+    if mode == dsm.DSM_SIGN_DET:
+        for dec in (True, False):
+            s_ = r.decay == dec
+            if not s_.any():
+                continue
+            args = ([x0[s_]], [m0[s_]], [[rp[s_]] for rp in reps])
+            o32 = O.global_step(*args, decay=[dec], prec="fp32", **kw)
+            o64 = O.global_step(*args, decay=[dec], prec="fp64", **kw)
+            nonbit += rel_check(gx[s_], o32["x"][0], f"{w.name} global x")
+            nonbit += rel_check(gm[s_], o32["m"][0], f"{w.name} global m")
+            lam_p = w.glob["lam"] if dec else 0.0
+            _, s_m, s_x = global_scales(x0[s_], m0[s_], [rp[s_] for rp in reps], o64["S"][0],
+                                        gamma=w.local["lr"], eta=w.glob["eta"],
+                                        beta1=w.glob["beta1"], beta2=w.glob["beta2"], lam_p=lam_p)
+            scaled_check(gm[s_], o64["m"][0], s_m, f"{w.name} global m vs fp64")
+            flip = o32["S"][0] != o64["S"][0]
+            if flip.any():
+                assert np.all(np.abs(o64["u"][0][flip]) < 1e-6 * rms(o64["u"][0]))
+            flips += int(flip.sum())
+            scaled_check(gx[s_], o64["x"][0], s_x, f"{w.name} global x vs fp64", mask=~flip)
+        return nonbit, flips
+    B = dsm.dsm_read_bounds(r.ar.ctx, len(w.numel))
+    qs = np.unique(r.p)
+    sel = [r.p == q for q in qs]
+    o = O.global_step([x0[s_] for s_ in sel], [m0[s_] for s_ in sel],
+                      [[rp[s_] for s_ in sel] for rp in reps], decay=[w.decay[q] for q in qs],
+                      tensor_ids=qs, element_ids=[r.j[s_] for s_ in sel], bounds=[B[q] for q in qs],
+                      mode=mode, prec="fp32", **kw)
+    for a, s_ in enumerate(sel):
+        nonbit += rel_check(gm[s_], o["m"][a], f"{w.name} rand m tensor {qs[a]}")
+        nonbit += rel_check(gx[s_], o["x"][a], f"{w.name} rand x tensor {qs[a]}")
+    return nonbit, flips
 
 
-def test_fullsize_global_randomized(xl):
-    w, ar, p, j, idx = xl
-    n = w.n_workers
-    t, seed = 2, w.philox_seed
-    _local_round(w, ar, t)
-    torch.cuda.synchronize()
-    whole = [q for q, (name, _) in enumerate(w.tensors)
-             if name in ("wpe", "ln_f.weight", "ln_f.bias") or name.startswith("h0.")
-             or name.startswith("h47.")]
-    wx = [ar.views(ar.x)[q].cpu().numpy().copy() for q in whole]
-    wm = [ar.views(ar.m)[q].cpu().numpy().copy() for q in whole]
-    wr = [[ar.views(ar.x_rep[i])[q].cpu().numpy().copy() for q in whole] for i in range(n)]
-    x0, m0 = _gather(ar.x, idx), _gather(ar.m, idx)
-    reps = [_gather(ar.x_rep[i], idx) for i in range(n)]
-    dsm.dsm_global_step(ar.ctx, t, gamma=w.local["lr"], mode=dsm.DSM_SIGN_RAND_FLIP, seed=seed,
-                        **w.glob)
+def _whole_subset(r):
+    return [q for q, (name, _) in enumerate(r.w.tensors)
+            if name in ("wpe", "ln_f.weight", "ln_f.bias") or name.startswith("h0.")]
+
+
+def _check_bounds(r, t, whole, wx, wm, wr, mode):
+    """B_p = max |u| over every whole tensor (on the GPU, exact), and the
+    oracle's u and B on the whole tensors of the subset."""
+    w, ar = r.w, r.ar
     B = dsm.dsm_read_bounds(ar.ctx, len(w.numel))
-    # B_p is max |u| over each whole tensor: checked on the GPU from u_scratch
-    # for every tensor (an exact maximum, computed independently by torch).
     u_views = ar.views(ar.u)
     Bt = torch.stack([uv.abs().max() for uv in u_views]).cpu().numpy()
     np.testing.assert_array_equal(B.view(np.uint32), Bt.view(np.uint32))
-    # Whole tensors against the oracle: u and B bit-identical.
-    gargs = dict(gamma=w.local["lr"], t=t, seed=seed, prec="fp32", **w.glob)
-    ow = O.global_step(wx, wm, wr, decay=[w.decay[q] for q in whole], tensor_ids=whole,
-                       mode=O.SIGN_RAND_FLIP, **gargs)
+    ow = O.global_step(wx, wm, wr, gamma=w.local["lr"], decay=[w.decay[q] for q in whole], t=t,
+                       seed=w.philox_seed, tensor_ids=whole, mode=mode, prec="fp32", **w.glob)
     for a, q in enumerate(whole):
         assert np.float32(ow["B"][a]).view(np.uint32) == B[q].view(np.uint32), w.tensors[q][0]
         np.testing.assert_array_equal(u_views[q].cpu().numpy().view(np.uint32),
                                       ow["u"][a].view(np.uint32))
-        np.testing.assert_array_equal(ar.views(ar.x)[q].cpu().numpy().view(np.uint32),
-                                      ow["x"][a].view(np.uint32))
-    # Sampled elements of every tensor, with the tensor's bound from the GPU
-    # (checked above) and each element's own Philox draw.
-    torch.cuda.synchronize()
-    gx, gm = _gather(ar.x, idx), _gather(ar.m, idx)
-    qs = np.unique(p)
-    sel = [p == q for q in qs]
-    o = O.global_step([x0[s_] for s_ in sel], [m0[s_] for s_ in sel],
-                      [[r[s_] for s_ in sel] for r in reps], decay=[w.decay[q] for q in qs],
-                      tensor_ids=qs, element_ids=[j[s_] for s_ in sel],
-                      bounds=[B[q] for q in qs], mode=O.SIGN_RAND_FLIP, **gargs)
+
+
+def test_fullsize_split_rounds_sampled(run):
+    r = run
+    w, ar = r.w, r.ar
+    H = w.local_steps
+    nonbit = flips = 0
+    # Round 1 sees a non-zero momentum.  A workload with both signs runs the
+    # deterministic one in round 0 and the randomized one in round 1.
+    modes = (dsm.DSM_SIGN_DET, r.mode) if 0 in w.sign_modes else (r.mode, r.mode)
+    for t in (0, 1):
+        mode = modes[t]
+        dsm.dsm_sync(ar.ctx)
+        for k in range(H):
+            r.grads(t * H + k + 1)
+            r.local(t * H + k + 1)
+        torch.cuda.synchronize()
+        x0, m0 = _gather(ar.x, r.idx), _gather(ar.m, r.idx)
+        reps = [_gather(ar.x_rep[i], r.idx) for i in range(w.n_workers)]
+        whole = _whole_subset(r)
+        if mode != dsm.DSM_SIGN_DET:
+            wx = [ar.views(ar.x)[q].cpu().numpy().copy() for q in whole]
+            wm = [ar.views(ar.m)[q].cpu().numpy().copy() for q in whole]
+            wr = [[ar.views(ar.x_rep[i])[q].cpu().numpy().copy() for q in whole]
+                  for i in range(w.n_workers)]
+        dsm.dsm_global_step(ar.ctx, t, mode=mode, **r.glob_kw())
+        torch.cuda.synchronize()
+        if mode != dsm.DSM_SIGN_DET:
+            _check_bounds(r, t, whole, wx, wm, wr, mode)
+        gx, gm = _gather(ar.x, r.idx), _gather(ar.m, r.idx)
+        nb, fl = _check_global_sampled(r, x0, m0, reps, t, gx, gm, mode)
+        nonbit += nb
+        flips += fl
+        for i in range(w.n_workers):
+            for a, b in zip(ar.views(ar.x_rep[i]), ar.views(ar.x)):
+                assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+    print(f"{w.name} split rounds: {r.p.size} sampled elements, {nonbit} not bit-identical, "
+          f"{flips} flips vs fp64")
+
+
+def test_fullsize_fused_round_sampled(run):
+    """H-1 local steps, then dsm_round_end with the lazy broadcast; the
+    oracle recomputes step H from the sampled step-(H-1) state."""
+    r = run
+    w, ar = r.w, r.ar
+    H = w.local_steps
+    t = 2
+    dsm.dsm_sync(ar.ctx)
+    for k in range(H - 1):
+        r.grads(t * H + k + 1)
+        r.local(t * H + k + 1)
+    r.grads(t * H + H)
+    before = r.sample_state(r.state_keys)
+    x0, m0 = _gather(ar.x, r.idx), _gather(ar.m, r.idx)
+    dsm.dsm_round_end(ar.ctx, t * H + H, w.local, t, mode=r.mode, broadcast=False, **r.glob_kw())
+    after = r.sample_state(("s1_rep",) + (("s2_rep",) if r.adamw else ()))
+    gx, gm = _gather(ar.x, r.idx), _gather(ar.m, r.idx)
     nonbit = 0
-    for a, s_ in enumerate(sel):
-        nonbit += rel_check(gm[s_], o["m"][a], f"xl rand m tensor {qs[a]}")
-        nonbit += rel_check(gx[s_], o["x"][a], f"xl rand x tensor {qs[a]}")
-    for i in range(n):
-        assert torch.equal(ar.x_rep[i].view(torch.int32), ar.x.view(torch.int32))
-    print(f"xl randomized: {len(whole)} whole tensors and {p.size} sampled elements, "
-          f"{nonbit} not bit-identical")
+    reps = []
+    for i in range(w.n_workers):
+        xr = np.empty_like(x0)
+        for dec in (True, False):
+            sel = r.decay == dec
+            if not sel.any():
+                continue
+            o = _local_oracle(r, before, i, sel, t * H + H, dec, "fp32")
+            nonbit += rel_check(after["s1_rep"][i][sel], o[1], f"{w.name} fused s1")
+            if r.adamw:
+                nonbit += rel_check(after["s2_rep"][i][sel], o[2], f"{w.name} fused s2")
+            xr[sel] = o[0]
+        reps.append(xr.astype(np.float32))
+    nb, flips = _check_global_sampled(r, x0, m0, reps, t, gx, gm, r.mode)
+    print(f"{w.name} fused round: {r.p.size} sampled elements, {nonbit + nb} not bit-identical, "
+          f"{flips} flips vs fp64")
