@@ -7,6 +7,13 @@ import torch
 
 from . import dsm
 
+# Each buffer's base is moved by a different multiple of this many floats
+# (1 MiB + 1 KiB).  Large allocations start on 2 MiB boundaries, so without it
+# the same element of x, m and the replicas shares its low address bits across
+# buffers; on MI355X the global step then runs ~15% slower in a
+# placement-dependent way (13.8-14.1 ms against 11.8-12.1 ms at GPT-2 xl).
+STAGGER_FLOATS = (1 << 18) + 256
+
 
 class Arenas:
     """The arenas and workspace of one problem, allocated with torch, plus the
@@ -28,16 +35,29 @@ class Arenas:
         self.problem = dsm.make_problem(self.numel, self.n, self.H, self.base, self.decay)
         self.arena_elems, self.offsets, self.workspace_bytes = dsm.dsm_layout(self.problem)
         a = max(self.arena_elems, 64)
-        f32 = torch.float32
-        self.x = torch.zeros(a, dtype=f32, device=device)
-        self.m = torch.zeros(a, dtype=f32, device=device)
-        self.x_rep = torch.zeros(self.n, a, dtype=f32, device=device)
-        self.g_rep = torch.zeros(self.n, a, dtype=f32, device=device)
-        self.s1_rep = torch.zeros(self.n, a, dtype=f32, device=device)
-        self.s2_rep = (torch.zeros(self.n, a, dtype=f32, device=device)
-                       if self.base == dsm.DSM_BASE_ADAMW else None)
-        self.u = torch.zeros(a, dtype=f32, device=device) if randomized else None
-        self.v = torch.zeros(a, dtype=f32, device=device) if global_adamw else None
+        self._storage = []
+        self._k = 0
+
+        def alloc(*shape):
+            # A view at a buffer-specific offset (a multiple of 64 floats, so
+            # 256-byte alignment is kept) into a slightly larger allocation.
+            pad = self._k * STAGGER_FLOATS
+            self._k += 1
+            count = 1
+            for s_ in shape:
+                count *= s_
+            flat = torch.zeros(count + pad, dtype=torch.float32, device=device)
+            self._storage.append(flat)
+            return flat[pad:].view(*shape)
+
+        self.x = alloc(a)
+        self.m = alloc(a)
+        self.x_rep = alloc(self.n, a)
+        self.g_rep = alloc(self.n, a)
+        self.s1_rep = alloc(self.n, a)
+        self.s2_rep = alloc(self.n, a) if self.base == dsm.DSM_BASE_ADAMW else None
+        self.u = alloc(a) if randomized else None
+        self.v = alloc(a) if global_adamw else None
         self.workspace = torch.zeros(max(self.workspace_bytes, 256), dtype=torch.uint8,
                                      device=device)
         self.ctx = None
