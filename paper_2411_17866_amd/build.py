@@ -57,8 +57,10 @@ def _run(cmd, verbose):
 def build(verbose=False, out=LIBPATH, defines=()):
     """Compiles the kernels and the host runtime and links libdsm.so.
 
-    defines: extra -D settings of the build-time tuning knobs (DSM_UNROLL,
-    DSM_NT, DSM_CHUNK_ELEMS); the defaults are the tuned values.
+    defines: extra -D settings of the build-time tuning knobs (DSM_BLOCK_THREADS,
+    DSM_UNROLL, DSM_ITERS, DSM_NT, DSM_CHUNK_ELEMS, DSM_XCD_MAP,
+    DSM_XCD_MAP_LOCAL, DSM_XCD_MAP_ROUND_END); the defaults are the tuned
+    values.
     """
     os.makedirs(os.path.dirname(out), exist_ok=True)
     objdir = os.path.join(OBJDIR, "_".join(d.replace("=", "") for d in defines) or "default")

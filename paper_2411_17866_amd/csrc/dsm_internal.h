@@ -16,7 +16,11 @@ namespace dsm {
 #endif
 constexpr int kChunkElems = DSM_CHUNK_ELEMS;
 static_assert(kChunkElems % 1024 == 0, "chunk must be a multiple of 256 threads x 4");
-constexpr int kBlockThreads = 256;
+#ifndef DSM_BLOCK_THREADS
+#define DSM_BLOCK_THREADS 256
+#endif
+constexpr int kBlockThreads = DSM_BLOCK_THREADS;
+static_assert(kBlockThreads % 64 == 0 && kBlockThreads <= 1024, "whole waves, at most 1024 threads");
 // float4 groups per stream in flight per thread, and loop iterations per
 // work-group: a work-group takes one piece of kBlockThreads * kUnroll *
 // kIters float4 groups of a chunk (build-time tuning knobs).
@@ -24,7 +28,7 @@ constexpr int kBlockThreads = 256;
 #define DSM_UNROLL 1
 #endif
 #ifndef DSM_ITERS
-#define DSM_ITERS 2
+#define DSM_ITERS 1
 #endif
 constexpr int kUnroll = DSM_UNROLL;
 constexpr int kIters = DSM_ITERS;

@@ -62,21 +62,59 @@ __device__ __forceinline__ void store_group(f4 v, f4* p, int q, int nfull, int l
         store_head(v, reinterpret_cast<float*>(p + q), len - 4 * q);
 }
 
-// The piece of a chunk this work-group processes: work-group b takes piece
-// b % kSplit of chunk b / kSplit, float4 groups [q_lo, q_hi).  Work-groups
-// are short-lived and dispatched in address order, so the addresses in
-// flight form one compact front across the arena.
+// The piece of a chunk this work-group processes: work item w (below) takes
+// piece w % kSplit of chunk w / kSplit, float4 groups [q_lo, q_hi).
+// Work-groups are short-lived and handle one piece each, so the addresses in
+// flight form compact fronts that sweep the arena.
 struct Piece {
     Chunk c;
     int q_lo, q_hi;  // float4 groups of the chunk handled here
     int nfull;       // groups of four valid lanes in the chunk
 };
 
+#ifndef DSM_XCD_MAP
+#define DSM_XCD_MAP 0
+#endif
+#ifndef DSM_XCD_MAP_LOCAL
+#define DSM_XCD_MAP_LOCAL 1
+#endif
+#ifndef DSM_XCD_MAP_ROUND_END
+#define DSM_XCD_MAP_ROUND_END 2
+#endif
+constexpr uint32_t kXcds = 8;  // MI355X: work-groups go to its 8 XCDs round-robin
+constexpr int kMapLocal = DSM_XCD_MAP_LOCAL;         // local-step kernels
+constexpr int kMapRoundEnd = DSM_XCD_MAP_ROUND_END;  // fused round end
+constexpr int kMapOther = DSM_XCD_MAP;               // every other chunk kernel
+
+// Work item of this work-group.  MAP 0: the work-group index itself (XCD k
+// takes piece k mod 8 of every chunk).  1: XCD k takes the k-th eighth of the
+// grid row, in order.  2: XCD k takes whole chunks (chunk 8r + k in group r).
+// Modes 1 and 2 are bijections on a prefix of the row and the identity on the
+// rest.
+template <int MAP>
+__device__ __forceinline__ uint32_t work_index() {
+    const uint32_t b = blockIdx.x;
+    if constexpr (MAP == 1) {
+        const uint32_t per = gridDim.x / kXcds;
+        if (b >= per * kXcds) return b;
+        return (b % kXcds) * per + b / kXcds;
+    } else if constexpr (MAP == 2) {
+        const uint32_t group = kXcds * kSplit;
+        if (b >= (gridDim.x / group) * group) return b;
+        const uint32_t r = b / kXcds, x = b % kXcds;
+        return (r / kSplit) * group + x * kSplit + r % kSplit;
+    } else {
+        return b;
+    }
+}
+
+template <int MAP = kMapOther>
 __device__ __forceinline__ Piece piece_of(const Chunk* __restrict__ chunks) {
     Piece pc;
-    pc.c = chunks[blockIdx.x / kSplit];
+    const uint32_t wi = work_index<MAP>();
+    pc.c = chunks[wi / kSplit];
     const int nvec = (pc.c.len + 3) >> 2;
-    pc.q_lo = static_cast<int>(blockIdx.x % kSplit) * kPieceVec;
+    pc.q_lo = static_cast<int>(wi % kSplit) * kPieceVec;
     pc.q_hi = min(nvec, pc.q_lo + kPieceVec);
     pc.nfull = pc.c.len >> 2;
     return pc;
@@ -117,7 +155,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_local_adamw(
     const Chunk* __restrict__ chunks, float* __restrict__ x_rep, const float* __restrict__ x_src,
     int64_t src_stride, const float* __restrict__ g_rep, float* __restrict__ s1,
     float* __restrict__ s2, int64_t stride, int worker0, AdamScalars sc) {
-    const Piece pc = piece_of(chunks);
+    const Piece pc = piece_of<kMapLocal>(chunks);
     const Chunk& c = pc.c;
     const int64_t w = worker0 + static_cast<int>(blockIdx.y);
     const int64_t base = w * stride + c.off;
@@ -168,7 +206,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_local_sgdm(
     const Chunk* __restrict__ chunks, float* __restrict__ x_rep, const float* __restrict__ x_src,
     int64_t src_stride, const float* __restrict__ g_rep, float* __restrict__ s1, int64_t stride,
     int worker0, SgdScalars sc) {
-    const Piece pc = piece_of(chunks);
+    const Piece pc = piece_of<kMapLocal>(chunks);
     const Chunk& c = pc.c;
     const int64_t w = worker0 + static_cast<int>(blockIdx.y);
     const int64_t base = w * stride + c.off;
@@ -508,7 +546,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_round_end(
     float* __restrict__ u_out, uint32_t* __restrict__ bound_bits, int64_t stride,
     AdamScalars as, SgdScalars ss, GlobalScalars gs) {
     __shared__ uint32_t wave_max[kBlockThreads / 64];
-    const Piece pc = piece_of(chunks);
+    const Piece pc = piece_of<kMapRoundEnd>(chunks);
     const Chunk& c = pc.c;
     const int n = N > 0 ? N : gs.n;
     f4* __restrict__ xp = reinterpret_cast<f4*>(x + c.off);
