@@ -1,0 +1,758 @@
+// Host-only check of the library's runtime (paper_2411_17866_amd/csrc/dsm_runtime.cpp).
+//
+// Built with g++ and the address and undefined-behaviour sanitizers, and
+// linked against stubs of the four HIP runtime calls the runtime makes and of
+// the kernel launchers, so no GPU and no HIP runtime library are involved.
+// "Device" buffers are host allocations and the stub copy is memcpy.  Each
+// launch stub records its arguments, so the checks see exactly what every
+// entry point would enqueue:
+//   * dsm_layout on random valid and invalid problems;
+//   * the chunk table dsm_init uploads (every element once, no chunk across a
+//     tensor, decay flags);
+//   * the state machine of Algorithm 1 and which source each local step reads
+//     (the replica, or x after a global step without broadcast);
+//   * the fp32 coefficients formed on the host, against long double;
+//   * error paths: no device, failed launches, bad hyperparameters, NULLs.
+// Prints "all checks passed" and exits 0, or lists the failures and exits 1.
+#include <cmath>
+#include <cstdint>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <random>
+#include <string>
+#include <vector>
+
+#include "dsm.h"
+#include "dsm_internal.h"
+
+namespace {
+
+int g_devices = 1;
+hipError_t g_launch_status = hipSuccess;
+int g_failures = 0;
+int g_checks = 0;
+
+#define CHECK(cond, ...)                                                          \
+    do {                                                                          \
+        ++g_checks;                                                               \
+        if (!(cond)) {                                                            \
+            ++g_failures;                                                         \
+            std::fprintf(stderr, "FAIL line %d: %s: ", __LINE__, #cond);          \
+            std::fprintf(stderr, __VA_ARGS__);                                    \
+            std::fprintf(stderr, "\n");                                           \
+        }                                                                         \
+    } while (0)
+
+struct Launch {
+    std::string kind;
+    const dsm::Chunk* chunks = nullptr;
+    int64_t n_chunks = -1;
+    const float* x = nullptr;
+    const float* x_rep = nullptr;
+    const float* x_src = nullptr;
+    int64_t src_stride = -1;
+    const float* s2 = nullptr;
+    const float* u = nullptr;
+    const float* v = nullptr;
+    const uint32_t* bounds = nullptr;
+    int worker0 = -1, n_workers = -1, n_tensors = -1;
+    int64_t stride = -1;
+    bool broadcast = false, adamw = false;
+    dsm::AdamScalars as{};
+    dsm::SgdScalars ss{};
+    dsm::GlobalScalars gs{};
+};
+std::vector<Launch> g_log;
+
+hipError_t record(const Launch& l) {
+    g_log.push_back(l);
+    return g_launch_status;
+}
+
+}  // namespace
+
+// ------------------------------------------------------------ HIP runtime stubs
+
+extern "C" {
+hipError_t hipGetDeviceCount(int* count) {
+    *count = g_devices;
+    return hipSuccess;
+}
+const char* hipGetErrorString(hipError_t) { return "stubbed HIP error"; }
+hipError_t hipMemcpyAsync(void* dst, const void* src, size_t bytes, hipMemcpyKind, hipStream_t) {
+    std::memcpy(dst, src, bytes);
+    return hipSuccess;
+}
+hipError_t hipStreamSynchronize(hipStream_t) { return hipSuccess; }
+}
+
+// ------------------------------------------------------------ launcher stubs
+
+namespace dsm {
+hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float*, float* v,
+                       float* x_rep, float*, float* s2, int64_t stride, int n, hipStream_t) {
+    Launch l;
+    l.kind = "init";
+    l.chunks = chunks;
+    l.n_chunks = n_chunks;
+    l.x = x;
+    l.x_rep = x_rep;
+    l.v = v;
+    l.s2 = s2;
+    l.stride = stride;
+    l.n_workers = n;
+    return record(l);
+}
+hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_rep,
+                              const float* x_src, int64_t src_stride, const float*, float*,
+                              float* s2, int64_t stride, int worker0, int n_workers,
+                              const AdamScalars& sc, hipStream_t) {
+    Launch l;
+    l.kind = "local_adamw";
+    l.chunks = chunks;
+    l.n_chunks = n_chunks;
+    l.x_rep = x_rep;
+    l.x_src = x_src;
+    l.src_stride = src_stride;
+    l.s2 = s2;
+    l.stride = stride;
+    l.worker0 = worker0;
+    l.n_workers = n_workers;
+    l.as = sc;
+    return record(l);
+}
+hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep,
+                             const float* x_src, int64_t src_stride, const float*, float*,
+                             int64_t stride, int worker0, int n_workers, const SgdScalars& sc,
+                             hipStream_t) {
+    Launch l;
+    l.kind = "local_sgdm";
+    l.chunks = chunks;
+    l.n_chunks = n_chunks;
+    l.x_rep = x_rep;
+    l.x_src = x_src;
+    l.src_stride = src_stride;
+    l.stride = stride;
+    l.worker0 = worker0;
+    l.n_workers = n_workers;
+    l.ss = sc;
+    return record(l);
+}
+hipError_t launch_round_end(const Chunk* chunks, int64_t n_chunks, int n_tensors, bool adamw,
+                            const RoundEndArgs& a, bool broadcast, hipStream_t) {
+    Launch l;
+    l.kind = "round_end";
+    l.chunks = chunks;
+    l.n_chunks = n_chunks;
+    l.n_tensors = n_tensors;
+    l.adamw = adamw;
+    l.x = a.x;
+    l.x_rep = a.x_rep;
+    l.x_src = a.x_src;
+    l.src_stride = a.src_stride;
+    l.s2 = a.s2;
+    l.u = a.u;
+    l.bounds = a.bound_bits;
+    l.stride = a.stride;
+    l.broadcast = broadcast;
+    l.as = a.as;
+    l.ss = a.ss;
+    l.gs = a.gs;
+    return record(l);
+}
+hipError_t launch_global_det(const Chunk* chunks, int64_t n_chunks, float* x, float*, float* v,
+                             float* x_rep, int64_t stride, const GlobalScalars& sc, bool broadcast,
+                             hipStream_t) {
+    Launch l;
+    l.kind = "global_det";
+    l.chunks = chunks;
+    l.n_chunks = n_chunks;
+    l.x = x;
+    l.v = v;
+    l.x_rep = x_rep;
+    l.stride = stride;
+    l.gs = sc;
+    l.broadcast = broadcast;
+    return record(l);
+}
+hipError_t launch_global_rand(const Chunk* chunks, int64_t n_chunks, int n_tensors, float* x,
+                              float*, float* x_rep, float* u, uint32_t* bound_bits, int64_t stride,
+                              const GlobalScalars& sc, bool broadcast, hipStream_t) {
+    Launch l;
+    l.kind = "global_rand";
+    l.chunks = chunks;
+    l.n_chunks = n_chunks;
+    l.n_tensors = n_tensors;
+    l.x = x;
+    l.x_rep = x_rep;
+    l.u = u;
+    l.bounds = bound_bits;
+    l.stride = stride;
+    l.gs = sc;
+    l.broadcast = broadcast;
+    return record(l);
+}
+hipError_t launch_broadcast(const Chunk* chunks, int64_t n_chunks, const float* x, float* x_rep,
+                            int64_t stride, int n, hipStream_t) {
+    Launch l;
+    l.kind = "broadcast";
+    l.chunks = chunks;
+    l.n_chunks = n_chunks;
+    l.x = x;
+    l.x_rep = x_rep;
+    l.stride = stride;
+    l.n_workers = n;
+    return record(l);
+}
+hipError_t launch_test_philox(uint32_t, uint32_t, uint32_t, uint32_t, uint32_t, int64_t,
+                              uint32_t* out, hipStream_t) {
+    Launch l;
+    l.kind = "test_philox";
+    l.bounds = out;
+    return record(l);
+}
+}  // namespace dsm
+
+// ------------------------------------------------------------ helpers
+
+namespace {
+
+int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
+
+struct Problem {
+    std::vector<int64_t> numel;
+    std::vector<uint8_t> decay;
+    dsm_problem p{};
+    Problem(std::vector<int64_t> ne, int n, int H, int base, std::vector<uint8_t> dec = {})
+        : numel(std::move(ne)), decay(std::move(dec)) {
+        p.n_workers = n;
+        p.local_steps = H;
+        p.n_tensors = static_cast<int32_t>(numel.size());
+        p.base = base;
+        p.numel = numel.empty() ? nullptr : numel.data();
+        p.decay = decay.empty() ? nullptr : decay.data();
+    }
+};
+
+// Host allocations standing in for the caller's device buffers.
+struct Buffers {
+    std::vector<void*> owned;
+    dsm_buffers b{};
+    int64_t arena = 0;
+    float* alloc(int64_t floats) {
+        const size_t bytes = static_cast<size_t>(round_up(std::max<int64_t>(floats, 1) * 4, 256));
+        void* p = std::aligned_alloc(256, bytes);
+        std::memset(p, 0, bytes);
+        owned.push_back(p);
+        return static_cast<float*>(p);
+    }
+    Buffers(const Problem& P, bool randomized, bool global_adamw) {
+        int64_t ws = 0;
+        std::vector<int64_t> off(P.numel.size() + 1);
+        dsm_status st = dsm_layout(&P.p, &arena, off.data(), &ws);
+        CHECK(st == DSM_OK, "layout of a valid problem");
+        const int n = P.p.n_workers;
+        b.x = alloc(arena);
+        b.m = alloc(arena);
+        b.x_rep = alloc(n * arena);
+        b.g_rep = alloc(n * arena);
+        b.s1_rep = alloc(n * arena);
+        b.s2_rep = P.p.base == DSM_BASE_ADAMW ? alloc(n * arena) : nullptr;
+        b.u_scratch = randomized ? alloc(arena) : nullptr;
+        b.v = global_adamw ? alloc(arena) : nullptr;
+        b.workspace = alloc(ws / 4 + 64);
+        b.workspace_bytes = ws;
+        b.stream = nullptr;
+    }
+    ~Buffers() {
+        for (void* p : owned) std::free(p);
+    }
+    Buffers(const Buffers&) = delete;
+    Buffers& operator=(const Buffers&) = delete;
+};
+
+dsm_local_hparams adam_hp() { return dsm_local_hparams{1e-3f, 0.9f, 0.95f, 1e-8f, 0.1f}; }
+dsm_local_hparams sgd_hp() { return dsm_local_hparams{0.05f, 0.5f, 0.0f, 0.0f, 0.0f}; }
+dsm_global_hparams glob_hp(int mode = DSM_SIGN_DET, int rule = DSM_RULE_SIGN_MOMENTUM) {
+    dsm_global_hparams h{};
+    h.gamma = 1e-3f;
+    h.eta = 0.8f;
+    h.beta1 = 0.95f;
+    h.beta2 = 0.98f;
+    h.lambda = 0.1f;
+    h.mode = mode;
+    h.seed = 0x0123456789ABCDEFull;
+    h.rule = rule;
+    h.eps = 1e-8f;
+    return h;
+}
+
+// fp32 rounding of a long double value, as the host coefficients promise
+// (fp64 formation rounded once can sit one fp32 ulp away at a tie boundary).
+bool close_f32(float got, long double want) {
+    const float w = static_cast<float>(want);
+    return got == w || got == std::nextafter(w, INFINITY) || got == std::nextafter(w, -INFINITY);
+}
+
+// ------------------------------------------------------------ checks
+
+void check_layout_fuzz() {
+    std::mt19937_64 rng(12345);
+    const int64_t special[] = {0, 1, 3, 63, 64, 65, 1000, 16383, 16384, 16385, 40003, 100000};
+    for (int iter = 0; iter < 3000; ++iter) {
+        const int nt = static_cast<int>(rng() % 40);
+        std::vector<int64_t> ne(nt);
+        for (auto& v : ne)
+            v = (rng() % 3) ? special[rng() % 12] : static_cast<int64_t>(rng() % 300000);
+        int n = 1 + static_cast<int>(rng() % 64), H = 1 + static_cast<int>(rng() % 30);
+        int base = static_cast<int>(rng() % 2);
+        std::vector<uint8_t> dec;
+        if (rng() % 2) {
+            dec.resize(nt);
+            for (auto& d : dec) d = static_cast<uint8_t>(rng() % 2);
+        }
+        // One in four problems gets exactly one invalid field.
+        const int bad = (rng() % 4 == 0) ? 1 + static_cast<int>(rng() % 6) : 0;
+        if (bad == 1) n = (rng() % 2) ? 0 : 65;
+        if (bad == 2) H = 0;
+        if (bad == 3) base = 2 + static_cast<int>(rng() % 5);
+        if (bad == 4 && nt > 0) ne[rng() % nt] = -1 - static_cast<int64_t>(rng() % 5);
+        if (bad == 5 && nt > 0) ne[rng() % nt] = (int64_t(1) << 34) + static_cast<int64_t>(rng() % 7);
+        const bool invalid = bad == 1 || bad == 2 || bad == 3 || ((bad == 4 || bad == 5) && nt > 0);
+        Problem P(ne, n, H, base, dec);
+        int64_t arena = -7, ws = -7;
+        std::vector<int64_t> off(nt + 1, -7);
+        const dsm_status st = dsm_layout(&P.p, &arena, off.data(), &ws);
+        if (invalid) {
+            CHECK(st == DSM_ERR_INVALID_ARG, "iter %d: invalid field %d accepted (status %d)", iter,
+                  bad, st);
+            CHECK(std::strlen(dsm_last_error(nullptr)) > 0, "iter %d: no error text", iter);
+            CHECK(arena == -7 && ws == -7, "iter %d: outputs written on error", iter);
+            continue;
+        }
+        CHECK(st == DSM_OK, "iter %d: valid problem rejected: %s", iter, dsm_last_error(nullptr));
+        int64_t o = 0, chunks = 0;
+        for (int i = 0; i < nt; ++i) {
+            CHECK(off[i] == o, "iter %d: offset %d is %lld, expected %lld", iter, i,
+                  static_cast<long long>(off[i]), static_cast<long long>(o));
+            o += round_up(ne[i], 64);
+            chunks += (ne[i] + dsm::kChunkElems - 1) / dsm::kChunkElems;
+        }
+        CHECK(arena == o, "iter %d: arena %lld, expected %lld", iter, static_cast<long long>(arena),
+              static_cast<long long>(o));
+        CHECK(ws == round_up(chunks * 32, 256) + round_up(int64_t(nt) * 4, 256),
+              "iter %d: workspace %lld", iter, static_cast<long long>(ws));
+        CHECK(off[nt] == -7, "iter %d: wrote past tensor_offsets", iter);
+    }
+    // NULL outputs are allowed; a NULL problem is an argument error.
+    Problem P({5, 7}, 2, 2, DSM_BASE_ADAMW);
+    CHECK(dsm_layout(&P.p, nullptr, nullptr, nullptr) == DSM_OK, "NULL outputs");
+    CHECK(dsm_layout(nullptr, nullptr, nullptr, nullptr) == DSM_ERR_INVALID_ARG, "NULL problem");
+    Problem Q({5, 7}, 2, 2, DSM_BASE_ADAMW);
+    Q.p.numel = nullptr;
+    CHECK(dsm_layout(&Q.p, nullptr, nullptr, nullptr) == DSM_ERR_INVALID_ARG, "NULL numel");
+}
+
+// The uploaded chunk table covers every element of every tensor once, in
+// order, with no chunk crossing a tensor, and carries the decay flags.
+void check_chunk_table(const Problem& P, const Buffers& B, const Launch& init) {
+    const auto* c = static_cast<const dsm::Chunk*>(B.b.workspace);
+    CHECK(init.chunks == c, "init reads the chunk table from the workspace");
+    int64_t k = 0, off = 0;
+    for (size_t i = 0; i < P.numel.size(); ++i) {
+        const uint32_t dec = P.decay.empty() ? 1u : (P.decay[i] ? 1u : 0u);
+        for (int64_t j = 0; j < P.numel[i]; ++k) {
+            CHECK(k < init.n_chunks, "tensor %zu element %lld beyond the chunk table", i,
+                  static_cast<long long>(j));
+            if (k >= init.n_chunks) return;
+            CHECK(c[k].tensor == i && c[k].j0 == j && c[k].off == off + j,
+                  "chunk %lld: tensor %u j0 %lld off %lld", static_cast<long long>(k), c[k].tensor,
+                  static_cast<long long>(c[k].j0), static_cast<long long>(c[k].off));
+            CHECK(c[k].len >= 1 && c[k].len <= dsm::kChunkElems && j + c[k].len <= P.numel[i],
+                  "chunk %lld length %d", static_cast<long long>(k), c[k].len);
+            CHECK(c[k].decay == dec, "chunk %lld decay flag", static_cast<long long>(k));
+            j += c[k].len;
+        }
+        off += round_up(P.numel[i], 64);
+    }
+    CHECK(k == init.n_chunks, "chunk count %lld, table has %lld", static_cast<long long>(k),
+          static_cast<long long>(init.n_chunks));
+}
+
+void check_init_and_chunks() {
+    const std::vector<std::vector<int64_t>> shapes = {
+        {1, 3, 4, 5, 63, 64, 65, 0, 1000, 16383, 16384, 16385, 40003}, {0}, {16384 * 3}, {7}};
+    for (size_t s = 0; s < shapes.size(); ++s) {
+        std::vector<uint8_t> dec(shapes[s].size());
+        for (size_t i = 0; i < dec.size(); ++i) dec[i] = (i % 3 != 1);
+        for (int with_decay = 0; with_decay < 2; ++with_decay) {
+            Problem P(shapes[s], 3, 2, DSM_BASE_ADAMW, with_decay ? dec : std::vector<uint8_t>{});
+            Buffers B(P, false, true);
+            g_log.clear();
+            dsm_ctx* ctx = nullptr;
+            CHECK(dsm_init(&P.p, &B.b, &ctx) == DSM_OK, "init: %s", dsm_last_error(nullptr));
+            const bool empty = B.arena == 0;
+            CHECK(g_log.size() == (empty ? 0u : 1u), "init launches %zu kernels", g_log.size());
+            if (!empty && !g_log.empty()) {
+                const Launch& l = g_log[0];
+                CHECK(l.kind == "init" && l.x == B.b.x && l.x_rep == B.b.x_rep && l.v == B.b.v &&
+                          l.s2 == B.b.s2_rep && l.stride == B.arena && l.n_workers == 3,
+                      "init arguments");
+                check_chunk_table(P, B, l);
+            }
+            CHECK(dsm_destroy(ctx) == DSM_OK, "destroy");
+        }
+    }
+}
+
+void check_init_rejections() {
+    Problem P({1000, 7}, 2, 3, DSM_BASE_ADAMW);
+    {
+        Buffers B(P, false, false);
+        dsm_ctx* ctx = reinterpret_cast<dsm_ctx*>(0x1);
+        B.b.s2_rep = nullptr;
+        CHECK(dsm_init(&P.p, &B.b, &ctx) == DSM_ERR_INVALID_ARG && ctx == nullptr,
+              "AdamW without s2_rep");
+    }
+    {
+        Buffers B(P, false, false);
+        dsm_ctx* ctx = nullptr;
+        B.b.m = reinterpret_cast<float*>(reinterpret_cast<char*>(B.b.m) + 4);
+        CHECK(dsm_init(&P.p, &B.b, &ctx) == DSM_ERR_INVALID_ARG, "misaligned m");
+    }
+    {
+        Buffers B(P, false, false);
+        dsm_ctx* ctx = nullptr;
+        B.b.workspace_bytes -= 1;
+        CHECK(dsm_init(&P.p, &B.b, &ctx) == DSM_ERR_INVALID_ARG, "short workspace");
+        CHECK(std::strstr(dsm_last_error(nullptr), "workspace") != nullptr, "workspace message");
+    }
+    {
+        Buffers B(P, false, false);
+        dsm_ctx* ctx = nullptr;
+        CHECK(dsm_init(&P.p, &B.b, nullptr) == DSM_ERR_INVALID_ARG, "NULL out");
+        CHECK(dsm_init(&P.p, nullptr, &ctx) == DSM_ERR_INVALID_ARG, "NULL buffers");
+        g_devices = 0;
+        g_log.clear();
+        CHECK(dsm_init(&P.p, &B.b, &ctx) == DSM_ERR_HIP && ctx == nullptr, "no device");
+        CHECK(std::strstr(dsm_last_error(nullptr), "no HIP device") != nullptr, "device message");
+        CHECK(g_log.empty(), "no launch without a device");
+        g_devices = 1;
+        g_launch_status = hipErrorLaunchFailure;
+        CHECK(dsm_init(&P.p, &B.b, &ctx) == DSM_ERR_HIP && ctx == nullptr, "failed init launch");
+        g_launch_status = hipSuccess;
+    }
+}
+
+// Which replica source each local launch reads, for workers [w0, w0 + nw).
+void expect_local(const Launch& l, const Buffers& B, bool adamw, bool from_x, int w0, int nw,
+                  const char* what) {
+    CHECK(l.kind == (adamw ? "local_adamw" : "local_sgdm"), "%s: kind %s", what, l.kind.c_str());
+    CHECK(l.x_rep == B.b.x_rep && l.stride == B.arena, "%s: replica buffer", what);
+    CHECK(l.x_src == (from_x ? B.b.x : B.b.x_rep) && l.src_stride == (from_x ? 0 : B.arena),
+          "%s: source %s expected", what, from_x ? "x" : "x_rep");
+    CHECK(l.worker0 == w0 && l.n_workers == nw, "%s: workers [%d, +%d) expected, got [%d, +%d)",
+          what, w0, nw, l.worker0, l.n_workers);
+    CHECK(l.chunks == B.b.workspace, "%s: chunk table", what);
+}
+
+void check_state_machine_adamw() {
+    Problem P({100, 16385, 7}, 5, 3, DSM_BASE_ADAMW, {1, 1, 0});
+    Buffers B(P, true, false);
+    dsm_ctx* ctx = nullptr;
+    CHECK(dsm_init(&P.p, &B.b, &ctx) == DSM_OK, "init");
+    const dsm_local_hparams lh = adam_hp();
+    const dsm_global_hparams gh = glob_hp();
+    g_log.clear();
+    // Round 0: all workers, then worker 2 alone: a global step is refused
+    // until every worker has taken H steps; a step past H is refused.
+    CHECK(dsm_local_step(ctx, -1, 1, &lh) == DSM_OK, "local all");
+    CHECK(dsm_local_step(ctx, 2, 2, &lh) == DSM_OK, "local worker 2");
+    CHECK(dsm_global_step(ctx, 0, &gh, 1) == DSM_ERR_STATE, "global before H");
+    CHECK(dsm_round_end(ctx, 3, &lh, 0, &gh, 1) == DSM_ERR_STATE, "round end with uneven counts");
+    CHECK(dsm_local_step(ctx, 2, 3, &lh) == DSM_OK, "worker 2 step 3");
+    CHECK(dsm_local_step(ctx, 2, 4, &lh) == DSM_ERR_STATE, "worker 2 past H");
+    CHECK(dsm_local_step(ctx, -1, 4, &lh) == DSM_ERR_STATE, "all workers past H for worker 2");
+    CHECK(g_log.size() == 3, "three launches so far, got %zu", g_log.size());
+    if (g_log.size() == 3) {
+        expect_local(g_log[0], B, true, false, 0, 5, "round 0 all");
+        expect_local(g_log[1], B, true, false, 2, 1, "round 0 worker 2");
+        expect_local(g_log[2], B, true, false, 2, 1, "round 0 worker 2 again");
+    }
+    for (int w : {0, 1, 3, 4}) CHECK(dsm_local_step(ctx, w, 2, &lh) == DSM_OK, "worker %d", w);
+    for (int w : {0, 1, 3, 4}) CHECK(dsm_local_step(ctx, w, 3, &lh) == DSM_OK, "worker %d", w);
+    CHECK(dsm_read_bounds(ctx, nullptr) == DSM_ERR_STATE, "bounds before a randomized step");
+    // Global step without broadcast: every replica becomes stale.
+    g_log.clear();
+    CHECK(dsm_global_step(ctx, 0, &gh, 0) == DSM_OK, "global, no broadcast");
+    CHECK(g_log.size() == 1 && g_log[0].kind == "global_det" && !g_log[0].broadcast &&
+              g_log[0].x == B.b.x && g_log[0].x_rep == B.b.x_rep && g_log[0].stride == B.arena,
+          "global launch");
+    // Round 1: worker 1 first (reads x), then all: runs [0], [1], [2, 5) with
+    // sources x, x_rep, x.
+    g_log.clear();
+    CHECK(dsm_local_step(ctx, 1, 4, &lh) == DSM_OK, "stale worker 1");
+    CHECK(dsm_local_step(ctx, -1, 5, &lh) == DSM_OK, "mixed all");
+    CHECK(g_log.size() == 4, "four launches, got %zu", g_log.size());
+    if (g_log.size() == 4) {
+        expect_local(g_log[0], B, true, true, 1, 1, "stale worker 1");
+        expect_local(g_log[1], B, true, true, 0, 1, "run [0]");
+        expect_local(g_log[2], B, true, false, 1, 1, "run [1]");
+        expect_local(g_log[3], B, true, true, 2, 3, "run [2, 5)");
+    }
+    // Workers 0 and 2-4 have 1 step, worker 1 has 2: finish to H - 1 = 2
+    // and end the round fused, randomized, with broadcast.
+    for (int w : {0, 2, 3, 4}) CHECK(dsm_local_step(ctx, w, 6, &lh) == DSM_OK, "worker %d", w);
+    const dsm_global_hparams gr = glob_hp(DSM_SIGN_RAND_FLIP);
+    g_log.clear();
+    CHECK(dsm_round_end(ctx, 7, &lh, 1, &gr, 1) == DSM_OK, "fused round end: %s",
+          dsm_last_error(ctx));
+    CHECK(g_log.size() == 1, "one round-end launch");
+    if (g_log.size() == 1) {
+        const Launch& l = g_log[0];
+        CHECK(l.kind == "round_end" && l.adamw && l.broadcast && l.n_tensors == 3, "round end");
+        CHECK(l.x_src == B.b.x_rep && l.src_stride == B.arena, "round end reads the replicas");
+        CHECK(l.u == B.b.u_scratch && l.s2 == B.b.s2_rep, "round end buffers");
+        const auto* ws = static_cast<const char*>(B.b.workspace);
+        CHECK(reinterpret_cast<const char*>(l.bounds) ==
+                  ws + round_up(static_cast<int64_t>(l.n_chunks) * 32, 256),
+              "bound words follow the chunk table");
+        CHECK(l.gs.mode == DSM_SIGN_RAND_FLIP && l.gs.t == 1 && l.gs.key0 == 0x89ABCDEFu &&
+                  l.gs.key1 == 0x01234567u,
+              "Philox key and counter word");
+    }
+    // The bounds of that step are read back from the workspace.
+    if (!g_log.empty()) {
+        auto* words = const_cast<uint32_t*>(g_log[0].bounds);
+        const float want[3] = {0.5f, 2.0f, 0.0f};
+        std::memcpy(words, want, sizeof want);
+        float got[3] = {-1, -1, -1};
+        CHECK(dsm_read_bounds(ctx, got) == DSM_OK, "read bounds");
+        CHECK(std::memcmp(got, want, sizeof want) == 0, "bounds round trip");
+        CHECK(dsm_read_bounds(ctx, nullptr) == DSM_ERR_INVALID_ARG, "NULL bounds output");
+    }
+    // Variants are refused by the fused round end; round end with H - 1
+    // steps only.
+    dsm_global_hparams gl = glob_hp(DSM_SIGN_DET, DSM_RULE_LOOKAHEAD);
+    CHECK(dsm_local_step(ctx, -1, 8, &lh) == DSM_OK, "round 2 step 1");
+    CHECK(dsm_local_step(ctx, -1, 9, &lh) == DSM_OK, "round 2 step 2");
+    CHECK(dsm_round_end(ctx, 10, &lh, 2, &gl, 1) == DSM_ERR_UNSUPPORTED, "variant in round end");
+    gl.mode = DSM_SIGN_RAND_FLIP;
+    CHECK(dsm_round_end(ctx, 10, &lh, 2, &gl, 1) == DSM_ERR_INVALID_ARG, "randomized variant");
+    // dsm_sync resets the round: local counts restart at 0.
+    g_log.clear();
+    CHECK(dsm_sync(ctx) == DSM_OK, "sync");
+    CHECK(g_log.size() == 1 && g_log[0].kind == "broadcast" && g_log[0].n_workers == 5 &&
+              g_log[0].x == B.b.x && g_log[0].x_rep == B.b.x_rep,
+          "broadcast launch");
+    for (int k = 0; k < 3; ++k) CHECK(dsm_local_step(ctx, -1, 11 + k, &lh) == DSM_OK, "after sync");
+    CHECK(dsm_local_step(ctx, -1, 14, &lh) == DSM_ERR_STATE, "H after sync");
+    // A failed launch reports DSM_ERR_HIP and leaves the round where it was.
+    g_launch_status = hipErrorLaunchFailure;
+    CHECK(dsm_global_step(ctx, 3, &gh, 1) == DSM_ERR_HIP, "failed global launch");
+    g_launch_status = hipSuccess;
+    CHECK(dsm_global_step(ctx, 3, &gh, 1) == DSM_OK, "global after the failure");
+    CHECK(dsm_destroy(ctx) == DSM_OK, "destroy");
+}
+
+void check_state_machine_sgd_h1() {
+    // H = 1: the fused round end takes the only local step; after a lazy
+    // round end it reads x, after a broadcast the replicas.
+    Problem P({64, 65}, 3, 1, DSM_BASE_SGD_MOMENTUM);
+    Buffers B(P, false, false);
+    dsm_ctx* ctx = nullptr;
+    CHECK(dsm_init(&P.p, &B.b, &ctx) == DSM_OK, "init");
+    const dsm_local_hparams lh = sgd_hp();
+    const dsm_global_hparams gh = glob_hp();
+    g_log.clear();
+    CHECK(dsm_round_end(ctx, 1, &lh, 0, &gh, 0) == DSM_OK, "round end 0 (lazy)");
+    CHECK(dsm_round_end(ctx, 2, &lh, 1, &gh, 1) == DSM_OK, "round end 1 (broadcast)");
+    CHECK(dsm_round_end(ctx, 3, &lh, 2, &gh, 1) == DSM_OK, "round end 2");
+    CHECK(g_log.size() == 3, "three launches");
+    if (g_log.size() == 3) {
+        CHECK(g_log[0].x_src == B.b.x_rep && g_log[0].src_stride == B.arena, "fresh after init");
+        CHECK(g_log[1].x_src == B.b.x && g_log[1].src_stride == 0, "stale after lazy round end");
+        CHECK(g_log[2].x_src == B.b.x_rep, "fresh after broadcast");
+        CHECK(!g_log[0].adamw && g_log[0].ss.mu == 0.5f && g_log[0].ss.lr == 0.05f, "SGD scalars");
+        CHECK(g_log[0].s2 == nullptr, "no second moment for SGD");
+    }
+    CHECK(dsm_local_step(ctx, -1, 4, &lh) == DSM_OK, "split step");
+    CHECK(dsm_round_end(ctx, 5, &lh, 3, &gh, 1) == DSM_ERR_STATE, "round end after the H-th step");
+    const dsm_global_hparams gr = glob_hp(DSM_SIGN_RAND_ZERO);
+    CHECK(dsm_global_step(ctx, 3, &gr, 1) == DSM_ERR_INVALID_ARG, "randomized without u_scratch");
+    dsm_global_hparams ga = glob_hp(DSM_SIGN_DET, DSM_RULE_GLOBAL_ADAMW);
+    CHECK(dsm_global_step(ctx, 3, &ga, 1) == DSM_ERR_INVALID_ARG, "Global AdamW without v");
+    CHECK(dsm_global_step(ctx, 3, &gh, 1) == DSM_OK, "global");
+    CHECK(dsm_destroy(ctx) == DSM_OK, "destroy");
+}
+
+void check_coefficients() {
+    Problem P({300}, 3, 1000000, DSM_BASE_ADAMW);
+    Buffers B(P, false, true);
+    dsm_ctx* ctx = nullptr;
+    CHECK(dsm_init(&P.p, &B.b, &ctx) == DSM_OK, "init");
+    const dsm_local_hparams lh = adam_hp();
+    const int64_t steps[] = {1, 2, 3, 10, 100, 1000, 54321, 999999};
+    for (int64_t s : steps) {
+        g_log.clear();
+        CHECK(dsm_local_step(ctx, -1, s, &lh) == DSM_OK, "local step %lld", static_cast<long long>(s));
+        if (g_log.size() != 1) continue;
+        const dsm::AdamScalars& a = g_log[0].as;
+        const long double b1 = lh.beta1, b2 = lh.beta2;
+        CHECK(close_f32(a.bc1, 1.0L - std::pow(b1, static_cast<long double>(s))), "bc1 at s=%lld: %.9g",
+              static_cast<long long>(s), a.bc1);
+        CHECK(close_f32(a.bc2, 1.0L - std::pow(b2, static_cast<long double>(s))), "bc2 at s=%lld: %.9g",
+              static_cast<long long>(s), a.bc2);
+        CHECK(a.one_minus_beta1 == static_cast<float>(1.0L - b1) &&
+                  a.one_minus_beta2 == static_cast<float>(1.0L - b2),
+              "1 - beta");
+        CHECK(a.lr == lh.lr && a.eps == lh.eps && a.wd == lh.weight_decay && a.beta1 == lh.beta1,
+              "passed-through scalars");
+    }
+    dsm_destroy(ctx);
+    // Global coefficients for n = 3 (not a power of two) and n = 4.
+    for (int n : {3, 4}) {
+        Problem Q({300}, n, 1, DSM_BASE_SGD_MOMENTUM);
+        Buffers C(Q, false, true);
+        CHECK(dsm_init(&Q.p, &C.b, &ctx) == DSM_OK, "init");
+        const dsm_local_hparams sh = sgd_hp();
+        for (int rule : {DSM_RULE_SIGN_MOMENTUM, DSM_RULE_GLOBAL_ADAMW}) {
+            dsm_global_hparams g = glob_hp(DSM_SIGN_DET, rule);
+            const int64_t t = rule == DSM_RULE_GLOBAL_ADAMW ? 77 : 4000000000LL;
+            CHECK(dsm_local_step(ctx, -1, 1, &sh) == DSM_OK, "local");
+            g_log.clear();
+            CHECK(dsm_global_step(ctx, t, &g, 1) == DSM_OK, "global: %s", dsm_last_error(ctx));
+            if (g_log.size() != 1) continue;
+            const dsm::GlobalScalars& s = g_log[0].gs;
+            const long double gam = g.gamma, eta = g.eta, b1 = g.beta1, b2 = g.beta2;
+            CHECK(close_f32(s.c1, (1.0L - b1) / gam) && close_f32(s.c2, (1.0L - b2) / gam),
+                  "c1 %.9g c2 %.9g", s.c1, s.c2);
+            CHECK(close_f32(s.step, eta * gam), "eta gamma %.9g", s.step);
+            CHECK(s.n == n && s.n_f == static_cast<float>(n) && s.n_pow2 == ((n & (n - 1)) == 0),
+                  "worker count");
+            CHECK(s.t == static_cast<uint32_t>(t) && s.rule == rule && s.lam == g.lambda, "t, rule");
+            CHECK(g_log[0].v == C.b.v, "v passed");
+            if (rule == DSM_RULE_GLOBAL_ADAMW) {
+                CHECK(close_f32(s.bc1, 1.0L - std::pow(b1, static_cast<long double>(t + 1))) &&
+                          close_f32(s.bc2, 1.0L - std::pow(b2, static_cast<long double>(t + 1))),
+                      "Global AdamW bias corrections");
+                CHECK(close_f32(s.inv_gamma, 1.0L / gam), "1/gamma");
+            }
+        }
+        dsm_destroy(ctx);
+    }
+}
+
+void check_hyperparameter_errors() {
+    Problem P({100}, 2, 2, DSM_BASE_ADAMW);
+    Buffers B(P, true, false);
+    dsm_ctx* ctx = nullptr;
+    CHECK(dsm_init(&P.p, &B.b, &ctx) == DSM_OK, "init");
+    g_log.clear();
+    const float nan = std::nanf("");
+    const float bad_lr[] = {0.0f, -1.0f, nan, INFINITY};
+    for (float v : bad_lr) {
+        dsm_local_hparams h = adam_hp();
+        h.lr = v;
+        CHECK(dsm_local_step(ctx, -1, 1, &h) == DSM_ERR_INVALID_ARG, "lr %g", v);
+    }
+    const float bad_beta[] = {-0.1f, 1.5f, nan, 1.0f};
+    for (float v : bad_beta) {
+        dsm_local_hparams h = adam_hp();
+        h.beta1 = v;
+        CHECK(dsm_local_step(ctx, -1, 1, &h) == DSM_ERR_INVALID_ARG, "beta1 %g", v);
+        h = adam_hp();
+        h.beta2 = v;
+        CHECK(dsm_local_step(ctx, -1, 1, &h) == DSM_ERR_INVALID_ARG, "beta2 %g", v);
+    }
+    dsm_local_hparams h = adam_hp();
+    h.eps = -1e-8f;
+    CHECK(dsm_local_step(ctx, -1, 1, &h) == DSM_ERR_INVALID_ARG, "eps < 0");
+    h = adam_hp();
+    h.weight_decay = nan;
+    CHECK(dsm_local_step(ctx, -1, 1, &h) == DSM_ERR_INVALID_ARG, "weight decay NaN");
+    h = adam_hp();
+    CHECK(dsm_local_step(ctx, -1, 0, &h) == DSM_ERR_INVALID_ARG, "step 0");
+    CHECK(dsm_local_step(ctx, 2, 1, &h) == DSM_ERR_INVALID_ARG, "worker n");
+    CHECK(dsm_local_step(ctx, -2, 1, &h) == DSM_ERR_INVALID_ARG, "worker -2");
+    CHECK(dsm_local_step(ctx, -1, 1, nullptr) == DSM_ERR_INVALID_ARG, "NULL hparams");
+    CHECK(g_log.empty(), "no launch after rejected local steps");
+    CHECK(std::strlen(dsm_last_error(ctx)) > 0, "context error text");
+    CHECK(dsm_local_step(ctx, -1, 1, &h) == DSM_OK, "step 1");
+    CHECK(dsm_local_step(ctx, -1, 2, &h) == DSM_OK, "step 2");
+    g_log.clear();
+    struct {
+        int field;
+        float value;
+    } bad_global[] = {{0, 0.0f}, {0, nan}, {1, -1.0f}, {2, 1.01f}, {3, -0.5f}, {4, -1.0f}, {4, INFINITY}};
+    for (const auto& b : bad_global) {
+        dsm_global_hparams g = glob_hp();
+        float* f[] = {&g.gamma, &g.eta, &g.beta1, &g.beta2, &g.lambda};
+        *f[b.field] = b.value;
+        CHECK(dsm_global_step(ctx, 0, &g, 1) == DSM_ERR_INVALID_ARG, "global field %d = %g",
+              b.field, b.value);
+    }
+    dsm_global_hparams g = glob_hp();
+    g.mode = 3;
+    CHECK(dsm_global_step(ctx, 0, &g, 1) == DSM_ERR_INVALID_ARG, "mode 3");
+    g = glob_hp();
+    g.rule = 4;
+    CHECK(dsm_global_step(ctx, 0, &g, 1) == DSM_ERR_INVALID_ARG, "rule 4");
+    g = glob_hp();
+    CHECK(dsm_global_step(ctx, -1, &g, 1) == DSM_ERR_INVALID_ARG, "t < 0");
+    CHECK(dsm_global_step(ctx, int64_t(1) << 32, &g, 1) == DSM_ERR_INVALID_ARG, "t = 2^32");
+    CHECK(dsm_global_step(ctx, 0, nullptr, 1) == DSM_ERR_INVALID_ARG, "NULL global hparams");
+    CHECK(g_log.empty(), "no launch after rejected global steps");
+    CHECK(dsm_global_step(ctx, (int64_t(1) << 32) - 1, &g, 1) == DSM_OK, "largest t");
+    CHECK(dsm_destroy(ctx) == DSM_OK, "destroy");
+    // Calls on a NULL context.
+    CHECK(dsm_local_step(nullptr, -1, 1, &h) == DSM_ERR_INVALID_ARG, "NULL ctx local");
+    CHECK(dsm_global_step(nullptr, 0, &g, 1) == DSM_ERR_INVALID_ARG, "NULL ctx global");
+    CHECK(dsm_round_end(nullptr, 1, &h, 0, &g, 1) == DSM_ERR_INVALID_ARG, "NULL ctx round end");
+    CHECK(dsm_sync(nullptr) == DSM_ERR_INVALID_ARG, "NULL ctx sync");
+    CHECK(dsm_read_bounds(nullptr, nullptr) == DSM_ERR_INVALID_ARG, "NULL ctx bounds");
+    CHECK(dsm_destroy(nullptr) == DSM_OK, "NULL ctx destroy");
+}
+
+void check_test_philox_args() {
+    uint32_t* out = static_cast<uint32_t*>(std::aligned_alloc(256, 256));
+    g_log.clear();
+    CHECK(dsm_test_philox(1, 0, 0, 0, 16, out, nullptr) == DSM_OK, "valid");
+    CHECK(dsm_test_philox(1, 0, 0, (int64_t(1) << 32) - 16, 16, out, nullptr) == DSM_OK,
+          "last counter");
+    CHECK(dsm_test_philox(1, 0, 0, (int64_t(1) << 32) - 15, 16, out, nullptr) == DSM_ERR_INVALID_ARG,
+          "counter overflow");
+    CHECK(dsm_test_philox(1, 0, -1, 0, 16, out, nullptr) == DSM_ERR_INVALID_ARG, "t < 0");
+    CHECK(dsm_test_philox(1, 0, 0, 0, (int64_t(1) << 30) + 1, out, nullptr) == DSM_ERR_INVALID_ARG,
+          "count above 2^30");
+    CHECK(dsm_test_philox(1, 0, 0, 0, 16, out + 0, nullptr) == DSM_OK, "aligned");
+    CHECK(dsm_test_philox(1, 0, 0, 0, 16,
+                          reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(out) + 2),
+                          nullptr) == DSM_ERR_INVALID_ARG,
+          "misaligned output");
+    CHECK(g_log.size() == 3, "three accepted calls launched, got %zu", g_log.size());
+    g_devices = 0;
+    CHECK(dsm_test_philox(1, 0, 0, 0, 16, out, nullptr) == DSM_ERR_HIP, "no device");
+    g_devices = 1;
+    std::free(out);
+}
+
+}  // namespace
+
+int main() {
+    check_layout_fuzz();
+    check_init_and_chunks();
+    check_init_rejections();
+    check_state_machine_adamw();
+    check_state_machine_sgd_h1();
+    check_coefficients();
+    check_hyperparameter_errors();
+    check_test_philox_args();
+    if (g_failures) {
+        std::fprintf(stderr, "%d of %d checks failed\n", g_failures, g_checks);
+        return 1;
+    }
+    std::printf("all checks passed (%d)\n", g_checks);
+    return 0;
+}
