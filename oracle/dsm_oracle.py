@@ -195,14 +195,19 @@ def _exact_less(a_int, B, au):
     """Elementwise exact test  a_int * B < au * 2^24  for integers a_int.
 
     a_int: int64 array with |a_int| <= 2^24; B: scalar >= 0; au: array >= 0.
-    Evaluated in fp64; every element whose two sides are within a relative
-    2^-45 of each other is re-decided with exact rationals.
+    Evaluated in fp64; every element whose two finite sides are within a
+    relative 2^-45 of each other is re-decided with exact rationals.  Where a
+    side is infinite or NaN (u or B not finite) the fp64 comparison is already
+    the IEEE one: infinities compare exactly, 0 * inf is NaN, and NaN compares
+    false.
     """
     B = float(B)
-    lhs = a_int.astype(np.float64) * B
-    rhs = au.astype(np.float64) * _TWO24
-    res = lhs < rhs
-    close = np.abs(lhs - rhs) <= 2.0 ** -45 * np.maximum(np.abs(lhs), np.abs(rhs))
+    with np.errstate(invalid="ignore"):
+        lhs = a_int.astype(np.float64) * B
+        rhs = au.astype(np.float64) * _TWO24
+        res = lhs < rhs
+        close = (np.isfinite(lhs) & np.isfinite(rhs) &
+                 (np.abs(lhs - rhs) <= 2.0 ** -45 * np.maximum(np.abs(lhs), np.abs(rhs))))
     if np.any(close):
         fb = Fraction(B)
         for idx in np.flatnonzero(close):

@@ -411,6 +411,41 @@ def test_randomized_sign_threshold_is_exact():
     assert O.randomized_sign(u1, B, np.array([k1 - 1]), O.SIGN_RAND_FLIP)[0] == 1.0
 
 
+def test_randomized_sign_nonfinite_limits():
+    """Non-finite u or B, from the limits of Eqs. (9)/(10) and IEEE compares.
+
+    B = +inf: Eq. (9) keeps sign(u) with probability 1/2 + |u|/(2B) -> 1/2,
+    i.e. iff U < 1/2 (k < 2^23); Eq. (10) with |u|/B -> 0, never.  B = NaN:
+    no comparison holds, so Eq. (9) gives -sign(u) and Eq. (10) gives 0.
+    u = NaN: Eq. (9) gives NaN (either branch), Eq. (10) gives 0.
+    """
+    half = 1 << 23
+    k = np.array([0, 1, half - 1, half, half + 1, (1 << 24) - 1], dtype=np.int64)
+    keep9 = k < half
+    for uval in (1.5, -0.25, np.inf, -np.inf):
+        u = np.full(k.size, uval, dtype=np.float32)
+        s = np.float32(np.sign(uval))
+        np.testing.assert_array_equal(O.randomized_sign(u, np.float32(np.inf), k, O.SIGN_RAND_FLIP),
+                                      np.where(keep9, s, -s))
+        np.testing.assert_array_equal(O.randomized_sign(u, np.float32(np.inf), k, O.SIGN_RAND_ZERO),
+                                      np.zeros(k.size, np.float32))
+        np.testing.assert_array_equal(O.randomized_sign(u, np.float32(np.nan), k, O.SIGN_RAND_FLIP),
+                                      np.full(k.size, -s))
+        np.testing.assert_array_equal(O.randomized_sign(u, np.float32(np.nan), k, O.SIGN_RAND_ZERO),
+                                      np.zeros(k.size, np.float32))
+    un = np.full(k.size, np.nan, dtype=np.float32)
+    for B in (np.float32(2.0), np.float32(np.inf), np.float32(np.nan)):
+        assert np.all(np.isnan(O.randomized_sign(un, B, k, O.SIGN_RAND_FLIP)))
+        np.testing.assert_array_equal(O.randomized_sign(un, B, k, O.SIGN_RAND_ZERO),
+                                      np.zeros(k.size, np.float32))
+    # A finite bound with an infinite |u| (only possible when B = max |u| is
+    # itself infinite, but the decision is still defined): always kept.
+    u = np.full(k.size, -np.inf, dtype=np.float32)
+    for variant in (O.SIGN_RAND_FLIP, O.SIGN_RAND_ZERO):
+        np.testing.assert_array_equal(O.randomized_sign(u, np.float32(3.0), k, variant),
+                                      np.full(k.size, -1.0, np.float32))
+
+
 @pytest.mark.parametrize("variant", [O.SIGN_RAND_FLIP, O.SIGN_RAND_ZERO])
 def test_lemma1_monte_carlo(variant):
     """Lemma 1: E[S_r(v)] = v/B, and per element Var = 1 - (v/B)^2 (Eq. (9))
