@@ -1,0 +1,115 @@
+"""Non-finite gradients through the whole path, against the oracle.
+
+A diverging worker can hand the optimizer NaN or infinite gradients.  NaN,
++inf and -inf are planted in chosen gradient elements, including a ragged
+tensor end and an element where every worker is infinite.  Two rounds then
+run, each of H local steps and a global step with broadcast, for both bases
+and all three signs.
+
+Every output is compared with the fp32 oracle run from the same device
+state.  NaN positions must agree, and every other value must be
+bit-identical.  That covers the local states, x and m, and for the randomized
+sign also u and the per-tensor bound B, which turns NaN or inf with its
+tensor.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2411_17866_amd import arena as A
+from paper_2411_17866_amd import dsm
+
+pytestmark = pytest.mark.gpu
+
+NUMEL = [1, 3, 5, 64, 65, 1000, 16385, 40003]
+DECAY = [i % 3 != 1 for i in range(len(NUMEL))]
+N, H = 3, 2
+# (round, local step) -> [(worker or None for every worker, tensor, element, value)]
+PLANTS = {
+    (0, 0): [(1, 5, 17, np.nan)],
+    (0, 1): [(0, 6, 16384, np.inf)],
+    (1, 0): [(2, 7, 20000, -np.inf), (0, 2, 4, np.nan)],
+    (1, 1): [(None, 3, 10, np.inf)],
+}
+ADAM = dict(lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1)
+SGD = dict(lr=0.05, beta1=0.9)
+GLOB = dict(gamma=1e-3, eta=0.8, beta1=0.95, beta2=0.98, lam=0.1)
+SEED = 0xC0FFEE
+
+
+def tensors(ar, flat):
+    torch.cuda.synchronize()
+    h = flat.detach().cpu().numpy()
+    return [h[o:o + k].copy() for o, k in zip(ar.offsets, ar.numel)]
+
+
+def same(gpu, ora, what):
+    g = np.asarray(gpu, dtype=np.float32)
+    o = np.asarray(ora, dtype=np.float32)
+    gn, on = np.isnan(g), np.isnan(o)
+    assert np.array_equal(gn, on), f"{what}: NaN positions differ ({gn.sum()} vs {on.sum()})"
+    bad = g[~gn].view(np.uint32) != o[~on].view(np.uint32)
+    assert not bad.any(), f"{what}: {bad.sum()} finite-or-inf values differ"
+
+
+@pytest.mark.parametrize("mode", [dsm.DSM_SIGN_DET, dsm.DSM_SIGN_RAND_FLIP,
+                                  dsm.DSM_SIGN_RAND_ZERO])
+@pytest.mark.parametrize("base", [dsm.DSM_BASE_ADAMW, dsm.DSM_BASE_SGD_MOMENTUM])
+def test_nonfinite_gradients_match_oracle(base, mode):
+    adamw = base == dsm.DSM_BASE_ADAMW
+    local = ADAM if adamw else SGD
+    ar = A.Arenas(NUMEL, N, H, base, decay=DECAY, randomized=True)
+    gen = torch.Generator(device="cuda").manual_seed(99 + 3 * base + mode)
+    ar.x.normal_(0.0, 0.02, generator=gen)
+    ar.init()
+    keys = ("x_rep", "s1_rep") + (("s2_rep",) if adamw else ())
+    seen_nan = seen_inf = False
+    with np.errstate(invalid="ignore", over="ignore", divide="ignore"):
+        for t in range(2):
+            for k in range(H):
+                s = t * H + k + 1
+                ar.g_rep.normal_(0.0, 1e-3, generator=gen)
+                for w, p, j, val in PLANTS[(t, k)]:
+                    for i in (range(N) if w is None else (w,)):
+                        ar.g_rep[i, ar.offsets[p] + j] = float(val)
+                before = {name: [tensors(ar, getattr(ar, name)[i]) for i in range(N)]
+                          for name in keys + ("g_rep",)}
+                dsm.dsm_local_step(ar.ctx, -1, s, **local)
+                for i in range(N):
+                    after = {name: tensors(ar, getattr(ar, name)[i]) for name in keys}
+                    for p in range(len(NUMEL)):
+                        args = [before[name][i][p] for name in ("x_rep", "g_rep", "s1_rep")]
+                        if adamw:
+                            kw = dict(ADAM, step=s)
+                            kw["weight_decay"] = ADAM["weight_decay"] if DECAY[p] else 0.0
+                            o = O.local_adamw_step(*args, before["s2_rep"][i][p], prec="fp32",
+                                                   **kw)
+                        else:
+                            o = O.local_sgdm_step(*args, lr=SGD["lr"], momentum=SGD["beta1"],
+                                                  prec="fp32")
+                        for name, want in zip(keys, o):
+                            same(after[name][p], want, f"t {t} k {k} worker {i} {name} tensor {p}")
+            x0, m0 = tensors(ar, ar.x), tensors(ar, ar.m)
+            reps = [tensors(ar, ar.x_rep[i]) for i in range(N)]
+            dsm.dsm_global_step(ar.ctx, t, mode=mode, seed=SEED, broadcast=True, **GLOB)
+            o = O.global_step(x0, m0, reps, decay=DECAY, t=t, mode=mode, seed=SEED, prec="fp32",
+                              **GLOB)
+            gx, gm = tensors(ar, ar.x), tensors(ar, ar.m)
+            if mode != dsm.DSM_SIGN_DET:
+                B = dsm.dsm_read_bounds(ar.ctx, len(NUMEL))
+                gu = tensors(ar, ar.u)
+            for p in range(len(NUMEL)):
+                same(gx[p], o["x"][p], f"t {t} x tensor {p}")
+                same(gm[p], o["m"][p], f"t {t} m tensor {p}")
+                seen_nan |= bool(np.isnan(gx[p]).any() or np.isnan(gm[p]).any())
+                seen_inf |= bool(np.isinf(gm[p]).any())
+                if mode != dsm.DSM_SIGN_DET:
+                    same(gu[p], o["u"][p], f"t {t} u tensor {p}")
+                    same(B[p:p + 1], np.asarray([o["B"][p]], np.float32), f"t {t} B tensor {p}")
+            for i in range(N):
+                for a, b in zip(ar.views(ar.x_rep[i]), ar.views(ar.x)):
+                    assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+    # The planted values did reach the global state.
+    assert seen_nan and (seen_inf or adamw)
+    ar.destroy()
