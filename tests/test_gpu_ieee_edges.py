@@ -1,4 +1,5 @@
-"""Non-finite gradients through the whole path, against the oracle.
+"""IEEE edge cases through the whole path, against the oracle: non-finite
+gradients, and subnormal values (the build keeps denormals).
 
 A diverging worker can hand the optimizer NaN or infinite gradients.  NaN,
 +inf and -inf are planted in chosen gradient elements, including a ragged
@@ -113,3 +114,74 @@ def test_nonfinite_gradients_match_oracle(base, mode):
     # The planted values did reach the global state.
     assert seen_nan and (seen_inf or adamw)
     ar.destroy()
+
+
+# Gradients down to the smallest subnormal.  Where one worker alone moves an
+# element whose x is 0, the averaged difference and u of the global step end
+# up subnormal, and the sign must still be +-1: a flushed denormal would make
+# it 0.
+TINY = [1e-36, 3e-38, 1e-39, 1e-40, 1e-41, 1e-42, 1e-43, 1e-44, 1.4e-45]
+TINY_NUMEL = [1000, 64]
+TINY_DECAY = [True, True]
+MIN_NORMAL = np.float32(2.0 ** -126)
+# gamma = 1 keeps (1 - beta1)/gamma small, so u stays subnormal for both bases.
+GLOB_TINY = dict(GLOB, gamma=1.0)
+
+
+@pytest.mark.parametrize("base", [dsm.DSM_BASE_ADAMW, dsm.DSM_BASE_SGD_MOMENTUM])
+def test_subnormal_values_match_oracle(base):
+    adamw = base == dsm.DSM_BASE_ADAMW
+    local = ADAM if adamw else SGD
+    nt = len(TINY)
+    ar = A.Arenas(TINY_NUMEL, N, H, base, decay=TINY_DECAY, randomized=False)
+    gen = torch.Generator(device="cuda").manual_seed(5 + base)
+    ar.x.normal_(0.0, 0.02, generator=gen)
+    o0, o1 = ar.offsets
+    ar.x[o0:o0 + 2 * nt] = 0.0
+    ar.x[o1:o1 + nt] = torch.tensor(TINY, dtype=torch.float32, device="cuda") * 100.0
+    ar.x[o1 + nt:o1 + 2 * nt] = -torch.tensor(TINY, dtype=torch.float32, device="cuda")
+    ar.init()
+    keys = ("x_rep", "s1_rep") + (("s2_rep",) if adamw else ())
+    subnormal_signs = 0
+    tiny = torch.tensor(TINY, dtype=torch.float32, device="cuda")
+    for t in range(2):
+        for k in range(H):
+            s = t * H + k + 1
+            ar.g_rep.normal_(0.0, 1e-3, generator=gen)
+            ar.g_rep[:, o0:o0 + 2 * nt] = 0.0
+            ar.g_rep[0, o0:o0 + nt] = tiny              # one worker moves these
+            ar.g_rep[:, o0 + nt:o0 + 2 * nt] = -tiny    # every worker moves these
+            before = {name: [tensors_of(ar, getattr(ar, name)[i], TINY_NUMEL) for i in range(N)]
+                      for name in keys + ("g_rep",)}
+            dsm.dsm_local_step(ar.ctx, -1, s, **local)
+            for i in range(N):
+                after = {name: tensors_of(ar, getattr(ar, name)[i], TINY_NUMEL) for name in keys}
+                for p in range(len(TINY_NUMEL)):
+                    args = [before[name][i][p] for name in ("x_rep", "g_rep", "s1_rep")]
+                    if adamw:
+                        o = O.local_adamw_step(*args, before["s2_rep"][i][p], prec="fp32",
+                                               **dict(ADAM, step=s))
+                    else:
+                        o = O.local_sgdm_step(*args, lr=SGD["lr"], momentum=SGD["beta1"],
+                                              prec="fp32")
+                    for name, want in zip(keys, o):
+                        same(after[name][p], want, f"t {t} k {k} worker {i} {name} tensor {p}")
+        x0, m0 = tensors_of(ar, ar.x, TINY_NUMEL), tensors_of(ar, ar.m, TINY_NUMEL)
+        reps = [tensors_of(ar, ar.x_rep[i], TINY_NUMEL) for i in range(N)]
+        dsm.dsm_global_step(ar.ctx, t, broadcast=True, **GLOB_TINY)
+        o = O.global_step(x0, m0, reps, decay=TINY_DECAY, t=t, prec="fp32", **GLOB_TINY)
+        gx, gm = tensors_of(ar, ar.x, TINY_NUMEL), tensors_of(ar, ar.m, TINY_NUMEL)
+        for p in range(len(TINY_NUMEL)):
+            same(gx[p], o["x"][p], f"t {t} x tensor {p}")
+            same(gm[p], o["m"][p], f"t {t} m tensor {p}")
+            u, S = o["u"][p], o["S"][p]
+            subnormal_signs += int(np.sum((np.abs(u) > 0) & (np.abs(u) < MIN_NORMAL) & (S != 0)))
+    # The case did reach subnormal momenta whose sign is +-1.
+    assert subnormal_signs > 0
+    ar.destroy()
+
+
+def tensors_of(ar, flat, numel):
+    torch.cuda.synchronize()
+    h = flat.detach().cpu().numpy()
+    return [h[o:o + k].copy() for o, k in zip(ar.offsets, numel)]
