@@ -152,6 +152,17 @@ DSM_API dsm_status dsm_layout(const dsm_problem* problem, int64_t* arena_elems,
  * workspace and enqueues the initialisation kernel on buffers->stream.
  * Errors: DSM_ERR_INVALID_ARG (problem, NULL or misaligned pointers, small
  * workspace); DSM_ERR_HIP (no device, copy or launch failure).
+ *
+ * Resume.  A context keeps no state beyond the caller's buffers and the
+ * explicit counters (s, t, seed), so a run saved at a round boundary resumes
+ * exactly, in any allocation:
+ *   1. write the saved x;
+ *   2. call dsm_init;
+ *   3. after it on the stream, write back m, s1_rep, s2_rep and v;
+ *   4. continue with the saved s and t.
+ * A round boundary is the point after dsm_global_step, dsm_round_end or
+ * dsm_sync.  The replicas need not be saved: at a round boundary they equal
+ * x, or are stale after broadcast = 0, which is the same thing.
  */
 DSM_API dsm_status dsm_init(const dsm_problem* problem, const dsm_buffers* buffers,
                     dsm_ctx** out);
