@@ -78,6 +78,10 @@ MUTATIONS = [
      "    st['s1'] = [[a * 0 for a in w] for w in st['s1']]\n"
      "    local_steps(st, grads, H=H, decay=decay, first_step=t * H + 1, prec=prec, **local)",
      "worker momentum reset every round"),
+    ("dsm_oracle.py", "close = (np.isfinite(lhs) & np.isfinite(rhs) &",
+     "close = (np.ones_like(res) &", "exact re-check applied to infinite sides"),
+    ("dsm_oracle.py", "res = lhs < rhs", "res = ~(lhs >= rhs)",
+     "a NaN comparison keeps the sign"),
 ]
 
 
