@@ -273,6 +273,51 @@ def test_tiny_rounds_free_running_bit_identical():
     ar.destroy()
 
 
+def test_tiny_long_free_run_all_signs_and_paths():
+    """Twelve free-running rounds of the tiny workload, cycling the three
+    signs and alternating the fused round end (lazy broadcast) with the split
+    path (broadcast).  GPU and fp32 oracle start from the same inputs and are
+    never re-seeded from each other; after every round x, m and every
+    worker's AdamW state must be bit-identical."""
+    from paper_2411_17866_amd import workloads as W
+    w = W.get("tiny")
+    H = w.local_steps
+    ar, gen = make(w.numel, w.n_workers, H, w.base, decay=w.decay, seed=w.seed + 1)
+    st = O.init_state(per_tensor(ar, ar.x), w.n_workers, "adamw")
+    modes = (dsm.DSM_SIGN_DET, dsm.DSM_SIGN_RAND_FLIP, dsm.DSM_SIGN_RAND_ZERO)
+    seed = 0x5EED0000000D5
+    for t in range(12):
+        mode = modes[t % 3]
+        fused = t % 2 == 1
+        grads = {}
+        for k in range(H):
+            for i in range(w.n_workers):
+                W.fill_grads_(ar.g_rep[i], w, i, t * H + k)
+                grads[(i, k)] = per_tensor(ar, ar.g_rep[i])
+            s = t * H + k + 1
+            if fused and k == H - 1:
+                dsm.dsm_round_end(ar.ctx, s, w.local, t, gamma=w.local["lr"], mode=mode,
+                                  seed=seed, broadcast=False, **w.glob)
+            else:
+                dsm.dsm_local_step(ar.ctx, -1, s, **w.local)
+        if not fused:
+            dsm.dsm_global_step(ar.ctx, t, gamma=w.local["lr"], mode=mode, seed=seed,
+                                broadcast=True, **w.glob)
+        O.communication_round(st, lambda i, k: grads[(i, k)], t, H=H, local=w.local,
+                              glob=dict(w.glob, mode=mode, seed=seed), decay=w.decay,
+                              prec="fp32")
+        gx, gm = per_tensor(ar, ar.x), per_tensor(ar, ar.m)
+        for p in range(len(w.numel)):
+            assert np.array_equal(gx[p].view(np.uint32), st["x"][p].view(np.uint32)), (t, "x", p)
+            assert np.array_equal(gm[p].view(np.uint32), st["m"][p].view(np.uint32)), (t, "m", p)
+        for i in range(w.n_workers):
+            g1, g2 = per_tensor(ar, ar.s1_rep[i]), per_tensor(ar, ar.s2_rep[i])
+            for p in range(len(w.numel)):
+                assert np.array_equal(g1[p].view(np.uint32), st["s1"][i][p].view(np.uint32))
+                assert np.array_equal(g2[p].view(np.uint32), st["s2"][i][p].view(np.uint32))
+    ar.destroy()
+
+
 def test_rerun_is_bitwise_deterministic():
     """Two identical runs (local steps, randomized global step) agree bit for bit."""
     outs = []
