@@ -29,7 +29,7 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 #define DSM_NT 1
 #endif
 #ifndef DSM_ROUND_END_UNROLL
-#define DSM_ROUND_END_UNROLL 1
+#define DSM_ROUND_END_UNROLL 0
 #endif
 
 __device__ __forceinline__ f4 ntload(const f4* p) {
@@ -567,7 +567,9 @@ __global__ __launch_bounds__(kBlockThreads) void k_round_end(
             }
         }
         // Worker loop: unrolled DSM_ROUND_END_UNROLL workers at a time (0: fully,
-        // for a compile-time worker count); fewer registers, higher occupancy.
+        // for a compile-time worker count).  Fully unrolled, every worker's loads
+        // are in flight together; that measured faster than the rolled loop's
+        // lower register count and higher occupancy.
 #if DSM_ROUND_END_UNROLL == 0
 #pragma unroll
 #elif DSM_ROUND_END_UNROLL == 1
