@@ -50,7 +50,7 @@ typedef enum dsm_status {
     DSM_ERR_INVALID_ARG = 1, /* bad pointer, size, alignment or hyperparameter */
     DSM_ERR_STATE = 2,       /* call out of the order Algorithm 1 requires */
     DSM_ERR_HIP = 3,         /* HIP runtime error (no device, launch, copy) */
-    DSM_ERR_UNSUPPORTED = 4  /* valid request this build does not implement */
+    DSM_ERR_UNSUPPORTED = 4  /* valid request the library does not implement */
 } dsm_status;
 
 /* Base optimizer of the local steps (Section 2, "any base optimizer"). */

@@ -81,7 +81,7 @@ def build(verbose=False, out=LIBPATH, defines=()):
 
 
 def kernel_isa(path=None):
-    """Writes the gfx950 assembly of the kernels (of this build) for review."""
+    """Writes the gfx950 assembly of the kernels, compiled with the library's flags, for review."""
     out = path or os.path.join(OBJDIR, "dsm_kernels.s")
     _run([hipcc(), "-x", "hip", *COMMON_FLAGS, *DEVICE_FLAGS, "--offload-device-only", "-S",
           os.path.join(CSRC, "dsm_kernels.hip"), "-o", out], False)

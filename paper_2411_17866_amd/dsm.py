@@ -81,7 +81,7 @@ def load_library(path=LIBPATH):
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(f"{path} not found: build the HIP library first "
-                           "(python -m paper_2411_17866_amd.build or __graft_entry__.build())")
+                           "(python -m paper_2411_17866_amd.build)")
     lib = ctypes.CDLL(path)
     c_int64_p = ctypes.POINTER(ctypes.c_int64)
     lib.dsm_layout.argtypes = [ctypes.POINTER(dsm_problem), c_int64_p, c_int64_p, c_int64_p]

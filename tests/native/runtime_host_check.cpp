@@ -465,7 +465,7 @@ void check_state_machine_adamw() {
     const dsm_local_hparams lh = adam_hp();
     const dsm_global_hparams gh = glob_hp();
     g_log.clear();
-    // Round 0: all workers, then worker 2 alone: a global step is refused
+    // Round t = 0: all workers, then worker 2 alone: a global step is refused
     // until every worker has taken H steps; a step past H is refused.
     CHECK(dsm_local_step(ctx, -1, 1, &lh) == DSM_OK, "local all");
     CHECK(dsm_local_step(ctx, 2, 2, &lh) == DSM_OK, "local worker 2");
@@ -489,7 +489,7 @@ void check_state_machine_adamw() {
     CHECK(g_log.size() == 1 && g_log[0].kind == "global_det" && !g_log[0].broadcast &&
               g_log[0].x == B.b.x && g_log[0].x_rep == B.b.x_rep && g_log[0].stride == B.arena,
           "global launch");
-    // Round 1: worker 1 first (reads x), then all: runs [0], [1], [2, 5) with
+    // Round t = 1: worker 1 first (reads x), then all: runs [0], [1], [2, 5) with
     // sources x, x_rep, x.
     g_log.clear();
     CHECK(dsm_local_step(ctx, 1, 4, &lh) == DSM_OK, "stale worker 1");
@@ -535,8 +535,8 @@ void check_state_machine_adamw() {
     // Variants are refused by the fused round end; round end with H - 1
     // steps only.
     dsm_global_hparams gl = glob_hp(DSM_SIGN_DET, DSM_RULE_LOOKAHEAD);
-    CHECK(dsm_local_step(ctx, -1, 8, &lh) == DSM_OK, "round 2 step 1");
-    CHECK(dsm_local_step(ctx, -1, 9, &lh) == DSM_OK, "round 2 step 2");
+    CHECK(dsm_local_step(ctx, -1, 8, &lh) == DSM_OK, "round t = 2, step 1");
+    CHECK(dsm_local_step(ctx, -1, 9, &lh) == DSM_OK, "round t = 2, step 2");
     CHECK(dsm_round_end(ctx, 10, &lh, 2, &gl, 1) == DSM_ERR_UNSUPPORTED, "variant in round end");
     gl.mode = DSM_SIGN_RAND_FLIP;
     CHECK(dsm_round_end(ctx, 10, &lh, 2, &gl, 1) == DSM_ERR_INVALID_ARG, "randomized variant");

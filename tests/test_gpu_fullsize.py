@@ -207,8 +207,8 @@ def test_fullsize_split_rounds_sampled(run):
     w, ar = r.w, r.ar
     H = w.local_steps
     nonbit = flips = 0
-    # Round 1 sees a non-zero momentum.  A workload with both signs runs the
-    # deterministic one in round 0 and the randomized one in round 1.
+    # Round t = 1 sees a non-zero momentum.  A workload with both signs runs the
+    # deterministic one in round t = 0 and the randomized one in round t = 1.
     modes = (dsm.DSM_SIGN_DET, r.mode) if 0 in w.sign_modes else (r.mode, r.mode)
     for t in (0, 1):
         mode = modes[t]

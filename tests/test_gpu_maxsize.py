@@ -173,7 +173,7 @@ def test_max_size_split_then_fused_round(big):
     b, ar, c = big, big.ar, big.c
     glob = dict(gamma=b.lr, seed=SEED, **GLOB)
     nonbit = 0
-    # Round 0: one local step, then the randomized global step with broadcast.
+    # Round t = 0: one local step, then the randomized global step with broadcast.
     ar.g_rep.normal_(0.0, 1e-3, generator=b.gen)
     before = b.sample_state(b.state)
     dsm.dsm_local_step(ar.ctx, -1, 1, **c["local"])
@@ -186,7 +186,7 @@ def test_max_size_split_then_fused_round(big):
     dsm.dsm_global_step(ar.ctx, 0, mode=c["modes"][0], broadcast=True, **glob)
     nonbit += b.check_global(x0, m0, after["x_rep"], 0, c["modes"][0])
     b.replicas_equal_x()
-    # Round 1: the fused round end (its only local step folded in), lazy
+    # Round t = 1: the fused round end (its only local step folded in), lazy
     # broadcast, then an explicit sync.
     ar.g_rep.normal_(0.0, 1e-3, generator=b.gen)
     before = b.sample_state(b.state)
