@@ -268,6 +268,7 @@ def main():
     traffic = committed_traffic(khash, "local_adamw")
     achieved = local_bytes / (ms_local / 1e3) / 1e9
     local_state = 16 if adamw else 12        # x, g, s1 (, s2) read per worker
+    local_written = 8 if adamw else 4        # s1 (, s2) written per worker by the round end
     out = {
         "metric": METRIC,
         "value": value,
@@ -304,10 +305,11 @@ def main():
         },
         "breakdown": {
             "local_step": kern(ev["local"], local_bytes, n * d),
-            "round_end_fused_det": kern(ev["fused_det"], (16 + (local_state + 8) * n) * d,
-                                        n * d + d),
+            "round_end_fused_det": kern(ev["fused_det"],
+                                        (16 + (local_state + local_written) * n) * d, n * d + d),
             "round_end_fused_rand_flip": kern(ev["fused_rand"],
-                                              (28 + (local_state + 8) * n) * d, n * d + d),
+                                              (28 + (local_state + local_written) * n) * d,
+                                              n * d + d),
             "global_det": kern(ev["split_det"], bytes_global(n, False) * d, d),
             "global_rand_flip": kern(ev["split_rand"], bytes_global(n, True) * d, d),
             "global_lookahead": kern(ev["lookahead"], bytes_global(n, False) * d, d),
