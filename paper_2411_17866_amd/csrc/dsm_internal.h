@@ -99,6 +99,13 @@ hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep
                              float* s1, int64_t stride, int worker0, int n_workers,
                              const SgdScalars& sc, hipStream_t st);
 
+// Local step of all n workers from the global model x (every replica stale):
+// x is read once per element and each worker's result goes to its replica.
+hipError_t launch_local_from_x(const Chunk* chunks, int64_t n_chunks, const float* x,
+                               float* x_rep, const float* g_rep, float* s1, float* s2,
+                               int64_t stride, int n, bool adamw, const AdamScalars& as,
+                               const SgdScalars& ss, hipStream_t st);
+
 // Arguments of the fused last-local-step + global-step launch.
 struct RoundEndArgs {
     float *x, *m, *x_rep;

@@ -84,6 +84,10 @@ struct Piece {
 constexpr uint32_t kXcds = 8;  // MI355X: work-groups go to its 8 XCDs round-robin
 constexpr int kMapLocal = DSM_XCD_MAP_LOCAL;         // local-step kernels
 constexpr int kMapRoundEnd = DSM_XCD_MAP_ROUND_END;  // fused round end
+#ifndef DSM_XCD_MAP_FROM_X
+#define DSM_XCD_MAP_FROM_X DSM_XCD_MAP_ROUND_END
+#endif
+constexpr int kMapFromX = DSM_XCD_MAP_FROM_X;        // all-worker local step from x
 constexpr int kMapOther = DSM_XCD_MAP;               // every other chunk kernel
 
 // Work item of this work-group.  MAP 0: the work-group index itself (XCD k
@@ -538,6 +542,72 @@ __global__ __launch_bounds__(kBlockThreads) void k_global_rand_pass2(
 constexpr int kBaseAdamW = 0;
 constexpr int kBaseSgd = 1;
 
+// Local step of every worker when every replica is stale (after a global
+// step without broadcast): each worker's x_{t+1,0} is the global model, so
+// the work-group reads x once and takes the step of all n workers on it,
+// writing each replica, instead of one pass per worker that re-reads x.  The
+// per-element arithmetic is adamw4 / sgdm4, as in the per-worker kernels.
+template <int N, int BASE>
+__global__ __launch_bounds__(kBlockThreads) void k_local_from_x(
+    const Chunk* __restrict__ chunks, const float* __restrict__ x, float* __restrict__ x_rep,
+    const float* __restrict__ g_rep, float* __restrict__ s1, float* __restrict__ s2,
+    int64_t stride, int n_rt, AdamScalars as, SgdScalars ss) {
+    const Piece pc = piece_of<kMapFromX>(chunks);
+    const Chunk& c = pc.c;
+    const int n = N > 0 ? N : n_rt;
+    const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + c.off);
+    const float lam = c.decay ? as.wd : 0.0f;
+    const int nvec = pc.q_hi;
+    const int nfull = pc.nfull;
+    for (int q0 = pc.q_lo + threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+        f4 xv[kUnroll];
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) {
+            const int q = q0 + k * kBlockThreads;
+            if (q < nvec) xv[k] = ntload(xp + q);
+        }
+#if DSM_ROUND_END_UNROLL == 0
+#pragma unroll
+#elif DSM_ROUND_END_UNROLL == 1
+#pragma unroll 1
+#elif DSM_ROUND_END_UNROLL == 2
+#pragma unroll 2
+#endif
+        for (int i = 0; i < (N > 0 ? N : n); ++i) {
+            const int64_t wo = i * stride + c.off;
+            f4* __restrict__ xr = reinterpret_cast<f4*>(x_rep + wo);
+            const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + wo);
+            f4* __restrict__ s1p = reinterpret_cast<f4*>(s1 + wo);
+            f4* __restrict__ s2p = reinterpret_cast<f4*>(s2 + wo);
+            f4 gi[kUnroll], mi[kUnroll], vi[kUnroll];
+#pragma unroll
+            for (int k = 0; k < kUnroll; ++k) {
+                const int q = q0 + k * kBlockThreads;
+                if (q < nvec) {
+                    gi[k] = ntload(gp + q);
+                    mi[k] = ntload(s1p + q);
+                    if (BASE == kBaseAdamW) vi[k] = ntload(s2p + q);
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < kUnroll; ++k) {
+                const int q = q0 + k * kBlockThreads;
+                if (q < nvec) {
+                    f4 xi = xv[k];
+                    if (BASE == kBaseAdamW) {
+                        adamw4(xi, gi[k], mi[k], vi[k], lam, as);
+                        store_group(vi[k], s2p, q, nfull, c.len);
+                    } else {
+                        sgdm4(xi, gi[k], mi[k], ss);
+                    }
+                    store_group(xi, xr, q, nfull, c.len);
+                    store_group(mi[k], s1p, q, nfull, c.len);
+                }
+            }
+        }
+    }
+}
+
 template <int N, int BASE, int KIND>
 __global__ __launch_bounds__(kBlockThreads) void k_round_end(
     const Chunk* __restrict__ chunks, float* __restrict__ x, float* __restrict__ m,
@@ -770,6 +840,39 @@ static void launch_round_end_base(const Chunk* chunks, int64_t n_chunks, const R
         launch_round_end_n<BASE, 1>(chunks, n_chunks, a, st);
     else
         launch_round_end_n<BASE, 2>(chunks, n_chunks, a, st);
+}
+
+template <int BASE>
+static void launch_local_from_x_n(const Chunk* chunks, int64_t n_chunks, const float* x,
+                                  float* x_rep, const float* g_rep, float* s1, float* s2,
+                                  int64_t stride, int n, const AdamScalars& as,
+                                  const SgdScalars& ss, hipStream_t st) {
+    const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
+#define DSM_LOCAL_FROM_X(NW)                                                                   \
+    hipLaunchKernelGGL((k_local_from_x<NW, BASE>), grid, block, 0, st, chunks, x, x_rep, g_rep, \
+                       s1, s2, stride, n, as, ss)
+    switch (n) {
+        case 1: DSM_LOCAL_FROM_X(1); break;
+        case 2: DSM_LOCAL_FROM_X(2); break;
+        case 4: DSM_LOCAL_FROM_X(4); break;
+        case 8: DSM_LOCAL_FROM_X(8); break;
+        default: DSM_LOCAL_FROM_X(0); break;
+    }
+#undef DSM_LOCAL_FROM_X
+}
+
+hipError_t launch_local_from_x(const Chunk* chunks, int64_t n_chunks, const float* x,
+                               float* x_rep, const float* g_rep, float* s1, float* s2,
+                               int64_t stride, int n, bool adamw, const AdamScalars& as,
+                               const SgdScalars& ss, hipStream_t st) {
+    if (n_chunks == 0) return hipSuccess;
+    if (adamw)
+        launch_local_from_x_n<kBaseAdamW>(chunks, n_chunks, x, x_rep, g_rep, s1, s2, stride, n,
+                                          as, ss, st);
+    else
+        launch_local_from_x_n<kBaseSgd>(chunks, n_chunks, x, x_rep, g_rep, s1, s2, stride, n,
+                                        as, ss, st);
+    return hipGetLastError();
 }
 
 hipError_t launch_round_end(const Chunk* chunks, int64_t n_chunks, int n_tensors, bool adamw,

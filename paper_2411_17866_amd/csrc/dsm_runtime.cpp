@@ -392,9 +392,20 @@ dsm_status dsm_local_step(dsm_ctx* ctx, int32_t worker, int64_t step, const dsm_
                         i, ctx->H);
     }
     // Workers whose replica is stale read the global model (the
-    // synchronisation step folded into their first local step).  One launch
-    // per run of consecutive workers with the same source.
-    for (int a = w0; a < w0 + nw;) {
+    // synchronisation step folded into their first local step).  When every
+    // worker steps and every replica is stale, one launch reads x once for all
+    // of them; otherwise one launch per run of consecutive workers with the
+    // same source.
+    bool all_stale = worker < 0 && ctx->n > 1;
+    for (int i = 0; i < ctx->n && all_stale; ++i) all_stale = ctx->stale[i] != 0;
+    if (all_stale) {
+        hipError_t e = dsm::launch_local_from_x(
+            ctx->d_chunks, static_cast<int64_t>(ctx->chunks.size()), ctx->buf.x, ctx->buf.x_rep,
+            ctx->buf.g_rep, ctx->buf.s1_rep, ctx->buf.s2_rep, ctx->arena_elems, ctx->n,
+            ctx->base == DSM_BASE_ADAMW, lc.adam, lc.sgd, ctx->stream);
+        if (e != hipSuccess) return hip_fail(ctx, "launching the local step", e);
+    }
+    for (int a = w0; a < w0 + nw && !all_stale;) {
         int b = a + 1;
         while (b < w0 + nw && ctx->stale[b] == ctx->stale[a]) ++b;
         const bool from_x = ctx->stale[a] != 0;

@@ -139,6 +139,24 @@ hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep
     l.ss = sc;
     return record(l);
 }
+hipError_t launch_local_from_x(const Chunk* chunks, int64_t n_chunks, const float* x,
+                               float* x_rep, const float*, float*, float* s2, int64_t stride,
+                               int n, bool adamw, const AdamScalars& as, const SgdScalars& ss,
+                               hipStream_t) {
+    Launch l;
+    l.kind = "local_from_x";
+    l.chunks = chunks;
+    l.n_chunks = n_chunks;
+    l.x = x;
+    l.x_rep = x_rep;
+    l.s2 = s2;
+    l.stride = stride;
+    l.n_workers = n;
+    l.adamw = adamw;
+    l.as = as;
+    l.ss = ss;
+    return record(l);
+}
 hipError_t launch_round_end(const Chunk* chunks, int64_t n_chunks, int n_tensors, bool adamw,
                             const RoundEndArgs& a, bool broadcast, hipStream_t) {
     Launch l;
@@ -587,6 +605,49 @@ void check_state_machine_sgd_h1() {
     CHECK(dsm_destroy(ctx) == DSM_OK, "destroy");
 }
 
+// After a global step without broadcast every replica is stale: a local
+// step of all workers reads x once in one launch (n >= 2); one worker, or
+// n = 1, keeps the per-worker launch reading x.
+void check_local_from_x() {
+    for (int base : {DSM_BASE_ADAMW, DSM_BASE_SGD_MOMENTUM}) {
+        const bool adamw = base == DSM_BASE_ADAMW;
+        const dsm_local_hparams lh = adamw ? adam_hp() : sgd_hp();
+        const dsm_global_hparams gh = glob_hp();
+        for (int n : {1, 2, 3, 8}) {
+            Problem P({100, 16385}, n, 2, base);
+            Buffers B(P, false, false);
+            dsm_ctx* ctx = nullptr;
+            CHECK(dsm_init(&P.p, &B.b, &ctx) == DSM_OK, "init");
+            for (int k = 0; k < 2; ++k) CHECK(dsm_local_step(ctx, -1, k + 1, &lh) == DSM_OK, "local");
+            CHECK(dsm_global_step(ctx, 0, &gh, 0) == DSM_OK, "lazy global step");
+            g_log.clear();
+            CHECK(dsm_local_step(ctx, -1, 3, &lh) == DSM_OK, "first local step after it");
+            CHECK(g_log.size() == 1, "one launch, got %zu", g_log.size());
+            if (g_log.size() == 1) {
+                const Launch& l = g_log[0];
+                if (n >= 2) {
+                    CHECK(l.kind == "local_from_x" && l.x == B.b.x && l.x_rep == B.b.x_rep &&
+                              l.stride == B.arena && l.n_workers == n && l.adamw == adamw &&
+                              l.s2 == B.b.s2_rep && l.chunks == B.b.workspace,
+                          "n = %d: all-worker launch from x", n);
+                } else {
+                    expect_local(l, B, adamw, true, 0, 1, "n = 1 from x");
+                }
+            }
+            // The step counts and clears the stale flags like any local step.
+            CHECK(dsm_local_step(ctx, -1, 4, &lh) == DSM_OK, "second local step");
+            if (g_log.size() == 2) expect_local(g_log[1], B, adamw, false, 0, n, "then from replicas");
+            CHECK(dsm_local_step(ctx, -1, 5, &lh) == DSM_ERR_STATE, "H reached");
+            CHECK(dsm_global_step(ctx, 1, &gh, 0) == DSM_OK, "lazy again");
+            // One worker alone after a lazy step still uses the per-worker path.
+            g_log.clear();
+            CHECK(dsm_local_step(ctx, 0, 5, &lh) == DSM_OK, "worker 0 alone");
+            if (g_log.size() == 1) expect_local(g_log[0], B, adamw, true, 0, 1, "worker 0 from x");
+            CHECK(dsm_destroy(ctx) == DSM_OK, "destroy");
+        }
+    }
+}
+
 void check_coefficients() {
     Problem P({300}, 3, 1000000, DSM_BASE_ADAMW);
     Buffers B(P, false, true);
@@ -746,6 +807,7 @@ int main() {
     check_init_rejections();
     check_state_machine_adamw();
     check_state_machine_sgd_h1();
+    check_local_from_x();
     check_coefficients();
     check_hyperparameter_errors();
     check_test_philox_args();

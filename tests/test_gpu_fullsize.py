@@ -274,3 +274,39 @@ def test_fullsize_fused_round_sampled(run):
     nb, flips = _check_global_sampled(r, x0, m0, reps, t, gx, gm, r.mode)
     print(f"{w.name} fused round: {r.p.size} sampled elements, {nonbit + nb} not bit-identical, "
           f"{flips} flips vs fp64")
+
+
+def test_fullsize_first_step_after_lazy_round_end(run):
+    """A fused round that ends without broadcast leaves every replica stale,
+    so the next local step of all workers reads x once in one launch.  Each
+    worker's step is checked against the oracle's step from x."""
+    r = run
+    w, ar = r.w, r.ar
+    H = w.local_steps
+    t = 3
+    dsm.dsm_sync(ar.ctx)
+    for k in range(H - 1):
+        r.grads(t * H + k + 1)
+        r.local(t * H + k + 1)
+    r.grads(t * H + H)
+    dsm.dsm_round_end(ar.ctx, t * H + H, w.local, t, mode=r.mode, broadcast=False, **r.glob_kw())
+    s = (t + 1) * H + 1
+    r.grads(s)
+    before = r.sample_state(r.state_keys)
+    x0 = _gather(ar.x, r.idx)
+    r.local(s)
+    after = r.sample_state([k for k in r.state_keys if k != "g_rep"])
+    nonbit = 0
+    for i in range(w.n_workers):
+        start = dict(before)
+        start["x_rep"] = [x0] * w.n_workers      # a stale replica's step starts from x
+        for dec in (True, False):
+            sel = r.decay == dec
+            if not sel.any():
+                continue
+            o = _local_oracle(r, start, i, sel, s, dec, "fp32")
+            names = ("x_rep", "s1_rep") + (("s2_rep",) if r.adamw else ())
+            for k, name in enumerate(names):
+                nonbit += rel_check(after[name][i][sel], o[k], f"{w.name} from-x worker {i} {name}")
+    print(f"{w.name} first step after a lazy round end: {r.p.size} sampled elements x "
+          f"{w.n_workers} workers, {nonbit} not bit-identical")

@@ -169,3 +169,50 @@ def test_round_end_state_errors():
     assert e.value.status == dsm.DSM_ERR_INVALID_ARG       # step 0
     dsm.dsm_round_end(ar.ctx, 3, ADAM, 0, gamma=1e-3, **GLOB)
     ar.destroy()
+
+
+@pytest.mark.parametrize("base", [dsm.DSM_BASE_ADAMW, dsm.DSM_BASE_SGD_MOMENTUM])
+@pytest.mark.parametrize("n", [2, 3, 4, 5, 8])
+def test_all_worker_step_from_x_equals_per_worker_steps(base, n):
+    """After a global step without broadcast every replica is stale.  A local
+    step of all workers then reads x once in one launch; it must equal n
+    single-worker steps (each reading x) bit for bit, and so must the rest of
+    the round."""
+    local = ADAM if base == dsm.DSM_BASE_ADAMW else SGD
+    H = 2
+    outs = []
+    for per_worker in (False, True):
+        ar = A.Arenas(NUMEL, n, H, base, decay=DECAY, randomized=False)
+        gen = torch.Generator(device="cuda").manual_seed(5 + n)
+        ar.x.normal_(0.0, 0.02, generator=gen)
+        ar.init()
+        for k in range(H):
+            _grads(ar, 0, k)
+            dsm.dsm_local_step(ar.ctx, -1, k + 1, **local)
+        dsm.dsm_global_step(ar.ctx, 0, gamma=local["lr"], broadcast=False, **GLOB)
+        _grads(ar, 1, 0)
+        if per_worker:
+            for i in range(n):
+                dsm.dsm_local_step(ar.ctx, i, H + 1, **local)
+        else:
+            dsm.dsm_local_step(ar.ctx, -1, H + 1, **local)
+        first = {"x_rep": host(ar.x_rep), "s1": host(ar.s1_rep)}
+        if ar.s2_rep is not None:
+            first["s2"] = host(ar.s2_rep)
+        _grads(ar, 1, 1)
+        dsm.dsm_local_step(ar.ctx, -1, H + 2, **local)
+        dsm.dsm_global_step(ar.ctx, 1, gamma=local["lr"], broadcast=True, **GLOB)
+        after = {"x": host(ar.x), "m": host(ar.m), "x_rep_end": host(ar.x_rep)}
+        mask = _mask(list(ar.offsets), ar.x.numel())
+        ar.destroy()
+        outs.append((first, after, mask))
+    (fa, aa, mask), (fb, ab, _) = outs
+    for key in fa:
+        for i in range(n):
+            a, b = fa[key][i][mask], fb[key][i][mask]
+            assert np.array_equal(a.view(np.uint32), b.view(np.uint32)), (key, i)
+    for key in ("x", "m"):
+        assert np.array_equal(aa[key][mask].view(np.uint32), ab[key][mask].view(np.uint32)), key
+    for i in range(n):
+        assert np.array_equal(aa["x_rep_end"][i][mask].view(np.uint32),
+                              ab["x_rep_end"][i][mask].view(np.uint32))
