@@ -386,7 +386,9 @@ def test_empty_problem_is_a_no_op():
 
 def test_max_workers_every_entry_point():
     """n = 64 (the largest worker count): local AdamW, deterministic and
-    randomized global steps and the fused round end, against the oracle."""
+    randomized global steps and the fused round end without broadcast, then a
+    round whose first local step starts every worker from x, against the
+    oracle."""
     n, H = 64, 2
     numel = [5, 1000, 16385]
     decay = [False, True, True]
@@ -394,7 +396,7 @@ def test_max_workers_every_entry_point():
     ar, gen = make(numel, n, H, dsm.DSM_BASE_ADAMW, decay=decay, seed=64)
     st = O.init_state(per_tensor(ar, ar.x), n, "adamw")
     for t, (mode, fused) in enumerate(((dsm.DSM_SIGN_DET, False), (dsm.DSM_SIGN_RAND_ZERO, False),
-                                       (dsm.DSM_SIGN_RAND_FLIP, True))):
+                                       (dsm.DSM_SIGN_RAND_FLIP, True), (dsm.DSM_SIGN_DET, False))):
         grads = {}
         for k in range(H):
             ar.g_rep.normal_(0.0, 0.01, generator=gen)
@@ -402,7 +404,7 @@ def test_max_workers_every_entry_point():
                 grads[(i, k)] = per_tensor(ar, ar.g_rep[i])
             s = t * H + k + 1
             if fused and k == H - 1:
-                dsm.dsm_round_end(ar.ctx, s, local, t, mode=mode, seed=3, **GLOB)
+                dsm.dsm_round_end(ar.ctx, s, local, t, mode=mode, seed=3, broadcast=False, **GLOB)
             else:
                 dsm.dsm_local_step(ar.ctx, -1, s, **local)
         if not fused:
