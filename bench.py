@@ -261,15 +261,21 @@ def main():
     updates_per_step = n * H * d + d
     value = updates_per_step / (ms_per_step / 1e3)
 
+    def pct(vals, q):
+        v = sorted(vals)
+        return v[min(len(v) - 1, max(0, round(q * (len(v) - 1))))]
+
     def kern(pairs, nbytes, updates):
         ms = avg_ms(pairs)
         if ms is None:
             return None
+        times = [a.elapsed_time(b) for a, b in pairs]
         gbs = nbytes / (ms / 1e3) / 1e9
         return {"ms": round(ms, 4), "GB_per_s": round(gbs, 1),
                 "pct_peak_hbm": round(100 * gbs / PEAK_HBM_GBS, 2),
                 "param_updates_per_s": updates / (ms / 1e3), "algorithmic_bytes": nbytes,
-                "launches": len(pairs)}
+                "launches": len(pairs), "ms_p10": round(pct(times, 0.1), 4),
+                "ms_median": round(pct(times, 0.5), 4), "ms_p90": round(pct(times, 0.9), 4)}
 
     local_bytes = (BYTES_LOCAL_ADAMW if adamw else BYTES_LOCAL_SGDM) * n * d
     ms_local = avg_ms(ev["local"])
