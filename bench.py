@@ -38,10 +38,11 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def committed_traffic(kernel_hash, name):
+def committed_traffic(kernel_hash, workload, name):
     """HBM bytes per launch from the committed rocprofv3 counter summary, or
-    None when the counters were taken on a different kernel source."""
-    path = os.path.join(ROOT, "profiles", "hbm_traffic_xl.json")
+    None when the counters were taken on a different kernel source, another
+    workload, or do not cover the kernel."""
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -279,7 +280,7 @@ def main():
 
     local_bytes = (BYTES_LOCAL_ADAMW if adamw else BYTES_LOCAL_SGDM) * n * d
     ms_local = avg_ms(ev["local"])
-    traffic = committed_traffic(khash, "local_adamw")
+    traffic = committed_traffic(khash, w.name, "local_adamw" if adamw else "local_sgdm")
     achieved = local_bytes / (ms_local / 1e3) / 1e9
     local_state = 16 if adamw else 12        # x, g, s1 (, s2) read per worker
     local_written = 8 if adamw else 4        # s1 (, s2) written per worker by the round end
