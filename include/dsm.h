@@ -242,11 +242,13 @@ DSM_API dsm_status dsm_sync(dsm_ctx* ctx);
 
 /*
  * dsm_read_bounds - copies the per-tensor bounds B_p of the last randomized
- * global step into host_B[n_tensors] (host memory, caller-owned) and
- * synchronises the stream.  Errors: DSM_ERR_STATE if the last global step was
- * not randomized; DSM_ERR_INVALID_ARG; DSM_ERR_HIP.
+ * global step (Eqs. (9)/(10)) into host_B (host memory, caller-owned, room for
+ * capacity floats; n_tensors of them are written) and synchronises the stream.
+ * Errors: DSM_ERR_STATE if the last global step was not randomized;
+ * DSM_ERR_INVALID_ARG for a NULL context or output, or capacity < n_tensors
+ * (nothing is written); DSM_ERR_HIP.
  */
-DSM_API dsm_status dsm_read_bounds(dsm_ctx* ctx, float* host_B);
+DSM_API dsm_status dsm_read_bounds(dsm_ctx* ctx, float* host_B, int32_t capacity);
 
 /*
  * dsm_test_philox - diagnostic: writes Philox4x32-10 blocks for counters

@@ -513,13 +513,16 @@ dsm_status dsm_sync(dsm_ctx* ctx) {
     return DSM_OK;
 }
 
-dsm_status dsm_read_bounds(dsm_ctx* ctx, float* host_B) {
+dsm_status dsm_read_bounds(dsm_ctx* ctx, float* host_B, int32_t capacity) {
     dsm_status st = check_ctx(ctx);
     if (st != DSM_OK) return st;
     if (!ctx->bounds_valid)
         return fail(ctx, DSM_ERR_STATE, "the last global step did not use the randomized sign");
     if (ctx->n_tensors == 0) return DSM_OK;
     if (!host_B) return fail(ctx, DSM_ERR_INVALID_ARG, "host_B is NULL");
+    if (capacity < ctx->n_tensors)
+        return fail(ctx, DSM_ERR_INVALID_ARG, "host_B holds %d floats, the problem has %d tensors",
+                    capacity, ctx->n_tensors);
     hipError_t e = hipMemcpyAsync(host_B, ctx->d_bounds, sizeof(uint32_t) * ctx->n_tensors,
                                   hipMemcpyDeviceToHost, ctx->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);

@@ -95,7 +95,8 @@ def load_library(path=LIBPATH):
                                   ctypes.POINTER(dsm_local_hparams), ctypes.c_int64,
                                   ctypes.POINTER(dsm_global_hparams), ctypes.c_int32]
     lib.dsm_sync.argtypes = [ctypes.c_void_p]
-    lib.dsm_read_bounds.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_float)]
+    lib.dsm_read_bounds.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_float),
+                                    ctypes.c_int32]
     lib.dsm_test_philox.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int64,
                                     ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p,
                                     ctypes.c_void_p]
@@ -177,9 +178,11 @@ def dsm_sync(ctx):
 
 
 def dsm_read_bounds(ctx, n_tensors):
+    """The bounds of the last randomized global step; n_tensors is the size of
+    the array handed to the library (the call fails if the problem has more)."""
     out = np.zeros(max(n_tensors, 1), dtype=np.float32)
-    _check(load_library().dsm_read_bounds(ctx, out.ctypes.data_as(ctypes.POINTER(ctypes.c_float))),
-           ctx)
+    _check(load_library().dsm_read_bounds(ctx, out.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                                          out.size), ctx)
     return out[:n_tensors]
 
 

@@ -500,7 +500,7 @@ void check_state_machine_adamw() {
     }
     for (int w : {0, 1, 3, 4}) CHECK(dsm_local_step(ctx, w, 2, &lh) == DSM_OK, "worker %d", w);
     for (int w : {0, 1, 3, 4}) CHECK(dsm_local_step(ctx, w, 3, &lh) == DSM_OK, "worker %d", w);
-    CHECK(dsm_read_bounds(ctx, nullptr) == DSM_ERR_STATE, "bounds before a randomized step");
+    CHECK(dsm_read_bounds(ctx, nullptr, 0) == DSM_ERR_STATE, "bounds before a randomized step");
     // Global step without broadcast: every replica becomes stale.
     g_log.clear();
     CHECK(dsm_global_step(ctx, 0, &gh, 0) == DSM_OK, "global, no broadcast");
@@ -546,9 +546,12 @@ void check_state_machine_adamw() {
         const float want[3] = {0.5f, 2.0f, 0.0f};
         std::memcpy(words, want, sizeof want);
         float got[3] = {-1, -1, -1};
-        CHECK(dsm_read_bounds(ctx, got) == DSM_OK, "read bounds");
+        float small[2] = {-1, -1};
+        CHECK(dsm_read_bounds(ctx, small, 2) == DSM_ERR_INVALID_ARG, "capacity below n_tensors");
+        CHECK(small[0] == -1 && small[1] == -1, "nothing written on a short array");
+        CHECK(dsm_read_bounds(ctx, got, 3) == DSM_OK, "read bounds");
         CHECK(std::memcmp(got, want, sizeof want) == 0, "bounds round trip");
-        CHECK(dsm_read_bounds(ctx, nullptr) == DSM_ERR_INVALID_ARG, "NULL bounds output");
+        CHECK(dsm_read_bounds(ctx, nullptr, 3) == DSM_ERR_INVALID_ARG, "NULL bounds output");
     }
     // Variants are refused by the fused round end; round end with H - 1
     // steps only.
@@ -772,7 +775,7 @@ void check_hyperparameter_errors() {
     CHECK(dsm_global_step(nullptr, 0, &g, 1) == DSM_ERR_INVALID_ARG, "NULL ctx global");
     CHECK(dsm_round_end(nullptr, 1, &h, 0, &g, 1) == DSM_ERR_INVALID_ARG, "NULL ctx round end");
     CHECK(dsm_sync(nullptr) == DSM_ERR_INVALID_ARG, "NULL ctx sync");
-    CHECK(dsm_read_bounds(nullptr, nullptr) == DSM_ERR_INVALID_ARG, "NULL ctx bounds");
+    CHECK(dsm_read_bounds(nullptr, nullptr, 0) == DSM_ERR_INVALID_ARG, "NULL ctx bounds");
     CHECK(dsm_destroy(nullptr) == DSM_OK, "NULL ctx destroy");
 }
 

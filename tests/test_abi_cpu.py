@@ -131,7 +131,7 @@ def test_null_context_is_an_argument_error(lib):
         with pytest.raises(dsm.DsmError) as e:
             call()
         assert e.value.status == dsm.DSM_ERR_INVALID_ARG
-    assert lib.dsm_read_bounds(None, None) == dsm.DSM_ERR_INVALID_ARG
+    assert lib.dsm_read_bounds(None, None, 0) == dsm.DSM_ERR_INVALID_ARG
     assert lib.dsm_destroy(None) == dsm.DSM_OK
 
 

@@ -372,6 +372,21 @@ def test_state_machine_on_gpu():
     ar.destroy()
 
 
+def test_read_bounds_checks_the_output_capacity():
+    """dsm_read_bounds writes one float per tensor; an array with room for
+    fewer is an argument error, not an overrun."""
+    ar, gen = make(RAGGED, 2, 1, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, seed=8)
+    ar.g_rep.normal_(0.0, 1e-3, generator=gen)
+    dsm.dsm_local_step(ar.ctx, -1, 1, lr=0.05, beta1=0.5)
+    dsm.dsm_global_step(ar.ctx, 0, mode=dsm.DSM_SIGN_RAND_FLIP, seed=1, **GLOB)
+    with pytest.raises(dsm.DsmError) as e:
+        dsm.dsm_read_bounds(ar.ctx, len(RAGGED) - 1)
+    assert e.value.status == dsm.DSM_ERR_INVALID_ARG
+    B = dsm.dsm_read_bounds(ar.ctx, len(RAGGED))
+    assert B.shape == (len(RAGGED),) and np.all(B >= 0)
+    ar.destroy()
+
+
 def test_empty_problem_is_a_no_op():
     ar = A.Arenas([], 2, 1, dsm.DSM_BASE_ADAMW)
     ar.init()
