@@ -1,10 +1,11 @@
 // gfx950 kernels of distributed sign momentum with local steps
 // (arXiv 2411.17866, Algorithm 1).
 //
-// Every kernel streams fp32 arenas: each work-group takes one chunk of one
-// tensor (Chunk), each thread moves 128-bit (float4) groups with nontemporal
-// loads and stores, consecutive threads touch consecutive 16-byte groups,
-// and every element is read and written once per pass.  Nothing here is a
+// Every kernel streams fp32 arenas: each work-group takes one piece of one
+// chunk of one tensor (Chunk; by default 256 threads x one float4 = 1024
+// elements), each thread moves 128-bit (float4) groups with nontemporal loads
+// and stores, consecutive threads touch consecutive 16-byte groups, and every
+// element is read and written once per pass.  Nothing here is a
 // dense contraction, so there is no MFMA; the bound is HBM bandwidth.
 //
 // Arithmetic: fp32, one IEEE round-to-nearest operation per written
@@ -529,16 +530,9 @@ __global__ __launch_bounds__(kBlockThreads) void k_global_rand_pass2(
     }
 }
 
-// ---------------------------------------------------------------- fused round end
+// ---------------------------------------------------------------- local step from x
 
-// The last local step of every worker (Algorithm 2 or 3, Eq. (4)) fused with
-// the global step (all-reduce, Eqs. (6)-(8)): each worker's step-H replica
-// value stays in registers and is folded into the worker-order sum
-// sum_i (x - x_i) as it is produced, so the replicas are neither stored after
-// step H nor read back.  Per element the operations and their order are those
-// of k_local_* followed by k_global_det / k_global_rand_pass1, so the results
-// are bit-identical.  KIND: 0 deterministic sign, 1 deterministic sign with
-// broadcast, 2 randomized pass 1 (u, m and the bound; pass 2 follows).
+// Base optimizer of the kernels that take local steps of several workers.
 constexpr int kBaseAdamW = 0;
 constexpr int kBaseSgd = 1;
 
@@ -607,6 +601,17 @@ __global__ __launch_bounds__(kBlockThreads) void k_local_from_x(
         }
     }
 }
+
+// ---------------------------------------------------------------- fused round end
+
+// The last local step of every worker (Algorithm 2 or 3, Eq. (4)) fused with
+// the global step (all-reduce, Eqs. (6)-(8)): each worker's step-H replica
+// value stays in registers and is folded into the worker-order sum
+// sum_i (x - x_i) as it is produced, so the replicas are neither stored after
+// step H nor read back.  Per element the operations and their order are those
+// of k_local_* followed by k_global_det / k_global_rand_pass1, so the results
+// are bit-identical.  KIND: 0 deterministic sign, 1 deterministic sign with
+// broadcast, 2 randomized pass 1 (u, m and the bound; pass 2 follows).
 
 template <int N, int BASE, int KIND>
 __global__ __launch_bounds__(kBlockThreads) void k_round_end(
