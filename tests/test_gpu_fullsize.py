@@ -15,6 +15,8 @@ dsm_global_step, and a fused round ending in dsm_round_end (sampled).  The
 randomized bound B_p is checked against the exact max |u| of every whole
 tensor on the GPU, and against the oracle on whole tensors for a subset.
 """
+import gc
+
 import numpy as np
 import pytest
 import torch
@@ -92,10 +94,16 @@ class Run:
 def run(request):
     if torch.cuda.get_device_properties(0).total_memory < 200e9:
         pytest.skip("needs the full HBM of one MI355X")
+    gc.collect()
+    torch.cuda.empty_cache()
     r = Run(request.param)
     yield r
+    # Free the arenas now, not when pytest drops the fixture value, so the next
+    # workload (or module) never shares the device with them.
     r.ar.destroy()
-    del r
+    r.ar = r.idx = None
+    gc.collect()
+    torch.cuda.synchronize()
     torch.cuda.empty_cache()
 
 
