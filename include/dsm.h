@@ -27,6 +27,8 @@
  *    state errors are detected on the host before anything is enqueued, and
  *    then nothing is modified.  dsm_last_error gives the message.
  *  - A context is not thread-safe; use one context per thread or lock.
+ *    Contexts may share the model buffers (they then take turns on the same
+ *    state) but never a workspace.
  */
 #ifndef DSM_H
 #define DSM_H
@@ -103,7 +105,8 @@ typedef struct dsm_buffers {
     float* s2_rep;     /* [n * d_pad]  AdamW second moment; NULL for SGD */
     float* u_scratch;  /* [d_pad]      u_{t+1} staging for the randomized
                           sign; may be NULL if it is never used */
-    void* workspace;   /* device, >= workspace_bytes from dsm_layout */
+    void* workspace;   /* device, >= workspace_bytes from dsm_layout; holds the
+                          context's chunk table and bounds, so one per context */
     int64_t workspace_bytes;
     void* stream;      /* hipStream_t all work is enqueued on (NULL = default) */
     float* v;          /* [d_pad]      global second moment of DSM_RULE_GLOBAL_ADAMW
