@@ -89,7 +89,7 @@ def cpu_baseline(w, ar, sample_tensors):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="xl")
     ap.add_argument("--sign", choices=("det", "rand"), default="det",
@@ -97,7 +97,7 @@ def main():
     ap.add_argument("--path", choices=("fused", "split"), default="fused",
                     help="fused: H-1 local steps + dsm_round_end with the lazy broadcast; "
                          "split: H local steps + dsm_global_step with broadcast")
-    ap.add_argument("--extra-steps", type=int, default=2,
+    ap.add_argument("--extra-steps", type=int, default=4,
                     help="rounds of each other path/sign combination, timed separately")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
