@@ -1,0 +1,147 @@
+/*
+ * The C ABI of include/dsm.h used from plain C (no Python, no torch): device
+ * buffers from hipMalloc, one fused round with the lazy broadcast, then one
+ * split round with broadcast, then checks on the host:
+ *   - every replica equals x bit for bit after the broadcast (Algorithm 1
+ *     synchronisation step);
+ *   - with lambda = 0, x moved by exactly eta * gamma per element on which the
+ *     sign of u is +-1, and not at all where it is 0 (Eq. (7));
+ *   - every error path returns a status and a message.
+ * Prints "c abi example ok" and exits 0, or names the failed check and
+ * exits 1.
+ */
+#include <hip/hip_runtime_api.h>
+#include <math.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "dsm.h"
+
+#define HIP_OK(call)                                                                  \
+    do {                                                                              \
+        hipError_t e_ = (call);                                                       \
+        if (e_ != hipSuccess) {                                                       \
+            printf("HIP error %d at line %d\n", (int)e_, __LINE__);                   \
+            return 1;                                                                 \
+        }                                                                             \
+    } while (0)
+#define DSM_OK_(call)                                                                 \
+    do {                                                                              \
+        dsm_status s_ = (call);                                                       \
+        if (s_ != DSM_OK) {                                                           \
+            printf("dsm status %d at line %d: %s\n", (int)s_, __LINE__, dsm_last_error(NULL)); \
+            return 1;                                                                 \
+        }                                                                             \
+    } while (0)
+
+static uint32_t lcg(uint32_t* s) {
+    *s = *s * 1664525u + 1013904223u;
+    return *s;
+}
+
+int main(void) {
+    const int64_t numel[3] = {5, 1000, 16385};
+    const uint8_t decay[3] = {0, 1, 1};
+    const int n = 3, H = 2;
+    dsm_problem prob = {n, H, 3, DSM_BASE_ADAMW, numel, decay};
+    int64_t arena = 0, offs[3], ws = 0;
+    DSM_OK_(dsm_layout(&prob, &arena, offs, &ws));
+
+    const size_t one = (size_t)arena * sizeof(float), many = one * (size_t)n;
+    float *x, *m, *x_rep, *g_rep, *s1, *s2;
+    void* work;
+    HIP_OK(hipMalloc((void**)&x, one));
+    HIP_OK(hipMalloc((void**)&m, one));
+    HIP_OK(hipMalloc((void**)&x_rep, many));
+    HIP_OK(hipMalloc((void**)&g_rep, many));
+    HIP_OK(hipMalloc((void**)&s1, many));
+    HIP_OK(hipMalloc((void**)&s2, many));
+    HIP_OK(hipMalloc(&work, (size_t)ws));
+
+    float* hx = (float*)malloc(one);
+    float* hx1 = (float*)malloc(one);
+    float* hg = (float*)malloc(many);
+    float* hr = (float*)malloc(many);
+    if (!hx || !hx1 || !hg || !hr) return 1;
+    uint32_t seed = 12345u;
+    for (int64_t j = 0; j < arena; ++j) hx[j] = ((float)(lcg(&seed) >> 8) / 16777216.0f - 0.5f) * 0.04f;
+    HIP_OK(hipMemcpy(x, hx, one, hipMemcpyHostToDevice));
+
+    hipStream_t st;
+    HIP_OK(hipStreamCreate(&st));
+    dsm_buffers buf = {x, m, x_rep, g_rep, s1, s2, NULL, work, ws, st, NULL};
+    dsm_ctx* ctx = NULL;
+    DSM_OK_(dsm_init(&prob, &buf, &ctx));
+
+    dsm_local_hparams lh = {1e-3f, 0.9f, 0.95f, 1e-8f, 0.1f};
+    dsm_global_hparams gh = {1e-3f, 0.8f, 0.95f, 0.98f, 0.0f, DSM_SIGN_DET, 0, DSM_RULE_SIGN_MOMENTUM, 1e-8f};
+    int64_t s = 0;
+    for (int t = 0; t < 2; ++t) {
+        for (int k = 0; k < H; ++k) {
+            for (size_t j = 0; j < (size_t)arena * (size_t)n; ++j)
+                hg[j] = ((float)(lcg(&seed) >> 8) / 16777216.0f - 0.5f) * 0.02f;
+            HIP_OK(hipMemcpyAsync(g_rep, hg, many, hipMemcpyHostToDevice, st));
+            HIP_OK(hipStreamSynchronize(st));
+            ++s;
+            if (t == 0 && k == H - 1)
+                DSM_OK_(dsm_round_end(ctx, s, &lh, t, &gh, 0));       /* fused, lazy */
+            else
+                DSM_OK_(dsm_local_step(ctx, -1, s, &lh));
+        }
+        if (t == 1) {
+            HIP_OK(hipStreamSynchronize(st));
+            HIP_OK(hipMemcpy(hx, x, one, hipMemcpyDeviceToHost));   /* x before the step */
+            DSM_OK_(dsm_global_step(ctx, t, &gh, 1));              /* split, broadcast */
+        }
+    }
+    HIP_OK(hipStreamSynchronize(st));
+    HIP_OK(hipMemcpy(hx1, x, one, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(hr, x_rep, many, hipMemcpyDeviceToHost));
+
+    /* Replicas equal x on every tensor element. */
+    for (int i = 0; i < n; ++i)
+        for (int p = 0; p < 3; ++p)
+            if (memcmp(hr + (size_t)i * (size_t)arena + offs[p], hx1 + offs[p],
+                       (size_t)numel[p] * sizeof(float)) != 0) {
+                printf("replica %d differs from x on tensor %d\n", i, p);
+                return 1;
+            }
+    /* lambda = 0: x - x_new is +-eta*gamma rounded, or 0. */
+    const float step = (float)((double)0.8f * (double)1e-3f);   /* as the runtime forms eta * gamma */
+    int64_t moved = 0;
+    for (int p = 0; p < 3; ++p)
+        for (int64_t j = 0; j < numel[p]; ++j) {
+            const float a = hx[offs[p] + j], b = hx1[offs[p] + j];
+            const float d = a - b;
+            const float plus = a - step, minus = a + step;
+            if (!(b == a || b == plus || b == minus)) {
+                printf("tensor %d element %lld moved by %g, not +-%g\n", p, (long long)j, d, step);
+                return 1;
+            }
+            moved += (b != a);
+        }
+    if (moved == 0) {
+        printf("no element moved\n");
+        return 1;
+    }
+
+    /* Error paths return a status and a message. */
+    if (dsm_global_step(ctx, 2, &gh, 1) != DSM_ERR_STATE || strlen(dsm_last_error(ctx)) == 0) {
+        printf("global step before H local steps was not refused\n");
+        return 1;
+    }
+    float bounds[3];
+    if (dsm_read_bounds(ctx, bounds, 3) != DSM_ERR_STATE) {
+        printf("bounds of a deterministic step were not refused\n");
+        return 1;
+    }
+    DSM_OK_(dsm_destroy(ctx));
+    HIP_OK(hipFree(x)); HIP_OK(hipFree(m)); HIP_OK(hipFree(x_rep)); HIP_OK(hipFree(g_rep));
+    HIP_OK(hipFree(s1)); HIP_OK(hipFree(s2)); HIP_OK(hipFree(work));
+    HIP_OK(hipStreamDestroy(st));
+    free(hx); free(hx1); free(hg); free(hr);
+    printf("c abi example ok (%lld elements moved by one sign step)\n", (long long)moved);
+    return 0;
+}
