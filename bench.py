@@ -62,6 +62,10 @@ def cpu_baseline(w, ar, sample_tensors):
     import oracle as O
 
     idx = [i for i, (name, _) in enumerate(w.tensors) if name in sample_tensors]
+    which = f"{len(idx)} tensors of transformer layer 0"
+    if not idx:                      # a workload with no transformer layer: all of it
+        idx = list(range(len(w.tensors)))
+        which = f"all {len(idx)} tensors"
     torch.cuda.synchronize()
 
     def take(flat):
@@ -80,8 +84,8 @@ def cpu_baseline(w, ar, sample_tensors):
     updates = w.n_workers * w.local_steps * d_s + d_s
     return {"value": updates / dt, "unit": "param-updates/s", "cores": 1, "kind": "oracle",
             "sample": (f"one round (n={w.n_workers}, H={w.local_steps} {base} local steps + "
-                       f"deterministic global step) of the oracle in fp64 on the {len(idx)} "
-                       f"tensors of transformer layer 0 ({d_s} of {w.d} parameters); "
+                       f"deterministic global step) of the oracle in fp64 on the {which} "
+                       f"({d_s} of {w.d} parameters); "
                        f"{dt:.1f} s on one host thread"),
             "seconds": dt, "host_threads_available": len(os.sched_getaffinity(0))}
 
@@ -97,8 +101,12 @@ def main():
     ap.add_argument("--path", choices=("fused", "split"), default="fused",
                     help="fused: H-1 local steps + dsm_round_end with the lazy broadcast; "
                          "split: H local steps + dsm_global_step with broadcast")
-    ap.add_argument("--extra-steps", type=int, default=4,
+    ap.add_argument("--extra-steps", type=int, default=20,
                     help="rounds of each other path/sign combination, timed separately")
+    ap.add_argument("--flush-mb", type=int, default=0,
+                    help="if > 0, also time rounds in which every call follows a write of this "
+                         "many MB to a separate buffer, which evicts the arenas from the caches "
+                         "(reported under breakdown_flushed; the timed steps stay unflushed)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="accepted for the counter runs; the plain 4 GiB device copy that "
@@ -142,7 +150,11 @@ def main():
     # kernel with fewer bytes, timed on its own.
     stale = [False]
 
+    flush_buf = [None]
+
     def timed(key, fn):
+        if flush_buf[0] is not None:
+            flush_buf[0].fill_(0.0)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         fn()
@@ -206,6 +218,26 @@ def main():
                                                **ghp))
         t += 1
     torch.cuda.synchronize()
+
+    # The same calls with cold caches: each one follows a write of flush_mb MB
+    # to another buffer (outside its events), so no arena line is left in L2
+    # or the MALL (Infinity Cache, 256 MB) when it starts.  This matters only
+    # where the arenas fit in the caches (the tiny workload, ~80 MB).
+    ev_flushed = None
+    if args.flush_mb > 0:
+        main_lists = {k: v for k, v in ev.items()}
+        for k in ev:
+            ev[k] = []
+        flush_buf[0] = torch.empty(args.flush_mb * (1 << 20) // 4, dtype=torch.float32,
+                                   device="cuda")
+        for path in ("fused", "split"):
+            for _ in range(max(1, args.extra_steps)):
+                one_round(t, dsm.DSM_SIGN_DET, path, True)
+                t += 1
+        torch.cuda.synchronize()
+        flush_buf[0] = None
+        ev_flushed = {k: v for k, v in ev.items()}
+        ev.update(main_lists)
 
     # Row a2 (local SGD + Polyak momentum, Algorithm 3) and row a6 on its own
     # (dsm_sync) at the same scale: a second context, SGD base, over the same
@@ -334,6 +366,15 @@ def main():
             "global_adamw": kern(ev["global_adamw"], (bytes_global(n, False) + 8) * d, d),
             "local_sgdm": kern(ev_sgd, BYTES_LOCAL_SGDM * n * d, n * d),
             "sync": kern(ev_sync, (4 + 4 * n) * d, n * d),
+        },
+        "breakdown_flushed": None if ev_flushed is None else {
+            "flush_mb": args.flush_mb,
+            "local_step": kern(ev_flushed["local"], local_bytes, n * d),
+            "local_step_from_x": kern(ev_flushed["local_from_x"],
+                                      (4 + (local_state - 4 + local_written + 4) * n) * d, n * d),
+            "round_end_fused_det": kern(ev_flushed["fused_det"],
+                                        (16 + (local_state + local_written) * n) * d, n * d + d),
+            "global_det": kern(ev_flushed["split_det"], bytes_global(n, False) * d, d),
         },
         "device_ceiling": {"torch_copy_GB_per_s": round(copy_gbs, 1),
                            "torch_fill_GB_per_s": round(fill_gbs, 1)},

@@ -106,7 +106,8 @@ typedef struct dsm_buffers {
     float* u_scratch;  /* [d_pad]      u_{t+1} staging for the randomized
                           sign; may be NULL if it is never used */
     void* workspace;   /* device, >= workspace_bytes from dsm_layout; holds the
-                          context's chunk table and bounds, so one per context */
+                          context's chunk table and the randomized sign's bound
+                          words, so one per context */
     int64_t workspace_bytes;
     void* stream;      /* hipStream_t all work is enqueued on (NULL = default) */
     float* v;          /* [d_pad]      global second moment of DSM_RULE_GLOBAL_ADAMW
@@ -140,8 +141,10 @@ typedef struct dsm_global_hparams {
  * Computes the arena layout for a problem: *arena_elems = d_pad, the length
  * of one arena copy; tensor_offsets[p] = element offset of tensor p (the
  * caller provides an array of n_tensors entries, or NULL); and
- * *workspace_bytes = device workspace the context needs (tensor chunk table
- * and the per-tensor bounds of the randomized sign).  Any output may be NULL.
+ * *workspace_bytes = device workspace the context needs: the tensor chunk
+ * table, and for the randomized sign the per-tensor bounds with their
+ * first-level partial maxima (4 bytes per 1024 elements).  Any output may be
+ * NULL.
  * Errors: DSM_ERR_INVALID_ARG for an invalid problem.
  */
 DSM_API dsm_status dsm_layout(const dsm_problem* problem, int64_t* arena_elems,
@@ -194,7 +197,8 @@ DSM_API dsm_status dsm_local_step(dsm_ctx* ctx, int32_t worker, int64_t step,
 
 /*
  * dsm_global_step - Algorithm 1 all-reduce and global step of outer
- * iteration t, fused in one pass (two for the randomized sign):
+ * iteration t, fused in one pass (for the randomized sign two, with the
+ * per-tensor bound reduced in between):
  *   delta = (1/n) sum_{i=0}^{n-1} (x - x^(i))        (worker order)
  *   u     = b1*m + ((1-b1)/gamma)*delta               Eq. (6)
  *   x     = x - (eta*gamma)*(S(u) + lambda_p*x)       Eq. (7)

@@ -106,6 +106,14 @@ hipError_t launch_local_from_x(const Chunk* chunks, int64_t n_chunks, const floa
                                int64_t stride, int n, bool adamw, const AdamScalars& as,
                                const SgdScalars& ss, hipStream_t st);
 
+// Workspace words of the randomized sign's per-tensor bound B_p = max |u|,
+// reduced in two levels without atomics.
+struct BoundWords {
+    uint32_t* bits;         // [n_tensors] B_p, fp32 bit patterns
+    uint32_t* piece_max;    // [n_chunks * kSplit] level one: max |u| of each piece
+    const int32_t* chunk0;  // [n_tensors + 1] first chunk of each tensor; last = n_chunks
+};
+
 // Arguments of the fused last-local-step + global-step launch.
 struct RoundEndArgs {
     float *x, *m, *x_rep;
@@ -113,7 +121,7 @@ struct RoundEndArgs {
     int64_t src_stride;
     const float* g_rep;
     float *s1, *s2, *u;
-    uint32_t* bound_bits;
+    BoundWords bound;
     int64_t stride;
     AdamScalars as;
     SgdScalars ss;
@@ -126,7 +134,7 @@ hipError_t launch_global_det(const Chunk* chunks, int64_t n_chunks, float* x, fl
                              float* v, float* x_rep, int64_t stride, const GlobalScalars& sc,
                              bool broadcast, hipStream_t st);
 hipError_t launch_global_rand(const Chunk* chunks, int64_t n_chunks, int n_tensors, float* x,
-                              float* m, float* x_rep, float* u, uint32_t* bound_bits,
+                              float* m, float* x_rep, float* u, const BoundWords& bw,
                               int64_t stride, const GlobalScalars& sc, bool broadcast,
                               hipStream_t st);
 hipError_t launch_broadcast(const Chunk* chunks, int64_t n_chunks, const float* x, float* x_rep,

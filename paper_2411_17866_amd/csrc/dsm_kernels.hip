@@ -69,6 +69,7 @@ __device__ __forceinline__ void store_group(f4 v, f4* p, int q, int nfull, int l
 // flight form compact fronts that sweep the arena.
 struct Piece {
     Chunk c;
+    uint32_t wi;     // piece index: chunk wi / kSplit, piece wi % kSplit of it
     int q_lo, q_hi;  // float4 groups of the chunk handled here
     int nfull;       // groups of four valid lanes in the chunk
 };
@@ -117,6 +118,7 @@ template <int MAP = kMapOther>
 __device__ __forceinline__ Piece piece_of(const Chunk* __restrict__ chunks) {
     Piece pc;
     const uint32_t wi = work_index<MAP>();
+    pc.wi = wi;
     pc.c = chunks[wi / kSplit];
     const int nvec = (pc.c.len + 3) >> 2;
     pc.q_lo = static_cast<int>(wi % kSplit) * kPieceVec;
@@ -390,10 +392,10 @@ __global__ __launch_bounds__(kBlockThreads) void k_global_det(
     }
 }
 
-// Largest of the bit patterns of non-negative floats of a work-group, then
-// one atomic max per work-group into the tensor's bound.  For non-negative
-// IEEE floats the unsigned order of the bit patterns is the numeric order.
-__device__ __forceinline__ void block_max_to(uint32_t bits, uint32_t* wave_max, uint32_t* dst) {
+// Largest of the values of a work-group of THREADS threads, valid in thread
+// 0.  wave_max holds THREADS / 64 words of LDS.
+template <int THREADS>
+__device__ __forceinline__ uint32_t block_max(uint32_t bits, uint32_t* wave_max) {
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
         const uint32_t o = __shfl_xor(bits, off, 64);
@@ -403,16 +405,23 @@ __device__ __forceinline__ void block_max_to(uint32_t bits, uint32_t* wave_max, 
     const int wave = threadIdx.x >> 6;
     if (lane == 0) wave_max[wave] = bits;
     __syncthreads();
+    uint32_t b = wave_max[0];
     if (threadIdx.x == 0) {
-        uint32_t b = wave_max[0];
 #pragma unroll
-        for (int w = 1; w < kBlockThreads / 64; ++w) b = wave_max[w] > b ? wave_max[w] : b;
-        // The bound only grows, so a work-group whose maximum does not exceed
-        // the value already stored has nothing to add; skipping its atomic
-        // keeps the many work-groups of a large tensor off one address.
-        const uint32_t cur = __hip_atomic_load(dst, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (b > cur) atomicMax(dst, b);
+        for (int w = 1; w < THREADS / 64; ++w) b = wave_max[w] > b ? wave_max[w] : b;
     }
+    return b;
+}
+
+// The tensor bound B_p = max |u| is reduced in two levels, with plain loads
+// and stores and no atomics.  Level one: each work-group stores the largest
+// |u| of its piece, as a bit pattern, in the piece's own slot (for
+// non-negative IEEE floats the unsigned order of the bit patterns is the
+// numeric order).  Level two is k_bound_reduce.
+__device__ __forceinline__ void store_piece_max(uint32_t bits, uint32_t* wave_max,
+                                                uint32_t* slot) {
+    const uint32_t b = block_max<kBlockThreads>(bits, wave_max);
+    if (threadIdx.x == 0) *slot = b;
 }
 
 // Randomized sign, pass 1: the all-reduce difference, u_{t+1} (staged to u)
@@ -420,7 +429,7 @@ __device__ __forceinline__ void block_max_to(uint32_t bits, uint32_t* wave_max, 
 template <int N>
 __global__ __launch_bounds__(kBlockThreads) void k_global_rand_pass1(
     const Chunk* __restrict__ chunks, const float* __restrict__ x, float* __restrict__ m,
-    const float* __restrict__ x_rep, float* __restrict__ u_out, uint32_t* __restrict__ bound_bits,
+    const float* __restrict__ x_rep, float* __restrict__ u_out, uint32_t* __restrict__ piece_max,
     int64_t stride, GlobalScalars sc) {
     const Piece pc = piece_of(chunks);
     const Chunk& c = pc.c;
@@ -463,7 +472,36 @@ __global__ __launch_bounds__(kBlockThreads) void k_global_rand_pass1(
             }
         }
     }
-    block_max_to(maxbits, wave_max, bound_bits + c.tensor);
+    store_piece_max(maxbits, wave_max, piece_max + pc.wi);
+}
+
+// Level two of the tensor bound: work-group p takes the piece maxima of
+// tensor p (slots chunk0[p] * kSplit up to chunk0[p + 1] * kSplit, the pieces
+// of its chunks) and stores their largest in bound_bits[p]; an empty tensor
+// has no slots and gets 0.
+constexpr int kReduceThreads = 1024;
+__global__ __launch_bounds__(kReduceThreads) void k_bound_reduce(
+    const uint32_t* __restrict__ piece_max, const int32_t* __restrict__ chunk0,
+    uint32_t* __restrict__ bound_bits) {
+    __shared__ uint32_t wave_max[kReduceThreads / 64];
+    const int p = blockIdx.x;
+    const int64_t lo = static_cast<int64_t>(chunk0[p]) * kSplit;
+    const int64_t hi = static_cast<int64_t>(chunk0[p + 1]) * kSplit;
+    uint32_t b = 0;
+    if constexpr (kSplit % 4 == 0) {
+        // lo is a multiple of 4 slots, and the slots start 256-byte aligned.
+        const uint4* __restrict__ v = reinterpret_cast<const uint4*>(piece_max + lo);
+        const int64_t nv = (hi - lo) / 4;
+#pragma unroll 4
+        for (int64_t i = threadIdx.x; i < nv; i += kReduceThreads) {
+            const uint4 w = v[i];
+            b = max(b, max(max(w.x, w.y), max(w.z, w.w)));
+        }
+    } else {
+        for (int64_t i = lo + threadIdx.x; i < hi; i += kReduceThreads) b = max(b, piece_max[i]);
+    }
+    b = block_max<kReduceThreads>(b, wave_max);
+    if (threadIdx.x == 0) bound_bits[p] = b;
 }
 
 // S_r(u) of Eq. (9) (MODE 1) or Eq. (10) (MODE 2) for one element, given the
@@ -618,7 +656,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_round_end(
     const Chunk* __restrict__ chunks, float* __restrict__ x, float* __restrict__ m,
     float* __restrict__ x_rep, const float* __restrict__ x_src, int64_t src_stride,
     const float* __restrict__ g_rep, float* __restrict__ s1, float* __restrict__ s2,
-    float* __restrict__ u_out, uint32_t* __restrict__ bound_bits, int64_t stride,
+    float* __restrict__ u_out, uint32_t* __restrict__ piece_max, int64_t stride,
     AdamScalars as, SgdScalars ss, GlobalScalars gs) {
     __shared__ uint32_t wave_max[kBlockThreads / 64];
     const Piece pc = piece_of<kMapRoundEnd>(chunks);
@@ -716,13 +754,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_round_end(
             }
         }
     }
-    if (KIND == 2) block_max_to(maxbits, wave_max, bound_bits + c.tensor);
-}
-
-__global__ __launch_bounds__(kBlockThreads) void k_fill_u32(uint32_t* __restrict__ p, int count,
-                                                           uint32_t value) {
-    const int i = blockIdx.x * kBlockThreads + threadIdx.x;
-    if (i < count) p[i] = value;
+    if (KIND == 2) store_piece_max(maxbits, wave_max, piece_max + pc.wi);
 }
 
 // ---------------------------------------------------------------- sync / init
@@ -824,7 +856,7 @@ static void launch_round_end_n(const Chunk* chunks, int64_t n_chunks, const Roun
     const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
 #define DSM_ROUND_END(NW)                                                                        \
     hipLaunchKernelGGL((k_round_end<NW, BASE, KIND>), grid, block, 0, st, chunks, a.x, a.m,      \
-                       a.x_rep, a.x_src, a.src_stride, a.g_rep, a.s1, a.s2, a.u, a.bound_bits,  \
+                       a.x_rep, a.x_src, a.src_stride, a.g_rep, a.s1, a.s2, a.u, a.bound.piece_max, \
                        a.stride, a.as, a.ss, a.gs)
     switch (a.gs.n) {
         case 1: DSM_ROUND_END(1); break;
@@ -880,33 +912,44 @@ hipError_t launch_local_from_x(const Chunk* chunks, int64_t n_chunks, const floa
     return hipGetLastError();
 }
 
+// Level two of the tensor bound, after a first pass has stored its piece
+// maxima.  Also run with no chunks at all, so that every bound is written.
+static void launch_bound_reduce(const BoundWords& bw, int n_tensors, hipStream_t st) {
+    hipLaunchKernelGGL(k_bound_reduce, dim3(static_cast<unsigned>(n_tensors)),
+                       dim3(kReduceThreads), 0, st, bw.piece_max, bw.chunk0, bw.bits);
+}
+
+static void launch_rand_pass2(const Chunk* chunks, int64_t n_chunks, float* x, float* x_rep,
+                              const float* u, const uint32_t* bits, int64_t stride,
+                              const GlobalScalars& sc, bool broadcast, hipStream_t st) {
+    const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
+    if (sc.mode == 1) {
+        if (broadcast)
+            hipLaunchKernelGGL((k_global_rand_pass2<1, true>), grid, block, 0, st, chunks, x, x_rep, u, bits, stride, sc);
+        else
+            hipLaunchKernelGGL((k_global_rand_pass2<1, false>), grid, block, 0, st, chunks, x, x_rep, u, bits, stride, sc);
+    } else {
+        if (broadcast)
+            hipLaunchKernelGGL((k_global_rand_pass2<2, true>), grid, block, 0, st, chunks, x, x_rep, u, bits, stride, sc);
+        else
+            hipLaunchKernelGGL((k_global_rand_pass2<2, false>), grid, block, 0, st, chunks, x, x_rep, u, bits, stride, sc);
+    }
+}
+
 hipError_t launch_round_end(const Chunk* chunks, int64_t n_chunks, int n_tensors, bool adamw,
                             const RoundEndArgs& a, bool broadcast, hipStream_t st) {
     const bool randomized = a.gs.mode != 0;
-    if (randomized && n_tensors > 0) {
-        hipLaunchKernelGGL(k_fill_u32, dim3((n_tensors + kBlockThreads - 1) / kBlockThreads),
-                           dim3(kBlockThreads), 0, st, a.bound_bits, n_tensors, 0u);
-    }
-    if (n_chunks == 0) return hipGetLastError();
     const int kind = randomized ? 2 : (broadcast ? 1 : 0);
-    if (adamw)
-        launch_round_end_base<kBaseAdamW>(chunks, n_chunks, a, kind, st);
-    else
-        launch_round_end_base<kBaseSgd>(chunks, n_chunks, a, kind, st);
-    if (randomized) {
-        const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
-        if (a.gs.mode == 1) {
-            if (broadcast)
-                hipLaunchKernelGGL((k_global_rand_pass2<1, true>), grid, block, 0, st, chunks, a.x, a.x_rep, a.u, a.bound_bits, a.stride, a.gs);
-            else
-                hipLaunchKernelGGL((k_global_rand_pass2<1, false>), grid, block, 0, st, chunks, a.x, a.x_rep, a.u, a.bound_bits, a.stride, a.gs);
-        } else {
-            if (broadcast)
-                hipLaunchKernelGGL((k_global_rand_pass2<2, true>), grid, block, 0, st, chunks, a.x, a.x_rep, a.u, a.bound_bits, a.stride, a.gs);
-            else
-                hipLaunchKernelGGL((k_global_rand_pass2<2, false>), grid, block, 0, st, chunks, a.x, a.x_rep, a.u, a.bound_bits, a.stride, a.gs);
-        }
+    if (n_chunks > 0) {
+        if (adamw)
+            launch_round_end_base<kBaseAdamW>(chunks, n_chunks, a, kind, st);
+        else
+            launch_round_end_base<kBaseSgd>(chunks, n_chunks, a, kind, st);
     }
+    if (randomized && n_tensors > 0) launch_bound_reduce(a.bound, n_tensors, st);
+    if (randomized && n_chunks > 0)
+        launch_rand_pass2(chunks, n_chunks, a.x, a.x_rep, a.u, a.bound.bits, a.stride, a.gs,
+                          broadcast, st);
     return hipGetLastError();
 }
 
@@ -964,33 +1007,22 @@ hipError_t launch_global_det(const Chunk* chunks, int64_t n_chunks, float* x, fl
 }
 
 hipError_t launch_global_rand(const Chunk* chunks, int64_t n_chunks, int n_tensors, float* x,
-                              float* m, float* x_rep, float* u, uint32_t* bound_bits,
+                              float* m, float* x_rep, float* u, const BoundWords& bw,
                               int64_t stride, const GlobalScalars& sc, bool broadcast,
                               hipStream_t st) {
-    if (n_tensors > 0) {
-        hipLaunchKernelGGL(k_fill_u32, dim3((n_tensors + kBlockThreads - 1) / kBlockThreads),
-                           dim3(kBlockThreads), 0, st, bound_bits, n_tensors, 0u);
+    if (n_chunks > 0) {
+        const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
+        uint32_t* pm = bw.piece_max;
+        switch (sc.n) {
+            case 1: hipLaunchKernelGGL(k_global_rand_pass1<1>, grid, block, 0, st, chunks, x, m, x_rep, u, pm, stride, sc); break;
+            case 2: hipLaunchKernelGGL(k_global_rand_pass1<2>, grid, block, 0, st, chunks, x, m, x_rep, u, pm, stride, sc); break;
+            case 4: hipLaunchKernelGGL(k_global_rand_pass1<4>, grid, block, 0, st, chunks, x, m, x_rep, u, pm, stride, sc); break;
+            case 8: hipLaunchKernelGGL(k_global_rand_pass1<8>, grid, block, 0, st, chunks, x, m, x_rep, u, pm, stride, sc); break;
+            default: hipLaunchKernelGGL(k_global_rand_pass1<0>, grid, block, 0, st, chunks, x, m, x_rep, u, pm, stride, sc); break;
+        }
     }
-    if (n_chunks == 0) return hipGetLastError();
-    const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
-    switch (sc.n) {
-        case 1: hipLaunchKernelGGL(k_global_rand_pass1<1>, grid, block, 0, st, chunks, x, m, x_rep, u, bound_bits, stride, sc); break;
-        case 2: hipLaunchKernelGGL(k_global_rand_pass1<2>, grid, block, 0, st, chunks, x, m, x_rep, u, bound_bits, stride, sc); break;
-        case 4: hipLaunchKernelGGL(k_global_rand_pass1<4>, grid, block, 0, st, chunks, x, m, x_rep, u, bound_bits, stride, sc); break;
-        case 8: hipLaunchKernelGGL(k_global_rand_pass1<8>, grid, block, 0, st, chunks, x, m, x_rep, u, bound_bits, stride, sc); break;
-        default: hipLaunchKernelGGL(k_global_rand_pass1<0>, grid, block, 0, st, chunks, x, m, x_rep, u, bound_bits, stride, sc); break;
-    }
-    if (sc.mode == 1) {
-        if (broadcast)
-            hipLaunchKernelGGL((k_global_rand_pass2<1, true>), grid, block, 0, st, chunks, x, x_rep, u, bound_bits, stride, sc);
-        else
-            hipLaunchKernelGGL((k_global_rand_pass2<1, false>), grid, block, 0, st, chunks, x, x_rep, u, bound_bits, stride, sc);
-    } else {
-        if (broadcast)
-            hipLaunchKernelGGL((k_global_rand_pass2<2, true>), grid, block, 0, st, chunks, x, x_rep, u, bound_bits, stride, sc);
-        else
-            hipLaunchKernelGGL((k_global_rand_pass2<2, false>), grid, block, 0, st, chunks, x, x_rep, u, bound_bits, stride, sc);
-    }
+    if (n_tensors > 0) launch_bound_reduce(bw, n_tensors, st);
+    if (n_chunks > 0) launch_rand_pass2(chunks, n_chunks, x, x_rep, u, bw.bits, stride, sc, broadcast, st);
     return hipGetLastError();
 }
 

@@ -20,9 +20,10 @@ struct dsm_ctx {
     std::vector<uint8_t> decay;
     int64_t arena_elems = 0;
     std::vector<dsm::Chunk> chunks;  // host copy; the device copy lives in the workspace
+    std::vector<int32_t> chunk0;     // first chunk of each tensor, then n_chunks (host copy)
     dsm_buffers buf{};
     dsm::Chunk* d_chunks = nullptr;
-    uint32_t* d_bounds = nullptr;
+    dsm::BoundWords bound{};         // workspace words of the randomized sign's bound
     hipStream_t stream = nullptr;
     std::vector<int> local_count;  // local steps per worker since the last synchronisation
     std::vector<uint8_t> stale;    // replica not yet reset to x after a global step
@@ -67,6 +68,8 @@ struct Layout {
     int64_t n_chunks = 0;
     int64_t chunk_bytes = 0;
     int64_t bounds_off = 0;
+    int64_t chunk0_off = 0;
+    int64_t piece_max_off = 0;
     int64_t workspace_bytes = 0;
 };
 
@@ -91,10 +94,14 @@ dsm_status check_problem(const dsm_problem* p) {
     return DSM_OK;
 }
 
-// Tensors back to back, each starting at a multiple of 64 elements; the
-// chunk table (kChunkElems elements per chunk, never crossing a tensor)
-// followed by the per-tensor bound words, each at a 256-byte boundary.
-dsm_status make_layout(const dsm_problem* p, Layout* L, std::vector<dsm::Chunk>* chunks) {
+// Tensors back to back, each starting at a multiple of 64 elements.  The
+// workspace holds, each part at a 256-byte boundary: the chunk table
+// (kChunkElems elements per chunk, never crossing a tensor); the per-tensor
+// bound words; the first chunk of each tensor (n_tensors + 1 words); and one
+// piece-maximum word per work-group piece (n_chunks * kSplit), level one of
+// the bound.
+dsm_status make_layout(const dsm_problem* p, Layout* L, std::vector<dsm::Chunk>* chunks,
+                       std::vector<int32_t>* chunk0 = nullptr) {
     L->offsets.resize(p->n_tensors);
     int64_t off = 0, n_chunks = 0;
     for (int i = 0; i < p->n_tensors; ++i) {
@@ -109,7 +116,19 @@ dsm_status make_layout(const dsm_problem* p, Layout* L, std::vector<dsm::Chunk>*
     L->n_chunks = n_chunks;
     L->chunk_bytes = round_up(n_chunks * static_cast<int64_t>(sizeof(dsm::Chunk)), 256);
     L->bounds_off = L->chunk_bytes;
-    L->workspace_bytes = L->chunk_bytes + round_up(int64_t(p->n_tensors) * 4, 256);
+    L->chunk0_off = L->bounds_off + round_up(int64_t(p->n_tensors) * 4, 256);
+    L->piece_max_off =
+        L->chunk0_off + (p->n_tensors > 0 ? round_up((int64_t(p->n_tensors) + 1) * 4, 256) : 0);
+    L->workspace_bytes = L->piece_max_off + round_up(n_chunks * dsm::kSplit * 4, 256);
+    if (chunk0) {
+        chunk0->assign(p->n_tensors + 1, 0);
+        int64_t k = 0;
+        for (int i = 0; i < p->n_tensors; ++i) {
+            (*chunk0)[i] = static_cast<int32_t>(k);
+            k += (p->numel[i] + dsm::kChunkElems - 1) / dsm::kChunkElems;
+        }
+        (*chunk0)[p->n_tensors] = static_cast<int32_t>(k);
+    }
     if (chunks) {
         chunks->clear();
         chunks->reserve(n_chunks);
@@ -302,7 +321,8 @@ dsm_status dsm_init(const dsm_problem* problem, const dsm_buffers* b, dsm_ctx** 
     if (!b) return fail(nullptr, DSM_ERR_INVALID_ARG, "buffers is NULL");
     Layout L;
     std::vector<dsm::Chunk> chunks;
-    st = make_layout(problem, &L, &chunks);
+    std::vector<int32_t> chunk0;
+    st = make_layout(problem, &L, &chunks, &chunk0);
     if (st != DSM_OK) return st;
     const bool adamw = problem->base == DSM_BASE_ADAMW;
     if (L.arena_elems > 0) {
@@ -346,13 +366,27 @@ dsm_status dsm_init(const dsm_problem* problem, const dsm_buffers* b, dsm_ctx** 
     ctx->offsets = L.offsets;
     ctx->arena_elems = L.arena_elems;
     ctx->chunks = std::move(chunks);
+    ctx->chunk0 = std::move(chunk0);
     ctx->buf = *b;
     ctx->stream = static_cast<hipStream_t>(b->stream);
-    ctx->d_chunks = static_cast<dsm::Chunk*>(b->workspace);
-    ctx->d_bounds = reinterpret_cast<uint32_t*>(static_cast<char*>(b->workspace) + L.bounds_off);
+    char* ws = static_cast<char*>(b->workspace);
+    ctx->d_chunks = reinterpret_cast<dsm::Chunk*>(ws);
+    ctx->bound.bits = reinterpret_cast<uint32_t*>(ws + L.bounds_off);
+    ctx->bound.chunk0 = reinterpret_cast<const int32_t*>(ws + L.chunk0_off);
+    ctx->bound.piece_max = reinterpret_cast<uint32_t*>(ws + L.piece_max_off);
     ctx->local_count.assign(ctx->n, 0);
     ctx->stale.assign(ctx->n, 0);
 
+    if (ctx->n_tensors > 0) {
+        hipError_t e = hipMemcpyAsync(const_cast<int32_t*>(ctx->bound.chunk0), ctx->chunk0.data(),
+                                      ctx->chunk0.size() * sizeof(int32_t),
+                                      hipMemcpyHostToDevice, ctx->stream);
+        if (e != hipSuccess) {
+            dsm_status r = hip_fail(nullptr, "uploading the tensor chunk index", e);
+            delete ctx;
+            return r;
+        }
+    }
     if (!ctx->chunks.empty()) {
         hipError_t e = hipMemcpyAsync(ctx->d_chunks, ctx->chunks.data(),
                                       ctx->chunks.size() * sizeof(dsm::Chunk),
@@ -443,7 +477,7 @@ dsm_status dsm_global_step(dsm_ctx* ctx, int64_t t, const dsm_global_hparams* hp
                                    ctx->stream);
     } else {
         e = dsm::launch_global_rand(ctx->d_chunks, n_chunks, ctx->n_tensors, ctx->buf.x, ctx->buf.m,
-                                    ctx->buf.x_rep, ctx->buf.u_scratch, ctx->d_bounds,
+                                    ctx->buf.x_rep, ctx->buf.u_scratch, ctx->bound,
                                     ctx->arena_elems, sc, broadcast != 0, ctx->stream);
     }
     if (e != hipSuccess) return hip_fail(ctx, "launching the global step", e);
@@ -485,7 +519,7 @@ dsm_status dsm_round_end(dsm_ctx* ctx, int64_t step, const dsm_local_hparams* lo
     a.s1 = ctx->buf.s1_rep;
     a.s2 = ctx->buf.s2_rep;
     a.u = ctx->buf.u_scratch;
-    a.bound_bits = ctx->d_bounds;
+    a.bound = ctx->bound;
     a.stride = ctx->arena_elems;
     a.as = lc.adam;
     a.ss = lc.sgd;
@@ -523,7 +557,7 @@ dsm_status dsm_read_bounds(dsm_ctx* ctx, float* host_B, int32_t capacity) {
     if (capacity < ctx->n_tensors)
         return fail(ctx, DSM_ERR_INVALID_ARG, "host_B holds %d floats, the problem has %d tensors",
                     capacity, ctx->n_tensors);
-    hipError_t e = hipMemcpyAsync(host_B, ctx->d_bounds, sizeof(uint32_t) * ctx->n_tensors,
+    hipError_t e = hipMemcpyAsync(host_B, ctx->bound.bits, sizeof(uint32_t) * ctx->n_tensors,
                                   hipMemcpyDeviceToHost, ctx->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
     if (e != hipSuccess) return hip_fail(ctx, "reading the bounds", e);

@@ -56,6 +56,8 @@ struct Launch {
     const float* u = nullptr;
     const float* v = nullptr;
     const uint32_t* bounds = nullptr;
+    const uint32_t* piece_max = nullptr;
+    const int32_t* chunk0 = nullptr;
     int worker0 = -1, n_workers = -1, n_tensors = -1;
     int64_t stride = -1;
     bool broadcast = false, adamw = false;
@@ -171,7 +173,9 @@ hipError_t launch_round_end(const Chunk* chunks, int64_t n_chunks, int n_tensors
     l.src_stride = a.src_stride;
     l.s2 = a.s2;
     l.u = a.u;
-    l.bounds = a.bound_bits;
+    l.bounds = a.bound.bits;
+    l.piece_max = a.bound.piece_max;
+    l.chunk0 = a.bound.chunk0;
     l.stride = a.stride;
     l.broadcast = broadcast;
     l.as = a.as;
@@ -195,8 +199,8 @@ hipError_t launch_global_det(const Chunk* chunks, int64_t n_chunks, float* x, fl
     return record(l);
 }
 hipError_t launch_global_rand(const Chunk* chunks, int64_t n_chunks, int n_tensors, float* x,
-                              float*, float* x_rep, float* u, uint32_t* bound_bits, int64_t stride,
-                              const GlobalScalars& sc, bool broadcast, hipStream_t) {
+                              float*, float* x_rep, float* u, const BoundWords& bw,
+                              int64_t stride, const GlobalScalars& sc, bool broadcast, hipStream_t) {
     Launch l;
     l.kind = "global_rand";
     l.chunks = chunks;
@@ -205,7 +209,9 @@ hipError_t launch_global_rand(const Chunk* chunks, int64_t n_chunks, int n_tenso
     l.x = x;
     l.x_rep = x_rep;
     l.u = u;
-    l.bounds = bound_bits;
+    l.bounds = bw.bits;
+    l.piece_max = bw.piece_max;
+    l.chunk0 = bw.chunk0;
     l.stride = stride;
     l.gs = sc;
     l.broadcast = broadcast;
@@ -280,6 +286,8 @@ struct Buffers {
         b.u_scratch = randomized ? alloc(arena) : nullptr;
         b.v = global_adamw ? alloc(arena) : nullptr;
         b.workspace = alloc(ws / 4 + 64);
+        // Garbage, so that a part the runtime fails to upload shows.
+        std::memset(b.workspace, 0xA5, static_cast<size_t>(ws));
         b.workspace_bytes = ws;
         b.stream = nullptr;
     }
@@ -359,7 +367,9 @@ void check_layout_fuzz() {
         }
         CHECK(arena == o, "iter %d: arena %lld, expected %lld", iter, static_cast<long long>(arena),
               static_cast<long long>(o));
-        CHECK(ws == round_up(chunks * 32, 256) + round_up(int64_t(nt) * 4, 256),
+        CHECK(ws == round_up(chunks * 32, 256) + round_up(int64_t(nt) * 4, 256) +
+                        (nt > 0 ? round_up((int64_t(nt) + 1) * 4, 256) : 0) +
+                        round_up(chunks * dsm::kSplit * 4, 256),
               "iter %d: workspace %lld", iter, static_cast<long long>(ws));
         CHECK(off[nt] == -7, "iter %d: wrote past tensor_offsets", iter);
     }
@@ -398,6 +408,36 @@ void check_chunk_table(const Problem& P, const Buffers& B, const Launch& init) {
           static_cast<long long>(init.n_chunks));
 }
 
+// The randomized sign's bound words in the workspace, each part at a
+// 256-byte boundary: the bounds after the chunk table, then the first chunk
+// of each tensor (uploaded at init, n_tensors + 1 words), then one
+// piece-maximum word per work-group piece.
+void check_bound_words(const Problem& P, const Buffers& B, const uint32_t* bits,
+                       const int32_t* chunk0, const uint32_t* piece_max, const char* what) {
+    const auto* ws = static_cast<const char*>(B.b.workspace);
+    const int64_t nt = static_cast<int64_t>(P.numel.size());
+    std::vector<int32_t> want;
+    int64_t n_chunks = 0;
+    for (int64_t ne : P.numel) {
+        want.push_back(static_cast<int32_t>(n_chunks));
+        n_chunks += (ne + dsm::kChunkElems - 1) / dsm::kChunkElems;
+    }
+    want.push_back(static_cast<int32_t>(n_chunks));
+    const int64_t bounds_off = round_up(n_chunks * 32, 256);
+    const int64_t chunk0_off = bounds_off + round_up(nt * 4, 256);
+    const int64_t pmax_off = chunk0_off + round_up((nt + 1) * 4, 256);
+    CHECK(reinterpret_cast<const char*>(bits) == ws + bounds_off,
+          "%s: bound words follow the chunk table", what);
+    CHECK(reinterpret_cast<const char*>(chunk0) == ws + chunk0_off,
+          "%s: tensor chunk index follows the bounds", what);
+    CHECK(reinterpret_cast<const char*>(piece_max) == ws + pmax_off,
+          "%s: piece maxima follow the tensor chunk index", what);
+    CHECK(pmax_off + n_chunks * dsm::kSplit * 4 <= B.b.workspace_bytes,
+          "%s: piece maxima inside the workspace", what);
+    CHECK(std::memcmp(ws + chunk0_off, want.data(), want.size() * sizeof(int32_t)) == 0,
+          "%s: uploaded tensor chunk index", what);
+}
+
 void check_init_and_chunks() {
     const std::vector<std::vector<int64_t>> shapes = {
         {1, 3, 4, 5, 63, 64, 65, 0, 1000, 16383, 16384, 16385, 40003}, {0}, {16384 * 3}, {7}};
@@ -418,6 +458,17 @@ void check_init_and_chunks() {
                           l.s2 == B.b.s2_rep && l.stride == B.arena && l.n_workers == 3,
                       "init arguments");
                 check_chunk_table(P, B, l);
+            }
+            if (!P.numel.empty()) {
+                int64_t n_chunks = 0;
+                for (int64_t ne : P.numel) n_chunks += (ne + dsm::kChunkElems - 1) / dsm::kChunkElems;
+                const char* ws = static_cast<const char*>(B.b.workspace);
+                const int64_t bo = round_up(n_chunks * 32, 256);
+                const int64_t co = bo + round_up(static_cast<int64_t>(P.numel.size()) * 4, 256);
+                const int64_t po = co + round_up((static_cast<int64_t>(P.numel.size()) + 1) * 4, 256);
+                check_bound_words(P, B, reinterpret_cast<const uint32_t*>(ws + bo),
+                                  reinterpret_cast<const int32_t*>(ws + co),
+                                  reinterpret_cast<const uint32_t*>(ws + po), "init");
             }
             CHECK(dsm_destroy(ctx) == DSM_OK, "destroy");
         }
@@ -532,10 +583,7 @@ void check_state_machine_adamw() {
         CHECK(l.kind == "round_end" && l.adamw && l.broadcast && l.n_tensors == 3, "round end");
         CHECK(l.x_src == B.b.x_rep && l.src_stride == B.arena, "round end reads the replicas");
         CHECK(l.u == B.b.u_scratch && l.s2 == B.b.s2_rep, "round end buffers");
-        const auto* ws = static_cast<const char*>(B.b.workspace);
-        CHECK(reinterpret_cast<const char*>(l.bounds) ==
-                  ws + round_up(static_cast<int64_t>(l.n_chunks) * 32, 256),
-              "bound words follow the chunk table");
+        check_bound_words(P, B, l.bounds, l.chunk0, l.piece_max, "round end");
         CHECK(l.gs.mode == DSM_SIGN_RAND_FLIP && l.gs.t == 1 && l.gs.key0 == 0x89ABCDEFu &&
                   l.gs.key1 == 0x01234567u,
               "Philox key and counter word");
@@ -804,6 +852,32 @@ void check_test_philox_args() {
 
 }  // namespace
 
+// A split randomized global step passes the workspace's bound words, also
+// for a problem with an empty tensor and for one with no chunks at all.
+void check_global_rand_args() {
+    for (const auto& shape : {std::vector<int64_t>{100, 16385, 0, 7}, std::vector<int64_t>{0, 0}}) {
+        Problem P(shape, 2, 1, DSM_BASE_SGD_MOMENTUM);
+        Buffers B(P, true, false);
+        dsm_ctx* ctx = nullptr;
+        CHECK(dsm_init(&P.p, &B.b, &ctx) == DSM_OK, "init: %s", dsm_last_error(nullptr));
+        const dsm_local_hparams sh = sgd_hp();
+        CHECK(dsm_local_step(ctx, -1, 1, &sh) == DSM_OK, "local");
+        const dsm_global_hparams gr = glob_hp(DSM_SIGN_RAND_ZERO);
+        g_log.clear();
+        CHECK(dsm_global_step(ctx, 5, &gr, 0) == DSM_OK, "randomized global: %s",
+              dsm_last_error(ctx));
+        CHECK(g_log.size() == 1, "one randomized launch, got %zu", g_log.size());
+        if (g_log.size() == 1) {
+            const Launch& l = g_log[0];
+            CHECK(l.kind == "global_rand" && !l.broadcast && l.u == B.b.u_scratch &&
+                      l.n_tensors == static_cast<int>(shape.size()),
+                  "randomized launch arguments");
+            check_bound_words(P, B, l.bounds, l.chunk0, l.piece_max, "global step");
+        }
+        CHECK(dsm_destroy(ctx) == DSM_OK, "destroy");
+    }
+}
+
 int main() {
     check_layout_fuzz();
     check_init_and_chunks();
@@ -812,6 +886,7 @@ int main() {
     check_state_machine_sgd_h1();
     check_local_from_x();
     check_coefficients();
+    check_global_rand_args();
     check_hyperparameter_errors();
     check_test_philox_args();
     if (g_failures) {

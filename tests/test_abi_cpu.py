@@ -56,8 +56,13 @@ def test_layout_offsets_aligned_and_packed(lib):
         o += -(-n // 64) * 64
     assert list(offs) == expect
     assert arena == o
+    # Chunk table (32 B per chunk), bound words (4 B per tensor), first chunk
+    # of each tensor (4 B per tensor, plus one), one piece-maximum word per
+    # 1024-element work-group piece; each part rounded up to 256 B.
     n_chunks = sum(-(-n // 16384) for n in numel)
-    assert ws == -(-n_chunks * 32 // 256) * 256 + -(-len(numel) * 4 // 256) * 256
+    up = lambda b: -(-b // 256) * 256
+    assert ws == (up(n_chunks * 32) + up(len(numel) * 4) + up((len(numel) + 1) * 4)
+                  + up(n_chunks * 16 * 4))
 
 
 def test_layout_empty_problem(lib):

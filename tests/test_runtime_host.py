@@ -6,6 +6,7 @@ HIP calls the runtime makes and of the kernel launchers, so the whole C ABI
 runs without a GPU.  Its checks are:
   * dsm_layout on 3000 random valid and invalid problems;
   * the uploaded chunk table;
+  * the randomized sign's bound words in the workspace;
   * the Algorithm 1 state machine;
   * the replica source of each local launch, fresh or stale;
   * the fp32 host coefficients against long double;
