@@ -239,6 +239,48 @@ def test_global_randomized_parity(n, mode, seed):
     ar.destroy()
 
 
+@pytest.mark.parametrize("fused", [False, True])
+def test_bound_is_recomputed_when_it_shrinks(fused):
+    """B_p is max |u| of the current step only: after a step whose u is
+    large, a step with u a thousand times smaller (smaller gradients, m reset
+    to 0) gets the smaller bound, exactly, and the signs that go with it.  Split steps and fused round ends
+    (H = 1, so the round end takes the only local step)."""
+    n, H, mode, seed = 3, 1, dsm.DSM_SIGN_RAND_FLIP, 2024
+    ar, gen = make(RAGGED, n, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, seed=77)
+    local = dict(lr=0.05, beta1=0.0)   # no local momentum carries the large step over
+    B_prev = None
+    for t, scale in enumerate((1e3, 1.0)):
+        ar.g_rep.normal_(0.0, 1e-3 * scale, generator=gen)
+        if t > 0:
+            ar.m.zero_()     # else beta1 m keeps u as large as before
+        if fused:
+            x0, m0 = per_tensor(ar, ar.x), per_tensor(ar, ar.m)
+            dsm.dsm_round_end(ar.ctx, t + 1, local, t, mode=mode, seed=seed, broadcast=True,
+                              **GLOB)
+            reps = None
+        else:
+            dsm.dsm_local_step(ar.ctx, -1, t + 1, **local)
+            x0, m0 = per_tensor(ar, ar.x), per_tensor(ar, ar.m)
+            reps = [per_tensor(ar, ar.x_rep[i]) for i in range(n)]
+            dsm.dsm_global_step(ar.ctx, t, mode=mode, seed=seed, broadcast=True, **GLOB)
+        gx, gu = per_tensor(ar, ar.x), per_tensor(ar, ar.u)
+        B = dsm.dsm_read_bounds(ar.ctx, len(RAGGED))
+        for p in range(len(RAGGED)):
+            want = np.float32(np.max(np.abs(gu[p]))) if gu[p].size else np.float32(0.0)
+            assert B[p].view(np.uint32) == want.view(np.uint32), (t, p)
+        if reps is not None:
+            o32 = O.global_step(x0, m0, reps, decay=DECAY, prec="fp32", t=t, mode=mode, seed=seed,
+                                **GLOB)
+            for p in range(len(RAGGED)):
+                assert B[p].view(np.uint32) == np.float32(o32["B"][p]).view(np.uint32)
+                rel_check(gx[p], o32["x"][p], f"x tensor {p}, step {t}")
+        if B_prev is not None:
+            nonempty = np.array([k > 0 for k in RAGGED])
+            assert np.all(B[nonempty] < 1e-2 * B_prev[nonempty]), "the bound did not shrink"
+        B_prev = B
+    ar.destroy()
+
+
 # ---------------------------------------------------------------- whole rounds
 
 def test_tiny_rounds_free_running_bit_identical():
