@@ -1,0 +1,89 @@
+"""Planted mistakes in the host runtime must fail its CPU harness.
+
+Each case copies the runtime source into a temporary directory, plants one
+plausible mistake (in the state machine, the layout, the launch arguments or
+the host coefficients), builds tests/native/runtime_host_check.cpp against
+the copy with g++ and runs it.  The harness must fail for every mistake.
+CPU only, host code only; the real source is untouched.
+"""
+import os
+import shutil
+import subprocess
+import tempfile
+from concurrent.futures import ThreadPoolExecutor
+
+import pytest
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+CSRC = os.path.join(ROOT, "paper_2411_17866_amd", "csrc")
+ROCM_INCLUDE = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "include")
+
+# (original text of dsm_runtime.cpp, planted mistake, what it breaks)
+MUTATIONS = [
+    ("const int64_t src_stride = from_x ? 0 : ctx->arena_elems;",
+     "const int64_t src_stride = ctx->arena_elems;", "stale workers read their own replica"),
+    ("while (b < w0 + nw && ctx->stale[b] == ctx->stale[a]) ++b;",
+     "while (b < w0 + nw) ++b;", "runs not split by replica source"),
+    ("ctx->stale[i] = broadcast ? 0 : 1;", "ctx->stale[i] = 0;",
+     "lazy broadcast leaves replicas marked fresh"),
+    ("bool all_stale = worker < 0 && ctx->n > 1;", "bool all_stale = worker < 0;",
+     "all-worker step from x taken for n = 1"),
+    ("c.off = L->offsets[i] + j;", "c.off = L->offsets[i];", "chunk offset ignores its start"),
+    ("sc.bc1 = static_cast<float>(1.0 - beta_power(b1, step));",
+     "sc.bc1 = static_cast<float>(1.0 - beta_power(b1, step - 1));", "bias-correction power"),
+    ("sc.c2 = static_cast<float>((1.0 - static_cast<double>(hp->beta2)) / gamma);",
+     "sc.c2 = static_cast<float>((1.0 - static_cast<double>(hp->beta1)) / gamma);",
+     "momentum coefficient uses beta1"),
+    ("if (ctx->local_count[i] >= ctx->H)", "if (ctx->local_count[i] > ctx->H)",
+     "a local step past H accepted"),
+    ("L->bounds_off = L->chunk_bytes;", "L->bounds_off = 0;", "bound words over the chunk table"),
+    ("L->chunk0_off = L->bounds_off + round_up(int64_t(p->n_tensors) * 4, 256);",
+     "L->chunk0_off = L->bounds_off;", "tensor chunk index over the bounds"),
+    ("(*chunk0)[i] = static_cast<int32_t>(k);", "(*chunk0)[i] = static_cast<int32_t>(k + (i > 0));",
+     "tensor chunk index off by one"),
+    ("round_up(n_chunks * dsm::kSplit * 4, 256)", "round_up(n_chunks * 4, 256)",
+     "one piece-maximum word per chunk"),
+    ("    if (ctx->n_tensors > 0) {\n        hipError_t e = hipMemcpyAsync(",
+     "    if (!ctx->chunks.empty()) {\n        hipError_t e = hipMemcpyAsync(",
+     "tensor chunk index not uploaded without chunks"),
+    ("ctx->bound.piece_max = reinterpret_cast<uint32_t*>(ws + L.piece_max_off);",
+     "ctx->bound.piece_max = reinterpret_cast<uint32_t*>(ws + L.chunk0_off);",
+     "piece maxima over the tensor chunk index"),
+]
+
+
+def _run(case, gxx, work):
+    original, planted, what = case
+    d = os.path.join(work, str(abs(hash(what))))
+    shutil.copytree(CSRC, d)
+    path = os.path.join(d, "dsm_runtime.cpp")
+    src = open(path).read()
+    if src.count(original) != 1:
+        return what, "original text not found exactly once"
+    with open(path, "w") as f:
+        f.write(src.replace(original, planted))
+    exe = os.path.join(d, "check")
+    cmd = [gxx, "-std=c++17", "-O1", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+           "-static-libasan", "-D__HIP_PLATFORM_AMD__", f"-I{ROCM_INCLUDE}",
+           f"-I{os.path.join(ROOT, 'include')}", f"-I{d}",
+           os.path.join(ROOT, "tests", "native", "runtime_host_check.cpp"), path, "-o", exe]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        return what, "did not build: " + r.stderr[-300:]
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=600,
+                       env=dict(os.environ, ASAN_OPTIONS="detect_leaks=0"))
+    return what, None if r.returncode != 0 else "harness passed"
+
+
+def test_every_planted_runtime_mistake_fails_the_harness():
+    gxx = shutil.which("g++")
+    if gxx is None:
+        pytest.skip("no g++")
+    if not os.path.exists(os.path.join(ROCM_INCLUDE, "hip", "hip_runtime_api.h")):
+        pytest.skip("HIP headers not installed")
+    with tempfile.TemporaryDirectory() as work:
+        with ThreadPoolExecutor(max_workers=4) as pool:
+            results = list(pool.map(lambda c: _run(c, gxx, work), MUTATIONS))
+    missed = [f"{what}: {why}" for what, why in results if why is not None]
+    assert not missed, "planted runtime mistakes not caught:\n" + "\n".join(missed)
