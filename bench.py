@@ -94,7 +94,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="xl")
     ap.add_argument("--sign", choices=("det", "rand"), default="det",
                     help="global sign of the timed steps")
@@ -102,7 +102,8 @@ def main():
                     help="fused: H-1 local steps + dsm_round_end with the lazy broadcast; "
                          "split: H local steps + dsm_global_step with broadcast")
     ap.add_argument("--extra-steps", type=int, default=20,
-                    help="rounds of each other path/sign combination, timed separately")
+                    help="rounds of every path/sign combination (and launches of each variant, of "
+                         "the SGD local step and of the standalone sync), timed for the breakdown")
     ap.add_argument("--flush-mb", type=int, default=0,
                     help="if > 0, also time rounds in which every call follows a write of this "
                          "many MB to a separate buffer, which evicts the arenas from the caches "
@@ -197,26 +198,12 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     print("[bench] timed steps done", file=sys.stderr, flush=True)
+    # Breakdown: extra rounds of every path and sign combination.
     for path in ("fused", "split"):
         for mode in (dsm.DSM_SIGN_DET, dsm.DSM_SIGN_RAND_FLIP):
-            if (path, mode) == (args.path, mode_main):
-                continue
             for _ in range(args.extra_steps):
                 one_round(t, mode, path, True)
                 t += 1
-    # The ablation variants of the global step (Section 4.1, Algorithm 7),
-    # one split round each.
-    variants = (("lookahead", dsm.DSM_RULE_LOOKAHEAD, w.glob),
-                ("signed_slowmo", dsm.DSM_RULE_SIGNED_SLOWMO, w.glob),
-                ("global_adamw", dsm.DSM_RULE_GLOBAL_ADAMW,
-                 dict(eta=1e-3, beta1=0.9, beta2=0.95, lam=w.glob["lam"], eps=1e-8)))
-    for key, rule, ghp in variants:
-        for k in range(H):
-            s_count[0] += 1
-            dsm.dsm_local_step(ar.ctx, -1, s_count[0], **w.local)
-        timed(key, lambda: dsm.dsm_global_step(ar.ctx, t, gamma=lr, rule=rule, broadcast=True,
-                                               **ghp))
-        t += 1
     torch.cuda.synchronize()
 
     # The same calls with cold caches: each one follows a write of flush_mb MB
@@ -238,24 +225,43 @@ def main():
         flush_buf[0] = None
         ev_flushed = {k: v for k, v in ev.items()}
         ev.update(main_lists)
+    ar.destroy()
+
+    # Further contexts over the same arenas (each after the previous one is
+    # destroyed, so that they never share the workspace at the same time).
+    reps = max(1, args.extra_steps)
+    bufs = ar.buffers()
+
+    # The ablation variants of the global step (Section 4.1, Algorithm 7): a
+    # context with H = 1, so each timed global step follows one local step.
+    variants = (("lookahead", dsm.DSM_RULE_LOOKAHEAD, w.glob),
+                ("signed_slowmo", dsm.DSM_RULE_SIGNED_SLOWMO, w.glob),
+                ("global_adamw", dsm.DSM_RULE_GLOBAL_ADAMW,
+                 dict(eta=1e-3, beta1=0.9, beta2=0.95, lam=w.glob["lam"], eps=1e-8)))
+    ctx_v = dsm.dsm_init(dsm.make_problem(w.numel, n, 1, w.base, w.decay), bufs)
+    for key, rule, ghp in variants:
+        for r in range(reps + 1):
+            dsm.dsm_local_step(ctx_v, -1, r + 1, **w.local)
+            timed(key if r > 0 else None,
+                  lambda: dsm.dsm_global_step(ctx_v, r, gamma=lr, rule=rule, broadcast=True, **ghp))
+    torch.cuda.synchronize()
+    dsm.dsm_destroy(ctx_v)
 
     # Row a2 (local SGD + Polyak momentum, Algorithm 3) and row a6 on its own
-    # (dsm_sync) at the same scale: a second context, SGD base, over the same
-    # arenas, after the timed steps.
-    ar.destroy()
-    sgd_problem = dsm.make_problem(w.numel, n, H, dsm.DSM_BASE_SGD_MOMENTUM, w.decay)
-    bufs = ar.buffers()
+    # (dsm_sync) at the same scale: a context with the SGD base and room for
+    # reps + 1 local steps in one round.
+    sgd_problem = dsm.make_problem(w.numel, n, reps + 1, dsm.DSM_BASE_SGD_MOMENTUM, w.decay)
     bufs.s2_rep = None
     ctx2 = dsm.dsm_init(sgd_problem, bufs)
     ev_sgd, ev_sync = [], []
-    for k in range(min(H, 6)):
+    for k in range(reps + 1):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         dsm.dsm_local_step(ctx2, -1, k + 1, lr=0.1, beta1=0.9)
         e1.record(stream)
         if k > 0:
             ev_sgd.append((e0, e1))
-    for k in range(4):
+    for k in range(reps + 1):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         dsm.dsm_sync(ctx2)
