@@ -52,6 +52,14 @@ Readings where the paper is silent (each is listed in the design notes):
     and counter (j div 4, tensor index, t, 1), word j mod 4, where j is the
     element's index inside its tensor.  "w.p. p" is the exact comparison
     U < p.
+
+Parity unpinned: every function here is checked against independent facts
+(worked examples, closed forms, library and textbook reductions, Monte Carlo
+of Lemma 1, a Philox known-answer test), but these aspects are fixed by the
+readings above, not by the paper, and no pin can tie them to it: the worker
+order of the difference form (pinned only up to rounding), the persistence
+of the base-optimizer state and of s across rounds, the Philox stream
+layout, and the momentum of the signed-SlowMo variant (Section 4.1).
 """
 from fractions import Fraction
 
