@@ -6,6 +6,9 @@
  *     synchronisation step);
  *   - with lambda = 0, x moved by exactly eta * gamma per element on which the
  *     sign of u is +-1, and not at all where it is 0 (Eq. (7));
+ * then one round with the randomized sign of Eq. (10), whose per-tensor
+ * bounds must equal max |u| of the staged u, and whose steps must be 0 or
+ * eta * gamma in the direction of sign(u);
  *   - every error path returns a status and a message.
  * Prints "c abi example ok" and exits 0, or names the failed check and
  * exits 1.
@@ -50,7 +53,7 @@ int main(void) {
     DSM_OK_(dsm_layout(&prob, &arena, offs, &ws));
 
     const size_t one = (size_t)arena * sizeof(float), many = one * (size_t)n;
-    float *x, *m, *x_rep, *g_rep, *s1, *s2;
+    float *x, *m, *x_rep, *g_rep, *s1, *s2, *u;
     void* work;
     HIP_OK(hipMalloc((void**)&x, one));
     HIP_OK(hipMalloc((void**)&m, one));
@@ -58,20 +61,22 @@ int main(void) {
     HIP_OK(hipMalloc((void**)&g_rep, many));
     HIP_OK(hipMalloc((void**)&s1, many));
     HIP_OK(hipMalloc((void**)&s2, many));
+    HIP_OK(hipMalloc((void**)&u, one));
     HIP_OK(hipMalloc(&work, (size_t)ws));
 
     float* hx = (float*)malloc(one);
     float* hx1 = (float*)malloc(one);
     float* hg = (float*)malloc(many);
     float* hr = (float*)malloc(many);
-    if (!hx || !hx1 || !hg || !hr) return 1;
+    float* hu = (float*)malloc(one);
+    if (!hx || !hx1 || !hg || !hr || !hu) return 1;
     uint32_t seed = 12345u;
     for (int64_t j = 0; j < arena; ++j) hx[j] = ((float)(lcg(&seed) >> 8) / 16777216.0f - 0.5f) * 0.04f;
     HIP_OK(hipMemcpy(x, hx, one, hipMemcpyHostToDevice));
 
     hipStream_t st;
     HIP_OK(hipStreamCreate(&st));
-    dsm_buffers buf = {x, m, x_rep, g_rep, s1, s2, NULL, work, ws, st, NULL};
+    dsm_buffers buf = {x, m, x_rep, g_rep, s1, s2, u, work, ws, st, NULL};
     dsm_ctx* ctx = NULL;
     DSM_OK_(dsm_init(&prob, &buf, &ctx));
 
@@ -127,21 +132,76 @@ int main(void) {
         return 1;
     }
 
+    float no_bounds[3];
+    if (dsm_read_bounds(ctx, no_bounds, 3) != DSM_ERR_STATE) {
+        printf("bounds of a deterministic step were not refused\n");
+        return 1;
+    }
+
+    /* Round t = 2 with the randomized sign of Eq. (10), split, with broadcast. */
+    for (int k = 0; k < H; ++k) {
+        for (size_t j = 0; j < (size_t)arena * (size_t)n; ++j)
+            hg[j] = ((float)(lcg(&seed) >> 8) / 16777216.0f - 0.5f) * 0.02f;
+        HIP_OK(hipMemcpyAsync(g_rep, hg, many, hipMemcpyHostToDevice, st));
+        HIP_OK(hipStreamSynchronize(st));
+        DSM_OK_(dsm_local_step(ctx, -1, ++s, &lh));
+    }
+    dsm_global_hparams gz = gh;
+    gz.mode = DSM_SIGN_RAND_ZERO;
+    gz.seed = 0x0123456789ABCDEFull;
+    HIP_OK(hipStreamSynchronize(st));
+    HIP_OK(hipMemcpy(hx, x, one, hipMemcpyDeviceToHost));
+    DSM_OK_(dsm_global_step(ctx, 2, &gz, 1));
+    HIP_OK(hipStreamSynchronize(st));
+    HIP_OK(hipMemcpy(hx1, x, one, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(hu, u, one, hipMemcpyDeviceToHost));
+    float bound[3] = {-1.0f, -1.0f, -1.0f};
+    DSM_OK_(dsm_read_bounds(ctx, bound, 3));
+    int64_t kept = 0;
+    for (int p = 0; p < 3; ++p) {
+        float want = 0.0f;
+        for (int64_t j = 0; j < numel[p]; ++j) {
+            const float a = fabsf(hu[offs[p] + j]);
+            if (a > want) want = a;
+        }
+        if (memcmp(&want, &bound[p], sizeof want) != 0) {
+            printf("tensor %d: bound %g, max |u| %g\n", p, bound[p], want);
+            return 1;
+        }
+        for (int64_t j = 0; j < numel[p]; ++j) {
+            /* Eq. (10) keeps sign(u) or gives 0: x moves by eta*gamma against
+               sign(u), or not at all (lambda = 0). */
+            const float a = hx[offs[p] + j], b = hx1[offs[p] + j], uu = hu[offs[p] + j];
+            const float moved = uu > 0.0f ? a - step : (uu < 0.0f ? a + step : a);
+            if (!(b == a || b == moved)) {
+                printf("randomized step: tensor %d element %lld moved to %g from %g\n", p,
+                       (long long)j, b, a);
+                return 1;
+            }
+            kept += (b != a);
+        }
+    }
+    if (kept == 0) {
+        printf("the randomized sign kept no sign\n");
+        return 1;
+    }
+
     /* Error paths return a status and a message. */
     if (dsm_global_step(ctx, 2, &gh, 1) != DSM_ERR_STATE || strlen(dsm_last_error(ctx)) == 0) {
         printf("global step before H local steps was not refused\n");
         return 1;
     }
-    float bounds[3];
-    if (dsm_read_bounds(ctx, bounds, 3) != DSM_ERR_STATE) {
-        printf("bounds of a deterministic step were not refused\n");
+    float small_bounds[2];
+    if (dsm_read_bounds(ctx, small_bounds, 2) != DSM_ERR_INVALID_ARG) {
+        printf("a bound array shorter than n_tensors was not refused\n");
         return 1;
     }
     DSM_OK_(dsm_destroy(ctx));
     HIP_OK(hipFree(x)); HIP_OK(hipFree(m)); HIP_OK(hipFree(x_rep)); HIP_OK(hipFree(g_rep));
-    HIP_OK(hipFree(s1)); HIP_OK(hipFree(s2)); HIP_OK(hipFree(work));
+    HIP_OK(hipFree(s1)); HIP_OK(hipFree(s2)); HIP_OK(hipFree(u)); HIP_OK(hipFree(work));
     HIP_OK(hipStreamDestroy(st));
-    free(hx); free(hx1); free(hg); free(hr);
-    printf("c abi example ok (%lld elements moved by one sign step)\n", (long long)moved);
+    free(hx); free(hx1); free(hg); free(hr); free(hu);
+    printf("c abi example ok (%lld elements moved by one sign step, %lld signs kept by the "
+           "randomized step)\n", (long long)moved, (long long)kept);
     return 0;
 }

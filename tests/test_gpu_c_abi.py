@@ -1,7 +1,9 @@
 """The C ABI from plain C on the GPU: tests/native/c_abi_example.c, built
 with gcc against libdsm.so, allocates with hipMalloc and runs a fused lazy
 round and a split round with broadcast, then checks the synchronisation
-step, the size of the sign step (Eq. (7) with lambda = 0) and error paths."""
+step, the size of the sign step (Eq. (7) with lambda = 0), a round with the
+randomized sign of Eq. (10) (its per-tensor bounds against max |u|, its steps
+0 or along sign(u)) and error paths."""
 import os
 import subprocess
 import sys
