@@ -143,7 +143,8 @@ def main():
 
     stream = torch.cuda.current_stream()
     lr = w.local["lr"]
-    ev = {"local": [], "local_from_x": [], "split_det": [], "split_rand": [], "fused_det": [],
+    ev = {"local": [], "local_timed": [], "local_from_x": [], "split_det": [], "split_rand": [],
+          "fused_det": [],
           "fused_rand": [], "lookahead": [], "signed_slowmo": [], "global_adamw": []}
     s_count = [0]
     # After a fused round (no broadcast) every replica is stale, and the next
@@ -154,32 +155,64 @@ def main():
     flush_buf = [None]
 
     def timed(key, fn):
+        """fn between two events on the launch stream, kept under key (None:
+        no events).  A pending flush (cold-cache timing) runs before."""
         if flush_buf[0] is not None:
             flush_buf[0].fill_(0.0)
+        if key is None:
+            fn()
+            return
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         fn()
         e1.record(stream)
-        if key is not None:
-            ev[key].append((e0, e1))
+        ev[key].append((e0, e1, 1))
 
-    def one_round(t, mode, path, record):
+    def one_round(t, mode, path, record=None):
+        """One outer iteration.  record: None (no events); "timed" (one event
+        pair around the run of ordinary local steps, so that the timed region
+        holds two event records per round); "extra" (that, plus one pair
+        around each other call); "flushed" (one pair around every call, each
+        after a cache flush)."""
         sign = "rand" if mode else "det"
+        others = record in ("extra", "flushed")
+        run = []   # [start event, launches] of the open run of ordinary local steps
+
+        def end_run():
+            if run:
+                e1 = torch.cuda.Event(enable_timing=True)
+                e1.record(stream)
+                ev["local"].append((run[0], e1, run[1]))
+                if record == "timed":
+                    ev["local_timed"].append((run[0], e1, run[1]))
+                run.clear()
+
         for k in range(H):
             s_count[0] += 1
             s = s_count[0]
             if path == "fused" and k == H - 1:
-                timed(f"fused_{sign}" if record else None,
+                end_run()
+                timed(f"fused_{sign}" if others else None,
                       lambda: dsm.dsm_round_end(ar.ctx, s, w.local, t, gamma=lr, mode=mode,
                                                 seed=w.philox_seed, broadcast=False, **w.glob))
                 stale[0] = True
+                continue
+            step = lambda: dsm.dsm_local_step(ar.ctx, -1, s, **w.local)
+            if k == 0 and stale[0] and n > 1:
+                timed("local_from_x" if others else None, step)
+            elif record in ("timed", "extra"):
+                if not run:
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                    run.extend([e0, 0])
+                step()
+                run[1] += 1
             else:
-                key = "local_from_x" if (k == 0 and stale[0] and n > 1) else "local"
-                timed(key if record else None,
-                      lambda: dsm.dsm_local_step(ar.ctx, -1, s, **w.local))
-                stale[0] = False
+                timed("local" if record == "flushed" else None, step)
+            stale[0] = False
+        end_run()
         if path == "split":
-            timed(f"split_{sign}" if record else None,
+            timed(f"split_{sign}" if others else None,
                   lambda: dsm.dsm_global_step(ar.ctx, t, gamma=lr, mode=mode, seed=w.philox_seed,
                                               broadcast=True, **w.glob))
             stale[0] = False
@@ -187,13 +220,13 @@ def main():
     mode_main = dsm.DSM_SIGN_DET if args.sign == "det" else dsm.DSM_SIGN_RAND_FLIP
     t = 0
     for _ in range(args.warmup):
-        one_round(t, mode_main, args.path, False)
+        one_round(t, mode_main, args.path)
         t += 1
     torch.cuda.synchronize()
     print("[bench] warmup done", file=sys.stderr, flush=True)
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        one_round(t, mode_main, args.path, True)
+        one_round(t, mode_main, args.path, "timed")
         t += 1
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -202,7 +235,7 @@ def main():
     for path in ("fused", "split"):
         for mode in (dsm.DSM_SIGN_DET, dsm.DSM_SIGN_RAND_FLIP):
             for _ in range(args.extra_steps):
-                one_round(t, mode, path, True)
+                one_round(t, mode, path, "extra")
                 t += 1
     torch.cuda.synchronize()
 
@@ -219,7 +252,7 @@ def main():
                                    device="cuda")
         for path in ("fused", "split"):
             for _ in range(max(1, args.extra_steps)):
-                one_round(t, dsm.DSM_SIGN_DET, path, True)
+                one_round(t, dsm.DSM_SIGN_DET, path, "flushed")
                 t += 1
         torch.cuda.synchronize()
         flush_buf[0] = None
@@ -260,14 +293,14 @@ def main():
         dsm.dsm_local_step(ctx2, -1, k + 1, lr=0.1, beta1=0.9)
         e1.record(stream)
         if k > 0:
-            ev_sgd.append((e0, e1))
+            ev_sgd.append((e0, e1, 1))
     for k in range(reps + 1):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         dsm.dsm_sync(ctx2)
         e1.record(stream)
         if k > 0:
-            ev_sync.append((e0, e1))
+            ev_sync.append((e0, e1, 1))
     torch.cuda.synchronize()
     dsm.dsm_destroy(ctx2)
 
@@ -289,10 +322,11 @@ def main():
     fill_gbs = 3 * 4 * (1 << 30) / (e[1].elapsed_time(e[2]) / 1e3) / 1e9
     del src, dst
 
-    def avg_ms(pairs):
-        if not pairs:
+    def avg_ms(entries):
+        """Average launch duration over (start, end, launches) event entries."""
+        if not entries:
             return None
-        return sum(a.elapsed_time(b) for a, b in pairs) / len(pairs)
+        return sum(a.elapsed_time(b) for a, b, _ in entries) / sum(c for _, _, c in entries)
 
     d = w.d
     khash = kernel_source_hash()
@@ -304,22 +338,25 @@ def main():
         v = sorted(vals)
         return v[min(len(v) - 1, max(0, round(q * (len(v) - 1))))]
 
-    def kern(pairs, nbytes, updates):
-        ms = avg_ms(pairs)
+    def kern(entries, nbytes, updates):
+        ms = avg_ms(entries)
         if ms is None:
             return None
-        times = [a.elapsed_time(b) for a, b in pairs]
+        times = [a.elapsed_time(b) / c for a, b, c in entries]   # per launch, each entry
         gbs = nbytes / (ms / 1e3) / 1e9
         return {"ms": round(ms, 4), "GB_per_s": round(gbs, 1),
                 "pct_peak_hbm": round(100 * gbs / PEAK_HBM_GBS, 2),
                 "param_updates_per_s": updates / (ms / 1e3), "algorithmic_bytes": nbytes,
-                "launches": len(pairs), "ms_p10": round(pct(times, 0.1), 4),
+                "launches": sum(c for _, _, c in entries), "ms_p10": round(pct(times, 0.1), 4),
                 "ms_median": round(pct(times, 0.5), 4), "ms_p90": round(pct(times, 0.9), 4)}
 
     local_bytes = (BYTES_LOCAL_ADAMW if adamw else BYTES_LOCAL_SGDM) * n * d
-    ms_local = avg_ms(ev["local"])
+    # The roofline kernel's launches inside the timed region (every other
+    # local launch, when a round has no ordinary local step there).
+    ms_local = avg_ms(ev["local_timed"]) or avg_ms(ev["local"])
     traffic = committed_traffic(khash, w.name, "local_adamw" if adamw else "local_sgdm")
-    achieved = local_bytes / (ms_local / 1e3) / 1e9
+    achieved = None if ms_local is None else local_bytes / (ms_local / 1e3) / 1e9
+    shape = ("tiny parameter set" if w.name == "tiny" else f"GPT-2 {w.name}-shaped parameter set")
     local_state = 16 if adamw else 12        # x, g, s1 (, s2) read per worker
     local_written = 8 if adamw else 4        # s1 (, s2) written per worker by the round end
     out = {
@@ -336,7 +373,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": (f"GPT-2 {w.name}-shaped parameter set ({len(w.tensors)} fp32 tensors, "
+            "workload": (f"{shape} ({len(w.tensors)} fp32 tensors, "
                          f"d={d}), n={n} worker replicas; one step = one outer iteration of "
                          f"Algorithm 1: H={H} local {'AdamW' if adamw else 'SGD-momentum'} steps "
                          f"on every replica + the "
@@ -348,13 +385,13 @@ def main():
         "roofline": {
             "bound": "hbm",
             "kernel": f"k_local_{'adamw' if adamw else 'sgdm'} (dsm_local_step, all workers)",
-            "achieved": round(achieved, 1),
+            "achieved": None if achieved is None else round(achieved, 1),
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",
-            "frac": round(achieved / PEAK_HBM_GBS, 4),
+            "frac": None if achieved is None else round(achieved / PEAK_HBM_GBS, 4),
             "traffic": traffic,
             "algorithmic_bytes_per_launch": local_bytes,
-            "avg_launch_ms": round(ms_local, 4),
+            "avg_launch_ms": None if ms_local is None else round(ms_local, 4),
         },
         "breakdown": {
             "local_step": kern(ev["local"], local_bytes, n * d),
