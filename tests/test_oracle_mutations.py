@@ -82,6 +82,16 @@ MUTATIONS = [
      "close = (np.ones_like(res) &", "exact re-check applied to infinite sides"),
     ("dsm_oracle.py", "res = lhs < rhs", "res = ~(lhs >= rhs)",
      "a NaN comparison keeps the sign"),
+    ("dsm_oracle.py", "first_step=t * H + 1, prec=prec, **local)",
+     "first_step=1, prec=prec, **local)", "bias-correction count restarted every round"),
+    ("dsm_oracle.py",
+     "    local_steps(st, grads, H=H, decay=decay, first_step=t * H + 1, prec=prec, **local)",
+     "    if st['s2'] is not None:\n"
+     "        st['s2'] = [[a * 0 for a in w] for w in st['s2']]\n"
+     "    local_steps(st, grads, H=H, decay=decay, first_step=t * H + 1, prec=prec, **local)",
+     "AdamW second moment reset every round"),
+    ("dsm_oracle.py", "\n    v_hat = v_new / bc2", "\n    v_hat = v_new / bc1",
+     "AdamW second moment divided by the first moment's bias correction"),
 ]
 
 

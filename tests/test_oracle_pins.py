@@ -274,6 +274,63 @@ def test_closed_form_adamw_constant_gradient():
     np.testing.assert_allclose(x, xe, rtol=1e-5, atol=29 * 2.0 ** -24 * 0.1)
 
 
+@pytest.mark.parametrize("prec", ["fp64", "fp32"])
+def test_closed_form_adamw_sign_pattern_across_rounds(prec):
+    """Two rounds of Algorithm 1 with the AdamW base, where every gradient
+    element keeps its magnitude a but changes sign from step to step.
+
+    With a constant |g| = a, v_s = (1 - beta2^s) a^2 exactly, so with eps = 0
+    the bias-corrected step is the bias-corrected average of the signs,
+        m_hat_s / sqrt(v_hat_s) = (1 - beta1) sum_k beta1^(s-k) sign_k / (1 - beta1^s),
+    and x_i after the round's local steps is x_0 - gamma * (sum of those).
+    The global step (Eqs. (6)-(8)) then follows from the average.  Evaluated
+    here in exact rational arithmetic from that closed form.  The sign
+    history runs across the round boundary (steps s = 3, 4 see the signs of
+    steps 1, 2), so the persistence of the base state and of the count s
+    (one reading: neither is reset by the synchronisation) is pinned, and so
+    is which bias correction divides which moment.  Every u here is at least
+    0.026 in magnitude, far from a sign decision that rounding could flip.
+    """
+    from fractions import Fraction as F
+    H, n = 2, 2
+    b1, b2, gam, eta, gb1, gb2 = (O.f32(v) for v in (0.9, 0.95, 0.01, 0.8, 0.95, 0.98))
+    amp = [[1.0, 0.5, 2.0], [2.0, 0.25, 2.0]]                    # [worker][element]
+    sgn = [[[1, -1, 1, 1], [1, 1, 1, 1], [-1, 1, -1, -1]],        # [worker][element][step - 1]
+           [[1, 1, -1, 1], [-1, 1, 1, -1], [-1, -1, 1, -1]]]
+    x0 = np.array([0.5, -0.25, 0.125], dtype=np.float32)
+
+    B1, G, ETA, GB1, GB2 = (F(float(v)) for v in (b1, gam, eta, gb1, gb2))
+
+    def mu(i, j, s):
+        num = sum((1 - B1) * B1 ** (s - k) * sgn[i][j][k - 1] for k in range(1, s + 1))
+        return num / (1 - B1 ** s)
+
+    xs, ms = [F(float(v)) for v in x0], [F(0)] * 3
+    st = O.init_state([x0], n, "adamw")
+    for t in range(2):
+        steps = range(t * H + 1, t * H + H + 1)
+        delta = [sum(G * sum(mu(i, j, s) for s in steps) for i in range(n)) / n for j in range(3)]
+        u = [GB1 * ms[j] + (1 - GB1) / G * delta[j] for j in range(3)]
+        S = [(u_ > 0) - (u_ < 0) for u_ in u]
+        xs = [xs[j] - ETA * G * S[j] for j in range(3)]
+        ms = [GB2 * ms[j] + (1 - GB2) / G * delta[j] for j in range(3)]
+
+        def grads(i, k, t=t):
+            s_ = t * H + k + 1
+            return [np.array([amp[i][j] * sgn[i][j][s_ - 1] for j in range(3)], dtype=np.float32)]
+        res = O.communication_round(
+            st, grads, t, H=H, local=dict(lr=0.01, beta1=0.9, beta2=0.95, eps=0.0, weight_decay=0.1),
+            glob=dict(eta=0.8, beta1=0.95, beta2=0.98, lam=0.1, mode=O.SIGN_DET, seed=0),
+            decay=[False], prec=prec)
+        np.testing.assert_array_equal(res["S"][0], np.array(S, dtype=float))
+        # State is stored in fp32 between steps (a few 1e-8 relative on x, m);
+        # a reset base state, a restarted s or swapped bias corrections move
+        # u and m by 1e-2 relative or more.
+        np.testing.assert_allclose(res["u"][0], [float(v) for v in u], rtol=2e-5, atol=1e-9)
+        np.testing.assert_allclose(st["m"][0], [float(v) for v in ms], rtol=2e-5, atol=1e-9)
+        np.testing.assert_allclose(st["x"][0], [float(v) for v in xs], rtol=0, atol=4e-7)
+
+
 # ---------------------------------------------------------------- library routines
 
 def _torch_adamw_one_step(x, g, m, v, s, lr, b1, b2, eps, wd):
