@@ -92,6 +92,8 @@ MUTATIONS = [
      "AdamW second moment reset every round"),
     ("dsm_oracle.py", "\n    v_hat = v_new / bc2", "\n    v_hat = v_new / bc1",
      "AdamW second moment divided by the first moment's bias correction"),
+    ("dsm_oracle.py", "t=t, prec=prec, **glob, **extra)", "t=0, prec=prec, **glob, **extra)",
+     "round driver passes t = 0 to every global step"),
 ]
 
 

@@ -157,3 +157,28 @@ def test_global_adamw_round_driver_keeps_v():
         O.communication_round(st, lambda i, k: g[i], t, H=2, local=dict(lr=0.01, beta1=0.0),
                               glob=glob, decay=[True])
     assert "v" in st and np.all(st["v"][0] > 0)
+
+
+def test_global_adamw_round_driver_closed_form():
+    """Through the round driver (Algorithm 1, SGD base without momentum, the
+    same gradient g on every worker at every local step): the pseudo-gradient
+    of every round is the constant (x - x_i)/gamma = H g, so Algorithm 7 moves
+    x by eta (Hg/(|Hg|+eps) + lambda x) in every round, which holds only if
+    round t gets the bias corrections 1 - beta^(t+1)."""
+    rng = np.random.default_rng(11)
+    d = 256
+    x0 = rng.normal(0, 0.02, d).astype(np.float32)
+    g = (np.sign(rng.normal(size=d)) * (1e-2 + np.abs(rng.normal(0, 1e-2, d)))).astype(np.float32)
+    H, lr, eta, lam, eps = 2, 0.125, 1e-3, 0.1, 1e-8
+    st = O.init_state([x0], 2, "sgd")
+    glob = dict(eta=eta, beta1=0.9, beta2=0.95, lam=lam, eps=eps, mode=O.SIGN_DET, seed=0,
+                rule=O.RULE_GLOBAL_ADAMW)
+    for t in range(4):
+        x = st["x"][0].astype(np.float64)
+        O.communication_round(st, lambda i, k: [g], t, H=H, local=dict(lr=lr, beta1=0.0),
+                              glob=glob, decay=[True])
+        G = H * g.astype(np.float64)
+        expect = x - O.f32(eta) * (G / (np.abs(G) + O.f32(eps)) + O.f32(lam) * x)
+        # fp32 replicas move G by ~1e-6 relative; a bias correction of the
+        # wrong round moves the step by 10% or more.
+        np.testing.assert_allclose(st["x"][0], expect, rtol=0, atol=1e-4 * eta)
