@@ -94,6 +94,8 @@ MUTATIONS = [
      "AdamW second moment divided by the first moment's bias correction"),
     ("dsm_oracle.py", "t=t, prec=prec, **glob, **extra)", "t=0, prec=prec, **glob, **extra)",
      "round driver passes t = 0 to every global step"),
+    ("dsm_oracle.py", "        lam_p = lam_ if decay[p] else dt(0.0)\n        x_new = xp - eta_",
+     "        lam_p = lam_\n        x_new = xp - eta_", "Global AdamW ignores the decay mask"),
 ]
 
 

@@ -112,8 +112,10 @@ def test_global_adamw_matches_torch_adamw_on_the_pseudo_gradient():
         x, m, v = (a.astype(np.float32) for a in (res["x"][0], res["m"][0], res["v"][0]))
 
 
-def test_global_adamw_constant_pseudo_gradient_closed_form():
-    """Constant g: m_hat = g and v_hat = g^2, so x' = x - eta (g/(|g|+eps) + lambda x)."""
+@pytest.mark.parametrize("decayed", [True, False])
+def test_global_adamw_constant_pseudo_gradient_closed_form(decayed):
+    """Constant g: m_hat = g and v_hat = g^2, so x' = x - eta (g/(|g|+eps) + lambda x),
+    with lambda = 0 on a tensor whose decay flag is off."""
     rng = np.random.default_rng(5)
     d = 500
     x0 = rng.normal(0, 0.02, d).astype(np.float32)
@@ -126,9 +128,11 @@ def test_global_adamw_constant_pseudo_gradient_closed_form():
     for t in range(5):
         rep = (x - diff).astype(np.float32)
         res = O.global_step([x], [m], [[rep]], gamma=gamma, eta=eta, beta1=0.9, beta2=0.95,
-                            lam=lam, eps=eps, decay=[True], t=t, rule=O.RULE_GLOBAL_ADAMW, v=[v])
+                            lam=lam, eps=eps, decay=[decayed], t=t, rule=O.RULE_GLOBAL_ADAMW,
+                            v=[v])
         g = (x.astype(np.float64) - rep) / gamma
-        expect = x - O.f32(eta) * (g / (np.abs(g) + O.f32(eps)) + O.f32(lam) * x)
+        lam_p = O.f32(lam) if decayed else 0.0
+        expect = x - O.f32(eta) * (g / (np.abs(g) + O.f32(eps)) + lam_p * x)
         # The replicas are rounded to fp32, so g varies by ~1e-6 relative between
         # rounds; a wrong bias correction would move x by O(eta).
         np.testing.assert_allclose(res["x"][0], expect, rtol=1e-9, atol=1e-5 * eta)
