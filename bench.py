@@ -87,7 +87,9 @@ def cpu_baseline(w, ar, sample_tensors):
                        f"deterministic global step) of the oracle in fp64 on the {which} "
                        f"({d_s} of {w.d} parameters); "
                        f"{dt:.1f} s on one host thread"),
-            "seconds": dt, "host_threads_available": len(os.sched_getaffinity(0))}
+            "seconds": dt, "host_threads_available": len(os.sched_getaffinity(0)),
+            # every update is elementwise, so the rate carries over to the whole workload
+            "full_step_seconds_extrapolated": (w.n_workers * w.local_steps + 1) * w.d / (updates / dt)}
 
 
 def main():
