@@ -4,6 +4,7 @@ error detected on the host before any device work."""
 import ctypes
 import os
 import re
+import threading
 
 import numpy as np
 import pytest
@@ -189,3 +190,23 @@ def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
     monkeypatch.setattr(dsm, "_lib", None)
     with pytest.raises(RuntimeError, match="not found"):
         dsm.load_library(str(tmp_path / "missing.so"))
+
+
+def test_error_text_is_per_thread():
+    """A failing call in one thread does not change the error text another
+    thread reads for its own failure (no context: the thread's last error).
+    Host only."""
+    out = {}
+
+    def fail(tag, n_workers):
+        prob = dsm.make_problem([8], n_workers, 1, dsm.DSM_BASE_ADAMW)
+        with pytest.raises(dsm.DsmError):
+            dsm.dsm_layout(prob)
+        out[tag] = dsm.dsm_last_error()
+    ths = [threading.Thread(target=fail, args=("zero", 0)),
+           threading.Thread(target=fail, args=("many", 65))]
+    for th in ths:
+        th.start()
+    for th in ths:
+        th.join(timeout=60)
+    assert "got 0" in out["zero"] and "got 65" in out["many"]
