@@ -599,7 +599,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_local_from_x(
             if (q < nvec) xv[k] = ntload(xp + q);
         }
 #if DSM_ROUND_END_UNROLL == 0
-#pragma unroll
+#pragma unroll(N > 0 ? N : 1)
 #elif DSM_ROUND_END_UNROLL == 1
 #pragma unroll 1
 #elif DSM_ROUND_END_UNROLL == 2
@@ -684,7 +684,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_round_end(
         // are in flight together; that measured faster than the rolled loop's
         // lower register count and higher occupancy.
 #if DSM_ROUND_END_UNROLL == 0
-#pragma unroll
+#pragma unroll(N > 0 ? N : 1)
 #elif DSM_ROUND_END_UNROLL == 1
 #pragma unroll 1
 #elif DSM_ROUND_END_UNROLL == 2
