@@ -96,6 +96,10 @@ MUTATIONS = [
      "round driver passes t = 0 to every global step"),
     ("dsm_oracle.py", "        lam_p = lam_ if decay[p] else dt(0.0)\n        x_new = xp - eta_",
      "        lam_p = lam_\n        x_new = xp - eta_", "Global AdamW ignores the decay mask"),
+    ("dsm_oracle.py", "        keep = _exact_less(2 * k - (1 << 24), B, au)",
+     "        keep = _exact_less(2 * k - (1 << 24) + 1, B, au)", "Eq. (9) threshold one count off"),
+    ("dsm_oracle.py", "    B = float(B)\n", "    B = float(B) * (1 + 2.0 ** -40)\n",
+     "randomized decision not exact (bound off by 2^-40)"),
 ]
 
 

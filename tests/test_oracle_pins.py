@@ -468,6 +468,34 @@ def test_randomized_sign_threshold_is_exact():
     assert O.randomized_sign(u1, B, np.array([k1 - 1]), O.SIGN_RAND_FLIP)[0] == 1.0
 
 
+@pytest.mark.parametrize("dtype,B", [(np.float64, O.f32(0.37)), (np.float64, 0.5), (np.float32, 0.5)])
+def test_randomized_sign_threshold_one_ulp_either_side(dtype, B):
+    """The decision U < p is exact for every representable u: at the exact tie
+    |u| = k B 2^-24 (Eq. (10)) or |u| = (2k - 2^24) B 2^-24 (Eq. (9)) the sign
+    is not kept, one ulp above the tie it is, one ulp below it is not.  For
+    Eq. (9) also an odd multiple of B 2^-24, which its even steps in k never
+    hit: kept at k, not kept at k + 1."""
+    dt = dtype
+    up = lambda v: np.nextafter(dt(v), dt(np.inf))
+    down = lambda v: np.nextafter(dt(v), dt(0.0))
+    k0 = 5_000_000                                          # Eq. (10)
+    tie = dt(k0 * 2.0 ** -24 * B)
+    assert float(tie) == k0 * 2.0 ** -24 * B                # the tie is representable
+    for u, want in ((tie, 0.0), (up(tie), 1.0), (down(tie), 0.0)):
+        got = O.randomized_sign(np.array([u], dtype=dt), B, np.array([k0]), O.SIGN_RAND_ZERO)[0]
+        assert got == want, (u, got, want)
+    k1 = (1 << 23) + 2_500_000                              # Eq. (9)
+    tie = dt((2 * k1 - (1 << 24)) * 2.0 ** -24 * B)
+    assert float(tie) == (2 * k1 - (1 << 24)) * 2.0 ** -24 * B
+    for u, want in ((tie, -1.0), (up(tie), 1.0), (down(tie), -1.0)):
+        got = O.randomized_sign(np.array([u], dtype=dt), B, np.array([k1]), O.SIGN_RAND_FLIP)[0]
+        assert got == want, (u, got, want)
+    odd = dt((2 * k1 - (1 << 24) + 1) * 2.0 ** -24 * B)
+    assert float(odd) == (2 * k1 - (1 << 24) + 1) * 2.0 ** -24 * B
+    assert O.randomized_sign(np.array([odd], dtype=dt), B, np.array([k1]), O.SIGN_RAND_FLIP)[0] == 1.0
+    assert O.randomized_sign(np.array([odd], dtype=dt), B, np.array([k1 + 1]), O.SIGN_RAND_FLIP)[0] == -1.0
+
+
 def test_randomized_sign_nonfinite_limits():
     """Non-finite u or B, from the limits of Eqs. (9)/(10) and IEEE compares.
 
