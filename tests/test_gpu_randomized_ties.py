@@ -1,0 +1,74 @@
+"""The randomized sign's decision on the GPU is exact at its ties.
+
+Eq. (10) keeps sign(u) with probability |u|/B and Eq. (9) with probability
+1/2 + |u|/(2B); with U = k 2^-24 the comparisons U < p are
+    Eq. (10):  k B < |u| 2^24,        Eq. (9):  (2k - 2^24) B < |u| 2^24.
+The inputs make u exact and S readable (x = 0, one worker, one SGD step with
+lr = 1 and no momentum, a global step with beta1 = 0 and gamma = eta = 1, so
+u = g and x_new = -S), with B = 1 planted in element 0.  Every other element
+gets its own tie |u| = k_j 2^-24 (Eq. (10)) or (2k_j - 2^24) 2^-24 (Eq. (9)),
+or the fp32 value one ulp above or below it, with k_j from the generator's
+published stream (the oracle's Philox).  At the tie and below, the sign is
+not kept; one ulp above, it is.  The expected S follows from the two
+comparisons above, not from the oracle's decision function.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2411_17866_amd import arena as A
+from paper_2411_17866_amd import dsm
+
+pytestmark = pytest.mark.gpu
+
+N = 3 * 16384 + 5
+SEED, T = 0x0DDBA11, 9
+
+
+@pytest.mark.parametrize("mode", [dsm.DSM_SIGN_RAND_ZERO, dsm.DSM_SIGN_RAND_FLIP])
+def test_randomized_decision_at_and_around_its_ties(mode):
+    k = O.randomized_sign_uniforms(N, 0, T, SEED)              # U_j = k_j 2^-24
+    rng = np.random.default_rng(mode)
+    side = rng.integers(0, 3, N)                               # 0 tie, 1 one ulp up, 2 one ulp down
+    sgn = np.where(rng.random(N) < 0.5, -1.0, 1.0).astype(np.float32)
+    if mode == dsm.DSM_SIGN_RAND_ZERO:
+        thr = k.astype(np.float64) * 2.0 ** -24                # |u| threshold
+    else:
+        thr = (2 * k - (1 << 24)).astype(np.float64) * 2.0 ** -24
+    usable = (thr > 0) & (thr < 1)
+    usable[0] = False
+    tie = thr.astype(np.float32)
+    assert np.all(tie[usable].astype(np.float64) == thr[usable])   # exact in fp32
+    mag = np.where(side == 1, np.nextafter(tie, np.float32(2)),
+                   np.where(side == 2, np.nextafter(tie, np.float32(0)), tie)).astype(np.float32)
+    mag[~usable] = np.float32(0.25)
+    mag[0] = np.float32(1.0)                                   # B = 1
+    g = (sgn * mag).astype(np.float32)
+    # Expected S from the comparisons, in exact arithmetic (B = 1).
+    lhs = (k if mode == dsm.DSM_SIGN_RAND_ZERO else 2 * k - (1 << 24)).astype(np.float64)
+    keep = lhs < mag.astype(np.float64) * 2.0 ** 24
+    lost = 0.0 if mode == dsm.DSM_SIGN_RAND_ZERO else -1.0
+    want = np.where(keep, sgn, lost * sgn).astype(np.float32)
+
+    ar = A.Arenas([N], 1, 1, dsm.DSM_BASE_SGD_MOMENTUM, decay=[False], randomized=True)
+    ar.x.zero_()
+    ar.init()
+    ar.g_rep[0, :N] = torch.from_numpy(g).cuda()
+    dsm.dsm_local_step(ar.ctx, -1, 1, lr=1.0, beta1=0.0)
+    dsm.dsm_global_step(ar.ctx, T, gamma=1.0, eta=1.0, beta1=0.0, beta2=0.5, lam=0.0,
+                        mode=mode, seed=SEED, broadcast=True)
+    torch.cuda.synchronize()
+    u = ar.u[:N].cpu().numpy()
+    S = -ar.x[:N].cpu().numpy()
+    B = dsm.dsm_read_bounds(ar.ctx, 1)[0]
+    ar.destroy()
+    assert B == 1.0
+    np.testing.assert_array_equal(u.view(np.uint32), g.view(np.uint32))     # u = g exactly
+    for s_, name in ((0, "tie"), (1, "one ulp above"), (2, "one ulp below")):
+        sel = usable & (side == s_)
+        assert sel.sum() > 1000
+        bad = np.flatnonzero(sel & (S != want))
+        assert bad.size == 0, f"{name}: {bad.size} wrong decisions, first at {bad[:5]}"
+    # Only the ulp above the tie keeps the sign.
+    assert np.all(keep[usable & (side == 1)]) and not np.any(keep[usable & (side != 1)])
