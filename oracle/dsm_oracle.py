@@ -47,7 +47,9 @@ Readings where the paper is silent (each is listed in the design notes):
   * Weight decay (local and global) applies only to tensors whose decay flag
     is set; the flag selects lambda or 0 for the tensor.
   * The randomized bound B is max_j |u_j| over the tensor (the tightest
-    bound for which Eqs. (9)/(10) are probabilities); B = 0 gives S = 0.
+    bound for which Eqs. (9)/(10) are probabilities); B = 0 gives S = 0.  A
+    bound that is not finite leaves S_r undefined (Section 3.1 needs a finite
+    B): S is NaN over the whole tensor.
   * Random uniforms: U = (w >> 8) * 2^-24 from Philox4x32-10 with key = seed
     and counter (j div 4, tensor index, t, 1), word j mod 4, where j is the
     element's index inside its tensor.  "w.p. p" is the exact comparison
@@ -202,12 +204,11 @@ def randomized_sign_uniforms_at(j, tensor_index, t, seed):
 def _exact_less(a_int, B, au):
     """Elementwise exact test  a_int * B < au * 2^24  for integers a_int.
 
-    a_int: int64 array with |a_int| <= 2^24; B: scalar >= 0; au: array >= 0.
-    Evaluated in fp64; every element whose two finite sides are within a
-    relative 2^-45 of each other is re-decided with exact rationals.  Where a
-    side is infinite or NaN (u or B not finite) the fp64 comparison is already
-    the IEEE one: infinities compare exactly, 0 * inf is NaN, and NaN compares
-    false.
+    a_int: int64 array with |a_int| <= 2^24; B: finite scalar >= 0; au: array
+    >= 0.  Evaluated in fp64; every element whose two finite sides are within
+    a relative 2^-45 of each other is re-decided with exact rationals.  Where
+    u is infinite or NaN the fp64 comparison is already the IEEE one:
+    infinities compare exactly and NaN compares false.
     """
     B = float(B)
     with np.errstate(invalid="ignore"):
@@ -231,8 +232,17 @@ def randomized_sign(u, B, k, variant):
              i.e. (2k - 2^24) B < |u| 2^24; otherwise -sign(u).
     Eq. (10): keep sign(u) w.p. |u|/B, i.e. iff k B < |u| 2^24; otherwise 0.
     Both comparisons are exact.  u = 0 or B = 0 gives 0.
+
+    Section 3.1 defines S_r only for a finite bound B >= |v_j|.  A bound that
+    is NaN or infinite (B = max |u| over a tensor that holds a NaN or an
+    infinite u_j) leaves the randomized sign of the whole tensor undefined:
+    every element then gets NaN, so the tensor's step is NaN, as the
+    deterministic sign makes it at a NaN u, and never a finite step of a
+    reversed or zero sign.
     """
     dt = u.dtype.type
+    if not np.isfinite(B):
+        return np.full(np.shape(u), np.nan, dtype=u.dtype)
     s = sign(u)
     au = np.abs(u)
     if variant == SIGN_RAND_FLIP:

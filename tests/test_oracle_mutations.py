@@ -100,6 +100,12 @@ MUTATIONS = [
      "        keep = _exact_less(2 * k - (1 << 24) + 1, B, au)", "Eq. (9) threshold one count off"),
     ("dsm_oracle.py", "    B = float(B)\n", "    B = float(B) * (1 + 2.0 ** -40)\n",
      "randomized decision not exact (bound off by 2^-40)"),
+    ("dsm_oracle.py", "    if not np.isfinite(B):\n        return np.full(",
+     "    if np.isnan(B):\n        return np.full(",
+     "an infinite bound decided by the limit of the probabilities"),
+    ("dsm_oracle.py", "    if not np.isfinite(B):\n        return np.full(",
+     "    if False:\n        return np.full(",
+     "a non-finite bound decided by bare IEEE comparisons (reversed or frozen tensor)"),
 ]
 
 

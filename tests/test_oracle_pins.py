@@ -496,39 +496,71 @@ def test_randomized_sign_threshold_one_ulp_either_side(dtype, B):
     assert O.randomized_sign(np.array([odd], dtype=dt), B, np.array([k1 + 1]), O.SIGN_RAND_FLIP)[0] == -1.0
 
 
-def test_randomized_sign_nonfinite_limits():
-    """Non-finite u or B, from the limits of Eqs. (9)/(10) and IEEE compares.
-
-    B = +inf: Eq. (9) keeps sign(u) with probability 1/2 + |u|/(2B) -> 1/2,
-    i.e. iff U < 1/2 (k < 2^23); Eq. (10) with |u|/B -> 0, never.  B = NaN:
-    no comparison holds, so Eq. (9) gives -sign(u) and Eq. (10) gives 0.
-    u = NaN: Eq. (9) gives NaN (either branch), Eq. (10) gives 0.
-    """
+def test_randomized_sign_nonfinite_bound_is_undefined():
+    """Section 3.1 defines S_r(v) only for a finite bound B >= |v_j|, with
+    keep probabilities 1/2 + |v_j|/(2B) (Eq. (9)) and |v_j|/B (Eq. (10)).  At
+    B = NaN neither is a number, and at B = +inf the element whose |v_j| is
+    infinite has |v_j|/B = inf/inf, so the operator is undefined for the
+    tensor: every element gets NaN, whatever u and U are, for both variants.
+    No element may take a finite step (reversed under Eq. (9), frozen under
+    Eq. (10)), which is what the bare IEEE comparisons would give."""
     half = 1 << 23
     k = np.array([0, 1, half - 1, half, half + 1, (1 << 24) - 1], dtype=np.int64)
-    keep9 = k < half
-    for uval in (1.5, -0.25, np.inf, -np.inf):
-        u = np.full(k.size, uval, dtype=np.float32)
-        s = np.float32(np.sign(uval))
-        np.testing.assert_array_equal(O.randomized_sign(u, np.float32(np.inf), k, O.SIGN_RAND_FLIP),
-                                      np.where(keep9, s, -s))
-        np.testing.assert_array_equal(O.randomized_sign(u, np.float32(np.inf), k, O.SIGN_RAND_ZERO),
-                                      np.zeros(k.size, np.float32))
-        np.testing.assert_array_equal(O.randomized_sign(u, np.float32(np.nan), k, O.SIGN_RAND_FLIP),
-                                      np.full(k.size, -s))
-        np.testing.assert_array_equal(O.randomized_sign(u, np.float32(np.nan), k, O.SIGN_RAND_ZERO),
-                                      np.zeros(k.size, np.float32))
+    for dt in (np.float32, np.float64):
+        for B in (dt(np.inf), dt(np.nan)):
+            for uval in (1.5, -0.25, 0.0, np.inf, -np.inf, np.nan):
+                u = np.full(k.size, uval, dtype=dt)
+                for variant in (O.SIGN_RAND_FLIP, O.SIGN_RAND_ZERO):
+                    s = O.randomized_sign(u, B, k, variant)
+                    assert s.dtype == dt and np.all(np.isnan(s)), (dt, B, uval, variant, s)
+
+
+def test_randomized_sign_nonfinite_u_with_finite_bound():
+    """With a finite bound the decision is the exact comparison U < p.  A NaN u
+    is never kept: Eq. (9) gives -sign(NaN) = NaN and Eq. (10) gives 0.  An
+    infinite |u| above a finite B (not produced by B = max |u|, but the
+    comparison is defined) is always kept."""
+    half = 1 << 23
+    k = np.array([0, 1, half - 1, half, half + 1, (1 << 24) - 1], dtype=np.int64)
     un = np.full(k.size, np.nan, dtype=np.float32)
-    for B in (np.float32(2.0), np.float32(np.inf), np.float32(np.nan)):
+    for B in (np.float32(2.0), np.float32(0.0)):
         assert np.all(np.isnan(O.randomized_sign(un, B, k, O.SIGN_RAND_FLIP)))
         np.testing.assert_array_equal(O.randomized_sign(un, B, k, O.SIGN_RAND_ZERO),
                                       np.zeros(k.size, np.float32))
-    # A finite bound with an infinite |u| (only possible when B = max |u| is
-    # itself infinite, but the decision is still defined): always kept.
     u = np.full(k.size, -np.inf, dtype=np.float32)
     for variant in (O.SIGN_RAND_FLIP, O.SIGN_RAND_ZERO):
         np.testing.assert_array_equal(O.randomized_sign(u, np.float32(3.0), k, variant),
                                       np.full(k.size, -1.0, np.float32))
+
+
+@pytest.mark.parametrize("mode", [O.SIGN_RAND_FLIP, O.SIGN_RAND_ZERO])
+@pytest.mark.parametrize("bad", [np.nan, np.inf])
+def test_randomized_step_nonfinite_bound_spoils_only_its_tensor(mode, bad):
+    """Through the global step: one non-finite replica value makes u and so
+    B_p of its tensor non-finite.  That tensor's new x is NaN at every element
+    (the randomized sign is undefined there, Section 3.1), and m follows
+    Eq. (8), which does not depend on S: finite wherever its difference is.
+    The other tensor's bound, sign and step are unaffected, exactly as if the
+    bad tensor were absent (every update is per tensor)."""
+    rng = np.random.default_rng(5)
+    x = [rng.normal(0, 0.02, 200).astype(np.float32), rng.normal(0, 0.02, 77).astype(np.float32)]
+    m = [np.zeros(200, np.float32), rng.normal(0, 1e-3, 77).astype(np.float32)]
+    reps = [[a + rng.normal(0, 1e-4, a.size).astype(np.float32) for a in x] for _ in range(3)]
+    reps[1][0][123] = np.float32(bad)
+    kw = dict(gamma=1e-3, eta=0.8, beta1=0.95, beta2=0.98, lam=0.1, decay=[True, False], t=4,
+              mode=mode, seed=77)
+    with np.errstate(invalid="ignore"):
+        for prec in ("fp32", "fp64"):
+            o = O.global_step(x, m, reps, prec=prec, **kw)
+            assert not np.isfinite(o["B"][0])
+            assert np.all(np.isnan(o["S"][0])) and np.all(np.isnan(o["x"][0]))
+            finite_m = np.isfinite(o["m"][0])
+            assert finite_m.sum() == 199 and not finite_m[123]
+            alone = O.global_step([x[1]], [m[1]], [[r[1]] for r in reps], prec=prec,
+                                  tensor_ids=[1], **dict(kw, decay=[False]))
+            assert np.isfinite(o["B"][1]) and o["B"][1] == alone["B"][0]
+            np.testing.assert_array_equal(o["x"][1], alone["x"][0])
+            np.testing.assert_array_equal(o["S"][1], alone["S"][0])
 
 
 @pytest.mark.parametrize("variant", [O.SIGN_RAND_FLIP, O.SIGN_RAND_ZERO])
