@@ -11,8 +11,9 @@
  * On one GPU the n workers are n replicas resident in HBM, and the all-reduce
  * is a per-element sum over the replicas in worker order.  x in R^d is a list
  * of tensors; they live concatenated in one flat fp32 arena per buffer, each
- * tensor starting at a multiple of 64 elements (256 bytes).  dsm_layout gives
- * the arena length (d_pad) and every tensor's offset.
+ * tensor starting at a multiple of 64 elements (256 bytes; 1024 elements with
+ * blocked replicas).  dsm_layout gives the arena length (d_pad) and every
+ * tensor's offset.
  *
  * Conventions for every entry point:
  *  - All arithmetic state is fp32.  Hyperparameters are fp32 numbers.
@@ -82,6 +83,22 @@ typedef enum dsm_global_rule {
                                    needs buffers.v */
 } dsm_global_rule;
 
+/* How the n worker replicas x_rep share their buffer (dsm_problem.replica_layout).
+ * The other per-worker buffers (g_rep, s1_rep, s2_rep) always hold n
+ * contiguous copies. */
+typedef enum dsm_replica_layout {
+    DSM_REPLICAS_CONTIGUOUS = 0, /* copy i at element offset i * d_pad */
+    DSM_REPLICAS_BLOCKED = 1     /* 64 KiB blocks interleaved by worker: element e of
+                                    copy i at ((e / 16384) * n + i) * 16384 + e % 16384.
+                                    A work-group's n replica accesses then fall in one
+                                    n * 64 KiB span instead of n spans d_pad apart; the
+                                    global step and the synchronisation, which write
+                                    every replica, keep their bandwidth in every
+                                    physical placement.  d_pad is a multiple of 16384
+                                    and tensors start on multiples of 1024 elements. */
+} dsm_replica_layout;
+#define DSM_REPLICA_BLOCK_ELEMS 16384
+
 /* The problem of Eq. (1): x in R^d given as n_tensors tensors. */
 typedef struct dsm_problem {
     int32_t n_workers;     /* n, 1..64 */
@@ -91,10 +108,12 @@ typedef struct dsm_problem {
     const int64_t* numel;  /* host array [n_tensors], each in [0, 2^34) */
     const uint8_t* decay;  /* host array [n_tensors]: 1 = weight decay applies
                               (local and global); NULL = every tensor decays */
+    int32_t replica_layout; /* dsm_replica_layout of x_rep */
 } dsm_problem;
 
 /* Device buffers, all fp32 arenas of d_pad elements per copy.  The replica
- * buffers hold n copies back to back (copy i at element offset i * d_pad). */
+ * buffers hold n copies (copy i of g_rep, s1_rep, s2_rep at element offset
+ * i * d_pad; x_rep as problem->replica_layout says). */
 typedef struct dsm_buffers {
     float* x;          /* [d_pad]      global model x_{t,0} (in/out) */
     float* m;          /* [d_pad]      global momentum m_t (zeroed by init) */
@@ -207,7 +226,10 @@ DSM_API dsm_status dsm_local_step(dsm_ctx* ctx, int32_t worker, int64_t step,
  * bound B_p = max_j |u_j| over tensor p and uniforms U = (w >> 8) 2^-24 from
  * Philox4x32-10 keyed by `seed` with counter (j div 4, p, t, 1), word j mod 4
  * (j = index inside the tensor); S keeps sign(u) exactly when U < the
- * equation's probability.  When broadcast != 0 every replica is set to the
+ * equation's probability.  Section 3.1 defines the randomized sign only for a
+ * finite bound: a tensor whose B_p is NaN or infinite (it holds a non-finite
+ * u) gets S = NaN, so its new x is NaN at every element (dsm_read_bounds
+ * shows which tensors).  When broadcast != 0 every replica is set to the
  * new x (synchronisation step); otherwise the replicas are left stale and
  * each worker's next local step reads x (see dsm_local_step), or dsm_sync
  * copies x into them.  The randomized modes need buffers->u_scratch.
@@ -251,6 +273,8 @@ DSM_API dsm_status dsm_sync(dsm_ctx* ctx);
  * dsm_read_bounds - copies the per-tensor bounds B_p of the last randomized
  * global step (Eqs. (9)/(10)) into host_B (host memory, caller-owned, room for
  * capacity floats; n_tensors of them are written) and synchronises the stream.
+ * A bound that is NaN or infinite marks a tensor whose randomized sign was
+ * undefined (a non-finite u in it) and whose step made x NaN.
  * Errors: DSM_ERR_STATE if the last global step was not randomized;
  * DSM_ERR_INVALID_ARG for a NULL context or output, or capacity < n_tensors
  * (nothing is written); DSM_ERR_HIP.

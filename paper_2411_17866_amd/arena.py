@@ -23,17 +23,24 @@ class Arenas:
     numel: per-tensor element counts; n_workers, local_steps, base: the
     problem (dsm_problem); decay: per-tensor weight-decay flags or None;
     randomized: allocate u_scratch for the randomized sign; global_adamw:
-    allocate the global second moment v of the Global AdamW rule.
+    allocate the global second moment v of the Global AdamW rule;
+    replica_layout: how x_rep holds the replicas (dsm_replica_layout).
+
+    x_rep is an (n, d_pad) view with contiguous replicas, and an (n, blocks,
+    16384) strided view of the same memory with blocked replicas;
+    replica(i), replicas() and replica_index() read either the same way.
     """
 
     def __init__(self, numel, n_workers, local_steps, base, decay=None, randomized=True,
-                 global_adamw=False, device="cuda"):
+                 global_adamw=False, device="cuda", replica_layout=dsm.DSM_REPLICAS_CONTIGUOUS):
         self.numel = [int(v) for v in numel]
         self.n = int(n_workers)
         self.H = int(local_steps)
         self.base = int(base)
         self.decay = None if decay is None else [bool(v) for v in decay]
-        self.problem = dsm.make_problem(self.numel, self.n, self.H, self.base, self.decay)
+        self.replica_layout = int(replica_layout)
+        self.problem = dsm.make_problem(self.numel, self.n, self.H, self.base, self.decay,
+                                        self.replica_layout)
         self.arena_elems, self.offsets, self.workspace_bytes = dsm.dsm_layout(self.problem)
         a = max(self.arena_elems, 64)
         self._storage = []
@@ -53,7 +60,12 @@ class Arenas:
 
         self.x = alloc(a)
         self.m = alloc(a)
-        self.x_rep = alloc(self.n, a)
+        self.x_rep_flat = alloc(self.n * a)
+        if self.blocked and self.arena_elems > 0:
+            B = dsm.DSM_REPLICA_BLOCK_ELEMS
+            self.x_rep = self.x_rep_flat.view(a // B, self.n, B).permute(1, 0, 2)
+        else:
+            self.x_rep = self.x_rep_flat.view(self.n, a)
         self.g_rep = alloc(self.n, a)
         self.s1_rep = alloc(self.n, a)
         self.s2_rep = alloc(self.n, a) if self.base == dsm.DSM_BASE_ADAMW else None
@@ -69,7 +81,7 @@ class Arenas:
 
         def ptr(t):
             return None if t is None else t.data_ptr()
-        return dsm.dsm_buffers(ptr(self.x), ptr(self.m), ptr(self.x_rep), ptr(self.g_rep),
+        return dsm.dsm_buffers(ptr(self.x), ptr(self.m), ptr(self.x_rep_flat), ptr(self.g_rep),
                                ptr(self.s1_rep), ptr(self.s2_rep), ptr(self.u),
                                ptr(self.workspace), self.workspace.numel(), stream.cuda_stream,
                                ptr(self.v))
@@ -78,6 +90,37 @@ class Arenas:
         """dsm_init on the current contents of x."""
         self.ctx = dsm.dsm_init(self.problem, self.buffers(stream))
         return self.ctx
+
+    @property
+    def blocked(self):
+        return self.replica_layout == dsm.DSM_REPLICAS_BLOCKED
+
+    def replica_index(self, i, e):
+        """Index into x_rep_flat of element(s) e (arena indices) of replica i."""
+        if self.blocked:
+            B = dsm.DSM_REPLICA_BLOCK_ELEMS
+            return (e // B) * (self.n * B) + i * B + e % B
+        return i * self.arena_elems + e
+
+    def replica(self, i):
+        """Replica i as a 1-D arena copy (a view when contiguous, else a copy)."""
+        return self.x_rep[i].reshape(-1)
+
+    def worker(self, name, i):
+        """Worker i's copy of a per-worker buffer ("x_rep", "g_rep", "s1_rep" or
+        "s2_rep") as a 1-D arena (a copy for blocked replicas)."""
+        return self.replica(i) if name == "x_rep" else getattr(self, name)[i]
+
+    def gather(self, name, i, idx):
+        """Elements idx (arena indices, a device tensor) of worker i's copy of a
+        per-worker buffer, without materialising a blocked replica."""
+        if name == "x_rep":
+            return self.x_rep_flat[self.replica_index(i, idx)]
+        return getattr(self, name)[i][idx]
+
+    def replicas(self):
+        """All replicas as (n, d_pad) (a view when contiguous, else a copy)."""
+        return self.x_rep.reshape(self.n, -1)
 
     def views(self, flat):
         """Per-tensor views of one arena copy (a 1-D tensor of arena_elems)."""

@@ -40,6 +40,34 @@ constexpr int kSplit = (kChunkElems / 4) / kPieceVec;
 constexpr int64_t kTensorAlign = 64;
 constexpr int kMaxWorkers = 64;
 
+// Replica buffers in 64 KiB blocks (dsm_problem.replica_layout =
+// DSM_REPLICAS_BLOCKED): copy i of block b sits at element (b * n + i) *
+// kRepBlockElems.  Tensors then start on a multiple of the piece size (and of
+// 1024 elements), so a work-group's piece never crosses a block, and the
+// arena length is a whole number of blocks.
+constexpr int kRepBlockShift = 14;
+constexpr int64_t kRepBlockElems = int64_t(1) << kRepBlockShift;
+constexpr int64_t kPieceElems = int64_t(kPieceVec) * 4;
+static_assert(kRepBlockElems % kPieceElems == 0, "a block must hold whole pieces");
+constexpr int64_t kBlockedTensorAlign = kPieceElems > 1024 ? kPieceElems : 1024;
+
+// Where copy i of a replica buffer keeps arena element e:
+// (e >> shift) * block_stride + i * copy_stride + (e & (2^shift - 1)).
+struct RepLayout {
+    int64_t block_stride;
+    int64_t copy_stride;
+    int32_t shift;
+    int32_t pad;
+};
+// n contiguous copies of d_pad elements.
+inline RepLayout contiguous_copies(int64_t d_pad) { return RepLayout{0, d_pad, 62, 0}; }
+// n copies interleaved in 64 KiB blocks.
+inline RepLayout blocked_copies(int n) {
+    return RepLayout{int64_t(n) * kRepBlockElems, kRepBlockElems, kRepBlockShift, 0};
+}
+// Every copy is the same single buffer (stale replicas read the global x).
+inline RepLayout single_copy() { return RepLayout{0, 0, 62, 0}; }
+
 // One chunk of one tensor inside an arena copy.  32 bytes.
 struct Chunk {
     int64_t off;      // element offset of the chunk in the arena
@@ -84,27 +112,30 @@ struct GlobalScalars {
     float eta, eps;
 };
 
-// Kernel launchers (dsm_kernels.hip).  All return the launch status.
+// Kernel launchers (dsm_kernels.hip).  All return the launch status.  The
+// replica buffer x_rep is addressed through its RepLayout rl; g_rep, s1 and
+// s2 hold n contiguous copies of stride elements.
 hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float* m, float* v,
-                       float* x_rep, float* s1, float* s2, int64_t stride, int n, hipStream_t st);
-// Local steps: worker w reads its replica from x_src + w * src_stride (the
-// replica, or the shared global model with src_stride = 0) and writes it to
-// x_rep + w * stride.
-hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_rep,
-                              const float* x_src, int64_t src_stride, const float* g_rep,
-                              float* s1, float* s2, int64_t stride, int worker0, int n_workers,
+                       float* x_rep, RepLayout rl, float* s1, float* s2, int64_t stride, int n,
+                       hipStream_t st);
+// Local steps: worker w reads its starting point from x_src through sl (its
+// replica, or the shared global model with single_copy()) and writes its
+// replica through rl.
+hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_rep, RepLayout rl,
+                              const float* x_src, RepLayout sl, const float* g_rep, float* s1,
+                              float* s2, int64_t stride, int worker0, int n_workers,
                               const AdamScalars& sc, hipStream_t st);
-hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep,
-                             const float* x_src, int64_t src_stride, const float* g_rep,
-                             float* s1, int64_t stride, int worker0, int n_workers,
-                             const SgdScalars& sc, hipStream_t st);
+hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep, RepLayout rl,
+                             const float* x_src, RepLayout sl, const float* g_rep, float* s1,
+                             int64_t stride, int worker0, int n_workers, const SgdScalars& sc,
+                             hipStream_t st);
 
 // Local step of all n workers from the global model x (every replica stale):
 // x is read once per element and each worker's result goes to its replica.
 hipError_t launch_local_from_x(const Chunk* chunks, int64_t n_chunks, const float* x,
-                               float* x_rep, const float* g_rep, float* s1, float* s2,
-                               int64_t stride, int n, bool adamw, const AdamScalars& as,
-                               const SgdScalars& ss, hipStream_t st);
+                               float* x_rep, RepLayout rl, const float* g_rep, float* s1,
+                               float* s2, int64_t stride, int n, bool adamw,
+                               const AdamScalars& as, const SgdScalars& ss, hipStream_t st);
 
 // Workspace words of the randomized sign's per-tensor bound B_p = max |u|,
 // reduced in two levels without atomics.
@@ -117,8 +148,9 @@ struct BoundWords {
 // Arguments of the fused last-local-step + global-step launch.
 struct RoundEndArgs {
     float *x, *m, *x_rep;
-    const float* x_src;
-    int64_t src_stride;
+    RepLayout rl;           // the replicas
+    const float* x_src;     // where step H starts: the replicas, or x when they are stale
+    RepLayout sl;
     const float* g_rep;
     float *s1, *s2, *u;
     BoundWords bound;
@@ -131,14 +163,14 @@ hipError_t launch_round_end(const Chunk* chunks, int64_t n_chunks, int n_tensors
                             const RoundEndArgs& a, bool broadcast, hipStream_t st);
 // Deterministic global step of any rule; v is the Global AdamW second moment.
 hipError_t launch_global_det(const Chunk* chunks, int64_t n_chunks, float* x, float* m,
-                             float* v, float* x_rep, int64_t stride, const GlobalScalars& sc,
+                             float* v, float* x_rep, RepLayout rl, const GlobalScalars& sc,
                              bool broadcast, hipStream_t st);
 hipError_t launch_global_rand(const Chunk* chunks, int64_t n_chunks, int n_tensors, float* x,
-                              float* m, float* x_rep, float* u, const BoundWords& bw,
-                              int64_t stride, const GlobalScalars& sc, bool broadcast,
+                              float* m, float* x_rep, RepLayout rl, float* u,
+                              const BoundWords& bw, const GlobalScalars& sc, bool broadcast,
                               hipStream_t st);
 hipError_t launch_broadcast(const Chunk* chunks, int64_t n_chunks, const float* x, float* x_rep,
-                            int64_t stride, int n, hipStream_t st);
+                            RepLayout rl, int n, hipStream_t st);
 hipError_t launch_test_philox(uint32_t key0, uint32_t key1, uint32_t tensor, uint32_t t,
                               uint32_t q0, int64_t count, uint32_t* out, hipStream_t st);
 

@@ -55,23 +55,39 @@ __device__ __forceinline__ void store_head(f4 v, float* p, int k) {
     if (k > 2) p[2] = v.z;
 }
 
-// Stores v at group q of p: whole group, or only the lanes inside the chunk.
-__device__ __forceinline__ void store_group(f4 v, f4* p, int q, int nfull, int len) {
-    if (q < nfull)
-        ntstore(v, p + q);
+// Stores v at p: the whole group when its four lanes are inside the chunk
+// (valid >= 4), else only the valid lanes.
+__device__ __forceinline__ void store_vec(f4 v, f4* p, int valid) {
+    if (valid >= 4)
+        ntstore(v, p);
     else
-        store_head(v, reinterpret_cast<float*>(p + q), len - 4 * q);
+        store_head(v, reinterpret_cast<float*>(p), valid);
+}
+
+// Where copy i of a replica buffer keeps arena element e (RepLayout):
+// (e >> shift) * block_stride + i * copy_stride + (e & (2^shift - 1)).
+// Contiguous copies use shift 62 (the block term vanishes) and copy_stride =
+// d_pad; 64 KiB blocks interleaved by copy use shift 14, block_stride =
+// n * 16384 and copy_stride = 16384; "every copy is x" uses shift 62 and
+// copy_stride 0.  A piece never crosses a block, so one base per piece and
+// copy serves every thread of the work-group.
+__device__ __forceinline__ int64_t rep_index(const RepLayout& L, int64_t i, int64_t e) {
+    const int64_t mask = (int64_t(1) << L.shift) - 1;
+    return (e >> L.shift) * L.block_stride + i * L.copy_stride + (e & mask);
 }
 
 // The piece of a chunk this work-group processes: work item w (below) takes
-// piece w % kSplit of chunk w / kSplit, float4 groups [q_lo, q_hi).
+// piece w % kSplit of chunk w / kSplit, kPieceVec float4 groups from group
+// (w % kSplit) * kPieceVec of the chunk on (fewer at the chunk's end).
 // Work-groups are short-lived and handle one piece each, so the addresses in
 // flight form compact fronts that sweep the arena.
 struct Piece {
     Chunk c;
     uint32_t wi;     // piece index: chunk wi / kSplit, piece wi % kSplit of it
-    int q_lo, q_hi;  // float4 groups of the chunk handled here
-    int nfull;       // groups of four valid lanes in the chunk
+    int nq;          // float4 groups in the piece (0 past the chunk's end)
+    int valid0;      // lanes of the chunk from the piece's first group on
+    int64_t e0;      // arena element of the piece's first group
+    uint32_t j4;     // in-tensor index of the first group, divided by 4
 };
 
 #ifndef DSM_XCD_MAP
@@ -121,9 +137,11 @@ __device__ __forceinline__ Piece piece_of(const Chunk* __restrict__ chunks) {
     pc.wi = wi;
     pc.c = chunks[wi / kSplit];
     const int nvec = (pc.c.len + 3) >> 2;
-    pc.q_lo = static_cast<int>(wi % kSplit) * kPieceVec;
-    pc.q_hi = min(nvec, pc.q_lo + kPieceVec);
-    pc.nfull = pc.c.len >> 2;
+    const int q_lo = static_cast<int>(wi % kSplit) * kPieceVec;
+    pc.nq = max(0, min(nvec, q_lo + kPieceVec) - q_lo);
+    pc.valid0 = pc.c.len - 4 * q_lo;
+    pc.e0 = pc.c.off + 4 * static_cast<int64_t>(q_lo);
+    pc.j4 = static_cast<uint32_t>(pc.c.j0 >> 2) + static_cast<uint32_t>(q_lo);
     return pc;
 }
 
@@ -154,32 +172,31 @@ __device__ __forceinline__ void adamw4(f4& x, f4 g, f4& m, f4& v, float lam, con
     x = x - st;
 }
 
-// x_src/src_stride: where worker w reads its replica, x_src + w * src_stride
-// (the replica itself, or with src_stride = 0 the global model x when the
-// replicas are stale after a global step without broadcast); the result is
-// written to the replica x_rep + w * stride.
+// Worker w reads its step's starting point at x_src + rep_index(sl, w, e)
+// (its own replica, or with a zero copy stride the global model x when the
+// replicas are stale after a global step without broadcast) and writes the
+// result to its replica, x_rep + rep_index(rl, w, e).  The two may be the
+// same memory, so neither pointer is __restrict__; each thread loads every
+// stream of its group before it stores.
 __global__ __launch_bounds__(kBlockThreads) void k_local_adamw(
-    const Chunk* __restrict__ chunks, float* __restrict__ x_rep, const float* __restrict__ x_src,
-    int64_t src_stride, const float* __restrict__ g_rep, float* __restrict__ s1,
+    const Chunk* __restrict__ chunks, float* x_rep, RepLayout rl, const float* x_src,
+    RepLayout sl, const float* __restrict__ g_rep, float* __restrict__ s1,
     float* __restrict__ s2, int64_t stride, int worker0, AdamScalars sc) {
     const Piece pc = piece_of<kMapLocal>(chunks);
-    const Chunk& c = pc.c;
     const int64_t w = worker0 + static_cast<int>(blockIdx.y);
-    const int64_t base = w * stride + c.off;
-    f4* __restrict__ xp = reinterpret_cast<f4*>(x_rep + base);
-    const f4* __restrict__ xs = reinterpret_cast<const f4*>(x_src + w * src_stride + c.off);
-    const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + base);
-    f4* __restrict__ mp = reinterpret_cast<f4*>(s1 + base);
-    f4* __restrict__ vp = reinterpret_cast<f4*>(s2 + base);
-    const float lam = c.decay ? sc.wd : 0.0f;
-    const int nvec = pc.q_hi;
-    const int nfull = pc.nfull;
-    for (int q0 = pc.q_lo + threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+    const int64_t wo = w * stride + pc.e0;
+    f4* xp = reinterpret_cast<f4*>(x_rep + rep_index(rl, w, pc.e0));
+    const f4* xs = reinterpret_cast<const f4*>(x_src + rep_index(sl, w, pc.e0));
+    const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + wo);
+    f4* __restrict__ mp = reinterpret_cast<f4*>(s1 + wo);
+    f4* __restrict__ vp = reinterpret_cast<f4*>(s2 + wo);
+    const float lam = pc.c.decay ? sc.wd : 0.0f;
+    for (int q0 = threadIdx.x; q0 < pc.nq; q0 += kBlockThreads * kUnroll) {
         f4 xv[kUnroll], gv[kUnroll], mv[kUnroll], vv[kUnroll];
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = q0 + k * kBlockThreads;
-            if (q < nvec) {
+            if (q < pc.nq) {
                 xv[k] = ntload(xs + q);
                 gv[k] = ntload(gp + q);
                 mv[k] = ntload(mp + q);
@@ -189,11 +206,12 @@ __global__ __launch_bounds__(kBlockThreads) void k_local_adamw(
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = q0 + k * kBlockThreads;
-            if (q < nvec) {
+            if (q < pc.nq) {
+                const int valid = pc.valid0 - 4 * q;
                 adamw4(xv[k], gv[k], mv[k], vv[k], lam, sc);
-                store_group(xv[k], xp, q, nfull, c.len);
-                store_group(mv[k], mp, q, nfull, c.len);
-                store_group(vv[k], vp, q, nfull, c.len);
+                store_vec(xv[k], xp + q, valid);
+                store_vec(mv[k], mp + q, valid);
+                store_vec(vv[k], vp + q, valid);
             }
         }
     }
@@ -210,25 +228,22 @@ __device__ __forceinline__ void sgdm4(f4& x, f4 g, f4& m, const SgdScalars& s) {
 }
 
 __global__ __launch_bounds__(kBlockThreads) void k_local_sgdm(
-    const Chunk* __restrict__ chunks, float* __restrict__ x_rep, const float* __restrict__ x_src,
-    int64_t src_stride, const float* __restrict__ g_rep, float* __restrict__ s1, int64_t stride,
+    const Chunk* __restrict__ chunks, float* x_rep, RepLayout rl, const float* x_src,
+    RepLayout sl, const float* __restrict__ g_rep, float* __restrict__ s1, int64_t stride,
     int worker0, SgdScalars sc) {
     const Piece pc = piece_of<kMapLocal>(chunks);
-    const Chunk& c = pc.c;
     const int64_t w = worker0 + static_cast<int>(blockIdx.y);
-    const int64_t base = w * stride + c.off;
-    f4* __restrict__ xp = reinterpret_cast<f4*>(x_rep + base);
-    const f4* __restrict__ xs = reinterpret_cast<const f4*>(x_src + w * src_stride + c.off);
-    const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + base);
-    f4* __restrict__ mp = reinterpret_cast<f4*>(s1 + base);
-    const int nvec = pc.q_hi;
-    const int nfull = pc.nfull;
-    for (int q0 = pc.q_lo + threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+    const int64_t wo = w * stride + pc.e0;
+    f4* xp = reinterpret_cast<f4*>(x_rep + rep_index(rl, w, pc.e0));
+    const f4* xs = reinterpret_cast<const f4*>(x_src + rep_index(sl, w, pc.e0));
+    const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + wo);
+    f4* __restrict__ mp = reinterpret_cast<f4*>(s1 + wo);
+    for (int q0 = threadIdx.x; q0 < pc.nq; q0 += kBlockThreads * kUnroll) {
         f4 xv[kUnroll], gv[kUnroll], mv[kUnroll];
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = q0 + k * kBlockThreads;
-            if (q < nvec) {
+            if (q < pc.nq) {
                 xv[k] = ntload(xs + q);
                 gv[k] = ntload(gp + q);
                 mv[k] = ntload(mp + q);
@@ -237,10 +252,11 @@ __global__ __launch_bounds__(kBlockThreads) void k_local_sgdm(
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = q0 + k * kBlockThreads;
-            if (q < nvec) {
+            if (q < pc.nq) {
+                const int valid = pc.valid0 - 4 * q;
                 sgdm4(xv[k], gv[k], mv[k], sc);
-                store_group(xv[k], xp, q, nfull, c.len);
-                store_group(mv[k], mp, q, nfull, c.len);
+                store_vec(xv[k], xp + q, valid);
+                store_vec(mv[k], mp + q, valid);
             }
         }
     }
@@ -253,24 +269,27 @@ __device__ __forceinline__ float sign_of(float u) {
     return u > 0.0f ? 1.0f : (u < 0.0f ? -1.0f : (u == u ? 0.0f : u));
 }
 
-// Worker sum of (x - x_i) over the n replicas of group q, in worker order,
-// divided by n.  N > 0: compile-time worker count (a power of two, so the
-// division is the exact multiplication by 1/n); N == 0: runtime count.
+// Worker sum of (x - x_i) over the n replicas of group q of the piece that
+// starts at arena element e0, in worker order, divided by n.  N > 0:
+// compile-time worker count (a power of two, so the division is the exact
+// multiplication by 1/n); N == 0: runtime count.
 template <int N>
-__device__ __forceinline__ f4 worker_mean_diff(f4 xv, const float* __restrict__ rbase,
-                                               int64_t stride, int q, const GlobalScalars& s) {
+__device__ __forceinline__ f4 worker_mean_diff(f4 xv, const float* __restrict__ x_rep,
+                                               const RepLayout& rl, int64_t e0, int q,
+                                               const GlobalScalars& s) {
     if constexpr (N > 0) {
         f4 r[N];
 #pragma unroll
-        for (int i = 0; i < N; ++i) r[i] = ntload(reinterpret_cast<const f4*>(rbase + i * stride) + q);
+        for (int i = 0; i < N; ++i)
+            r[i] = ntload(reinterpret_cast<const f4*>(x_rep + rep_index(rl, i, e0)) + q);
         f4 acc = xv - r[0];
 #pragma unroll
         for (int i = 1; i < N; ++i) acc = acc + (xv - r[i]);
         return acc * s.inv_n;
     } else {
-        f4 acc = xv - ntload(reinterpret_cast<const f4*>(rbase) + q);
+        f4 acc = xv - ntload(reinterpret_cast<const f4*>(x_rep + rep_index(rl, 0, e0)) + q);
         for (int i = 1; i < s.n; ++i)
-            acc = acc + (xv - ntload(reinterpret_cast<const f4*>(rbase + i * stride) + q));
+            acc = acc + (xv - ntload(reinterpret_cast<const f4*>(x_rep + rep_index(rl, i, e0)) + q));
         if (s.n_pow2) return acc * s.inv_n;
         return acc / s.n_f;
     }
@@ -330,23 +349,19 @@ __device__ __forceinline__ f4 global_adamw4(f4 x, f4 delta, f4& m, f4& v, float 
 template <int N, int RULE, bool BCAST>
 __global__ __launch_bounds__(kBlockThreads) void k_global_det(
     const Chunk* __restrict__ chunks, float* __restrict__ x, float* __restrict__ m,
-    float* __restrict__ v, float* __restrict__ x_rep, int64_t stride, GlobalScalars sc) {
+    float* __restrict__ v, float* __restrict__ x_rep, RepLayout rl, GlobalScalars sc) {
     const Piece pc = piece_of(chunks);
-    const Chunk& c = pc.c;
     const int n = N > 0 ? N : sc.n;
-    f4* __restrict__ xp = reinterpret_cast<f4*>(x + c.off);
-    f4* __restrict__ mp = reinterpret_cast<f4*>(m + c.off);
-    f4* __restrict__ vp = reinterpret_cast<f4*>(v + c.off);
-    float* __restrict__ rbase = x_rep + c.off;
-    const float lam = c.decay ? sc.lam : 0.0f;
-    const int nvec = pc.q_hi;
-    const int nfull = pc.nfull;
-    for (int q0 = pc.q_lo + threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+    f4* __restrict__ xp = reinterpret_cast<f4*>(x + pc.e0);
+    f4* __restrict__ mp = reinterpret_cast<f4*>(m + pc.e0);
+    f4* __restrict__ vp = reinterpret_cast<f4*>(v + pc.e0);
+    const float lam = pc.c.decay ? sc.lam : 0.0f;
+    for (int q0 = threadIdx.x; q0 < pc.nq; q0 += kBlockThreads * kUnroll) {
         f4 xv[kUnroll], mv[kUnroll], vv[kUnroll], dv[kUnroll];
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = q0 + k * kBlockThreads;
-            if (q < nvec) {
+            if (q < pc.nq) {
                 xv[k] = ntload(xp + q);
                 mv[k] = ntload(mp + q);
                 if (RULE == kRuleGlobalAdamW) vv[k] = ntload(vp + q);
@@ -355,12 +370,13 @@ __global__ __launch_bounds__(kBlockThreads) void k_global_det(
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = q0 + k * kBlockThreads;
-            if (q < nvec) dv[k] = worker_mean_diff<N>(xv[k], rbase, stride, q, sc);
+            if (q < pc.nq) dv[k] = worker_mean_diff<N>(xv[k], x_rep, rl, pc.e0, q, sc);
         }
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = q0 + k * kBlockThreads;
-            if (q < nvec) {
+            if (q < pc.nq) {
+                const int valid = pc.valid0 - 4 * q;
                 f4 xn;
                 if constexpr (RULE == kRuleSignMomentum) {
                     const f4 u = momentum4(mv[k], dv[k], sc);
@@ -379,13 +395,14 @@ __global__ __launch_bounds__(kBlockThreads) void k_global_det(
                     xn = model4(xv[k], u, lam, sc);
                 } else {
                     xn = global_adamw4(xv[k], dv[k], mv[k], vv[k], lam, sc);
-                    store_group(vv[k], vp, q, nfull, c.len);
+                    store_vec(vv[k], vp + q, valid);
                 }
-                store_group(xn, xp, q, nfull, c.len);
-                store_group(mv[k], mp, q, nfull, c.len);
+                store_vec(xn, xp + q, valid);
+                store_vec(mv[k], mp + q, valid);
                 if (BCAST) {
                     for (int i = 0; i < n; ++i)
-                        store_group(xn, reinterpret_cast<f4*>(rbase + i * stride), q, nfull, c.len);
+                        store_vec(xn, reinterpret_cast<f4*>(x_rep + rep_index(rl, i, pc.e0)) + q,
+                                  valid);
                 }
             }
         }
@@ -429,24 +446,20 @@ __device__ __forceinline__ void store_piece_max(uint32_t bits, uint32_t* wave_ma
 template <int N>
 __global__ __launch_bounds__(kBlockThreads) void k_global_rand_pass1(
     const Chunk* __restrict__ chunks, const float* __restrict__ x, float* __restrict__ m,
-    const float* __restrict__ x_rep, float* __restrict__ u_out, uint32_t* __restrict__ piece_max,
-    int64_t stride, GlobalScalars sc) {
+    const float* __restrict__ x_rep, RepLayout rl, float* __restrict__ u_out,
+    uint32_t* __restrict__ piece_max, GlobalScalars sc) {
     const Piece pc = piece_of(chunks);
-    const Chunk& c = pc.c;
-    const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + c.off);
-    f4* __restrict__ mp = reinterpret_cast<f4*>(m + c.off);
-    f4* __restrict__ up = reinterpret_cast<f4*>(u_out + c.off);
-    const float* __restrict__ rbase = x_rep + c.off;
-    const int nvec = pc.q_hi;
-    const int nfull = pc.nfull;
+    const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + pc.e0);
+    f4* __restrict__ mp = reinterpret_cast<f4*>(m + pc.e0);
+    f4* __restrict__ up = reinterpret_cast<f4*>(u_out + pc.e0);
     __shared__ uint32_t wave_max[kBlockThreads / 64];
     uint32_t maxbits = 0;
-    for (int q0 = pc.q_lo + threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+    for (int q0 = threadIdx.x; q0 < pc.nq; q0 += kBlockThreads * kUnroll) {
         f4 xv[kUnroll], mv[kUnroll], dv[kUnroll];
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = q0 + k * kBlockThreads;
-            if (q < nvec) {
+            if (q < pc.nq) {
                 xv[k] = ntload(xp + q);
                 mv[k] = ntload(mp + q);
             }
@@ -454,16 +467,16 @@ __global__ __launch_bounds__(kBlockThreads) void k_global_rand_pass1(
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = q0 + k * kBlockThreads;
-            if (q < nvec) dv[k] = worker_mean_diff<N>(xv[k], rbase, stride, q, sc);
+            if (q < pc.nq) dv[k] = worker_mean_diff<N>(xv[k], x_rep, rl, pc.e0, q, sc);
         }
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = q0 + k * kBlockThreads;
-            if (q < nvec) {
+            if (q < pc.nq) {
+                const int valid = pc.valid0 - 4 * q;  // lanes inside the tensor
                 const f4 uv = momentum4(mv[k], dv[k], sc);
-                store_group(uv, up, q, nfull, c.len);
-                store_group(mv[k], mp, q, nfull, c.len);
-                const int valid = c.len - 4 * q;  // lanes inside the tensor
+                store_vec(uv, up + q, valid);
+                store_vec(mv[k], mp + q, valid);
                 uint32_t b = __float_as_uint(fabsf(uv.x));
                 if (valid > 1) b = max(b, __float_as_uint(fabsf(uv.y)));
                 if (valid > 2) b = max(b, __float_as_uint(fabsf(uv.z)));
@@ -523,27 +536,29 @@ __device__ __forceinline__ float rand_sign(float u, uint32_t w, double B) {
 }
 
 // Randomized sign, pass 2: S_r, Eq. (7) and the synchronisation step.
+// Section 3.1 defines S_r only for a finite bound: a tensor whose bound is
+// NaN or infinite (it holds a non-finite u) gets S = NaN at every element,
+// so its step is NaN rather than a step of a reversed or zero sign.
 template <int MODE, bool BCAST>
 __global__ __launch_bounds__(kBlockThreads) void k_global_rand_pass2(
     const Chunk* __restrict__ chunks, float* __restrict__ x, float* __restrict__ x_rep,
-    const float* __restrict__ u_in, const uint32_t* __restrict__ bound_bits, int64_t stride,
+    RepLayout rl, const float* __restrict__ u_in, const uint32_t* __restrict__ bound_bits,
     GlobalScalars sc) {
     const Piece pc = piece_of(chunks);
     const Chunk& c = pc.c;
-    f4* __restrict__ xp = reinterpret_cast<f4*>(x + c.off);
-    const f4* __restrict__ up = reinterpret_cast<const f4*>(u_in + c.off);
-    float* __restrict__ rbase = x_rep + c.off;
+    f4* __restrict__ xp = reinterpret_cast<f4*>(x + pc.e0);
+    const f4* __restrict__ up = reinterpret_cast<const f4*>(u_in + pc.e0);
     const float lam = c.decay ? sc.lam : 0.0f;
-    const double B = static_cast<double>(__uint_as_float(bound_bits[c.tensor]));
-    const uint32_t blk0 = static_cast<uint32_t>(c.j0 >> 2);
-    const int nvec = pc.q_hi;
-    const int nfull = pc.nfull;
-    for (int q0 = pc.q_lo + threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+    const uint32_t bbits = bound_bits[c.tensor];
+    const bool bound_finite = bbits < 0x7f800000u;   // B >= 0: below the +inf pattern
+    const double B = static_cast<double>(__uint_as_float(bbits));
+    const float undefined = __builtin_nanf("");
+    for (int q0 = threadIdx.x; q0 < pc.nq; q0 += kBlockThreads * kUnroll) {
         f4 xv[kUnroll], uv[kUnroll];
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = q0 + k * kBlockThreads;
-            if (q < nvec) {
+            if (q < pc.nq) {
                 xv[k] = ntload(xp + q);
                 uv[k] = ntload(up + q);
             }
@@ -551,17 +566,20 @@ __global__ __launch_bounds__(kBlockThreads) void k_global_rand_pass2(
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = q0 + k * kBlockThreads;
-            if (q < nvec) {
-                uint32_t w0 = blk0 + static_cast<uint32_t>(q), w1 = c.tensor, w2 = sc.t,
+            if (q < pc.nq) {
+                uint32_t w0 = pc.j4 + static_cast<uint32_t>(q), w1 = c.tensor, w2 = sc.t,
                          w3 = kSignStream;
                 philox4x32_10(w0, w1, w2, w3, sc.key0, sc.key1);
-                const f4 S = {rand_sign<MODE>(uv[k].x, w0, B), rand_sign<MODE>(uv[k].y, w1, B),
-                              rand_sign<MODE>(uv[k].z, w2, B), rand_sign<MODE>(uv[k].w, w3, B)};
+                f4 S = {rand_sign<MODE>(uv[k].x, w0, B), rand_sign<MODE>(uv[k].y, w1, B),
+                        rand_sign<MODE>(uv[k].z, w2, B), rand_sign<MODE>(uv[k].w, w3, B)};
+                if (!bound_finite) S = f4{undefined, undefined, undefined, undefined};
                 const f4 xn = model4(xv[k], S, lam, sc);
-                store_group(xn, xp, q, nfull, c.len);
+                const int valid = pc.valid0 - 4 * q;
+                store_vec(xn, xp + q, valid);
                 if (BCAST) {
                     for (int i = 0; i < sc.n; ++i)
-                        store_group(xn, reinterpret_cast<f4*>(rbase + i * stride), q, nfull, c.len);
+                        store_vec(xn, reinterpret_cast<f4*>(x_rep + rep_index(rl, i, pc.e0)) + q,
+                                  valid);
                 }
             }
         }
@@ -582,21 +600,18 @@ constexpr int kBaseSgd = 1;
 template <int N, int BASE>
 __global__ __launch_bounds__(kBlockThreads) void k_local_from_x(
     const Chunk* __restrict__ chunks, const float* __restrict__ x, float* __restrict__ x_rep,
-    const float* __restrict__ g_rep, float* __restrict__ s1, float* __restrict__ s2,
-    int64_t stride, int n_rt, AdamScalars as, SgdScalars ss) {
+    RepLayout rl, const float* __restrict__ g_rep, float* __restrict__ s1,
+    float* __restrict__ s2, int64_t stride, int n_rt, AdamScalars as, SgdScalars ss) {
     const Piece pc = piece_of<kMapFromX>(chunks);
-    const Chunk& c = pc.c;
     const int n = N > 0 ? N : n_rt;
-    const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + c.off);
-    const float lam = c.decay ? as.wd : 0.0f;
-    const int nvec = pc.q_hi;
-    const int nfull = pc.nfull;
-    for (int q0 = pc.q_lo + threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+    const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + pc.e0);
+    const float lam = pc.c.decay ? as.wd : 0.0f;
+    for (int q0 = threadIdx.x; q0 < pc.nq; q0 += kBlockThreads * kUnroll) {
         f4 xv[kUnroll];
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = q0 + k * kBlockThreads;
-            if (q < nvec) xv[k] = ntload(xp + q);
+            if (q < pc.nq) xv[k] = ntload(xp + q);
         }
 #if DSM_ROUND_END_UNROLL == 0
 #pragma unroll(N > 0 ? N : 1)
@@ -606,8 +621,8 @@ __global__ __launch_bounds__(kBlockThreads) void k_local_from_x(
 #pragma unroll 2
 #endif
         for (int i = 0; i < (N > 0 ? N : n); ++i) {
-            const int64_t wo = i * stride + c.off;
-            f4* __restrict__ xr = reinterpret_cast<f4*>(x_rep + wo);
+            const int64_t wo = i * stride + pc.e0;
+            f4* __restrict__ xr = reinterpret_cast<f4*>(x_rep + rep_index(rl, i, pc.e0));
             const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + wo);
             f4* __restrict__ s1p = reinterpret_cast<f4*>(s1 + wo);
             f4* __restrict__ s2p = reinterpret_cast<f4*>(s2 + wo);
@@ -615,7 +630,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_local_from_x(
 #pragma unroll
             for (int k = 0; k < kUnroll; ++k) {
                 const int q = q0 + k * kBlockThreads;
-                if (q < nvec) {
+                if (q < pc.nq) {
                     gi[k] = ntload(gp + q);
                     mi[k] = ntload(s1p + q);
                     if (BASE == kBaseAdamW) vi[k] = ntload(s2p + q);
@@ -624,16 +639,17 @@ __global__ __launch_bounds__(kBlockThreads) void k_local_from_x(
 #pragma unroll
             for (int k = 0; k < kUnroll; ++k) {
                 const int q = q0 + k * kBlockThreads;
-                if (q < nvec) {
+                if (q < pc.nq) {
+                    const int valid = pc.valid0 - 4 * q;
                     f4 xi = xv[k];
                     if (BASE == kBaseAdamW) {
                         adamw4(xi, gi[k], mi[k], vi[k], lam, as);
-                        store_group(vi[k], s2p, q, nfull, c.len);
+                        store_vec(vi[k], s2p + q, valid);
                     } else {
                         sgdm4(xi, gi[k], mi[k], ss);
                     }
-                    store_group(xi, xr, q, nfull, c.len);
-                    store_group(mi[k], s1p, q, nfull, c.len);
+                    store_vec(xi, xr + q, valid);
+                    store_vec(mi[k], s1p + q, valid);
                 }
             }
         }
@@ -653,28 +669,28 @@ __global__ __launch_bounds__(kBlockThreads) void k_local_from_x(
 
 template <int N, int BASE, int KIND>
 __global__ __launch_bounds__(kBlockThreads) void k_round_end(
-    const Chunk* __restrict__ chunks, float* __restrict__ x, float* __restrict__ m,
-    float* __restrict__ x_rep, const float* __restrict__ x_src, int64_t src_stride,
-    const float* __restrict__ g_rep, float* __restrict__ s1, float* __restrict__ s2,
-    float* __restrict__ u_out, uint32_t* __restrict__ piece_max, int64_t stride,
-    AdamScalars as, SgdScalars ss, GlobalScalars gs) {
+    const Chunk* __restrict__ chunks, float* x, float* __restrict__ m, float* x_rep,
+    RepLayout rl, const float* x_src, RepLayout sl, const float* __restrict__ g_rep,
+    float* __restrict__ s1, float* __restrict__ s2, float* __restrict__ u_out,
+    uint32_t* __restrict__ piece_max, int64_t stride, AdamScalars as, SgdScalars ss,
+    GlobalScalars gs) {
+    // x_src is the replicas or, when they are stale, x itself: it may alias
+    // x and x_rep, so none of the three is __restrict__.  Every load of a
+    // group precedes its stores.
     __shared__ uint32_t wave_max[kBlockThreads / 64];
     const Piece pc = piece_of<kMapRoundEnd>(chunks);
-    const Chunk& c = pc.c;
     const int n = N > 0 ? N : gs.n;
-    f4* __restrict__ xp = reinterpret_cast<f4*>(x + c.off);
-    f4* __restrict__ mp = reinterpret_cast<f4*>(m + c.off);
-    const float lam_local = c.decay ? as.wd : 0.0f;
-    const float lam = c.decay ? gs.lam : 0.0f;
-    const int nvec = pc.q_hi;
-    const int nfull = pc.nfull;
+    f4* xp = reinterpret_cast<f4*>(x + pc.e0);
+    f4* __restrict__ mp = reinterpret_cast<f4*>(m + pc.e0);
+    const float lam_local = pc.c.decay ? as.wd : 0.0f;
+    const float lam = pc.c.decay ? gs.lam : 0.0f;
     uint32_t maxbits = 0;
-    for (int q0 = pc.q_lo + threadIdx.x; q0 < nvec; q0 += kBlockThreads * kUnroll) {
+    for (int q0 = threadIdx.x; q0 < pc.nq; q0 += kBlockThreads * kUnroll) {
         f4 xv[kUnroll], mv[kUnroll], acc[kUnroll];
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = q0 + k * kBlockThreads;
-            if (q < nvec) {
+            if (q < pc.nq) {
                 xv[k] = ntload(xp + q);
                 mv[k] = ntload(mp + q);
             }
@@ -691,8 +707,8 @@ __global__ __launch_bounds__(kBlockThreads) void k_round_end(
 #pragma unroll 2
 #endif
         for (int i = 0; i < (N > 0 ? N : n); ++i) {
-            const int64_t wo = i * stride + c.off;
-            const f4* __restrict__ xs = reinterpret_cast<const f4*>(x_src + i * src_stride + c.off);
+            const int64_t wo = i * stride + pc.e0;
+            const f4* xs = reinterpret_cast<const f4*>(x_src + rep_index(sl, i, pc.e0));
             const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + wo);
             f4* __restrict__ s1p = reinterpret_cast<f4*>(s1 + wo);
             f4* __restrict__ s2p = reinterpret_cast<f4*>(s2 + wo);
@@ -700,7 +716,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_round_end(
 #pragma unroll
             for (int k = 0; k < kUnroll; ++k) {
                 const int q = q0 + k * kBlockThreads;
-                if (q < nvec) {
+                if (q < pc.nq) {
                     xi[k] = ntload(xs + q);
                     gi[k] = ntload(gp + q);
                     mi[k] = ntload(s1p + q);
@@ -710,14 +726,15 @@ __global__ __launch_bounds__(kBlockThreads) void k_round_end(
 #pragma unroll
             for (int k = 0; k < kUnroll; ++k) {
                 const int q = q0 + k * kBlockThreads;
-                if (q < nvec) {
+                if (q < pc.nq) {
+                    const int valid = pc.valid0 - 4 * q;
                     if (BASE == kBaseAdamW) {
                         adamw4(xi[k], gi[k], mi[k], vi[k], lam_local, as);
-                        store_group(vi[k], s2p, q, nfull, c.len);
+                        store_vec(vi[k], s2p + q, valid);
                     } else {
                         sgdm4(xi[k], gi[k], mi[k], ss);
                     }
-                    store_group(mi[k], s1p, q, nfull, c.len);
+                    store_vec(mi[k], s1p + q, valid);
                     const f4 d = xv[k] - xi[k];
                     acc[k] = (i == 0) ? d : acc[k] + d;
                 }
@@ -726,17 +743,17 @@ __global__ __launch_bounds__(kBlockThreads) void k_round_end(
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) {
             const int q = q0 + k * kBlockThreads;
-            if (q < nvec) {
+            if (q < pc.nq) {
+                const int valid = pc.valid0 - 4 * q;
                 f4 delta;
                 if (N > 0 || gs.n_pow2)
                     delta = acc[k] * gs.inv_n;
                 else
                     delta = acc[k] / gs.n_f;
                 const f4 u = momentum4(mv[k], delta, gs);
-                store_group(mv[k], mp, q, nfull, c.len);
+                store_vec(mv[k], mp + q, valid);
                 if (KIND == 2) {
-                    store_group(u, reinterpret_cast<f4*>(u_out + c.off), q, nfull, c.len);
-                    const int valid = c.len - 4 * q;
+                    store_vec(u, reinterpret_cast<f4*>(u_out + pc.e0) + q, valid);
                     uint32_t b = __float_as_uint(fabsf(u.x));
                     if (valid > 1) b = max(b, __float_as_uint(fabsf(u.y)));
                     if (valid > 2) b = max(b, __float_as_uint(fabsf(u.z)));
@@ -744,11 +761,12 @@ __global__ __launch_bounds__(kBlockThreads) void k_round_end(
                     maxbits = max(maxbits, b);
                 } else {
                     const f4 xn = model4(xv[k], sign4(u), lam, gs);
-                    store_group(xn, xp, q, nfull, c.len);
+                    store_vec(xn, xp + q, valid);
                     if (KIND == 1) {
                         for (int i = 0; i < n; ++i)
-                            store_group(xn, reinterpret_cast<f4*>(x_rep + i * stride + c.off), q,
-                                        nfull, c.len);
+                            store_vec(xn,
+                                      reinterpret_cast<f4*>(x_rep + rep_index(rl, i, pc.e0)) + q,
+                                      valid);
                     }
                 }
             }
@@ -762,40 +780,35 @@ __global__ __launch_bounds__(kBlockThreads) void k_round_end(
 // Synchronisation step: x_rep[i] <- x for every replica.
 __global__ __launch_bounds__(kBlockThreads) void k_broadcast(
     const Chunk* __restrict__ chunks, const float* __restrict__ x, float* __restrict__ x_rep,
-    int64_t stride, int n) {
+    RepLayout rl, int n) {
     const Piece pc = piece_of(chunks);
-    const Chunk& c = pc.c;
-    const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + c.off);
-    float* __restrict__ rbase = x_rep + c.off;
-    const int nvec = pc.q_hi;
-    const int nfull = pc.nfull;
-    for (int q = pc.q_lo + threadIdx.x; q < nvec; q += kBlockThreads) {
+    const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + pc.e0);
+    for (int q = threadIdx.x; q < pc.nq; q += kBlockThreads) {
         const f4 v = ntload(xp + q);
+        const int valid = pc.valid0 - 4 * q;
         for (int i = 0; i < n; ++i)
-            store_group(v, reinterpret_cast<f4*>(rbase + i * stride), q, nfull, c.len);
+            store_vec(v, reinterpret_cast<f4*>(x_rep + rep_index(rl, i, pc.e0)) + q, valid);
     }
 }
 
 // Algorithm 1 initialisation: m = 0, replicas = x, base state = 0.
 __global__ __launch_bounds__(kBlockThreads) void k_init(
     const Chunk* __restrict__ chunks, const float* __restrict__ x, float* __restrict__ m,
-    float* __restrict__ v, float* __restrict__ x_rep, float* __restrict__ s1,
+    float* __restrict__ v, float* __restrict__ x_rep, RepLayout rl, float* __restrict__ s1,
     float* __restrict__ s2, int64_t stride, int n) {
     const Piece pc = piece_of(chunks);
-    const Chunk& c = pc.c;
-    const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + c.off);
-    const int nvec = pc.q_hi;
-    const int nfull = pc.nfull;
+    const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + pc.e0);
     const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
-    for (int q = pc.q_lo + threadIdx.x; q < nvec; q += kBlockThreads) {
+    for (int q = threadIdx.x; q < pc.nq; q += kBlockThreads) {
         const f4 xv = ntload(xp + q);
-        store_group(zero, reinterpret_cast<f4*>(m + c.off), q, nfull, c.len);
-        if (v != nullptr) store_group(zero, reinterpret_cast<f4*>(v + c.off), q, nfull, c.len);
+        const int valid = pc.valid0 - 4 * q;
+        store_vec(zero, reinterpret_cast<f4*>(m + pc.e0) + q, valid);
+        if (v != nullptr) store_vec(zero, reinterpret_cast<f4*>(v + pc.e0) + q, valid);
         for (int i = 0; i < n; ++i) {
-            const int64_t o = i * stride + c.off;
-            store_group(xv, reinterpret_cast<f4*>(x_rep + o), q, nfull, c.len);
-            store_group(zero, reinterpret_cast<f4*>(s1 + o), q, nfull, c.len);
-            if (s2 != nullptr) store_group(zero, reinterpret_cast<f4*>(s2 + o), q, nfull, c.len);
+            const int64_t o = i * stride + pc.e0;
+            store_vec(xv, reinterpret_cast<f4*>(x_rep + rep_index(rl, i, pc.e0)) + q, valid);
+            store_vec(zero, reinterpret_cast<f4*>(s1 + o) + q, valid);
+            if (s2 != nullptr) store_vec(zero, reinterpret_cast<f4*>(s2 + o) + q, valid);
         }
     }
 }
@@ -823,30 +836,31 @@ dim3 chunk_grid(int64_t n_chunks, int n_workers) {
 // ---------------------------------------------------------------- launchers
 
 hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float* m, float* v,
-                       float* x_rep, float* s1, float* s2, int64_t stride, int n, hipStream_t st) {
+                       float* x_rep, RepLayout rl, float* s1, float* s2, int64_t stride, int n,
+                       hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_init, chunk_grid(n_chunks, 1), dim3(kBlockThreads), 0, st, chunks, x, m,
-                       v, x_rep, s1, s2, stride, n);
+                       v, x_rep, rl, s1, s2, stride, n);
     return hipGetLastError();
 }
 
-hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_rep,
-                              const float* x_src, int64_t src_stride, const float* g_rep,
-                              float* s1, float* s2, int64_t stride, int worker0, int n_workers,
+hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_rep, RepLayout rl,
+                              const float* x_src, RepLayout sl, const float* g_rep, float* s1,
+                              float* s2, int64_t stride, int worker0, int n_workers,
                               const AdamScalars& sc, hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_local_adamw, chunk_grid(n_chunks, n_workers), dim3(kBlockThreads), 0, st,
-                       chunks, x_rep, x_src, src_stride, g_rep, s1, s2, stride, worker0, sc);
+                       chunks, x_rep, rl, x_src, sl, g_rep, s1, s2, stride, worker0, sc);
     return hipGetLastError();
 }
 
-hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep,
-                             const float* x_src, int64_t src_stride, const float* g_rep,
-                             float* s1, int64_t stride, int worker0, int n_workers,
-                             const SgdScalars& sc, hipStream_t st) {
+hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep, RepLayout rl,
+                             const float* x_src, RepLayout sl, const float* g_rep, float* s1,
+                             int64_t stride, int worker0, int n_workers, const SgdScalars& sc,
+                             hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_local_sgdm, chunk_grid(n_chunks, n_workers), dim3(kBlockThreads), 0, st,
-                       chunks, x_rep, x_src, src_stride, g_rep, s1, stride, worker0, sc);
+                       chunks, x_rep, rl, x_src, sl, g_rep, s1, stride, worker0, sc);
     return hipGetLastError();
 }
 
@@ -856,7 +870,7 @@ static void launch_round_end_n(const Chunk* chunks, int64_t n_chunks, const Roun
     const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
 #define DSM_ROUND_END(NW)                                                                        \
     hipLaunchKernelGGL((k_round_end<NW, BASE, KIND>), grid, block, 0, st, chunks, a.x, a.m,      \
-                       a.x_rep, a.x_src, a.src_stride, a.g_rep, a.s1, a.s2, a.u, a.bound.piece_max, \
+                       a.x_rep, a.rl, a.x_src, a.sl, a.g_rep, a.s1, a.s2, a.u, a.bound.piece_max, \
                        a.stride, a.as, a.ss, a.gs)
     switch (a.gs.n) {
         case 1: DSM_ROUND_END(1); break;
@@ -881,13 +895,13 @@ static void launch_round_end_base(const Chunk* chunks, int64_t n_chunks, const R
 
 template <int BASE>
 static void launch_local_from_x_n(const Chunk* chunks, int64_t n_chunks, const float* x,
-                                  float* x_rep, const float* g_rep, float* s1, float* s2,
-                                  int64_t stride, int n, const AdamScalars& as,
+                                  float* x_rep, RepLayout rl, const float* g_rep, float* s1,
+                                  float* s2, int64_t stride, int n, const AdamScalars& as,
                                   const SgdScalars& ss, hipStream_t st) {
     const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
 #define DSM_LOCAL_FROM_X(NW)                                                                   \
-    hipLaunchKernelGGL((k_local_from_x<NW, BASE>), grid, block, 0, st, chunks, x, x_rep, g_rep, \
-                       s1, s2, stride, n, as, ss)
+    hipLaunchKernelGGL((k_local_from_x<NW, BASE>), grid, block, 0, st, chunks, x, x_rep, rl,    \
+                       g_rep, s1, s2, stride, n, as, ss)
     switch (n) {
         case 1: DSM_LOCAL_FROM_X(1); break;
         case 2: DSM_LOCAL_FROM_X(2); break;
@@ -899,15 +913,15 @@ static void launch_local_from_x_n(const Chunk* chunks, int64_t n_chunks, const f
 }
 
 hipError_t launch_local_from_x(const Chunk* chunks, int64_t n_chunks, const float* x,
-                               float* x_rep, const float* g_rep, float* s1, float* s2,
-                               int64_t stride, int n, bool adamw, const AdamScalars& as,
-                               const SgdScalars& ss, hipStream_t st) {
+                               float* x_rep, RepLayout rl, const float* g_rep, float* s1,
+                               float* s2, int64_t stride, int n, bool adamw,
+                               const AdamScalars& as, const SgdScalars& ss, hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
     if (adamw)
-        launch_local_from_x_n<kBaseAdamW>(chunks, n_chunks, x, x_rep, g_rep, s1, s2, stride, n,
-                                          as, ss, st);
+        launch_local_from_x_n<kBaseAdamW>(chunks, n_chunks, x, x_rep, rl, g_rep, s1, s2, stride,
+                                          n, as, ss, st);
     else
-        launch_local_from_x_n<kBaseSgd>(chunks, n_chunks, x, x_rep, g_rep, s1, s2, stride, n,
+        launch_local_from_x_n<kBaseSgd>(chunks, n_chunks, x, x_rep, rl, g_rep, s1, s2, stride, n,
                                         as, ss, st);
     return hipGetLastError();
 }
@@ -920,20 +934,17 @@ static void launch_bound_reduce(const BoundWords& bw, int n_tensors, hipStream_t
 }
 
 static void launch_rand_pass2(const Chunk* chunks, int64_t n_chunks, float* x, float* x_rep,
-                              const float* u, const uint32_t* bits, int64_t stride,
+                              RepLayout rl, const float* u, const uint32_t* bits,
                               const GlobalScalars& sc, bool broadcast, hipStream_t st) {
     const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
+#define DSM_PASS2(MODE, B) \
+    hipLaunchKernelGGL((k_global_rand_pass2<MODE, B>), grid, block, 0, st, chunks, x, x_rep, rl, u, bits, sc)
     if (sc.mode == 1) {
-        if (broadcast)
-            hipLaunchKernelGGL((k_global_rand_pass2<1, true>), grid, block, 0, st, chunks, x, x_rep, u, bits, stride, sc);
-        else
-            hipLaunchKernelGGL((k_global_rand_pass2<1, false>), grid, block, 0, st, chunks, x, x_rep, u, bits, stride, sc);
+        if (broadcast) DSM_PASS2(1, true); else DSM_PASS2(1, false);
     } else {
-        if (broadcast)
-            hipLaunchKernelGGL((k_global_rand_pass2<2, true>), grid, block, 0, st, chunks, x, x_rep, u, bits, stride, sc);
-        else
-            hipLaunchKernelGGL((k_global_rand_pass2<2, false>), grid, block, 0, st, chunks, x, x_rep, u, bits, stride, sc);
+        if (broadcast) DSM_PASS2(2, true); else DSM_PASS2(2, false);
     }
+#undef DSM_PASS2
 }
 
 hipError_t launch_round_end(const Chunk* chunks, int64_t n_chunks, int n_tensors, bool adamw,
@@ -948,19 +959,19 @@ hipError_t launch_round_end(const Chunk* chunks, int64_t n_chunks, int n_tensors
     }
     if (randomized && n_tensors > 0) launch_bound_reduce(a.bound, n_tensors, st);
     if (randomized && n_chunks > 0)
-        launch_rand_pass2(chunks, n_chunks, a.x, a.x_rep, a.u, a.bound.bits, a.stride, a.gs,
+        launch_rand_pass2(chunks, n_chunks, a.x, a.x_rep, a.rl, a.u, a.bound.bits, a.gs,
                           broadcast, st);
     return hipGetLastError();
 }
 
 template <int RULE, bool BCAST>
 static void launch_global_det_n(const Chunk* chunks, int64_t n_chunks, float* x, float* m,
-                                float* v, float* x_rep, int64_t stride, const GlobalScalars& sc,
+                                float* v, float* x_rep, RepLayout rl, const GlobalScalars& sc,
                                 hipStream_t st) {
     const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
 #define DSM_GLOBAL_DET(NW)                                                                     \
     hipLaunchKernelGGL((k_global_det<NW, RULE, BCAST>), grid, block, 0, st, chunks, x, m, v,   \
-                       x_rep, stride, sc)
+                       x_rep, rl, sc)
     switch (sc.n) {
         case 1: DSM_GLOBAL_DET(1); break;
         case 2: DSM_GLOBAL_DET(2); break;
@@ -973,64 +984,67 @@ static void launch_global_det_n(const Chunk* chunks, int64_t n_chunks, float* x,
 
 template <int RULE>
 static void launch_global_det_rule(const Chunk* chunks, int64_t n_chunks, float* x, float* m,
-                                   float* v, float* x_rep, int64_t stride,
-                                   const GlobalScalars& sc, bool broadcast, hipStream_t st) {
+                                   float* v, float* x_rep, RepLayout rl, const GlobalScalars& sc,
+                                   bool broadcast, hipStream_t st) {
     if (broadcast)
-        launch_global_det_n<RULE, true>(chunks, n_chunks, x, m, v, x_rep, stride, sc, st);
+        launch_global_det_n<RULE, true>(chunks, n_chunks, x, m, v, x_rep, rl, sc, st);
     else
-        launch_global_det_n<RULE, false>(chunks, n_chunks, x, m, v, x_rep, stride, sc, st);
+        launch_global_det_n<RULE, false>(chunks, n_chunks, x, m, v, x_rep, rl, sc, st);
 }
 
 hipError_t launch_global_det(const Chunk* chunks, int64_t n_chunks, float* x, float* m,
-                             float* v, float* x_rep, int64_t stride, const GlobalScalars& sc,
+                             float* v, float* x_rep, RepLayout rl, const GlobalScalars& sc,
                              bool broadcast, hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
     switch (sc.rule) {
         case kRuleLookahead:
-            launch_global_det_rule<kRuleLookahead>(chunks, n_chunks, x, m, v, x_rep, stride, sc,
+            launch_global_det_rule<kRuleLookahead>(chunks, n_chunks, x, m, v, x_rep, rl, sc,
                                                    broadcast, st);
             break;
         case kRuleSignedSlowMo:
-            launch_global_det_rule<kRuleSignedSlowMo>(chunks, n_chunks, x, m, v, x_rep, stride,
-                                                      sc, broadcast, st);
+            launch_global_det_rule<kRuleSignedSlowMo>(chunks, n_chunks, x, m, v, x_rep, rl, sc,
+                                                      broadcast, st);
             break;
         case kRuleGlobalAdamW:
-            launch_global_det_rule<kRuleGlobalAdamW>(chunks, n_chunks, x, m, v, x_rep, stride, sc,
+            launch_global_det_rule<kRuleGlobalAdamW>(chunks, n_chunks, x, m, v, x_rep, rl, sc,
                                                      broadcast, st);
             break;
         default:
-            launch_global_det_rule<kRuleSignMomentum>(chunks, n_chunks, x, m, v, x_rep, stride,
-                                                      sc, broadcast, st);
+            launch_global_det_rule<kRuleSignMomentum>(chunks, n_chunks, x, m, v, x_rep, rl, sc,
+                                                      broadcast, st);
             break;
     }
     return hipGetLastError();
 }
 
 hipError_t launch_global_rand(const Chunk* chunks, int64_t n_chunks, int n_tensors, float* x,
-                              float* m, float* x_rep, float* u, const BoundWords& bw,
-                              int64_t stride, const GlobalScalars& sc, bool broadcast,
+                              float* m, float* x_rep, RepLayout rl, float* u,
+                              const BoundWords& bw, const GlobalScalars& sc, bool broadcast,
                               hipStream_t st) {
     if (n_chunks > 0) {
         const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
         uint32_t* pm = bw.piece_max;
+#define DSM_PASS1(NW) \
+    hipLaunchKernelGGL(k_global_rand_pass1<NW>, grid, block, 0, st, chunks, x, m, x_rep, rl, u, pm, sc)
         switch (sc.n) {
-            case 1: hipLaunchKernelGGL(k_global_rand_pass1<1>, grid, block, 0, st, chunks, x, m, x_rep, u, pm, stride, sc); break;
-            case 2: hipLaunchKernelGGL(k_global_rand_pass1<2>, grid, block, 0, st, chunks, x, m, x_rep, u, pm, stride, sc); break;
-            case 4: hipLaunchKernelGGL(k_global_rand_pass1<4>, grid, block, 0, st, chunks, x, m, x_rep, u, pm, stride, sc); break;
-            case 8: hipLaunchKernelGGL(k_global_rand_pass1<8>, grid, block, 0, st, chunks, x, m, x_rep, u, pm, stride, sc); break;
-            default: hipLaunchKernelGGL(k_global_rand_pass1<0>, grid, block, 0, st, chunks, x, m, x_rep, u, pm, stride, sc); break;
+            case 1: DSM_PASS1(1); break;
+            case 2: DSM_PASS1(2); break;
+            case 4: DSM_PASS1(4); break;
+            case 8: DSM_PASS1(8); break;
+            default: DSM_PASS1(0); break;
         }
+#undef DSM_PASS1
     }
     if (n_tensors > 0) launch_bound_reduce(bw, n_tensors, st);
-    if (n_chunks > 0) launch_rand_pass2(chunks, n_chunks, x, x_rep, u, bw.bits, stride, sc, broadcast, st);
+    if (n_chunks > 0) launch_rand_pass2(chunks, n_chunks, x, x_rep, rl, u, bw.bits, sc, broadcast, st);
     return hipGetLastError();
 }
 
 hipError_t launch_broadcast(const Chunk* chunks, int64_t n_chunks, const float* x, float* x_rep,
-                            int64_t stride, int n, hipStream_t st) {
+                            RepLayout rl, int n, hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_broadcast, chunk_grid(n_chunks, 1), dim3(kBlockThreads), 0, st, chunks, x,
-                       x_rep, stride, n);
+                       x_rep, rl, n);
     return hipGetLastError();
 }
 

@@ -20,6 +20,7 @@ struct dsm_ctx {
     std::vector<uint8_t> decay;
     int64_t arena_elems = 0;
     std::vector<dsm::Chunk> chunks;  // host copy; the device copy lives in the workspace
+    dsm::RepLayout rep{};            // how x_rep holds the n replicas
     std::vector<int32_t> chunk0;     // first chunk of each tensor, then n_chunks (host copy)
     dsm_buffers buf{};
     dsm::Chunk* d_chunks = nullptr;
@@ -84,6 +85,8 @@ dsm_status check_problem(const dsm_problem* p) {
         return fail(nullptr, DSM_ERR_INVALID_ARG, "n_tensors must be >= 0, got %d", p->n_tensors);
     if (p->base != DSM_BASE_ADAMW && p->base != DSM_BASE_SGD_MOMENTUM)
         return fail(nullptr, DSM_ERR_INVALID_ARG, "unknown base optimizer %d", p->base);
+    if (p->replica_layout != DSM_REPLICAS_CONTIGUOUS && p->replica_layout != DSM_REPLICAS_BLOCKED)
+        return fail(nullptr, DSM_ERR_INVALID_ARG, "unknown replica layout %d", p->replica_layout);
     if (p->n_tensors > 0 && !p->numel)
         return fail(nullptr, DSM_ERR_INVALID_ARG, "numel is NULL");
     for (int i = 0; i < p->n_tensors; ++i) {
@@ -94,21 +97,25 @@ dsm_status check_problem(const dsm_problem* p) {
     return DSM_OK;
 }
 
-// Tensors back to back, each starting at a multiple of 64 elements.  The
-// workspace holds, each part at a 256-byte boundary: the chunk table
+// Tensors back to back, each starting at a multiple of 64 elements (of the
+// blocked alignment, with the arena a whole number of 64 KiB blocks, when the
+// replicas are blocked).  The workspace holds, each part at a 256-byte boundary: the chunk table
 // (kChunkElems elements per chunk, never crossing a tensor); the per-tensor
 // bound words; the first chunk of each tensor (n_tensors + 1 words); and one
 // piece-maximum word per work-group piece (n_chunks * kSplit), level one of
 // the bound.
 dsm_status make_layout(const dsm_problem* p, Layout* L, std::vector<dsm::Chunk>* chunks,
                        std::vector<int32_t>* chunk0 = nullptr) {
+    const bool blocked = p->replica_layout == DSM_REPLICAS_BLOCKED;
+    const int64_t align = blocked ? dsm::kBlockedTensorAlign : dsm::kTensorAlign;
     L->offsets.resize(p->n_tensors);
     int64_t off = 0, n_chunks = 0;
     for (int i = 0; i < p->n_tensors; ++i) {
         L->offsets[i] = off;
-        off += round_up(p->numel[i], dsm::kTensorAlign);
+        off += round_up(p->numel[i], align);
         n_chunks += (p->numel[i] + dsm::kChunkElems - 1) / dsm::kChunkElems;
     }
+    if (blocked) off = round_up(off, dsm::kRepBlockElems);
     if (n_chunks > kMaxChunks)
         return fail(nullptr, DSM_ERR_UNSUPPORTED, "problem needs %lld chunks, limit %lld",
                     static_cast<long long>(n_chunks), static_cast<long long>(kMaxChunks));
@@ -273,14 +280,14 @@ dsm_status global_coefs(dsm_ctx* ctx, int64_t t, const dsm_global_hparams* hp,
     return DSM_OK;
 }
 
-hipError_t launch_local(dsm_ctx* ctx, const LocalCoefs& lc, const float* src, int64_t src_stride,
+hipError_t launch_local(dsm_ctx* ctx, const LocalCoefs& lc, const float* src, dsm::RepLayout sl,
                         int w0, int nw) {
     const int64_t n_chunks = static_cast<int64_t>(ctx->chunks.size());
     if (ctx->base == DSM_BASE_ADAMW)
-        return dsm::launch_local_adamw(ctx->d_chunks, n_chunks, ctx->buf.x_rep, src, src_stride,
+        return dsm::launch_local_adamw(ctx->d_chunks, n_chunks, ctx->buf.x_rep, ctx->rep, src, sl,
                                        ctx->buf.g_rep, ctx->buf.s1_rep, ctx->buf.s2_rep,
                                        ctx->arena_elems, w0, nw, lc.adam, ctx->stream);
-    return dsm::launch_local_sgdm(ctx->d_chunks, n_chunks, ctx->buf.x_rep, src, src_stride,
+    return dsm::launch_local_sgdm(ctx->d_chunks, n_chunks, ctx->buf.x_rep, ctx->rep, src, sl,
                                   ctx->buf.g_rep, ctx->buf.s1_rep, ctx->arena_elems, w0, nw, lc.sgd,
                                   ctx->stream);
 }
@@ -365,6 +372,9 @@ dsm_status dsm_init(const dsm_problem* problem, const dsm_buffers* b, dsm_ctx** 
         ctx->decay[i] = problem->decay ? (problem->decay[i] ? 1 : 0) : 1;
     ctx->offsets = L.offsets;
     ctx->arena_elems = L.arena_elems;
+    ctx->rep = problem->replica_layout == DSM_REPLICAS_BLOCKED
+                   ? dsm::blocked_copies(problem->n_workers)
+                   : dsm::contiguous_copies(L.arena_elems);
     ctx->chunks = std::move(chunks);
     ctx->chunk0 = std::move(chunk0);
     ctx->buf = *b;
@@ -397,8 +407,8 @@ dsm_status dsm_init(const dsm_problem* problem, const dsm_buffers* b, dsm_ctx** 
             return r;
         }
         e = dsm::launch_init(ctx->d_chunks, static_cast<int64_t>(ctx->chunks.size()), b->x, b->m,
-                             b->v, b->x_rep, b->s1_rep, adamw ? b->s2_rep : nullptr, ctx->arena_elems,
-                             ctx->n, ctx->stream);
+                             b->v, b->x_rep, ctx->rep, b->s1_rep, adamw ? b->s2_rep : nullptr,
+                             ctx->arena_elems, ctx->n, ctx->stream);
         if (e != hipSuccess) {
             dsm_status r = hip_fail(nullptr, "launching the initialisation kernel", e);
             delete ctx;
@@ -435,7 +445,7 @@ dsm_status dsm_local_step(dsm_ctx* ctx, int32_t worker, int64_t step, const dsm_
     if (all_stale) {
         hipError_t e = dsm::launch_local_from_x(
             ctx->d_chunks, static_cast<int64_t>(ctx->chunks.size()), ctx->buf.x, ctx->buf.x_rep,
-            ctx->buf.g_rep, ctx->buf.s1_rep, ctx->buf.s2_rep, ctx->arena_elems, ctx->n,
+            ctx->rep, ctx->buf.g_rep, ctx->buf.s1_rep, ctx->buf.s2_rep, ctx->arena_elems, ctx->n,
             ctx->base == DSM_BASE_ADAMW, lc.adam, lc.sgd, ctx->stream);
         if (e != hipSuccess) return hip_fail(ctx, "launching the local step", e);
     }
@@ -444,8 +454,8 @@ dsm_status dsm_local_step(dsm_ctx* ctx, int32_t worker, int64_t step, const dsm_
         while (b < w0 + nw && ctx->stale[b] == ctx->stale[a]) ++b;
         const bool from_x = ctx->stale[a] != 0;
         const float* src = from_x ? ctx->buf.x : ctx->buf.x_rep;
-        const int64_t src_stride = from_x ? 0 : ctx->arena_elems;
-        hipError_t e = launch_local(ctx, lc, src, src_stride, a, b - a);
+        const dsm::RepLayout sl = from_x ? dsm::single_copy() : ctx->rep;
+        hipError_t e = launch_local(ctx, lc, src, sl, a, b - a);
         if (e != hipSuccess) return hip_fail(ctx, "launching the local step", e);
         a = b;
     }
@@ -473,12 +483,11 @@ dsm_status dsm_global_step(dsm_ctx* ctx, int64_t t, const dsm_global_hparams* hp
     hipError_t e;
     if (!randomized) {
         e = dsm::launch_global_det(ctx->d_chunks, n_chunks, ctx->buf.x, ctx->buf.m, ctx->buf.v,
-                                   ctx->buf.x_rep, ctx->arena_elems, sc, broadcast != 0,
-                                   ctx->stream);
+                                   ctx->buf.x_rep, ctx->rep, sc, broadcast != 0, ctx->stream);
     } else {
         e = dsm::launch_global_rand(ctx->d_chunks, n_chunks, ctx->n_tensors, ctx->buf.x, ctx->buf.m,
-                                    ctx->buf.x_rep, ctx->buf.u_scratch, ctx->bound,
-                                    ctx->arena_elems, sc, broadcast != 0, ctx->stream);
+                                    ctx->buf.x_rep, ctx->rep, ctx->buf.u_scratch, ctx->bound, sc,
+                                    broadcast != 0, ctx->stream);
     }
     if (e != hipSuccess) return hip_fail(ctx, "launching the global step", e);
     end_round(ctx, broadcast != 0, randomized);
@@ -513,8 +522,9 @@ dsm_status dsm_round_end(dsm_ctx* ctx, int64_t step, const dsm_local_hparams* lo
     a.x = ctx->buf.x;
     a.m = ctx->buf.m;
     a.x_rep = ctx->buf.x_rep;
+    a.rl = ctx->rep;
     a.x_src = from_x ? ctx->buf.x : ctx->buf.x_rep;
-    a.src_stride = from_x ? 0 : ctx->arena_elems;
+    a.sl = from_x ? dsm::single_copy() : ctx->rep;
     a.g_rep = ctx->buf.g_rep;
     a.s1 = ctx->buf.s1_rep;
     a.s2 = ctx->buf.s2_rep;
@@ -537,7 +547,7 @@ dsm_status dsm_sync(dsm_ctx* ctx) {
     dsm_status st = check_ctx(ctx);
     if (st != DSM_OK) return st;
     hipError_t e = dsm::launch_broadcast(ctx->d_chunks, static_cast<int64_t>(ctx->chunks.size()),
-                                         ctx->buf.x, ctx->buf.x_rep, ctx->arena_elems, ctx->n,
+                                         ctx->buf.x, ctx->buf.x_rep, ctx->rep, ctx->n,
                                          ctx->stream);
     if (e != hipSuccess) return hip_fail(ctx, "launching the synchronisation", e);
     for (int i = 0; i < ctx->n; ++i) {

@@ -33,6 +33,10 @@ DSM_RULE_LOOKAHEAD = 1
 DSM_RULE_SIGNED_SLOWMO = 2
 DSM_RULE_GLOBAL_ADAMW = 3
 
+DSM_REPLICAS_CONTIGUOUS = 0
+DSM_REPLICAS_BLOCKED = 1
+DSM_REPLICA_BLOCK_ELEMS = 16384
+
 EXPORTED = ("dsm_layout", "dsm_init", "dsm_local_step", "dsm_global_step", "dsm_round_end",
             "dsm_sync",
             "dsm_read_bounds", "dsm_test_philox", "dsm_destroy", "dsm_last_error")
@@ -49,7 +53,8 @@ class dsm_problem(ctypes.Structure):
     _fields_ = [("n_workers", ctypes.c_int32), ("local_steps", ctypes.c_int32),
                 ("n_tensors", ctypes.c_int32), ("base", ctypes.c_int32),
                 ("numel", ctypes.POINTER(ctypes.c_int64)),
-                ("decay", ctypes.POINTER(ctypes.c_uint8))]
+                ("decay", ctypes.POINTER(ctypes.c_uint8)),
+                ("replica_layout", ctypes.c_int32)]
 
 
 class dsm_buffers(ctypes.Structure):
@@ -119,12 +124,14 @@ def _check(status, ctx=None):
         raise DsmError(status, dsm_last_error(ctx))
 
 
-def make_problem(numel, n_workers, local_steps, base, decay=None):
+def make_problem(numel, n_workers, local_steps, base, decay=None,
+                 replica_layout=DSM_REPLICAS_CONTIGUOUS):
     """A dsm_problem plus the host arrays it points to (kept alive with it)."""
     numel = np.ascontiguousarray(np.asarray(numel, dtype=np.int64))
     keep = [numel]
     prob = dsm_problem(n_workers, local_steps, len(numel), base,
-                       numel.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), None)
+                       numel.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), None,
+                       replica_layout)
     if decay is not None:
         dec = np.ascontiguousarray(np.asarray(decay, dtype=np.uint8))
         keep.append(dec)

@@ -48,7 +48,7 @@ int main(void) {
     const int64_t numel[3] = {5, 1000, 16385};
     const uint8_t decay[3] = {0, 1, 1};
     const int n = 3, H = 2;
-    dsm_problem prob = {n, H, 3, DSM_BASE_ADAMW, numel, decay};
+    dsm_problem prob = {n, H, 3, DSM_BASE_ADAMW, numel, decay, DSM_REPLICAS_CONTIGUOUS};
     int64_t arena = 0, offs[3], ws = 0;
     DSM_OK_(dsm_layout(&prob, &arena, offs, &ws));
 

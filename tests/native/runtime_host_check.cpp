@@ -10,10 +10,12 @@
 //   * the chunk table dsm_init uploads (every element once, no chunk across a
 //     tensor, decay flags);
 //   * the state machine of Algorithm 1 and which source each local step reads
-//     (the replica, or x after a global step without broadcast);
+//     (the replica, or x after a global step without broadcast), with the
+//     replica addressing of both replica layouts;
 //   * the fp32 coefficients formed on the host, against long double;
 //   * error paths: no device, failed launches, bad hyperparameters, NULLs.
 // Prints "all checks passed" and exits 0, or lists the failures and exits 1.
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstdio>
@@ -51,7 +53,8 @@ struct Launch {
     const float* x = nullptr;
     const float* x_rep = nullptr;
     const float* x_src = nullptr;
-    int64_t src_stride = -1;
+    dsm::RepLayout rl{-1, -1, -1, 0};  // how the launch addresses x_rep
+    dsm::RepLayout sl{-1, -1, -1, 0};  // how it addresses its step's source
     const float* s2 = nullptr;
     const float* u = nullptr;
     const float* v = nullptr;
@@ -93,30 +96,33 @@ hipError_t hipStreamSynchronize(hipStream_t) { return hipSuccess; }
 
 namespace dsm {
 hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float*, float* v,
-                       float* x_rep, float*, float* s2, int64_t stride, int n, hipStream_t) {
+                       float* x_rep, RepLayout rl, float*, float* s2, int64_t stride, int n,
+                       hipStream_t) {
     Launch l;
     l.kind = "init";
     l.chunks = chunks;
     l.n_chunks = n_chunks;
     l.x = x;
     l.x_rep = x_rep;
+    l.rl = rl;
     l.v = v;
     l.s2 = s2;
     l.stride = stride;
     l.n_workers = n;
     return record(l);
 }
-hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_rep,
-                              const float* x_src, int64_t src_stride, const float*, float*,
-                              float* s2, int64_t stride, int worker0, int n_workers,
-                              const AdamScalars& sc, hipStream_t) {
+hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_rep, RepLayout rl,
+                              const float* x_src, RepLayout sl, const float*, float*, float* s2,
+                              int64_t stride, int worker0, int n_workers, const AdamScalars& sc,
+                              hipStream_t) {
     Launch l;
     l.kind = "local_adamw";
     l.chunks = chunks;
     l.n_chunks = n_chunks;
     l.x_rep = x_rep;
+    l.rl = rl;
     l.x_src = x_src;
-    l.src_stride = src_stride;
+    l.sl = sl;
     l.s2 = s2;
     l.stride = stride;
     l.worker0 = worker0;
@@ -124,8 +130,8 @@ hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_re
     l.as = sc;
     return record(l);
 }
-hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep,
-                             const float* x_src, int64_t src_stride, const float*, float*,
+hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep, RepLayout rl,
+                             const float* x_src, RepLayout sl, const float*, float*,
                              int64_t stride, int worker0, int n_workers, const SgdScalars& sc,
                              hipStream_t) {
     Launch l;
@@ -133,8 +139,9 @@ hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep
     l.chunks = chunks;
     l.n_chunks = n_chunks;
     l.x_rep = x_rep;
+    l.rl = rl;
     l.x_src = x_src;
-    l.src_stride = src_stride;
+    l.sl = sl;
     l.stride = stride;
     l.worker0 = worker0;
     l.n_workers = n_workers;
@@ -142,15 +149,16 @@ hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep
     return record(l);
 }
 hipError_t launch_local_from_x(const Chunk* chunks, int64_t n_chunks, const float* x,
-                               float* x_rep, const float*, float*, float* s2, int64_t stride,
-                               int n, bool adamw, const AdamScalars& as, const SgdScalars& ss,
-                               hipStream_t) {
+                               float* x_rep, RepLayout rl, const float*, float*, float* s2,
+                               int64_t stride, int n, bool adamw, const AdamScalars& as,
+                               const SgdScalars& ss, hipStream_t) {
     Launch l;
     l.kind = "local_from_x";
     l.chunks = chunks;
     l.n_chunks = n_chunks;
     l.x = x;
     l.x_rep = x_rep;
+    l.rl = rl;
     l.s2 = s2;
     l.stride = stride;
     l.n_workers = n;
@@ -169,8 +177,9 @@ hipError_t launch_round_end(const Chunk* chunks, int64_t n_chunks, int n_tensors
     l.adamw = adamw;
     l.x = a.x;
     l.x_rep = a.x_rep;
+    l.rl = a.rl;
     l.x_src = a.x_src;
-    l.src_stride = a.src_stride;
+    l.sl = a.sl;
     l.s2 = a.s2;
     l.u = a.u;
     l.bounds = a.bound.bits;
@@ -184,7 +193,7 @@ hipError_t launch_round_end(const Chunk* chunks, int64_t n_chunks, int n_tensors
     return record(l);
 }
 hipError_t launch_global_det(const Chunk* chunks, int64_t n_chunks, float* x, float*, float* v,
-                             float* x_rep, int64_t stride, const GlobalScalars& sc, bool broadcast,
+                             float* x_rep, RepLayout rl, const GlobalScalars& sc, bool broadcast,
                              hipStream_t) {
     Launch l;
     l.kind = "global_det";
@@ -193,14 +202,14 @@ hipError_t launch_global_det(const Chunk* chunks, int64_t n_chunks, float* x, fl
     l.x = x;
     l.v = v;
     l.x_rep = x_rep;
-    l.stride = stride;
+    l.rl = rl;
     l.gs = sc;
     l.broadcast = broadcast;
     return record(l);
 }
 hipError_t launch_global_rand(const Chunk* chunks, int64_t n_chunks, int n_tensors, float* x,
-                              float*, float* x_rep, float* u, const BoundWords& bw,
-                              int64_t stride, const GlobalScalars& sc, bool broadcast, hipStream_t) {
+                              float*, float* x_rep, RepLayout rl, float* u, const BoundWords& bw,
+                              const GlobalScalars& sc, bool broadcast, hipStream_t) {
     Launch l;
     l.kind = "global_rand";
     l.chunks = chunks;
@@ -208,24 +217,24 @@ hipError_t launch_global_rand(const Chunk* chunks, int64_t n_chunks, int n_tenso
     l.n_tensors = n_tensors;
     l.x = x;
     l.x_rep = x_rep;
+    l.rl = rl;
     l.u = u;
     l.bounds = bw.bits;
     l.piece_max = bw.piece_max;
     l.chunk0 = bw.chunk0;
-    l.stride = stride;
     l.gs = sc;
     l.broadcast = broadcast;
     return record(l);
 }
 hipError_t launch_broadcast(const Chunk* chunks, int64_t n_chunks, const float* x, float* x_rep,
-                            int64_t stride, int n, hipStream_t) {
+                            RepLayout rl, int n, hipStream_t) {
     Launch l;
     l.kind = "broadcast";
     l.chunks = chunks;
     l.n_chunks = n_chunks;
     l.x = x;
     l.x_rep = x_rep;
-    l.stride = stride;
+    l.rl = rl;
     l.n_workers = n;
     return record(l);
 }
@@ -244,11 +253,33 @@ namespace {
 
 int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
 
+bool same_layout(const dsm::RepLayout& a, const dsm::RepLayout& b) {
+    return a.block_stride == b.block_stride && a.copy_stride == b.copy_stride && a.shift == b.shift;
+}
+
+// The replica layout a launch must use, written out from dsm.h: contiguous
+// copies at i * d_pad, or 64 KiB blocks at ((e / 16384) * n + i) * 16384.
+dsm::RepLayout expected_layout(int replica_layout, int n, int64_t arena) {
+    if (replica_layout == DSM_REPLICAS_BLOCKED) return dsm::RepLayout{int64_t(n) * 16384, 16384, 14, 0};
+    return dsm::RepLayout{0, arena, 62, 0};
+}
+
+// The element index a RepLayout gives copy i of element e.
+int64_t rep_element(const dsm::RepLayout& L, int64_t i, int64_t e) {
+    const int64_t mask = (int64_t(1) << L.shift) - 1;
+    return (e >> L.shift) * L.block_stride + i * L.copy_stride + (e & mask);
+}
+
+int64_t tensor_align(int replica_layout) {
+    return replica_layout == DSM_REPLICAS_BLOCKED ? std::max<int64_t>(1024, dsm::kPieceElems) : 64;
+}
+
 struct Problem {
     std::vector<int64_t> numel;
     std::vector<uint8_t> decay;
     dsm_problem p{};
-    Problem(std::vector<int64_t> ne, int n, int H, int base, std::vector<uint8_t> dec = {})
+    Problem(std::vector<int64_t> ne, int n, int H, int base, std::vector<uint8_t> dec = {},
+            int layout = DSM_REPLICAS_CONTIGUOUS)
         : numel(std::move(ne)), decay(std::move(dec)) {
         p.n_workers = n;
         p.local_steps = H;
@@ -256,6 +287,7 @@ struct Problem {
         p.base = base;
         p.numel = numel.empty() ? nullptr : numel.data();
         p.decay = decay.empty() ? nullptr : decay.data();
+        p.replica_layout = layout;
     }
 };
 
@@ -264,6 +296,7 @@ struct Buffers {
     std::vector<void*> owned;
     dsm_buffers b{};
     int64_t arena = 0;
+    dsm::RepLayout rep{};  // the replica layout every launch must pass
     float* alloc(int64_t floats) {
         const size_t bytes = static_cast<size_t>(round_up(std::max<int64_t>(floats, 1) * 4, 256));
         void* p = std::aligned_alloc(256, bytes);
@@ -277,6 +310,7 @@ struct Buffers {
         dsm_status st = dsm_layout(&P.p, &arena, off.data(), &ws);
         CHECK(st == DSM_OK, "layout of a valid problem");
         const int n = P.p.n_workers;
+        rep = expected_layout(P.p.replica_layout, n, arena);
         b.x = alloc(arena);
         b.m = alloc(arena);
         b.x_rep = alloc(n * arena);
@@ -333,20 +367,23 @@ void check_layout_fuzz() {
             v = (rng() % 3) ? special[rng() % 12] : static_cast<int64_t>(rng() % 300000);
         int n = 1 + static_cast<int>(rng() % 64), H = 1 + static_cast<int>(rng() % 30);
         int base = static_cast<int>(rng() % 2);
+        int layout = static_cast<int>(rng() % 2);
         std::vector<uint8_t> dec;
         if (rng() % 2) {
             dec.resize(nt);
             for (auto& d : dec) d = static_cast<uint8_t>(rng() % 2);
         }
         // One in four problems gets exactly one invalid field.
-        const int bad = (rng() % 4 == 0) ? 1 + static_cast<int>(rng() % 6) : 0;
+        const int bad = (rng() % 4 == 0) ? 1 + static_cast<int>(rng() % 7) : 0;
         if (bad == 1) n = (rng() % 2) ? 0 : 65;
         if (bad == 2) H = 0;
         if (bad == 3) base = 2 + static_cast<int>(rng() % 5);
         if (bad == 4 && nt > 0) ne[rng() % nt] = -1 - static_cast<int64_t>(rng() % 5);
         if (bad == 5 && nt > 0) ne[rng() % nt] = (int64_t(1) << 34) + static_cast<int64_t>(rng() % 7);
-        const bool invalid = bad == 1 || bad == 2 || bad == 3 || ((bad == 4 || bad == 5) && nt > 0);
-        Problem P(ne, n, H, base, dec);
+        if (bad == 6) layout = (rng() % 2) ? -1 : 2 + static_cast<int>(rng() % 5);
+        const bool invalid =
+            bad == 1 || bad == 2 || bad == 3 || bad == 6 || ((bad == 4 || bad == 5) && nt > 0);
+        Problem P(ne, n, H, base, dec, layout);
         int64_t arena = -7, ws = -7;
         std::vector<int64_t> off(nt + 1, -7);
         const dsm_status st = dsm_layout(&P.p, &arena, off.data(), &ws);
@@ -362,9 +399,10 @@ void check_layout_fuzz() {
         for (int i = 0; i < nt; ++i) {
             CHECK(off[i] == o, "iter %d: offset %d is %lld, expected %lld", iter, i,
                   static_cast<long long>(off[i]), static_cast<long long>(o));
-            o += round_up(ne[i], 64);
+            o += round_up(ne[i], tensor_align(layout));
             chunks += (ne[i] + dsm::kChunkElems - 1) / dsm::kChunkElems;
         }
+        if (layout == DSM_REPLICAS_BLOCKED) o = round_up(o, 16384);
         CHECK(arena == o, "iter %d: arena %lld, expected %lld", iter, static_cast<long long>(arena),
               static_cast<long long>(o));
         CHECK(ws == round_up(chunks * 32, 256) + round_up(int64_t(nt) * 4, 256) +
@@ -402,7 +440,7 @@ void check_chunk_table(const Problem& P, const Buffers& B, const Launch& init) {
             CHECK(c[k].decay == dec, "chunk %lld decay flag", static_cast<long long>(k));
             j += c[k].len;
         }
-        off += round_up(P.numel[i], 64);
+        off += round_up(P.numel[i], tensor_align(P.p.replica_layout));
     }
     CHECK(k == init.n_chunks, "chunk count %lld, table has %lld", static_cast<long long>(k),
           static_cast<long long>(init.n_chunks));
@@ -444,8 +482,10 @@ void check_init_and_chunks() {
     for (size_t s = 0; s < shapes.size(); ++s) {
         std::vector<uint8_t> dec(shapes[s].size());
         for (size_t i = 0; i < dec.size(); ++i) dec[i] = (i % 3 != 1);
-        for (int with_decay = 0; with_decay < 2; ++with_decay) {
-            Problem P(shapes[s], 3, 2, DSM_BASE_ADAMW, with_decay ? dec : std::vector<uint8_t>{});
+        for (int with_decay = 0; with_decay < 4; ++with_decay) {
+            const int layout = with_decay / 2 ? DSM_REPLICAS_BLOCKED : DSM_REPLICAS_CONTIGUOUS;
+            Problem P(shapes[s], 3, 2, DSM_BASE_ADAMW,
+                      with_decay % 2 ? dec : std::vector<uint8_t>{}, layout);
             Buffers B(P, false, true);
             g_log.clear();
             dsm_ctx* ctx = nullptr;
@@ -455,7 +495,8 @@ void check_init_and_chunks() {
             if (!empty && !g_log.empty()) {
                 const Launch& l = g_log[0];
                 CHECK(l.kind == "init" && l.x == B.b.x && l.x_rep == B.b.x_rep && l.v == B.b.v &&
-                          l.s2 == B.b.s2_rep && l.stride == B.arena && l.n_workers == 3,
+                          l.s2 == B.b.s2_rep && l.stride == B.arena && l.n_workers == 3 &&
+                          same_layout(l.rl, B.rep),
                       "init arguments");
                 check_chunk_table(P, B, l);
             }
@@ -518,16 +559,18 @@ void check_init_rejections() {
 void expect_local(const Launch& l, const Buffers& B, bool adamw, bool from_x, int w0, int nw,
                   const char* what) {
     CHECK(l.kind == (adamw ? "local_adamw" : "local_sgdm"), "%s: kind %s", what, l.kind.c_str());
-    CHECK(l.x_rep == B.b.x_rep && l.stride == B.arena, "%s: replica buffer", what);
-    CHECK(l.x_src == (from_x ? B.b.x : B.b.x_rep) && l.src_stride == (from_x ? 0 : B.arena),
+    CHECK(l.x_rep == B.b.x_rep && l.stride == B.arena && same_layout(l.rl, B.rep),
+          "%s: replica buffer", what);
+    CHECK(l.x_src == (from_x ? B.b.x : B.b.x_rep) &&
+              same_layout(l.sl, from_x ? dsm::RepLayout{0, 0, 62, 0} : B.rep),
           "%s: source %s expected", what, from_x ? "x" : "x_rep");
     CHECK(l.worker0 == w0 && l.n_workers == nw, "%s: workers [%d, +%d) expected, got [%d, +%d)",
           what, w0, nw, l.worker0, l.n_workers);
     CHECK(l.chunks == B.b.workspace, "%s: chunk table", what);
 }
 
-void check_state_machine_adamw() {
-    Problem P({100, 16385, 7}, 5, 3, DSM_BASE_ADAMW, {1, 1, 0});
+void check_state_machine_adamw(int layout) {
+    Problem P({100, 16385, 7}, 5, 3, DSM_BASE_ADAMW, {1, 1, 0}, layout);
     Buffers B(P, true, false);
     dsm_ctx* ctx = nullptr;
     CHECK(dsm_init(&P.p, &B.b, &ctx) == DSM_OK, "init");
@@ -556,7 +599,7 @@ void check_state_machine_adamw() {
     g_log.clear();
     CHECK(dsm_global_step(ctx, 0, &gh, 0) == DSM_OK, "global, no broadcast");
     CHECK(g_log.size() == 1 && g_log[0].kind == "global_det" && !g_log[0].broadcast &&
-              g_log[0].x == B.b.x && g_log[0].x_rep == B.b.x_rep && g_log[0].stride == B.arena,
+              g_log[0].x == B.b.x && g_log[0].x_rep == B.b.x_rep && same_layout(g_log[0].rl, B.rep),
           "global launch");
     // Round t = 1: worker 1 first (reads x), then all: runs [0], [1], [2, 5) with
     // sources x, x_rep, x.
@@ -581,7 +624,8 @@ void check_state_machine_adamw() {
     if (g_log.size() == 1) {
         const Launch& l = g_log[0];
         CHECK(l.kind == "round_end" && l.adamw && l.broadcast && l.n_tensors == 3, "round end");
-        CHECK(l.x_src == B.b.x_rep && l.src_stride == B.arena, "round end reads the replicas");
+        CHECK(l.x_src == B.b.x_rep && same_layout(l.sl, B.rep) && same_layout(l.rl, B.rep),
+              "round end reads the replicas");
         CHECK(l.u == B.b.u_scratch && l.s2 == B.b.s2_rep, "round end buffers");
         check_bound_words(P, B, l.bounds, l.chunk0, l.piece_max, "round end");
         CHECK(l.gs.mode == DSM_SIGN_RAND_FLIP && l.gs.t == 1 && l.gs.key0 == 0x89ABCDEFu &&
@@ -613,7 +657,7 @@ void check_state_machine_adamw() {
     g_log.clear();
     CHECK(dsm_sync(ctx) == DSM_OK, "sync");
     CHECK(g_log.size() == 1 && g_log[0].kind == "broadcast" && g_log[0].n_workers == 5 &&
-              g_log[0].x == B.b.x && g_log[0].x_rep == B.b.x_rep,
+              g_log[0].x == B.b.x && g_log[0].x_rep == B.b.x_rep && same_layout(g_log[0].rl, B.rep),
           "broadcast launch");
     for (int k = 0; k < 3; ++k) CHECK(dsm_local_step(ctx, -1, 11 + k, &lh) == DSM_OK, "after sync");
     CHECK(dsm_local_step(ctx, -1, 14, &lh) == DSM_ERR_STATE, "H after sync");
@@ -625,10 +669,10 @@ void check_state_machine_adamw() {
     CHECK(dsm_destroy(ctx) == DSM_OK, "destroy");
 }
 
-void check_state_machine_sgd_h1() {
+void check_state_machine_sgd_h1(int layout) {
     // H = 1: the fused round end takes the only local step; after a lazy
     // round end it reads x, after a broadcast the replicas.
-    Problem P({64, 65}, 3, 1, DSM_BASE_SGD_MOMENTUM);
+    Problem P({64, 65}, 3, 1, DSM_BASE_SGD_MOMENTUM, {}, layout);
     Buffers B(P, false, false);
     dsm_ctx* ctx = nullptr;
     CHECK(dsm_init(&P.p, &B.b, &ctx) == DSM_OK, "init");
@@ -640,9 +684,13 @@ void check_state_machine_sgd_h1() {
     CHECK(dsm_round_end(ctx, 3, &lh, 2, &gh, 1) == DSM_OK, "round end 2");
     CHECK(g_log.size() == 3, "three launches");
     if (g_log.size() == 3) {
-        CHECK(g_log[0].x_src == B.b.x_rep && g_log[0].src_stride == B.arena, "fresh after init");
-        CHECK(g_log[1].x_src == B.b.x && g_log[1].src_stride == 0, "stale after lazy round end");
-        CHECK(g_log[2].x_src == B.b.x_rep, "fresh after broadcast");
+        const dsm::RepLayout x_only{0, 0, 62, 0};
+        CHECK(g_log[0].x_src == B.b.x_rep && same_layout(g_log[0].sl, B.rep), "fresh after init");
+        CHECK(g_log[1].x_src == B.b.x && same_layout(g_log[1].sl, x_only),
+              "stale after lazy round end");
+        CHECK(g_log[2].x_src == B.b.x_rep && same_layout(g_log[2].sl, B.rep),
+              "fresh after broadcast");
+        for (const Launch& l : g_log) CHECK(same_layout(l.rl, B.rep), "round end replica layout");
         CHECK(!g_log[0].adamw && g_log[0].ss.mu == 0.5f && g_log[0].ss.lr == 0.05f, "SGD scalars");
         CHECK(g_log[0].s2 == nullptr, "no second moment for SGD");
     }
@@ -659,13 +707,13 @@ void check_state_machine_sgd_h1() {
 // After a global step without broadcast every replica is stale: a local
 // step of all workers reads x once in one launch (n >= 2); one worker, or
 // n = 1, keeps the per-worker launch reading x.
-void check_local_from_x() {
+void check_local_from_x(int layout) {
     for (int base : {DSM_BASE_ADAMW, DSM_BASE_SGD_MOMENTUM}) {
         const bool adamw = base == DSM_BASE_ADAMW;
         const dsm_local_hparams lh = adamw ? adam_hp() : sgd_hp();
         const dsm_global_hparams gh = glob_hp();
         for (int n : {1, 2, 3, 8}) {
-            Problem P({100, 16385}, n, 2, base);
+            Problem P({100, 16385}, n, 2, base, {}, layout);
             Buffers B(P, false, false);
             dsm_ctx* ctx = nullptr;
             CHECK(dsm_init(&P.p, &B.b, &ctx) == DSM_OK, "init");
@@ -679,7 +727,8 @@ void check_local_from_x() {
                 if (n >= 2) {
                     CHECK(l.kind == "local_from_x" && l.x == B.b.x && l.x_rep == B.b.x_rep &&
                               l.stride == B.arena && l.n_workers == n && l.adamw == adamw &&
-                              l.s2 == B.b.s2_rep && l.chunks == B.b.workspace,
+                              l.s2 == B.b.s2_rep && l.chunks == B.b.workspace &&
+                              same_layout(l.rl, B.rep),
                           "n = %d: all-worker launch from x", n);
                 } else {
                     expect_local(l, B, adamw, true, 0, 1, "n = 1 from x");
@@ -878,13 +927,69 @@ void check_global_rand_args() {
     }
 }
 
+// Blocked replicas: every work-group piece of every chunk lies inside one
+// 64 KiB block, and (copy, element) -> slot covers each tensor element of each
+// copy exactly once inside the n * d_pad buffer, for random problems.
+void check_blocked_addressing() {
+    std::mt19937_64 rng(777);
+    const int64_t piece = dsm::kPieceElems;
+    for (int iter = 0; iter < 200; ++iter) {
+        const int nt = 1 + static_cast<int>(rng() % 12);
+        std::vector<int64_t> ne(nt);
+        for (auto& v : ne) v = (rng() % 4 == 0) ? static_cast<int64_t>(rng() % 70000) : 1 + rng() % 3000;
+        const int n = 1 + static_cast<int>(rng() % 9);
+        Problem P(ne, n, 2, DSM_BASE_SGD_MOMENTUM, {}, DSM_REPLICAS_BLOCKED);
+        Buffers B(P, false, false);
+        CHECK(B.arena % 16384 == 0, "iter %d: blocked arena %lld not whole blocks", iter,
+              static_cast<long long>(B.arena));
+        dsm_ctx* ctx = nullptr;
+        g_log.clear();
+        CHECK(dsm_init(&P.p, &B.b, &ctx) == DSM_OK, "iter %d: init: %s", iter, dsm_last_error(nullptr));
+        if (g_log.empty()) {
+            dsm_destroy(ctx);
+            continue;
+        }
+        const Launch& l = g_log[0];
+        CHECK(same_layout(l.rl, B.rep), "iter %d: init layout", iter);
+        const auto* c = static_cast<const dsm::Chunk*>(B.b.workspace);
+        std::vector<uint8_t> seen(static_cast<size_t>(n) * B.arena, 0);
+        bool ok_piece = true, ok_slot = true;
+        for (int64_t k = 0; k < l.n_chunks; ++k) {
+            for (int64_t e0 = c[k].off; e0 < c[k].off + c[k].len; e0 += piece) {
+                const int64_t e1 = std::min<int64_t>(e0 + piece, c[k].off + c[k].len) - 1;
+                ok_piece &= (e0 >> 14) == (e1 >> 14);
+            }
+            for (int i = 0; i < n; ++i) {
+                for (int64_t e = c[k].off; e < c[k].off + c[k].len; ++e) {
+                    const int64_t idx = rep_element(l.rl, i, e);
+                    if (idx < 0 || idx >= n * B.arena || seen[idx]) {
+                        ok_slot = false;
+                    } else {
+                        seen[idx] = 1;
+                        // A piece's base plus the in-piece offset is the same slot.
+                        const int64_t base = c[k].off + ((e - c[k].off) / piece) * piece;
+                        ok_slot &= rep_element(l.rl, i, base) + (e - base) == idx;
+                    }
+                }
+            }
+        }
+        CHECK(ok_piece, "iter %d: a piece crosses a 64 KiB block", iter);
+        CHECK(ok_slot, "iter %d: replica slots overlap, leave the buffer or break within a piece",
+              iter);
+        CHECK(dsm_destroy(ctx) == DSM_OK, "destroy");
+    }
+}
+
 int main() {
     check_layout_fuzz();
     check_init_and_chunks();
     check_init_rejections();
-    check_state_machine_adamw();
-    check_state_machine_sgd_h1();
-    check_local_from_x();
+    check_blocked_addressing();
+    for (int layout : {DSM_REPLICAS_CONTIGUOUS, DSM_REPLICAS_BLOCKED}) {
+        check_state_machine_adamw(layout);
+        check_state_machine_sgd_h1(layout);
+        check_local_from_x(layout);
+    }
     check_coefficients();
     check_global_rand_args();
     check_hyperparameter_errors();

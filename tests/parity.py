@@ -12,7 +12,9 @@ Two bars, per output element:
     number of fp32 roundings on the longest operation chain (16, AdamW).
     Sign decisions may differ from fp64 only where the fp64 decision margin is
     below 1e-6 * rms of u over the tensor; those flips are counted and the
-    flipped elements' x is excluded.
+    flipped elements' x is excluded.  For the randomized sign the margin is
+    the distance of |u| from the Eq. (9) / Eq. (10) threshold, both sides
+    drawing the same Philox words.
 """
 import numpy as np
 
@@ -88,6 +90,47 @@ def global_scales(x, m, reps, S, *, gamma, eta, beta1, beta2, lam_p):
     s_m = O.f32(beta2) * np.abs(m) + c2 * s_d
     s_x = np.abs(x) + O.f32(eta) * g_ * (np.abs(S) + O.f32(lam_p) * np.abs(x))
     return s_u, s_m, s_x
+
+
+FLIP_MARGIN = 1e-6
+
+
+def det_flip_check(S32, S64, u64, rms_u, what):
+    """Deterministic sign decisions of the fp32 oracle (bit-identical to the
+    GPU path's, whose x is checked bit for bit) against the fp64 oracle's.
+    A flip is allowed only where |u| < 1e-6 rms_p(u).  Returns the count."""
+    s32, s64 = np.asarray(S32, np.float64), np.asarray(S64, np.float64)
+    flip = ~((s32 == s64) | (np.isnan(s32) & np.isnan(s64)))
+    if flip.any():
+        au = np.abs(np.asarray(u64, np.float64)[flip])
+        bad = ~(au < FLIP_MARGIN * rms_u)
+        if bad.any():
+            raise AssertionError(f"{what}: {bad.sum()} of {flip.sum()} sign flips vs fp64 lie "
+                                 f"outside |u| < {FLIP_MARGIN} rms(u) = {FLIP_MARGIN * rms_u}: "
+                                 f"|u| {au[bad][:5]}")
+    return int(flip.sum())
+
+
+def rand_flip_check(S32, S64, u64, B64, k, variant, rms_u, what):
+    """Randomized sign decisions (Eq. (9) variant 1, Eq. (10) variant 2) of the
+    fp32 oracle against the fp64 oracle's, both drawn with the same Philox
+    words k (U = k 2^-24).  A decision may differ only where the fp64 decision
+    margin is below 1e-6 rms_p(u): |u| (the sign of u itself), or the distance
+    of |u| from the threshold, ||u| - B (2U - 1)| for Eq. (9) and ||u| - B U|
+    for Eq. (10).  Returns the number of differing decisions."""
+    s32, s64 = np.asarray(S32, np.float64), np.asarray(S64, np.float64)
+    flip = ~((s32 == s64) | (np.isnan(s32) & np.isnan(s64)))
+    if flip.any():
+        au = np.abs(np.asarray(u64, np.float64)[flip])
+        U = np.asarray(k, np.float64)[flip] * U32
+        thr = float(B64) * ((2.0 * U - 1.0) if variant == 1 else U)
+        margin = np.minimum(au, np.abs(au - thr))
+        bad = ~(margin < FLIP_MARGIN * rms_u)
+        if bad.any():
+            raise AssertionError(f"{what}: {bad.sum()} of {flip.sum()} randomized decisions "
+                                 f"differ from fp64 with margin >= {FLIP_MARGIN} rms(u) = "
+                                 f"{FLIP_MARGIN * rms_u}: margins {margin[bad][:5]}")
+    return int(flip.sum())
 
 
 def rms(a):

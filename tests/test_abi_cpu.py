@@ -157,8 +157,9 @@ def test_test_philox_rejects_bad_arguments(lib, args):
 
 def test_struct_layouts_match_header(lib):
     """ctypes mirrors of the header structs have the C sizes and offsets."""
-    assert ctypes.sizeof(dsm.dsm_problem) == 32
+    assert ctypes.sizeof(dsm.dsm_problem) == 40
     assert dsm.dsm_problem.numel.offset == 16
+    assert dsm.dsm_problem.replica_layout.offset == 32
     assert ctypes.sizeof(dsm.dsm_buffers) == 88
     assert dsm.dsm_buffers.stream.offset == 72
     assert ctypes.sizeof(dsm.dsm_local_hparams) == 20
@@ -175,15 +176,16 @@ def test_header_compiles_as_c_and_struct_sizes_agree(tmp_path):
         pytest.skip("no C compiler")
     src = tmp_path / "t.c"
     src.write_text('#include "dsm.h"\n#include <stdio.h>\n#include <stddef.h>\n'
-                   'int main(void){printf("%zu %zu %zu %zu %zu %zu\\n", sizeof(dsm_problem),'
+                   'int main(void){printf("%zu %zu %zu %zu %zu %zu %zu\\n", sizeof(dsm_problem),'
                    ' sizeof(dsm_buffers), sizeof(dsm_local_hparams), sizeof(dsm_global_hparams),'
-                   ' offsetof(dsm_buffers, stream), offsetof(dsm_global_hparams, seed));'
+                   ' offsetof(dsm_buffers, stream), offsetof(dsm_global_hparams, seed),'
+                   ' offsetof(dsm_problem, replica_layout));'
                    'return 0;}\n')
     exe = tmp_path / "t"
     subprocess.run([cc, "-std=c99", "-Wall", "-Werror", "-I", os.path.join(ROOT, "include"),
                     str(src), "-o", str(exe)], check=True)
     out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split()
-    assert [int(v) for v in out] == [32, 88, 20, 40, 72, 24]
+    assert [int(v) for v in out] == [40, 88, 20, 40, 72, 24, 32]
 
 
 def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):

@@ -37,9 +37,14 @@ def _grads(ar, t, k):
     ar.g_rep.normal_(0.0, 0.01, generator=gen)
 
 
-def run(base, mode, broadcast, n, H, fused, rounds=3, record_grads=False):
+LAYOUTS = [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_BLOCKED]
+
+
+def run(base, mode, broadcast, n, H, fused, rounds=3, record_grads=False,
+        layout=dsm.DSM_REPLICAS_CONTIGUOUS):
     local = ADAM if base == dsm.DSM_BASE_ADAMW else SGD
-    ar = A.Arenas(NUMEL, n, H, base, decay=DECAY, randomized=mode != dsm.DSM_SIGN_DET)
+    ar = A.Arenas(NUMEL, n, H, base, decay=DECAY, randomized=mode != dsm.DSM_SIGN_DET,
+                  replica_layout=layout)
     gen = torch.Generator(device="cuda").manual_seed(77)
     ar.x.normal_(0.0, 0.02, generator=gen)
     ar.init()
@@ -63,7 +68,7 @@ def run(base, mode, broadcast, n, H, fused, rounds=3, record_grads=False):
     if ar.s2_rep is not None:
         out["s2"] = host(ar.s2_rep)
     if broadcast:
-        out["x_rep"] = host(ar.x_rep)
+        out["x_rep"] = host(ar.replicas())
     if mode != dsm.DSM_SIGN_DET:
         out["B"] = dsm.dsm_read_bounds(ar.ctx, len(NUMEL))
         out["u"] = host(ar.u)
@@ -83,9 +88,10 @@ def _mask(offsets, arena):
 @pytest.mark.parametrize("mode", [dsm.DSM_SIGN_DET, dsm.DSM_SIGN_RAND_FLIP, dsm.DSM_SIGN_RAND_ZERO])
 @pytest.mark.parametrize("broadcast", [True, False])
 @pytest.mark.parametrize("n,H", [(4, 3), (3, 1), (1, 2)])
-def test_fused_round_end_bit_identical_to_unfused(base, mode, broadcast, n, H):
-    ref, _, offsets = run(base, mode, broadcast=True, n=n, H=H, fused=False)
-    got, _, _ = run(base, mode, broadcast=broadcast, n=n, H=H, fused=True)
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_fused_round_end_bit_identical_to_unfused(base, mode, broadcast, n, H, layout):
+    ref, _, offsets = run(base, mode, broadcast=True, n=n, H=H, fused=False, layout=layout)
+    got, _, _ = run(base, mode, broadcast=broadcast, n=n, H=H, fused=True, layout=layout)
     keep = _mask(offsets, ref["x"].size)
     for key in ("x", "m", "s1", "s2", "u"):
         if key in got:
@@ -100,14 +106,15 @@ def test_fused_round_end_bit_identical_to_unfused(base, mode, broadcast, n, H):
 
 
 @pytest.mark.parametrize("base", [dsm.DSM_BASE_ADAMW, dsm.DSM_BASE_SGD_MOMENTUM])
-def test_fused_lazy_rounds_match_oracle(base):
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_fused_lazy_rounds_match_oracle(base, layout):
     """Three fused rounds with the lazy broadcast against the oracle's rounds
     (fp32), free-running: x, m and the base state bit-identical."""
     n, H = 3, 2
     got, grads, offsets = run(base, dsm.DSM_SIGN_DET, broadcast=False, n=n, H=H, fused=True,
-                              record_grads=True)
+                              record_grads=True, layout=layout)
     local = ADAM if base == dsm.DSM_BASE_ADAMW else SGD
-    ar = A.Arenas(NUMEL, n, H, base, decay=DECAY, randomized=False)
+    ar = A.Arenas(NUMEL, n, H, base, decay=DECAY, randomized=False, replica_layout=layout)
     gen = torch.Generator(device="cuda").manual_seed(77)
     ar.x.normal_(0.0, 0.02, generator=gen)
     x0 = tensors(ar, ar.x)
@@ -123,12 +130,14 @@ def test_fused_lazy_rounds_match_oracle(base):
             assert np.array_equal(got["s1"][i, o:o + k], st["s1"][i][p])
 
 
-def test_mixed_stale_and_fresh_workers():
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_mixed_stale_and_fresh_workers(layout):
     """After a global step without broadcast, a single worker's local step
     reads x; a following all-worker step mixes stale and fresh replicas.
     SGD base (no bias-correction count), one gradient per worker per round."""
     n, H = 3, 2
-    ar = A.Arenas(NUMEL, n, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, randomized=False)
+    ar = A.Arenas(NUMEL, n, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, randomized=False,
+                  replica_layout=layout)
     gen = torch.Generator(device="cuda").manual_seed(5)
     ar.x.normal_(0.0, 0.02, generator=gen)
     ar.init()
@@ -173,7 +182,8 @@ def test_round_end_state_errors():
 
 @pytest.mark.parametrize("base", [dsm.DSM_BASE_ADAMW, dsm.DSM_BASE_SGD_MOMENTUM])
 @pytest.mark.parametrize("n", [2, 3, 4, 5, 8])
-def test_all_worker_step_from_x_equals_per_worker_steps(base, n):
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_all_worker_step_from_x_equals_per_worker_steps(base, n, layout):
     """After a global step without broadcast every replica is stale.  A local
     step of all workers then reads x once in one launch; it must equal n
     single-worker steps (each reading x) bit for bit, and so must the rest of
@@ -182,7 +192,7 @@ def test_all_worker_step_from_x_equals_per_worker_steps(base, n):
     H = 2
     outs = []
     for per_worker in (False, True):
-        ar = A.Arenas(NUMEL, n, H, base, decay=DECAY, randomized=False)
+        ar = A.Arenas(NUMEL, n, H, base, decay=DECAY, randomized=False, replica_layout=layout)
         gen = torch.Generator(device="cuda").manual_seed(5 + n)
         ar.x.normal_(0.0, 0.02, generator=gen)
         ar.init()
@@ -196,13 +206,13 @@ def test_all_worker_step_from_x_equals_per_worker_steps(base, n):
                 dsm.dsm_local_step(ar.ctx, i, H + 1, **local)
         else:
             dsm.dsm_local_step(ar.ctx, -1, H + 1, **local)
-        first = {"x_rep": host(ar.x_rep), "s1": host(ar.s1_rep)}
+        first = {"x_rep": host(ar.replicas()), "s1": host(ar.s1_rep)}
         if ar.s2_rep is not None:
             first["s2"] = host(ar.s2_rep)
         _grads(ar, 1, 1)
         dsm.dsm_local_step(ar.ctx, -1, H + 2, **local)
         dsm.dsm_global_step(ar.ctx, 1, gamma=local["lr"], broadcast=True, **GLOB)
-        after = {"x": host(ar.x), "m": host(ar.m), "x_rep_end": host(ar.x_rep)}
+        after = {"x": host(ar.x), "m": host(ar.m), "x_rep_end": host(ar.replicas())}
         mask = _mask(list(ar.offsets), ar.x.numel())
         ar.destroy()
         outs.append((first, after, mask))

@@ -11,7 +11,9 @@ Every output is compared with the fp32 oracle run from the same device
 state.  NaN positions must agree, and every other value must be
 bit-identical.  That covers the local states, x and m, and for the randomized
 sign also u and the per-tensor bound B, which turns NaN or inf with its
-tensor.
+tensor.  Section 3.1 defines the randomized sign only for a finite bound, so
+a tensor whose B is NaN or inf must take a NaN step at every element, never a
+finite step of a reversed (Eq. (9)) or zero (Eq. (10)) sign.
 """
 import numpy as np
 import pytest
@@ -57,15 +59,17 @@ def same(gpu, ora, what):
 @pytest.mark.parametrize("mode", [dsm.DSM_SIGN_DET, dsm.DSM_SIGN_RAND_FLIP,
                                   dsm.DSM_SIGN_RAND_ZERO])
 @pytest.mark.parametrize("base", [dsm.DSM_BASE_ADAMW, dsm.DSM_BASE_SGD_MOMENTUM])
-def test_nonfinite_gradients_match_oracle(base, mode):
+@pytest.mark.parametrize("layout", [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_BLOCKED])
+def test_nonfinite_gradients_match_oracle(base, mode, layout):
     adamw = base == dsm.DSM_BASE_ADAMW
     local = ADAM if adamw else SGD
-    ar = A.Arenas(NUMEL, N, H, base, decay=DECAY, randomized=True)
+    ar = A.Arenas(NUMEL, N, H, base, decay=DECAY, randomized=True, replica_layout=layout)
     gen = torch.Generator(device="cuda").manual_seed(99 + 3 * base + mode)
     ar.x.normal_(0.0, 0.02, generator=gen)
     ar.init()
     keys = ("x_rep", "s1_rep") + (("s2_rep",) if adamw else ())
     seen_nan = seen_inf = False
+    undefined_bounds = {"nan": 0, "inf": 0}
     with np.errstate(invalid="ignore", over="ignore", divide="ignore"):
         for t in range(2):
             for k in range(H):
@@ -74,11 +78,11 @@ def test_nonfinite_gradients_match_oracle(base, mode):
                 for w, p, j, val in PLANTS[(t, k)]:
                     for i in (range(N) if w is None else (w,)):
                         ar.g_rep[i, ar.offsets[p] + j] = float(val)
-                before = {name: [tensors(ar, getattr(ar, name)[i]) for i in range(N)]
+                before = {name: [tensors(ar, ar.worker(name, i)) for i in range(N)]
                           for name in keys + ("g_rep",)}
                 dsm.dsm_local_step(ar.ctx, -1, s, **local)
                 for i in range(N):
-                    after = {name: tensors(ar, getattr(ar, name)[i]) for name in keys}
+                    after = {name: tensors(ar, ar.worker(name, i)) for name in keys}
                     for p in range(len(NUMEL)):
                         args = [before[name][i][p] for name in ("x_rep", "g_rep", "s1_rep")]
                         if adamw:
@@ -92,7 +96,7 @@ def test_nonfinite_gradients_match_oracle(base, mode):
                         for name, want in zip(keys, o):
                             same(after[name][p], want, f"t {t} k {k} worker {i} {name} tensor {p}")
             x0, m0 = tensors(ar, ar.x), tensors(ar, ar.m)
-            reps = [tensors(ar, ar.x_rep[i]) for i in range(N)]
+            reps = [tensors(ar, ar.replica(i)) for i in range(N)]
             dsm.dsm_global_step(ar.ctx, t, mode=mode, seed=SEED, broadcast=True, **GLOB)
             o = O.global_step(x0, m0, reps, decay=DECAY, t=t, mode=mode, seed=SEED, prec="fp32",
                               **GLOB)
@@ -108,11 +112,20 @@ def test_nonfinite_gradients_match_oracle(base, mode):
                 if mode != dsm.DSM_SIGN_DET:
                     same(gu[p], o["u"][p], f"t {t} u tensor {p}")
                     same(B[p:p + 1], np.asarray([o["B"][p]], np.float32), f"t {t} B tensor {p}")
+                    if not np.isfinite(B[p]):
+                        assert np.all(np.isnan(gx[p])), \
+                            f"t {t} tensor {p}: bound {B[p]} but a finite step was taken"
+                        undefined_bounds["nan" if np.isnan(B[p]) else "inf"] += 1
             for i in range(N):
-                for a, b in zip(ar.views(ar.x_rep[i]), ar.views(ar.x)):
+                for a, b in zip(ar.views(ar.replica(i)), ar.views(ar.x)):
                     assert torch.equal(a.view(torch.int32), b.view(torch.int32))
-    # The planted values did reach the global state.
+    # The planted values did reach the global state, and the randomized sign
+    # met NaN bounds (and, for SGD, whose steps keep an infinite gradient
+    # infinite, inf bounds).
     assert seen_nan and (seen_inf or adamw)
+    if mode != dsm.DSM_SIGN_DET:
+        assert undefined_bounds["nan"] > 0 and (undefined_bounds["inf"] > 0 or adamw), \
+            undefined_bounds
     ar.destroy()
 
 
@@ -151,11 +164,11 @@ def test_subnormal_values_match_oracle(base):
             ar.g_rep[:, o0:o0 + 2 * nt] = 0.0
             ar.g_rep[0, o0:o0 + nt] = tiny              # one worker moves these
             ar.g_rep[:, o0 + nt:o0 + 2 * nt] = -tiny    # every worker moves these
-            before = {name: [tensors_of(ar, getattr(ar, name)[i], TINY_NUMEL) for i in range(N)]
+            before = {name: [tensors_of(ar, ar.worker(name, i), TINY_NUMEL) for i in range(N)]
                       for name in keys + ("g_rep",)}
             dsm.dsm_local_step(ar.ctx, -1, s, **local)
             for i in range(N):
-                after = {name: tensors_of(ar, getattr(ar, name)[i], TINY_NUMEL) for name in keys}
+                after = {name: tensors_of(ar, ar.worker(name, i), TINY_NUMEL) for name in keys}
                 for p in range(len(TINY_NUMEL)):
                     args = [before[name][i][p] for name in ("x_rep", "g_rep", "s1_rep")]
                     if adamw:
@@ -167,7 +180,7 @@ def test_subnormal_values_match_oracle(base):
                     for name, want in zip(keys, o):
                         same(after[name][p], want, f"t {t} k {k} worker {i} {name} tensor {p}")
         x0, m0 = tensors_of(ar, ar.x, TINY_NUMEL), tensors_of(ar, ar.m, TINY_NUMEL)
-        reps = [tensors_of(ar, ar.x_rep[i], TINY_NUMEL) for i in range(N)]
+        reps = [tensors_of(ar, ar.replica(i), TINY_NUMEL) for i in range(N)]
         dsm.dsm_global_step(ar.ctx, t, broadcast=True, **GLOB_TINY)
         o = O.global_step(x0, m0, reps, decay=TINY_DECAY, t=t, prec="fp32", **GLOB_TINY)
         gx, gm = tensors_of(ar, ar.x, TINY_NUMEL), tensors_of(ar, ar.m, TINY_NUMEL)

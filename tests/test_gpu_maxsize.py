@@ -42,9 +42,10 @@ CASES = {
     "adamw_n1": dict(base=dsm.DSM_BASE_ADAMW, n=1,
                      modes=(dsm.DSM_SIGN_RAND_FLIP, dsm.DSM_SIGN_DET),
                      local=dict(lr=2e-4, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1)),
-    "sgdm_n2": dict(base=dsm.DSM_BASE_SGD_MOMENTUM, n=2,
-                    modes=(dsm.DSM_SIGN_RAND_ZERO, dsm.DSM_SIGN_RAND_FLIP),
-                    local=dict(lr=0.1, beta1=0.9)),
+    # Blocked replicas: the 64 KiB-block addressing past 2^32 elements.
+    "sgdm_n2_blocked": dict(base=dsm.DSM_BASE_SGD_MOMENTUM, n=2,
+                            modes=(dsm.DSM_SIGN_RAND_ZERO, dsm.DSM_SIGN_RAND_FLIP),
+                            local=dict(lr=0.1, beta1=0.9), layout=dsm.DSM_REPLICAS_BLOCKED),
 }
 
 
@@ -74,7 +75,8 @@ class Big:
         self.c = c
         self.n = c["n"]
         self.adamw = c["base"] == dsm.DSM_BASE_ADAMW
-        self.ar = A.Arenas(NUMEL, self.n, 1, c["base"], decay=DECAY, randomized=True)
+        self.ar = A.Arenas(NUMEL, self.n, 1, c["base"], decay=DECAY, randomized=True,
+                           replica_layout=c.get("layout", dsm.DSM_REPLICAS_CONTIGUOUS))
         assert self.ar.arena_elems > (1 << 32)
         self.gen = torch.Generator(device="cuda").manual_seed(77 + self.n)
         self.ar.x.normal_(0.0, 0.02, generator=self.gen)
@@ -90,7 +92,8 @@ class Big:
 
     def sample_state(self, keys):
         torch.cuda.synchronize()
-        return {k: [self.sample(getattr(self.ar, k)[i]) for i in range(self.n)] for k in keys}
+        return {k: [self.ar.gather(k, i, self.idx).cpu().numpy().copy() for i in range(self.n)]
+                for k in keys}
 
     def local_oracle(self, before, i, s):
         """The oracle's local step s of worker i on the sampled elements."""
@@ -154,7 +157,7 @@ class Big:
     def replicas_equal_x(self):
         torch.cuda.synchronize()
         for i in range(self.n):
-            for a, b in zip(self.ar.views(self.ar.x_rep[i]), self.ar.views(self.ar.x)):
+            for a, b in zip(self.ar.views(self.ar.replica(i)), self.ar.views(self.ar.x)):
                 assert torch.equal(a.view(torch.int32), b.view(torch.int32)), f"replica {i}"
 
 
@@ -203,3 +206,4 @@ def test_max_size_split_then_fused_round(big):
     dsm.dsm_sync(ar.ctx)
     b.replicas_equal_x()
     print(f"max size n={b.n}: {b.p.size} sampled elements, {nonbit} not bit-identical")
+    assert nonbit == 0

@@ -14,12 +14,15 @@ import oracle as O
 from paper_2411_17866_amd import arena as A
 from paper_2411_17866_amd import dsm
 
-from parity import (adamw_scales, global_scales, rel_check, rms, scaled_check, sgdm_scales)
+from parity import (adamw_scales, det_flip_check, global_scales, rand_flip_check, rel_check, rms,
+                    scaled_check, sgdm_scales)
 
 pytestmark = pytest.mark.gpu
 
 RAGGED = [1, 3, 4, 5, 63, 64, 65, 0, 1000, 16383, 16384, 16385, 40003]
 DECAY = [i % 3 != 1 for i in range(len(RAGGED))]
+# Both replica layouts of dsm_problem.replica_layout.
+LAYOUTS = [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_BLOCKED]
 
 
 def host(t):
@@ -27,8 +30,9 @@ def host(t):
     return t.detach().cpu().numpy().copy()
 
 
-def make(numel, n, H, base, decay=None, seed=0, randomized=True):
-    ar = A.Arenas(numel, n, H, base, decay=decay, randomized=randomized)
+def make(numel, n, H, base, decay=None, seed=0, randomized=True,
+         layout=dsm.DSM_REPLICAS_CONTIGUOUS):
+    ar = A.Arenas(numel, n, H, base, decay=decay, randomized=randomized, replica_layout=layout)
     gen = torch.Generator(device="cuda").manual_seed(seed)
     ar.x.normal_(0.0, 0.02, generator=gen)
     ar.init()
@@ -76,18 +80,19 @@ def _randomize_state(ar, gen, adamw):
 
 
 @pytest.mark.parametrize("n,worker,step", [(3, -1, 1), (4, -1, 7), (4, 2, 3), (1, 0, 1000)])
-def test_local_adamw_parity(n, worker, step):
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_local_adamw_parity(n, worker, step, layout):
     hp = dict(lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1)
-    ar, gen = make(RAGGED, n, 4, dsm.DSM_BASE_ADAMW, decay=DECAY, seed=n + step)
+    ar, gen = make(RAGGED, n, 4, dsm.DSM_BASE_ADAMW, decay=DECAY, seed=n + step, layout=layout)
     _randomize_state(ar, gen, True)
     pad = padding_mask(ar)
-    before = {k: [per_tensor(ar, getattr(ar, k)[i]) for i in range(n)]
+    before = {k: [per_tensor(ar, ar.worker(k, i)) for i in range(n)]
               for k in ("x_rep", "g_rep", "s1_rep", "s2_rep")}
-    pad_before = host(ar.x_rep)[:, pad]
+    pad_before = host(ar.replicas())[:, pad]
     dsm.dsm_local_step(ar.ctx, worker, step, **hp)
-    after = {k: [per_tensor(ar, getattr(ar, k)[i]) for i in range(n)]
+    after = {k: [per_tensor(ar, ar.worker(k, i)) for i in range(n)]
              for k in ("x_rep", "s1_rep", "s2_rep")}
-    np.testing.assert_array_equal(host(ar.x_rep)[:, pad], pad_before)
+    np.testing.assert_array_equal(host(ar.replicas())[:, pad], pad_before)
     nonbit = 0
     for i in range(n):
         for p in range(len(RAGGED)):
@@ -108,18 +113,20 @@ def test_local_adamw_parity(n, worker, step):
             scaled_check(gm, o64[1], s_m, f"m vs fp64, worker {i} tensor {p}")
             scaled_check(gv, o64[2], s_v, f"v vs fp64, worker {i} tensor {p}")
     print(f"adamw n={n} worker={worker}: {nonbit} elements not bit-identical to the fp32 oracle")
+    assert nonbit == 0
     ar.destroy()
 
 
 @pytest.mark.parametrize("n,worker", [(2, -1), (5, -1), (3, 0)])
-def test_local_sgdm_parity(n, worker):
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_local_sgdm_parity(n, worker, layout):
     hp = dict(lr=0.1, beta1=0.9)
-    ar, gen = make(RAGGED, n, 2, dsm.DSM_BASE_SGD_MOMENTUM, seed=100 + n)
+    ar, gen = make(RAGGED, n, 2, dsm.DSM_BASE_SGD_MOMENTUM, seed=100 + n, layout=layout)
     _randomize_state(ar, gen, False)
-    before = {k: [per_tensor(ar, getattr(ar, k)[i]) for i in range(n)]
+    before = {k: [per_tensor(ar, ar.worker(k, i)) for i in range(n)]
               for k in ("x_rep", "g_rep", "s1_rep")}
     dsm.dsm_local_step(ar.ctx, worker, 1, **hp)
-    after = {k: [per_tensor(ar, getattr(ar, k)[i]) for i in range(n)] for k in ("x_rep", "s1_rep")}
+    after = {k: [per_tensor(ar, ar.worker(k, i)) for i in range(n)] for k in ("x_rep", "s1_rep")}
     nonbit = 0
     for i in range(n):
         for p in range(len(RAGGED)):
@@ -137,6 +144,7 @@ def test_local_sgdm_parity(n, worker):
             scaled_check(gx, o64[0], s_x, "sgd x vs fp64")
             scaled_check(gm, o64[1], s_m, "sgd m vs fp64")
     print(f"sgdm n={n}: {nonbit} elements not bit-identical to the fp32 oracle")
+    assert nonbit == 0
     ar.destroy()
 
 
@@ -156,13 +164,15 @@ GLOB = dict(gamma=1e-3, eta=0.8, beta1=0.95, beta2=0.98, lam=0.1)
 
 @pytest.mark.parametrize("n,broadcast", [(1, True), (2, True), (3, True), (4, True), (4, False),
                                           (5, True), (8, True)])
-def test_global_det_parity(n, broadcast):
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_global_det_parity(n, broadcast, layout):
     H = 2
-    ar, gen = make(RAGGED, n, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, seed=200 + n)
+    ar, gen = make(RAGGED, n, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, seed=200 + n,
+                   layout=layout)
     _ready_for_global(ar, gen, H, n)
     x0, m0 = per_tensor(ar, ar.x), per_tensor(ar, ar.m)
-    reps = [per_tensor(ar, ar.x_rep[i]) for i in range(n)]
-    rep_before = host(ar.x_rep)
+    reps = [per_tensor(ar, ar.replica(i)) for i in range(n)]
+    rep_before = host(ar.replicas())
     dsm.dsm_global_step(ar.ctx, 5, mode=dsm.DSM_SIGN_DET, broadcast=broadcast, **GLOB)
     gx, gm = per_tensor(ar, ar.x), per_tensor(ar, ar.m)
     o32 = O.global_step(x0, m0, reps, decay=DECAY, prec="fp32", **GLOB)
@@ -177,11 +187,10 @@ def test_global_det_parity(n, broadcast):
         scaled_check(gm[p], o64["m"][p], s_m, f"m vs fp64 tensor {p}")
         # Sign decisions vs fp64: only where |u| is tiny.
         flip = o32["S"][p] != o64["S"][p]
-        if flip.any():
-            assert np.all(np.abs(o64["u"][p][flip]) < 1e-6 * rms(o64["u"][p])), f"tensor {p}"
-        flips += int(flip.sum())
+        flips += det_flip_check(o32["S"][p], o64["S"][p], o64["u"][p], rms(o64["u"][p]),
+                                f"tensor {p}")
         scaled_check(gx[p], o64["x"][p], s_x, f"x vs fp64 tensor {p}", mask=~flip)
-    rep_after = host(ar.x_rep)
+    rep_after = host(ar.replicas())
     if broadcast:
         xa = host(ar.x)
         for i in range(n):
@@ -196,17 +205,18 @@ def test_global_det_parity(n, broadcast):
         g1 = [per_tensor(ar, ar.g_rep[i]) for i in range(n)]
         dsm.dsm_local_step(ar.ctx, -1, 1, lr=0.05, beta1=0.5)
         for i in range(n):
-            xi = per_tensor(ar, ar.x_rep[i])
+            xi = per_tensor(ar, ar.replica(i))
             for p in range(len(RAGGED)):
                 ox, _ = O.local_sgdm_step(gx_now[p], g1[i][p], m1[i][p], lr=0.05, momentum=0.5,
                                           prec="fp32")
                 assert np.array_equal(xi[p].view(np.uint32), ox.view(np.uint32)), (i, p)
         dsm.dsm_sync(ar.ctx)
-        xa, ra = host(ar.x), host(ar.x_rep)
+        xa, ra = host(ar.x), host(ar.replicas())
         for i in range(n):
             for o, k in zip(ar.offsets, ar.numel):
                 assert np.array_equal(ra[i, o:o + k].view(np.uint32), xa[o:o + k].view(np.uint32))
     print(f"global det n={n}: {nonbit} non-bit-identical vs fp32 oracle, {flips} sign flips vs fp64")
+    assert nonbit == 0
     ar.destroy()
 
 
@@ -214,39 +224,59 @@ def test_global_det_parity(n, broadcast):
                                          (4, dsm.DSM_SIGN_RAND_ZERO, (1 << 63) + 12345),
                                          (3, dsm.DSM_SIGN_RAND_FLIP, 2 ** 40 + 7),
                                          (8, dsm.DSM_SIGN_RAND_ZERO, 99)])
-def test_global_randomized_parity(n, mode, seed):
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_global_randomized_parity(n, mode, seed, layout):
     H = 1
-    ar, gen = make(RAGGED, n, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, seed=300 + n)
+    ar, gen = make(RAGGED, n, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, seed=300 + n,
+                   layout=layout)
     _ready_for_global(ar, gen, H, n)
     x0, m0 = per_tensor(ar, ar.x), per_tensor(ar, ar.m)
-    reps = [per_tensor(ar, ar.x_rep[i]) for i in range(n)]
+    reps = [per_tensor(ar, ar.replica(i)) for i in range(n)]
     t = 77
     dsm.dsm_global_step(ar.ctx, t, mode=mode, seed=seed, broadcast=True, **GLOB)
     gx, gm, gu = per_tensor(ar, ar.x), per_tensor(ar, ar.m), per_tensor(ar, ar.u)
     B = dsm.dsm_read_bounds(ar.ctx, len(RAGGED))
     o32 = O.global_step(x0, m0, reps, decay=DECAY, prec="fp32", t=t, mode=mode, seed=seed, **GLOB)
-    nonbit = 0
+    o64 = O.global_step(x0, m0, reps, decay=DECAY, prec="fp64", t=t, mode=mode, seed=seed, **GLOB)
+    nonbit = flips = 0
     for p in range(len(RAGGED)):
         assert B[p].view(np.uint32) == np.float32(o32["B"][p]).view(np.uint32), f"B tensor {p}"
         np.testing.assert_array_equal(gu[p].view(np.uint32), o32["u"][p].view(np.uint32))
         nonbit += rel_check(gm[p], o32["m"][p], f"m tensor {p}")
         nonbit += rel_check(gx[p], o32["x"][p], f"x tensor {p}")
-    ra, xa = host(ar.x_rep), host(ar.x)
+        # fp64 side: u and m within the error bound, and every randomized
+        # decision that differs from the fp64 oracle's (its own bound B_p =
+        # max |u| in fp64, the same Philox words) lies inside the 1e-6 rms(u)
+        # margin of Eq. (9) / Eq. (10).
+        lam_p = GLOB["lam"] if DECAY[p] else 0.0
+        s_u, s_m, s_x = global_scales(x0[p], m0[p], [r[p] for r in reps], o64["S"][p],
+                                      lam_p=lam_p, **{k: v for k, v in GLOB.items() if k != "lam"})
+        scaled_check(gu[p], o64["u"][p], s_u, f"u vs fp64 tensor {p}")
+        scaled_check(gm[p], o64["m"][p], s_m, f"m vs fp64 tensor {p}")
+        k = O.randomized_sign_uniforms(RAGGED[p], p, t, seed)
+        flips += rand_flip_check(o32["S"][p], o64["S"][p], o64["u"][p], o64["B"][p], k, mode,
+                                 rms(o64["u"][p]), f"tensor {p}")
+        flip = o32["S"][p] != o64["S"][p]
+        scaled_check(gx[p], o64["x"][p], s_x, f"x vs fp64 tensor {p}", mask=~flip)
+    ra, xa = host(ar.replicas()), host(ar.x)
     for i in range(n):
         for o, k in zip(ar.offsets, ar.numel):
             assert np.array_equal(ra[i, o:o + k].view(np.uint32), xa[o:o + k].view(np.uint32))
-    print(f"global rand n={n} mode={mode}: {nonbit} non-bit-identical vs fp32 oracle")
+    print(f"global rand n={n} mode={mode}: {nonbit} non-bit-identical vs fp32 oracle, "
+          f"{flips} randomized decisions differ from fp64 (all inside the margin)")
+    assert nonbit == 0
     ar.destroy()
 
 
 @pytest.mark.parametrize("fused", [False, True])
-def test_bound_is_recomputed_when_it_shrinks(fused):
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_bound_is_recomputed_when_it_shrinks(fused, layout):
     """B_p is max |u| of the current step only: after a step whose u is
     large, a step with u a thousand times smaller (smaller gradients, m reset
     to 0) gets the smaller bound, exactly, and the signs that go with it.  Split steps and fused round ends
     (H = 1, so the round end takes the only local step)."""
     n, H, mode, seed = 3, 1, dsm.DSM_SIGN_RAND_FLIP, 2024
-    ar, gen = make(RAGGED, n, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, seed=77)
+    ar, gen = make(RAGGED, n, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, seed=77, layout=layout)
     local = dict(lr=0.05, beta1=0.0)   # no local momentum carries the large step over
     B_prev = None
     for t, scale in enumerate((1e3, 1.0)):
@@ -261,7 +291,7 @@ def test_bound_is_recomputed_when_it_shrinks(fused):
         else:
             dsm.dsm_local_step(ar.ctx, -1, t + 1, **local)
             x0, m0 = per_tensor(ar, ar.x), per_tensor(ar, ar.m)
-            reps = [per_tensor(ar, ar.x_rep[i]) for i in range(n)]
+            reps = [per_tensor(ar, ar.replica(i)) for i in range(n)]
             dsm.dsm_global_step(ar.ctx, t, mode=mode, seed=seed, broadcast=True, **GLOB)
         gx, gu = per_tensor(ar, ar.x), per_tensor(ar, ar.u)
         B = dsm.dsm_read_bounds(ar.ctx, len(RAGGED))
@@ -273,7 +303,7 @@ def test_bound_is_recomputed_when_it_shrinks(fused):
                                 **GLOB)
             for p in range(len(RAGGED)):
                 assert B[p].view(np.uint32) == np.float32(o32["B"][p]).view(np.uint32)
-                rel_check(gx[p], o32["x"][p], f"x tensor {p}, step {t}")
+                assert rel_check(gx[p], o32["x"][p], f"x tensor {p}, step {t}") == 0
         if B_prev is not None:
             nonempty = np.array([k > 0 for k in RAGGED])
             assert np.all(B[nonempty] < 1e-2 * B_prev[nonempty]), "the bound did not shrink"
@@ -311,11 +341,12 @@ def test_tiny_rounds_free_running_bit_identical():
             for i in range(w.n_workers):
                 assert np.array_equal(per_tensor(ar, ar.s1_rep[i])[p], st["s1"][i][p])
                 assert np.array_equal(per_tensor(ar, ar.s2_rep[i])[p], st["s2"][i][p])
-                assert np.array_equal(per_tensor(ar, ar.x_rep[i])[p], st["replicas"][i][p])
+                assert np.array_equal(per_tensor(ar, ar.replica(i))[p], st["replicas"][i][p])
     ar.destroy()
 
 
-def test_tiny_long_free_run_all_signs_and_paths():
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_tiny_long_free_run_all_signs_and_paths(layout):
     """Twelve free-running rounds of the tiny workload, cycling the three
     signs and alternating the fused round end (lazy broadcast) with the split
     path (broadcast).  GPU and fp32 oracle start from the same inputs and are
@@ -324,7 +355,8 @@ def test_tiny_long_free_run_all_signs_and_paths():
     from paper_2411_17866_amd import workloads as W
     w = W.get("tiny")
     H = w.local_steps
-    ar, gen = make(w.numel, w.n_workers, H, w.base, decay=w.decay, seed=w.seed + 1)
+    ar, gen = make(w.numel, w.n_workers, H, w.base, decay=w.decay, seed=w.seed + 1,
+                   layout=layout)
     st = O.init_state(per_tensor(ar, ar.x), w.n_workers, "adamw")
     modes = (dsm.DSM_SIGN_DET, dsm.DSM_SIGN_RAND_FLIP, dsm.DSM_SIGN_RAND_ZERO)
     seed = 0x5EED0000000D5
@@ -370,7 +402,7 @@ def test_rerun_is_bitwise_deterministic():
             dsm.dsm_local_step(ar.ctx, -1, k + 1, lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8,
                                weight_decay=0.1)
         dsm.dsm_global_step(ar.ctx, 3, mode=dsm.DSM_SIGN_RAND_FLIP, seed=42, **GLOB)
-        outs.append([host(t) for t in (ar.x, ar.m, ar.x_rep, ar.s1_rep, ar.s2_rep, ar.u)])
+        outs.append([host(t) for t in (ar.x, ar.m, ar.replicas(), ar.s1_rep, ar.s2_rep, ar.u)])
         ar.destroy()
     for a, b in zip(*outs):
         assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
@@ -441,7 +473,8 @@ def test_empty_problem_is_a_no_op():
 
 # ---------------------------------------------------------------- limits, degenerate cases
 
-def test_max_workers_every_entry_point():
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_max_workers_every_entry_point(layout):
     """n = 64 (the largest worker count): local AdamW, deterministic and
     randomized global steps and the fused round end without broadcast, then a
     round whose first local step starts every worker from x, against the
@@ -450,7 +483,7 @@ def test_max_workers_every_entry_point():
     numel = [5, 1000, 16385]
     decay = [False, True, True]
     local = dict(lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1)
-    ar, gen = make(numel, n, H, dsm.DSM_BASE_ADAMW, decay=decay, seed=64)
+    ar, gen = make(numel, n, H, dsm.DSM_BASE_ADAMW, decay=decay, seed=64, layout=layout)
     st = O.init_state(per_tensor(ar, ar.x), n, "adamw")
     for t, (mode, fused) in enumerate(((dsm.DSM_SIGN_DET, False), (dsm.DSM_SIGN_RAND_ZERO, False),
                                        (dsm.DSM_SIGN_RAND_FLIP, True), (dsm.DSM_SIGN_DET, False))):
@@ -487,7 +520,7 @@ def test_global_step_degenerate_hyperparameters(hp):
     ar, gen = make(RAGGED, n, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, seed=77)
     _ready_for_global(ar, gen, H, n)
     x0, m0 = per_tensor(ar, ar.x), per_tensor(ar, ar.m)
-    reps = [per_tensor(ar, ar.x_rep[i]) for i in range(n)]
+    reps = [per_tensor(ar, ar.replica(i)) for i in range(n)]
     dsm.dsm_global_step(ar.ctx, 0, gamma=1e-3, **hp)
     gx, gm = per_tensor(ar, ar.x), per_tensor(ar, ar.m)
     o32 = O.global_step(x0, m0, reps, gamma=1e-3, decay=DECAY, prec="fp32", **hp)

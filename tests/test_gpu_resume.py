@@ -68,7 +68,7 @@ def final_state(ar):
     out = {"x": bits(ar, ar.x), "m": bits(ar, ar.m)}
     for name in ("x_rep", "s1_rep", "s2_rep"):
         for i in range(N):
-            out[f"{name}[{i}]"] = bits(ar, getattr(ar, name)[i])
+            out[f"{name}[{i}]"] = bits(ar, ar.worker(name, i))
     return out
 
 
@@ -112,7 +112,7 @@ def test_resume_after_lazy_round_end():
     run_round(ar, 0)
     torch.cuda.synchronize()
     ckpt = {name: getattr(ar, name).detach().clone() for name in ("x", "m", "s1_rep", "s2_rep")}
-    stale = any(not torch.equal(a, b) for a, b in zip(ar.views(ar.x_rep[0]), ar.views(ar.x)))
+    stale = any(not torch.equal(a, b) for a, b in zip(ar.views(ar.replica(0)), ar.views(ar.x)))
     assert stale, "the lazy round end left the replicas as they were"
     for t in range(cut, 3):
         run_round(ar, t)

@@ -27,12 +27,12 @@ def tensors(ar, flat):
     return [h[o:o + k].copy() for o, k in zip(ar.offsets, ar.numel)]
 
 
-def _run_variant(rule, n, broadcast, rounds, seed):
+def _run_variant(rule, n, broadcast, rounds, seed, layout=dsm.DSM_REPLICAS_CONTIGUOUS):
     adamw = rule == dsm.DSM_RULE_GLOBAL_ADAMW
     hp = ADAMW_GLOB if adamw else GLOB
     H = 2
     ar = A.Arenas(RAGGED, n, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, randomized=False,
-                  global_adamw=adamw)
+                  global_adamw=adamw, replica_layout=layout)
     gen = torch.Generator(device="cuda").manual_seed(seed)
     ar.x.normal_(0.0, 0.02, generator=gen)
     ar.init()
@@ -45,7 +45,7 @@ def _run_variant(rule, n, broadcast, rounds, seed):
             dsm.dsm_local_step(ar.ctx, -1, 1, **SGD)
         x0, m0 = tensors(ar, ar.x), tensors(ar, ar.m)
         v0 = tensors(ar, ar.v) if adamw else None
-        reps = [tensors(ar, ar.x_rep[i]) for i in range(n)]
+        reps = [tensors(ar, ar.replica(i)) for i in range(n)]
         dsm.dsm_global_step(ar.ctx, t, rule=rule, broadcast=broadcast, **hp)
         gx, gm = tensors(ar, ar.x), tensors(ar, ar.m)
         okw = dict(hp, decay=DECAY, t=t, rule=RULES[rule])
@@ -76,7 +76,7 @@ def _run_variant(rule, n, broadcast, rounds, seed):
         if broadcast:
             # Every replica equals x on the tensors' elements (padding untouched).
             for i in range(n):
-                for a, b in zip(ar.views(ar.x_rep[i]), ar.views(ar.x)):
+                for a, b in zip(ar.views(ar.replica(i)), ar.views(ar.x)):
                     assert torch.equal(a.view(torch.int32), b.view(torch.int32))
     ar.destroy()
     return nonbit
@@ -85,9 +85,11 @@ def _run_variant(rule, n, broadcast, rounds, seed):
 @pytest.mark.parametrize("rule", [dsm.DSM_RULE_LOOKAHEAD, dsm.DSM_RULE_SIGNED_SLOWMO,
                                   dsm.DSM_RULE_GLOBAL_ADAMW])
 @pytest.mark.parametrize("n,broadcast", [(1, True), (3, True), (4, False), (5, True)])
-def test_global_variant_parity(rule, n, broadcast):
-    nonbit = _run_variant(rule, n, broadcast, rounds=3, seed=31 * n + rule)
+@pytest.mark.parametrize("layout", [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_BLOCKED])
+def test_global_variant_parity(rule, n, broadcast, layout):
+    nonbit = _run_variant(rule, n, broadcast, rounds=3, seed=31 * n + rule, layout=layout)
     print(f"rule {rule} n={n}: {nonbit} elements not bit-identical to the fp32 oracle")
+    assert nonbit == 0
 
 
 def test_variant_argument_errors():

@@ -21,8 +21,17 @@ ROCM_INCLUDE = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "include")
 
 # (original text of dsm_runtime.cpp, planted mistake, what it breaks)
 MUTATIONS = [
-    ("const int64_t src_stride = from_x ? 0 : ctx->arena_elems;",
-     "const int64_t src_stride = ctx->arena_elems;", "stale workers read their own replica"),
+    ("const dsm::RepLayout sl = from_x ? dsm::single_copy() : ctx->rep;",
+     "const dsm::RepLayout sl = ctx->rep;", "stale workers read their own replica"),
+    ("const int64_t align = blocked ? dsm::kBlockedTensorAlign : dsm::kTensorAlign;",
+     "const int64_t align = dsm::kTensorAlign;", "blocked replicas without the piece alignment"),
+    ("    if (blocked) off = round_up(off, dsm::kRepBlockElems);\n", "",
+     "blocked arena not a whole number of blocks"),
+    ("                   ? dsm::blocked_copies(problem->n_workers)\n",
+     "                   ? dsm::contiguous_copies(L.arena_elems)\n",
+     "blocked replicas addressed as contiguous copies"),
+    ("    a.sl = from_x ? dsm::single_copy() : ctx->rep;", "    a.sl = ctx->rep;",
+     "round end after a lazy broadcast reads the stale replicas"),
     ("while (b < w0 + nw && ctx->stale[b] == ctx->stale[a]) ++b;",
      "while (b < w0 + nw) ++b;", "runs not split by replica source"),
     ("ctx->stale[i] = broadcast ? 0 : 1;", "ctx->stale[i] = 0;",
