@@ -7,6 +7,7 @@ H = 12 fused local AdamW steps over all replicas, then one fused global step
 input is resident in HBM before timing starts.  Prints one JSON line.
 
     python bench.py [--steps K] [--warmup W] [--workload xl] [--sign det|rand]
+                    [--path fused|split] [--replica-layout blocked|contiguous]
 """
 import argparse
 import hashlib
@@ -53,43 +54,172 @@ def committed_traffic(kernel_hash, workload, name):
     return None if k is None else k.get("bytes_per_launch")
 
 
-def cpu_baseline(w, ar, sample_tensors):
-    """The oracle (as it stands, fp64, one thread) on a bounded sample of the
-    same workload: one round of Algorithm 1 over a subset of the tensors."""
-    import numpy as np
-    import torch
-
-    import oracle as O
-
-    idx = [i for i, (name, _) in enumerate(w.tensors) if name in sample_tensors]
-    which = f"{len(idx)} tensors of transformer layer 0"
-    if not idx:                      # a workload with no transformer layer: all of it
-        idx = list(range(len(w.tensors)))
-        which = f"all {len(idx)} tensors"
-    torch.cuda.synchronize()
-
-    def take(flat):
-        h = [flat[ar.offsets[i]:ar.offsets[i] + ar.numel[i]].cpu().numpy() for i in idx]
-        return h
-    x0 = take(ar.x)
-    grads = [take(ar.g_rep[i]) for i in range(w.n_workers)]
-    d_s = int(sum(ar.numel[i] for i in idx))
-    decay = [w.decay[i] for i in idx]
+def _oracle_round_time(O, w, x0, grads, decay, prec):
+    """Seconds the oracle takes for one round of Algorithm 1 (n workers, H
+    local steps, deterministic global step) on the given whole tensors."""
     base = "adamw" if w.base == 0 else "sgd"
     st = O.init_state(x0, w.n_workers, base)
     t0 = time.perf_counter()
     O.communication_round(st, lambda i, k: grads[i], 0, H=w.local_steps, local=w.local,
-                          glob=dict(w.glob, mode=O.SIGN_DET, seed=0), decay=decay)
-    dt = time.perf_counter() - t0
-    updates = w.n_workers * w.local_steps * d_s + d_s
-    return {"value": updates / dt, "unit": "param-updates/s", "cores": 1, "kind": "oracle",
-            "sample": (f"one round (n={w.n_workers}, H={w.local_steps} {base} local steps + "
-                       f"deterministic global step) of the oracle in fp64 on the {which} "
-                       f"({d_s} of {w.d} parameters); "
-                       f"{dt:.1f} s on one host thread"),
-            "seconds": dt, "host_threads_available": len(os.sched_getaffinity(0)),
-            # every update is elementwise, so the rate carries over to the whole workload
-            "full_step_seconds_extrapolated": (w.n_workers * w.local_steps + 1) * w.d / (updates / dt)}
+                          glob=dict(w.glob, mode=O.SIGN_DET, seed=0), decay=decay, prec=prec)
+    return time.perf_counter() - t0
+
+
+def cpu_baseline(w, ar):
+    """The oracle as it stands (numpy, one host thread) on bounded samples of
+    the same workload: one round of Algorithm 1 over whole tensors, in fp64
+    (its accuracy mode) and in fp32 (the GPU path's arithmetic type).  The
+    samples cover every tensor shape class: fp64 runs on wpe, ln_f and
+    transformer layer 0, fp32 on wpe, ln_f and the last layer (each about
+    32M parameters at xl).  Every update is elementwise, so the rates carry
+    over to the whole workload (extrapolated, labelled so)."""
+    import torch
+
+    import oracle as O
+
+    names = [name for name, _ in w.tensors]
+    last = max((int(nm[1:].split(".")[0]) for nm in names if nm.startswith("h")), default=None)
+    subsets = {"fp64": ("h0.", "wpe", "ln_f."),
+               "fp32": (f"h{last}." if last is not None else "h0.", "wpe", "ln_f.")}
+    torch.cuda.synchronize()
+    out = {"unit": "param-updates/s", "cores": 1, "kind": "oracle",
+           "host_threads_available": len(os.sched_getaffinity(0))}
+    for prec, prefixes in subsets.items():
+        idx = [i for i, nm in enumerate(names) if nm.startswith(prefixes)]
+        if not idx:                       # a workload with no GPT-2 names: all of it
+            idx = list(range(len(names)))
+
+        def take(flat):
+            return [flat[ar.offsets[i]:ar.offsets[i] + ar.numel[i]].cpu().numpy() for i in idx]
+        x0 = take(ar.x)
+        grads = [take(ar.g_rep[i]) for i in range(w.n_workers)]
+        d_s = int(sum(ar.numel[i] for i in idx))
+        dt = _oracle_round_time(O, w, x0, grads, [w.decay[i] for i in idx], prec)
+        updates = w.n_workers * w.local_steps * d_s + d_s
+        out[prec] = {"value": updates / dt, "seconds": dt, "parameters": d_s,
+                     "tensors": ", ".join(sorted({names[i].split(".")[0] for i in idx})),
+                     "full_step_seconds_extrapolated":
+                         (w.n_workers * w.local_steps + 1) * w.d / (updates / dt)}
+    out["value"] = out["fp32"]["value"]
+    out["sample"] = (f"one round (n={w.n_workers}, H={w.local_steps} local steps + deterministic "
+                     f"global step) of the oracle on whole tensors, one host thread: fp32 on "
+                     f"{out['fp32']['tensors']} ({out['fp32']['parameters']} of {w.d} parameters, "
+                     f"{out['fp32']['seconds']:.1f} s), fp64 on {out['fp64']['tensors']} "
+                     f"({out['fp64']['parameters']} parameters, {out['fp64']['seconds']:.1f} s); "
+                     f"value is the fp32 rate")
+    return out
+
+
+def _sample_elements(ar, rng, n_random):
+    """(tensor p, in-tensor index j) pairs: the first and last four elements of
+    every tensor plus random ones spread by size."""
+    import numpy as np
+    ps, js = [], []
+    for p, k in enumerate(ar.numel):
+        if k == 0:
+            continue
+        e = np.unique(np.r_[np.arange(min(k, 4)), np.arange(max(k - 4, 0), k)])
+        ps.append(np.full(e.size, p))
+        js.append(e)
+    sizes = np.asarray(ar.numel, dtype=np.float64)
+    rp = rng.choice(len(ar.numel), size=n_random, p=sizes / sizes.sum())
+    rj = (rng.random(n_random) * sizes[rp]).astype(np.int64)
+    p = np.concatenate(ps + [rp]).astype(np.int64)
+    j = np.concatenate(js + [rj]).astype(np.int64)
+    key = np.unique(np.asarray(ar.offsets)[p] + j, return_index=True)[1]
+    return p[key], j[key]
+
+
+def parity_check(w, ar, run_round, t, mode, first_step, n_random=150_000):
+    """One more round of the timed path, untimed, checked against the oracle on
+    sampled elements: x and m, and every worker's base-optimizer state, bit for
+    bit against the fp32 oracle (Algorithm 1 with Algorithm 2/3 as the base);
+    the sign decisions of the global step against the fp64 oracle evaluated on
+    the same fp32 inputs, where a flip is allowed only inside the 1e-6 rms(u)
+    margin (Eq. (7), and Eqs. (9)/(10) for the randomized sign).  Every update
+    is elementwise given each tensor's bound, so sampled elements are exact;
+    the randomized sign takes each tensor's bound from the device."""
+    import numpy as np
+    import torch
+
+    import oracle as O
+    from paper_2411_17866_amd import dsm
+
+    n = w.n_workers
+    adamw = w.base == 0
+    p, j = _sample_elements(ar, np.random.default_rng(2411), n_random)
+    idx = torch.as_tensor(np.asarray(ar.offsets)[p] + j, device="cuda")
+    g = lambda t_: t_[idx].cpu().numpy().copy()
+    torch.cuda.synchronize()
+    x0, m0 = g(ar.x), g(ar.m)
+    s1 = [g(ar.s1_rep[i]) for i in range(n)]
+    s2 = [g(ar.s2_rep[i]) for i in range(n)] if adamw else None
+    grads = [g(ar.g_rep[i]) for i in range(n)]
+    run_round()
+    torch.cuda.synchronize()
+    got = {"x": g(ar.x), "m": g(ar.m)}
+    for i in range(n):
+        got[f"s1[{i}]"] = g(ar.s1_rep[i])
+        if adamw:
+            got[f"s2[{i}]"] = g(ar.s2_rep[i])
+    B = dsm.dsm_read_bounds(ar.ctx, len(ar.numel)) if mode != dsm.DSM_SIGN_DET else None
+    # The round's local steps, from the replicas equal to x (fresh after a
+    # broadcast, or stale and read as x after a lazy round end).
+    dec = np.asarray(w.decay)[p]
+    reps = [x0.copy() for _ in range(n)]
+    want = {}
+    for i in range(n):
+        xi, mi, vi = reps[i], s1[i], (s2[i] if adamw else None)
+        for k in range(w.local_steps):
+            for d_ in (True, False):
+                sel = dec == d_
+                if adamw:
+                    lw = dict(w.local, weight_decay=w.local["weight_decay"] if d_ else 0.0)
+                    a, b, c = O.local_adamw_step(xi[sel], grads[i][sel], mi[sel], vi[sel],
+                                                 step=first_step + k, prec="fp32", **lw)
+                    xi[sel], mi[sel], vi[sel] = a, b, c
+                else:
+                    a, b = O.local_sgdm_step(xi[sel], grads[i][sel], mi[sel], lr=w.local["lr"],
+                                             momentum=w.local["beta1"], prec="fp32")
+                    xi[sel], mi[sel] = a, b
+        want[f"s1[{i}]"] = mi
+        if adamw:
+            want[f"s2[{i}]"] = vi
+    # The global step, per tensor (the randomized sign needs each tensor's
+    # bound, its index and the in-tensor element indices for Philox).
+    tensors = np.unique(p)
+    sel = [p == q for q in tensors]
+    args = ([x0[s_] for s_ in sel], [m0[s_] for s_ in sel], [[r[s_] for s_ in sel] for r in reps])
+    kw = dict(gamma=w.local["lr"], decay=[w.decay[q] for q in tensors], t=t, mode=mode,
+              seed=w.philox_seed, tensor_ids=tensors, element_ids=[j[s_] for s_ in sel],
+              bounds=None if B is None else [B[q] for q in tensors], **w.glob)
+    o32 = O.global_step(*args, prec="fp32", **kw)
+    o64 = O.global_step(*args, prec="fp64", **kw)
+    want["x"], want["m"] = np.empty_like(x0), np.empty_like(m0)
+    flips = outside = 0
+    for a_, s_ in enumerate(sel):
+        want["x"][s_], want["m"][s_] = o32["x"][a_], o32["m"][a_]
+        S32, S64 = np.asarray(o32["S"][a_], np.float64), np.asarray(o64["S"][a_], np.float64)
+        flip = ~((S32 == S64) | (np.isnan(S32) & np.isnan(S64)))
+        if flip.any():
+            u64 = np.asarray(o64["u"][a_], np.float64)
+            margin = np.abs(u64[flip])
+            if mode != dsm.DSM_SIGN_DET:
+                U = O.randomized_sign_uniforms_at(j[s_], int(tensors[a_]), t, w.philox_seed)
+                U = U[flip].astype(np.float64) * 2.0 ** -24
+                thr = float(B[tensors[a_]]) * ((2 * U - 1) if mode == dsm.DSM_SIGN_RAND_FLIP else U)
+                margin = np.minimum(margin, np.abs(margin - thr))
+            rms_u = float(np.sqrt(np.mean(u64 * u64)))
+            flips += int(flip.sum())
+            outside += int(np.sum(~(margin < 1e-6 * rms_u)))
+    nonbit = sum(int(np.count_nonzero(got[k].view(np.uint32) != want[k].view(np.uint32)))
+                 for k in got)
+    return {"elements": int(p.size), "values_compared": int(sum(v.size for v in got.values())),
+            "non_bit_identical": nonbit, "flips_vs_fp64": flips,
+            "flips_outside_margin": outside,
+            "what": ("one untimed round of the timed path right after the timed region; x, m and "
+                     "every worker's optimizer state on the sampled elements against the fp32 "
+                     "oracle; sign decisions against the fp64 oracle on the same inputs")}
 
 
 def main():
@@ -110,6 +240,10 @@ def main():
                     help="if > 0, also time rounds in which every call follows a write of this "
                          "many MB to a separate buffer, which evicts the arenas from the caches "
                          "(reported under breakdown_flushed; the timed steps stay unflushed)")
+    ap.add_argument("--replica-layout", choices=("blocked", "contiguous"), default="blocked",
+                    help="how the replica buffer holds the n replicas (dsm_replica_layout)")
+    ap.add_argument("--no-parity", action="store_true",
+                    help="skip the oracle check of one untimed round after the timed region")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="accepted for the counter runs; the plain 4 GiB device copy that "
@@ -133,7 +267,10 @@ def main():
     adamw = w.base == W.BASE_ADAMW
     print(f"[bench] workload {w.name}: d={w.d} tensors={len(w.tensors)} n={n} H={H}",
           file=sys.stderr, flush=True)
-    ar = A.Arenas(w.numel, n, H, w.base, decay=w.decay, randomized=True, global_adamw=True)
+    layout = (dsm.DSM_REPLICAS_BLOCKED if args.replica_layout == "blocked"
+              else dsm.DSM_REPLICAS_CONTIGUOUS)
+    ar = A.Arenas(w.numel, n, H, w.base, decay=w.decay, randomized=True, global_adamw=True,
+                  replica_layout=layout)
     gen = torch.Generator(device="cuda").manual_seed(w.seed)
     W.fill_params_(ar.x, w, gen)
     for i in range(n):
@@ -233,6 +370,16 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     print("[bench] timed steps done", file=sys.stderr, flush=True)
+    # The state the timed steps produced, checked: one more round of the same
+    # path, untimed, against the oracle on sampled elements.
+    parity = None
+    if not args.no_parity:
+        parity = parity_check(w, ar, lambda: one_round(t, mode_main, args.path), t, mode_main,
+                              s_count[0] + 1)
+        t += 1
+        print(f"[bench] parity: {parity['non_bit_identical']} of {parity['values_compared']} "
+              f"values not bit-identical, {parity['flips_vs_fp64']} sign flips vs fp64",
+              file=sys.stderr, flush=True)
     # Breakdown: extra rounds of every path and sign combination.
     for path in ("fused", "split"):
         for mode in (dsm.DSM_SIGN_DET, dsm.DSM_SIGN_RAND_FLIP):
@@ -273,7 +420,7 @@ def main():
                 ("signed_slowmo", dsm.DSM_RULE_SIGNED_SLOWMO, w.glob),
                 ("global_adamw", dsm.DSM_RULE_GLOBAL_ADAMW,
                  dict(eta=1e-3, beta1=0.9, beta2=0.95, lam=w.glob["lam"], eps=1e-8)))
-    ctx_v = dsm.dsm_init(dsm.make_problem(w.numel, n, 1, w.base, w.decay), bufs)
+    ctx_v = dsm.dsm_init(dsm.make_problem(w.numel, n, 1, w.base, w.decay, layout), bufs)
     for key, rule, ghp in variants:
         for r in range(reps + 1):
             dsm.dsm_local_step(ctx_v, -1, r + 1, **w.local)
@@ -285,7 +432,8 @@ def main():
     # Row a2 (local SGD + Polyak momentum, Algorithm 3) and row a6 on its own
     # (dsm_sync) at the same scale: a context with the SGD base and room for
     # reps + 1 local steps in one round.
-    sgd_problem = dsm.make_problem(w.numel, n, reps + 1, dsm.DSM_BASE_SGD_MOMENTUM, w.decay)
+    sgd_problem = dsm.make_problem(w.numel, n, reps + 1, dsm.DSM_BASE_SGD_MOMENTUM, w.decay,
+                                   layout)
     bufs.s2_rep = None
     ctx2 = dsm.dsm_init(sgd_problem, bufs)
     ev_sgd, ev_sync = [], []
@@ -383,6 +531,7 @@ def main():
                          f"step ({args.path} path)"),
             "d": d, "n_workers": n, "local_steps": H, "base": "adamw" if adamw else "sgd_momentum",
             "sign": args.sign, "path": args.path, "updates_per_step": updates_per_step,
+            "replica_layout": args.replica_layout,
         },
         "roofline": {
             "bound": "hbm",
@@ -425,10 +574,10 @@ def main():
                            "torch_fill_GB_per_s": round(fill_gbs, 1)},
         "kernel_source_hash": khash,
     }
+    out["parity"] = parity
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(
-            w, ar, tuple(name for name, _ in w.tensors if name.startswith("h0.")))
+        out["cpu_baseline"] = cpu_baseline(w, ar)
     print(json.dumps(out), flush=True)
 
 

@@ -15,9 +15,11 @@ REQUIRED = ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step
             "higher_is_better", "scaling", "vs_baseline", "dtype", "data", "config", "roofline")
 
 
-def test_bench_prints_one_consistent_json_line():
+@pytest.mark.parametrize("extra", [[], ["--sign", "rand", "--path", "split",
+                                          "--replica-layout", "contiguous"]])
+def test_bench_prints_one_consistent_json_line(extra):
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--workload", "tiny",
-                        "--steps", "3", "--warmup", "1", "--extra-steps", "2"],
+                        "--steps", "3", "--warmup", "1", "--extra-steps", "2", *extra],
                        capture_output=True, text=True, timeout=600, cwd=ROOT)
     assert r.returncode == 0, r.stderr[-2000:]
     lines = [ln for ln in r.stdout.splitlines() if ln.strip()]
@@ -36,5 +38,10 @@ def test_bench_prints_one_consistent_json_line():
     assert roof["traffic"] is None or roof["traffic"] > 0
     cpu = out["cpu_baseline"]
     assert cpu["kind"] == "oracle" and cpu["cores"] >= 1 and cpu["value"] > 0 and cpu["sample"]
+    assert cpu["fp32"]["value"] > 0 and cpu["fp64"]["value"] > 0
+    # The untimed round after the timed ones matched the oracle.
+    par = out["parity"]
+    assert par["elements"] > 0 and par["values_compared"] >= par["elements"]
+    assert par["non_bit_identical"] == 0 and par["flips_outside_margin"] == 0
     for name, entry in out["breakdown"].items():
         assert entry is not None and entry["launches"] >= 2, name
