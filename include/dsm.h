@@ -193,6 +193,28 @@ DSM_API dsm_status dsm_init(const dsm_problem* problem, const dsm_buffers* buffe
                     dsm_ctx** out);
 
 /*
+ * dsm_init_static - dsm_init for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the context's workspace and the randomized sign's u staging
+ * live in a static array of the library, 64 MiB on each GPU it runs on, held
+ * until the process ends.  buffers->workspace, workspace_bytes and u_scratch
+ * are ignored; every other buffer is the caller's, as for dsm_init.  Nothing
+ * is allocated; the call uploads the chunk table and launches the
+ * initialisation kernel on buffers->stream like dsm_init.
+ * Limit: workspace_bytes (dsm_layout) rounded up to 256, plus 4 * d_pad
+ * rounded up to 256, at most 64 MiB (about 16M parameters).
+ * One such context may be alive per device at a time, since they would share
+ * the array: another dsm_init_static on that device fails until dsm_destroy.
+ * Calls on that context from several threads or streams at once race on the
+ * array, as they would on a workspace.
+ * Errors: as dsm_init; DSM_ERR_INVALID_ARG when the problem exceeds the limit;
+ * DSM_ERR_STATE while another context made by dsm_init_static is alive on
+ * the current device.
+ */
+DSM_API dsm_status dsm_init_static(const dsm_problem* problem, const dsm_buffers* buffers,
+                                   dsm_ctx** out);
+
+/*
  * dsm_local_step - one local step of Eq. (4), x^(i) <- x^(i) - gamma_t d^(i),
  * with d^(i) from the base optimizer (Algorithm 2 or 3) applied to the
  * direction input g_rep of worker `worker` (0..n-1), or of every worker in

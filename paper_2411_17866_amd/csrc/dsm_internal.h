@@ -174,4 +174,12 @@ hipError_t launch_broadcast(const Chunk* chunks, int64_t n_chunks, const float* 
 hipError_t launch_test_philox(uint32_t key0, uint32_t key1, uint32_t tensor, uint32_t t,
                               uint32_t q0, int64_t count, uint32_t* out, hipStream_t st);
 
+// The static device scratch of dsm_init_static: a file-scope array of
+// kStaticScratchBytes in dsm_kernels.hip, one copy per GPU.
+constexpr int64_t kStaticScratchBytes = int64_t(64) << 20;
+constexpr int kMaxDevices = 64;
+// Device address of the scratch on the current device, looked up once per
+// device (hipGetSymbolAddress) and kept.
+hipError_t static_scratch(void** ptr);
+
 }  // namespace dsm

@@ -14,6 +14,8 @@
 // square root, denormals kept.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "dsm_internal.h"
 #include "philox_device.h"
 
@@ -1046,6 +1048,32 @@ hipError_t launch_broadcast(const Chunk* chunks, int64_t n_chunks, const float* 
     hipLaunchKernelGGL(k_broadcast, chunk_grid(n_chunks, 1), dim3(kBlockThreads), 0, st, chunks, x,
                        x_rep, rl, n);
     return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- static scratch
+
+// Workspace and u staging of the contexts made by dsm_init_static, for
+// callers that cannot allocate device memory.  Host code never passes this
+// name to a kernel: it stands for a device address only through
+// hipGetSymbolAddress, below.
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+hipError_t static_scratch(void** ptr) {
+    static std::mutex mu;
+    static void* addr[kMaxDevices] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (addr[dev] == nullptr) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[dev] = p;
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
 }
 
 hipError_t launch_test_philox(uint32_t key0, uint32_t key1, uint32_t tensor, uint32_t t,

@@ -8,6 +8,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -30,12 +31,17 @@ struct dsm_ctx {
     std::vector<uint8_t> stale;    // replica not yet reset to x after a global step
                                    // without broadcast: its next local step reads x
     bool bounds_valid = false;     // the last global step was randomized
+    int static_device = -1;        // device whose static scratch the context holds (dsm_init_static)
     std::string last_error;
 };
 
 namespace {
 
 thread_local std::string g_last_error;
+
+// Which devices' static scratch a live context made by dsm_init_static holds.
+std::mutex g_static_mu;
+bool g_static_busy[dsm::kMaxDevices] = {};
 
 constexpr int64_t kMaxNumel = int64_t(1) << 34;
 // A launch has n_chunks * kSplit work-groups of kBlockThreads threads per
@@ -320,18 +326,59 @@ dsm_status dsm_layout(const dsm_problem* problem, int64_t* arena_elems, int64_t*
     return DSM_OK;
 }
 
-dsm_status dsm_init(const dsm_problem* problem, const dsm_buffers* b, dsm_ctx** out) {
+}  // extern "C"
+
+namespace {
+
+// dsm_init and dsm_init_static.  With use_static, the context's workspace and
+// the randomized sign's u staging are the static scratch of the current
+// device (the caller's workspace, workspace_bytes and u_scratch are ignored),
+// and the device is marked as held until dsm_destroy.
+dsm_status init_context(const dsm_problem* problem, const dsm_buffers* caller, dsm_ctx** out,
+                        bool use_static) {
     if (!out) return fail(nullptr, DSM_ERR_INVALID_ARG, "out is NULL");
     *out = nullptr;
     dsm_status st = check_problem(problem);
     if (st != DSM_OK) return st;
-    if (!b) return fail(nullptr, DSM_ERR_INVALID_ARG, "buffers is NULL");
+    if (!caller) return fail(nullptr, DSM_ERR_INVALID_ARG, "buffers is NULL");
     Layout L;
     std::vector<dsm::Chunk> chunks;
     std::vector<int32_t> chunk0;
     st = make_layout(problem, &L, &chunks, &chunk0);
     if (st != DSM_OK) return st;
     const bool adamw = problem->base == DSM_BASE_ADAMW;
+    dsm_buffers staged = *caller;
+    const dsm_buffers* b = &staged;
+    int device = -1;
+    std::unique_lock<std::mutex> hold;
+    if (use_static) {
+        const int64_t u_off = round_up(L.workspace_bytes, 256);
+        const int64_t need = u_off + round_up(L.arena_elems * 4, 256);
+        if (need > dsm::kStaticScratchBytes)
+            return fail(nullptr, DSM_ERR_INVALID_ARG,
+                        "problem needs %lld bytes of scratch (workspace and u staging); the "
+                        "static scratch of dsm_init_static holds %lld",
+                        static_cast<long long>(need),
+                        static_cast<long long>(dsm::kStaticScratchBytes));
+        st = check_device(nullptr);
+        if (st != DSM_OK) return st;
+        hipError_t e = hipGetDevice(&device);
+        if (e != hipSuccess) return hip_fail(nullptr, "querying the current device", e);
+        if (device < 0 || device >= dsm::kMaxDevices)
+            return fail(nullptr, DSM_ERR_UNSUPPORTED, "device %d beyond the static scratch table",
+                        device);
+        hold = std::unique_lock<std::mutex>(g_static_mu);
+        if (g_static_busy[device])
+            return fail(nullptr, DSM_ERR_STATE,
+                        "a context made by dsm_init_static is alive on device %d; destroy it first",
+                        device);
+        void* scratch = nullptr;
+        e = dsm::static_scratch(&scratch);
+        if (e != hipSuccess) return hip_fail(nullptr, "finding the static scratch", e);
+        staged.workspace = scratch;
+        staged.workspace_bytes = L.workspace_bytes;
+        staged.u_scratch = reinterpret_cast<float*>(static_cast<char*>(scratch) + u_off);
+    }
     if (L.arena_elems > 0) {
         struct {
             const void* p;
@@ -415,8 +462,25 @@ dsm_status dsm_init(const dsm_problem* problem, const dsm_buffers* b, dsm_ctx** 
             return r;
         }
     }
+    if (use_static) {
+        ctx->static_device = device;
+        g_static_busy[device] = true;
+    }
     *out = ctx;
     return DSM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+dsm_status dsm_init(const dsm_problem* problem, const dsm_buffers* buffers, dsm_ctx** out) {
+    return init_context(problem, buffers, out, false);
+}
+
+dsm_status dsm_init_static(const dsm_problem* problem, const dsm_buffers* buffers,
+                           dsm_ctx** out) {
+    return init_context(problem, buffers, out, true);
 }
 
 dsm_status dsm_local_step(dsm_ctx* ctx, int32_t worker, int64_t step, const dsm_local_hparams* hp) {
@@ -598,6 +662,12 @@ dsm_status dsm_test_philox(uint64_t seed, uint32_t tensor, int64_t t, int64_t q0
 dsm_status dsm_destroy(dsm_ctx* ctx) {
     if (!ctx) return DSM_OK;
     hipError_t e = hipStreamSynchronize(ctx->stream);
+    if (ctx->static_device >= 0) {
+        // The context's work has drained (or the stream failed); the next
+        // dsm_init_static on this device may reuse the scratch.
+        std::lock_guard<std::mutex> lock(g_static_mu);
+        g_static_busy[ctx->static_device] = false;
+    }
     delete ctx;
     if (e != hipSuccess) return hip_fail(nullptr, "synchronising the stream at destroy", e);
     return DSM_OK;

@@ -37,8 +37,8 @@ DSM_REPLICAS_CONTIGUOUS = 0
 DSM_REPLICAS_BLOCKED = 1
 DSM_REPLICA_BLOCK_ELEMS = 16384
 
-EXPORTED = ("dsm_layout", "dsm_init", "dsm_local_step", "dsm_global_step", "dsm_round_end",
-            "dsm_sync",
+EXPORTED = ("dsm_layout", "dsm_init", "dsm_init_static", "dsm_local_step", "dsm_global_step",
+            "dsm_round_end", "dsm_sync",
             "dsm_read_bounds", "dsm_test_philox", "dsm_destroy", "dsm_last_error")
 
 
@@ -92,6 +92,8 @@ def load_library(path=LIBPATH):
     lib.dsm_layout.argtypes = [ctypes.POINTER(dsm_problem), c_int64_p, c_int64_p, c_int64_p]
     lib.dsm_init.argtypes = [ctypes.POINTER(dsm_problem), ctypes.POINTER(dsm_buffers),
                              ctypes.POINTER(ctypes.c_void_p)]
+    lib.dsm_init_static.argtypes = [ctypes.POINTER(dsm_problem), ctypes.POINTER(dsm_buffers),
+                                    ctypes.POINTER(ctypes.c_void_p)]
     lib.dsm_local_step.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
                                    ctypes.POINTER(dsm_local_hparams)]
     lib.dsm_global_step.argtypes = [ctypes.c_void_p, ctypes.c_int64,
@@ -156,6 +158,15 @@ def dsm_init(problem, buffers):
     lib = load_library()
     ctx = ctypes.c_void_p()
     _check(lib.dsm_init(ctypes.byref(problem), ctypes.byref(buffers), ctypes.byref(ctx)))
+    return ctx.value
+
+
+def dsm_init_static(problem, buffers):
+    """dsm_init with the workspace and u staging in the library's static
+    scratch (buffers.workspace and u_scratch are ignored)."""
+    lib = load_library()
+    ctx = ctypes.c_void_p()
+    _check(lib.dsm_init_static(ctypes.byref(problem), ctypes.byref(buffers), ctypes.byref(ctx)))
     return ctx.value
 
 

@@ -31,6 +31,9 @@
 namespace {
 
 int g_devices = 1;
+int g_device = 0;            // hipGetDevice's answer
+void* g_scratch = nullptr;   // host stand-in for the static device scratch
+int g_scratch_lookups = 0;
 hipError_t g_launch_status = hipSuccess;
 int g_failures = 0;
 int g_checks = 0;
@@ -90,6 +93,10 @@ hipError_t hipMemcpyAsync(void* dst, const void* src, size_t bytes, hipMemcpyKin
     return hipSuccess;
 }
 hipError_t hipStreamSynchronize(hipStream_t) { return hipSuccess; }
+hipError_t hipGetDevice(int* device) {
+    *device = g_device;
+    return hipSuccess;
+}
 }
 
 // ------------------------------------------------------------ launcher stubs
@@ -237,6 +244,15 @@ hipError_t launch_broadcast(const Chunk* chunks, int64_t n_chunks, const float* 
     l.rl = rl;
     l.n_workers = n;
     return record(l);
+}
+hipError_t static_scratch(void** ptr) {
+    ++g_scratch_lookups;
+    if (g_scratch == nullptr) {
+        g_scratch = std::aligned_alloc(256, static_cast<size_t>(kStaticScratchBytes));
+        std::memset(g_scratch, 0x5A, static_cast<size_t>(kStaticScratchBytes));
+    }
+    *ptr = g_scratch;
+    return hipSuccess;
 }
 hipError_t launch_test_philox(uint32_t, uint32_t, uint32_t, uint32_t, uint32_t, int64_t,
                               uint32_t* out, hipStream_t) {
@@ -980,10 +996,86 @@ void check_blocked_addressing() {
     }
 }
 
+// dsm_init_static: the workspace and the u staging come from the static
+// scratch (the caller's are ignored), the size limit, one live context per
+// device, and the device released by dsm_destroy.
+void check_init_static() {
+    Problem P({100, 16385, 7}, 3, 2, DSM_BASE_ADAMW, {1, 1, 0}, DSM_REPLICAS_BLOCKED);
+    Buffers B(P, false, false);            // no u_scratch of its own
+    B.b.workspace = nullptr;               // and no workspace
+    B.b.workspace_bytes = 0;
+    int64_t arena = 0, ws = 0;
+    CHECK(dsm_layout(&P.p, &arena, nullptr, &ws) == DSM_OK, "layout");
+    dsm_ctx* a = nullptr;
+    g_log.clear();
+    CHECK(dsm_init_static(&P.p, &B.b, &a) == DSM_OK && a != nullptr, "static init: %s",
+          dsm_last_error(nullptr));
+    CHECK(g_log.size() == 1 && g_log[0].kind == "init" && g_log[0].chunks == g_scratch &&
+              same_layout(g_log[0].rl, B.rep),
+          "the chunk table lives in the static scratch");
+    const auto* c = static_cast<const dsm::Chunk*>(g_scratch);
+    CHECK(c[0].tensor == 0 && c[0].len == 100 && c[1].tensor == 1 && c[1].len == 16384,
+          "chunk table uploaded into the scratch");
+    // A second static context on the same device is refused; on another
+    // device it is allowed.
+    dsm_ctx* b2 = nullptr;
+    CHECK(dsm_init_static(&P.p, &B.b, &b2) == DSM_ERR_STATE && b2 == nullptr,
+          "second static context on device 0");
+    CHECK(std::strstr(dsm_last_error(nullptr), "dsm_init_static") != nullptr, "busy message");
+    // The randomized global step takes u from the scratch, after the workspace.
+    const dsm_local_hparams lh = adam_hp();
+    for (int k = 0; k < 2; ++k) CHECK(dsm_local_step(a, -1, k + 1, &lh) == DSM_OK, "local");
+    const dsm_global_hparams gr = glob_hp(DSM_SIGN_RAND_FLIP);
+    g_log.clear();
+    CHECK(dsm_global_step(a, 0, &gr, 1) == DSM_OK, "randomized step: %s", dsm_last_error(a));
+    if (g_log.size() == 1) {
+        const char* base = static_cast<const char*>(g_scratch);
+        CHECK(reinterpret_cast<const char*>(g_log[0].u) == base + round_up(ws, 256),
+              "u staging follows the workspace in the scratch");
+        CHECK(reinterpret_cast<const char*>(g_log[0].u) + arena * 4 <=
+                  base + dsm::kStaticScratchBytes,
+              "u staging inside the scratch");
+        B.b.workspace = g_scratch;         // where the words must be
+        B.b.workspace_bytes = ws;
+        check_bound_words(P, B, g_log[0].bounds, g_log[0].chunk0, g_log[0].piece_max, "static");
+    }
+    CHECK(dsm_destroy(a) == DSM_OK, "destroy");
+    // Released: the device's scratch can be taken again, by a smaller problem.
+    Problem Q({5000}, 2, 1, DSM_BASE_SGD_MOMENTUM);
+    Buffers C(Q, true, false);
+    dsm_ctx* q = nullptr;
+    CHECK(dsm_init_static(&Q.p, &C.b, &q) == DSM_OK, "static init after destroy");
+    CHECK(dsm_destroy(q) == DSM_OK, "destroy");
+    // Too large for the scratch: refused with the sizes, nothing launched.
+    const int64_t big = (dsm::kStaticScratchBytes / 4) + 1;
+    Problem R_({big}, 1, 1, DSM_BASE_SGD_MOMENTUM);
+    std::vector<uint8_t> dummy(512);
+    dsm_buffers rb{};
+    rb.x = rb.m = rb.x_rep = rb.g_rep = rb.s1_rep = reinterpret_cast<float*>(
+        reinterpret_cast<uintptr_t>(dummy.data() + 255) & ~uintptr_t(255));
+    g_log.clear();
+    dsm_ctx* r = nullptr;
+    CHECK(dsm_init_static(&R_.p, &rb, &r) == DSM_ERR_INVALID_ARG && r == nullptr,
+          "problem beyond the static scratch");
+    CHECK(std::strstr(dsm_last_error(nullptr), "static scratch") != nullptr, "limit message");
+    CHECK(g_log.empty(), "nothing launched for a rejected static context");
+    // Device 1: its own scratch slot, independent of device 0's.
+    g_device = 1;
+    dsm_ctx* d1 = nullptr;
+    dsm_ctx* d0 = nullptr;
+    CHECK(dsm_init_static(&Q.p, &C.b, &d1) == DSM_OK, "static context on device 1");
+    g_device = 0;
+    CHECK(dsm_init_static(&Q.p, &C.b, &d0) == DSM_OK, "and one on device 0");
+    CHECK(dsm_destroy(d1) == DSM_OK && dsm_destroy(d0) == DSM_OK, "destroy both");
+    std::free(g_scratch);
+    g_scratch = nullptr;
+}
+
 int main() {
     check_layout_fuzz();
     check_init_and_chunks();
     check_init_rejections();
+    check_init_static();
     check_blocked_addressing();
     for (int layout : {DSM_REPLICAS_CONTIGUOUS, DSM_REPLICAS_BLOCKED}) {
         check_state_machine_adamw(layout);

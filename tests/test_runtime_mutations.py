@@ -32,6 +32,13 @@ MUTATIONS = [
      "blocked replicas addressed as contiguous copies"),
     ("    a.sl = from_x ? dsm::single_copy() : ctx->rep;", "    a.sl = ctx->rep;",
      "round end after a lazy broadcast reads the stale replicas"),
+    ("        g_static_busy[ctx->static_device] = false;\n", "",
+     "a static-scratch context never releases its device"),
+    ("        if (need > dsm::kStaticScratchBytes)", "        if (need > 2 * dsm::kStaticScratchBytes)",
+     "static scratch limit not enforced"),
+    ("        staged.u_scratch = reinterpret_cast<float*>(static_cast<char*>(scratch) + u_off);",
+     "        staged.u_scratch = reinterpret_cast<float*>(scratch);",
+     "u staging over the static workspace"),
     ("while (b < w0 + nw && ctx->stale[b] == ctx->stale[a]) ++b;",
      "while (b < w0 + nw) ++b;", "runs not split by replica source"),
     ("ctx->stale[i] = broadcast ? 0 : 1;", "ctx->stale[i] = 0;",
