@@ -73,6 +73,7 @@ def cpu_baseline(w, ar):
     transformer layer 0, fp32 on wpe, ln_f and the last layer (each about
     32M parameters at xl).  Every update is elementwise, so the rates carry
     over to the whole workload (extrapolated, labelled so)."""
+    import numpy as np
     import torch
 
     import oracle as O
@@ -92,7 +93,14 @@ def cpu_baseline(w, ar):
         def take(flat):
             return [flat[ar.offsets[i]:ar.offsets[i] + ar.numel[i]].cpu().numpy() for i in idx]
         x0 = take(ar.x)
-        grads = [take(ar.g_rep[i]) for i in range(w.n_workers)]
+        elems = torch.cat([torch.arange(ar.offsets[i], ar.offsets[i] + ar.numel[i], device="cuda")
+                           for i in idx])
+        bounds = np.cumsum([0] + [ar.numel[i] for i in idx])
+        grads = []
+        for k in range(w.n_workers):
+            gk = ar.gather("g_rep", k, elems).cpu().numpy()
+            grads.append([gk[bounds[a]:bounds[a + 1]] for a in range(len(idx))])
+        del elems
         d_s = int(sum(ar.numel[i] for i in idx))
         dt = _oracle_round_time(O, w, x0, grads, [w.decay[i] for i in idx], prec)
         updates = w.n_workers * w.local_steps * d_s + d_s
@@ -151,17 +159,18 @@ def parity_check(w, ar, run_round, t, mode, first_step, n_random=150_000):
     idx = torch.as_tensor(np.asarray(ar.offsets)[p] + j, device="cuda")
     g = lambda t_: t_[idx].cpu().numpy().copy()
     torch.cuda.synchronize()
+    gw = lambda name, i: ar.gather(name, i, idx).cpu().numpy().copy()
     x0, m0 = g(ar.x), g(ar.m)
-    s1 = [g(ar.s1_rep[i]) for i in range(n)]
-    s2 = [g(ar.s2_rep[i]) for i in range(n)] if adamw else None
-    grads = [g(ar.g_rep[i]) for i in range(n)]
+    s1 = [gw("s1_rep", i) for i in range(n)]
+    s2 = [gw("s2_rep", i) for i in range(n)] if adamw else None
+    grads = [gw("g_rep", i) for i in range(n)]
     run_round()
     torch.cuda.synchronize()
     got = {"x": g(ar.x), "m": g(ar.m)}
     for i in range(n):
-        got[f"s1[{i}]"] = g(ar.s1_rep[i])
+        got[f"s1[{i}]"] = gw("s1_rep", i)
         if adamw:
-            got[f"s2[{i}]"] = g(ar.s2_rep[i])
+            got[f"s2[{i}]"] = gw("s2_rep", i)
     B = dsm.dsm_read_bounds(ar.ctx, len(ar.numel)) if mode != dsm.DSM_SIGN_DET else None
     # The round's local steps, from the replicas equal to x (fresh after a
     # broadcast, or stale and read as x after a lazy round end).
@@ -240,8 +249,10 @@ def main():
                     help="if > 0, also time rounds in which every call follows a write of this "
                          "many MB to a separate buffer, which evicts the arenas from the caches "
                          "(reported under breakdown_flushed; the timed steps stay unflushed)")
-    ap.add_argument("--replica-layout", choices=("blocked", "contiguous"), default="blocked",
-                    help="how the replica buffer holds the n replicas (dsm_replica_layout)")
+    ap.add_argument("--replica-layout", choices=("auto", "state-blocked", "blocked", "contiguous"),
+                    default="auto",
+                    help="how the per-worker buffers hold their n copies (dsm_replica_layout); "
+                         "auto: state-blocked for n <= 4, blocked replicas otherwise")
     ap.add_argument("--no-parity", action="store_true",
                     help="skip the oracle check of one untimed round after the timed region")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -267,8 +278,10 @@ def main():
     adamw = w.base == W.BASE_ADAMW
     print(f"[bench] workload {w.name}: d={w.d} tensors={len(w.tensors)} n={n} H={H}",
           file=sys.stderr, flush=True)
-    layout = (dsm.DSM_REPLICAS_BLOCKED if args.replica_layout == "blocked"
-              else dsm.DSM_REPLICAS_CONTIGUOUS)
+    if args.replica_layout == "auto":
+        args.replica_layout = "state-blocked" if n <= 4 else "blocked"
+    layout = {"state-blocked": dsm.DSM_REPLICAS_STATE_BLOCKED, "blocked": dsm.DSM_REPLICAS_BLOCKED,
+              "contiguous": dsm.DSM_REPLICAS_CONTIGUOUS}[args.replica_layout]
     ar = A.Arenas(w.numel, n, H, w.base, decay=w.decay, randomized=True, global_adamw=True,
                   replica_layout=layout)
     gen = torch.Generator(device="cuda").manual_seed(w.seed)

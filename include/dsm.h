@@ -84,11 +84,11 @@ typedef enum dsm_global_rule {
 } dsm_global_rule;
 
 /* How the n worker replicas x_rep share their buffer (dsm_problem.replica_layout).
- * The other per-worker buffers (g_rep, s1_rep, s2_rep) always hold n
- * contiguous copies. */
+ * The other per-worker buffers (g_rep, s1_rep, s2_rep) hold n contiguous
+ * copies, except in DSM_REPLICAS_STATE_BLOCKED. */
 typedef enum dsm_replica_layout {
     DSM_REPLICAS_CONTIGUOUS = 0, /* copy i at element offset i * d_pad */
-    DSM_REPLICAS_BLOCKED = 1     /* 64 KiB blocks interleaved by worker: element e of
+    DSM_REPLICAS_BLOCKED = 1,    /* 64 KiB blocks interleaved by worker: element e of
                                     copy i at ((e / 16384) * n + i) * 16384 + e % 16384.
                                     A work-group's n replica accesses then fall in one
                                     n * 64 KiB span instead of n spans d_pad apart; the
@@ -96,8 +96,22 @@ typedef enum dsm_replica_layout {
                                     every replica, keep their bandwidth in every
                                     physical placement.  d_pad is a multiple of 16384
                                     and tensors start on multiples of 1024 elements. */
+    DSM_REPLICAS_STATE_BLOCKED = 2 /* the replicas and their state in one allocation of
+                                    B * n * d_pad floats (B = 4 for AdamW, 3 for SGD) in
+                                    16 KiB blocks: block b holds the n x_rep copies, then
+                                    the n g_rep, the n s1_rep and (AdamW) the n s2_rep
+                                    copies of elements [4096 b, 4096 b + 4096), so element
+                                    e of copy i of buffer j is at ((e / 4096) * B * n +
+                                    j * n + i) * 4096 + e % 4096.  Pass x_rep = the
+                                    allocation, g_rep = x_rep + n * 4096, s1_rep = x_rep
+                                    + 2 n * 4096, s2_rep = x_rep + 3 n * 4096.  The
+                                    streams a work-group touches then share one
+                                    B * n * 16 KiB span; the local step measured faster
+                                    at n = 4.  d_pad is a multiple of 4096, tensors start
+                                    on multiples of 1024 elements. */
 } dsm_replica_layout;
 #define DSM_REPLICA_BLOCK_ELEMS 16384
+#define DSM_STATE_BLOCK_ELEMS 4096
 
 /* The problem of Eq. (1): x in R^d given as n_tensors tensors. */
 typedef struct dsm_problem {
@@ -113,7 +127,8 @@ typedef struct dsm_problem {
 
 /* Device buffers, all fp32 arenas of d_pad elements per copy.  The replica
  * buffers hold n copies (copy i of g_rep, s1_rep, s2_rep at element offset
- * i * d_pad; x_rep as problem->replica_layout says). */
+ * i * d_pad, x_rep as problem->replica_layout says; all four as that layout
+ * says in DSM_REPLICAS_STATE_BLOCKED). */
 typedef struct dsm_buffers {
     float* x;          /* [d_pad]      global model x_{t,0} (in/out) */
     float* m;          /* [d_pad]      global momentum m_t (zeroed by init) */

@@ -27,8 +27,10 @@ class Arenas:
     replica_layout: how x_rep holds the replicas (dsm_replica_layout).
 
     x_rep is an (n, d_pad) view with contiguous replicas, and an (n, blocks,
-    16384) strided view of the same memory with blocked replicas;
-    replica(i), replicas() and replica_index() read either the same way.
+    16384) strided view of the same memory with blocked replicas.  With the
+    replicas and their state blocked, x_rep, g_rep, s1_rep and s2_rep are
+    (n, blocks, 4096) strided views of one allocation.  worker(), workers(),
+    gather(), replica() and replicas() read every layout the same way.
     """
 
     def __init__(self, numel, n_workers, local_steps, base, decay=None, randomized=True,
@@ -46,10 +48,10 @@ class Arenas:
         self._storage = []
         self._k = 0
 
-        def alloc(*shape):
+        def alloc(*shape, stagger=True):
             # A view at a buffer-specific offset (a multiple of 64 floats, so
             # 256-byte alignment is kept) into a slightly larger allocation.
-            pad = self._k * STAGGER_FLOATS
+            pad = self._k * STAGGER_FLOATS if stagger else 0
             self._k += 1
             count = 1
             for s_ in shape:
@@ -60,15 +62,27 @@ class Arenas:
 
         self.x = alloc(a)
         self.m = alloc(a)
-        self.x_rep_flat = alloc(self.n * a)
-        if self.blocked and self.arena_elems > 0:
-            B = dsm.DSM_REPLICA_BLOCK_ELEMS
-            self.x_rep = self.x_rep_flat.view(a // B, self.n, B).permute(1, 0, 2)
+        adamw = self.base == dsm.DSM_BASE_ADAMW
+        self.n_state_buffers = 4 if adamw else 3
+        if self.state_blocked and self.arena_elems > 0:
+            # One allocation; block b holds the n copies of x_rep, g_rep,
+            # s1_rep (and s2_rep) of elements [4096 b, 4096 b + 4096).
+            K = dsm.DSM_STATE_BLOCK_ELEMS
+            # Unstaggered, so the blocks keep their place in the 2 MiB pages.
+            self.x_rep_flat = alloc(self.n_state_buffers * self.n * a, stagger=False)
+            sup = self.x_rep_flat.view(a // K, self.n_state_buffers, self.n, K)
+            self.x_rep, self.g_rep, self.s1_rep = (sup[:, j].permute(1, 0, 2) for j in range(3))
+            self.s2_rep = sup[:, 3].permute(1, 0, 2) if adamw else None
         else:
-            self.x_rep = self.x_rep_flat.view(self.n, a)
-        self.g_rep = alloc(self.n, a)
-        self.s1_rep = alloc(self.n, a)
-        self.s2_rep = alloc(self.n, a) if self.base == dsm.DSM_BASE_ADAMW else None
+            self.x_rep_flat = alloc(self.n * a)
+            if self.blocked and self.arena_elems > 0:
+                B = dsm.DSM_REPLICA_BLOCK_ELEMS
+                self.x_rep = self.x_rep_flat.view(a // B, self.n, B).permute(1, 0, 2)
+            else:
+                self.x_rep = self.x_rep_flat.view(self.n, a)
+            self.g_rep = alloc(self.n, a)
+            self.s1_rep = alloc(self.n, a)
+            self.s2_rep = alloc(self.n, a) if adamw else None
         self.u = alloc(a) if randomized else None
         self.v = alloc(a) if global_adamw else None
         self.workspace = torch.zeros(max(self.workspace_bytes, 256), dtype=torch.uint8,
@@ -95,9 +109,25 @@ class Arenas:
     def blocked(self):
         return self.replica_layout == dsm.DSM_REPLICAS_BLOCKED
 
+    @property
+    def state_blocked(self):
+        return self.replica_layout == dsm.DSM_REPLICAS_STATE_BLOCKED
+
+    _STATE_ORDER = ("x_rep", "g_rep", "s1_rep", "s2_rep")
+
     def replica_index(self, i, e):
         """Index into x_rep_flat of element(s) e (arena indices) of replica i."""
-        if self.blocked:
+        return self.state_index("x_rep", i, e)
+
+    def state_index(self, name, i, e):
+        """Index of element(s) e of worker i's copy of a per-worker buffer:
+        into x_rep_flat for x_rep (and for every buffer when state-blocked),
+        else into the buffer's own (n, d_pad) arena."""
+        if self.state_blocked:
+            K = dsm.DSM_STATE_BLOCK_ELEMS
+            j = self._STATE_ORDER.index(name)
+            return (e // K) * (self.n_state_buffers * self.n * K) + (j * self.n + i) * K + e % K
+        if name == "x_rep" and self.blocked:
             B = dsm.DSM_REPLICA_BLOCK_ELEMS
             return (e // B) * (self.n * B) + i * B + e % B
         return i * self.arena_elems + e
@@ -108,14 +138,19 @@ class Arenas:
 
     def worker(self, name, i):
         """Worker i's copy of a per-worker buffer ("x_rep", "g_rep", "s1_rep" or
-        "s2_rep") as a 1-D arena (a copy for blocked replicas)."""
-        return self.replica(i) if name == "x_rep" else getattr(self, name)[i]
+        "s2_rep") as a 1-D arena (a view when contiguous, else a copy)."""
+        return getattr(self, name)[i].reshape(-1)
+
+    def workers(self, name):
+        """All n copies of a per-worker buffer as (n, d_pad) (a view when
+        contiguous, else a copy)."""
+        return getattr(self, name).reshape(self.n, -1)
 
     def gather(self, name, i, idx):
         """Elements idx (arena indices, a device tensor) of worker i's copy of a
-        per-worker buffer, without materialising a blocked replica."""
-        if name == "x_rep":
-            return self.x_rep_flat[self.replica_index(i, idx)]
+        per-worker buffer, without materialising a blocked copy."""
+        if self.state_blocked or (name == "x_rep" and self.blocked):
+            return self.x_rep_flat[self.state_index(name, i, idx)]
         return getattr(self, name)[i][idx]
 
     def replicas(self):

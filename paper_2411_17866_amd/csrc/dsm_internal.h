@@ -68,6 +68,25 @@ inline RepLayout blocked_copies(int n) {
 // Every copy is the same single buffer (stale replicas read the global x).
 inline RepLayout single_copy() { return RepLayout{0, 0, 62, 0}; }
 
+// The replicas and their state in one allocation (dsm_problem.replica_layout =
+// DSM_REPLICAS_STATE_BLOCKED): 16 KiB blocks, and block b holds the n x_rep
+// copies, then the n g_rep copies, the n s1_rep copies and (AdamW) the n
+// s2_rep copies of elements [4096 b, 4096 b + 4096).  Buffer j of the
+// kStateBuffers starts j * n blocks into the allocation.
+constexpr int kStateBlockShift = 12;
+constexpr int64_t kStateBlockElems = int64_t(1) << kStateBlockShift;
+static_assert(kStateBlockElems % kPieceElems == 0, "a state block must hold whole pieces");
+inline RepLayout state_blocked_copies(int n, int buffers) {
+    return RepLayout{int64_t(buffers) * n * kStateBlockElems, kStateBlockElems, kStateBlockShift,
+                     0};
+}
+
+// Where the gradient and the base-optimizer moments of worker i keep their
+// elements (the same RepLayout addressing as the replicas).
+struct StateLayout {
+    RepLayout g, s1, s2;
+};
+
 // One chunk of one tensor inside an arena copy.  32 bytes.
 struct Chunk {
     int64_t off;      // element offset of the chunk in the arena
@@ -113,28 +132,28 @@ struct GlobalScalars {
 };
 
 // Kernel launchers (dsm_kernels.hip).  All return the launch status.  The
-// replica buffer x_rep is addressed through its RepLayout rl; g_rep, s1 and
-// s2 hold n contiguous copies of stride elements.
+// replica buffer x_rep is addressed through its RepLayout rl, and g_rep, s1
+// and s2 through the layouts of ml.
 hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float* m, float* v,
-                       float* x_rep, RepLayout rl, float* s1, float* s2, int64_t stride, int n,
+                       float* x_rep, RepLayout rl, float* s1, float* s2, StateLayout ml, int n,
                        hipStream_t st);
 // Local steps: worker w reads its starting point from x_src through sl (its
 // replica, or the shared global model with single_copy()) and writes its
 // replica through rl.
 hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_rep, RepLayout rl,
                               const float* x_src, RepLayout sl, const float* g_rep, float* s1,
-                              float* s2, int64_t stride, int worker0, int n_workers,
+                              float* s2, StateLayout ml, int worker0, int n_workers,
                               const AdamScalars& sc, hipStream_t st);
 hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep, RepLayout rl,
                              const float* x_src, RepLayout sl, const float* g_rep, float* s1,
-                             int64_t stride, int worker0, int n_workers, const SgdScalars& sc,
+                             StateLayout ml, int worker0, int n_workers, const SgdScalars& sc,
                              hipStream_t st);
 
 // Local step of all n workers from the global model x (every replica stale):
 // x is read once per element and each worker's result goes to its replica.
 hipError_t launch_local_from_x(const Chunk* chunks, int64_t n_chunks, const float* x,
                                float* x_rep, RepLayout rl, const float* g_rep, float* s1,
-                               float* s2, int64_t stride, int n, bool adamw,
+                               float* s2, StateLayout ml, int n, bool adamw,
                                const AdamScalars& as, const SgdScalars& ss, hipStream_t st);
 
 // Workspace words of the randomized sign's per-tensor bound B_p = max |u|,
@@ -154,7 +173,7 @@ struct RoundEndArgs {
     const float* g_rep;
     float *s1, *s2, *u;
     BoundWords bound;
-    int64_t stride;
+    StateLayout ml;
     AdamScalars as;
     SgdScalars ss;
     GlobalScalars gs;

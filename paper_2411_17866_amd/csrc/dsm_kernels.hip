@@ -177,21 +177,21 @@ __device__ __forceinline__ void adamw4(f4& x, f4 g, f4& m, f4& v, float lam, con
 // Worker w reads its step's starting point at x_src + rep_index(sl, w, e)
 // (its own replica, or with a zero copy stride the global model x when the
 // replicas are stale after a global step without broadcast) and writes the
-// result to its replica, x_rep + rep_index(rl, w, e).  The two may be the
+// result to its replica, x_rep + rep_index(rl, w, e); its gradient and
+// moments sit at rep_index(ml.g / ml.s1 / ml.s2, w, e) of their buffers.  The two may be the
 // same memory, so neither pointer is __restrict__; each thread loads every
 // stream of its group before it stores.
 __global__ __launch_bounds__(kBlockThreads) void k_local_adamw(
     const Chunk* __restrict__ chunks, float* x_rep, RepLayout rl, const float* x_src,
     RepLayout sl, const float* __restrict__ g_rep, float* __restrict__ s1,
-    float* __restrict__ s2, int64_t stride, int worker0, AdamScalars sc) {
+    float* __restrict__ s2, StateLayout ml, int worker0, AdamScalars sc) {
     const Piece pc = piece_of<kMapLocal>(chunks);
     const int64_t w = worker0 + static_cast<int>(blockIdx.y);
-    const int64_t wo = w * stride + pc.e0;
     f4* xp = reinterpret_cast<f4*>(x_rep + rep_index(rl, w, pc.e0));
     const f4* xs = reinterpret_cast<const f4*>(x_src + rep_index(sl, w, pc.e0));
-    const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + wo);
-    f4* __restrict__ mp = reinterpret_cast<f4*>(s1 + wo);
-    f4* __restrict__ vp = reinterpret_cast<f4*>(s2 + wo);
+    const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + rep_index(ml.g, w, pc.e0));
+    f4* __restrict__ mp = reinterpret_cast<f4*>(s1 + rep_index(ml.s1, w, pc.e0));
+    f4* __restrict__ vp = reinterpret_cast<f4*>(s2 + rep_index(ml.s2, w, pc.e0));
     const float lam = pc.c.decay ? sc.wd : 0.0f;
     for (int q0 = threadIdx.x; q0 < pc.nq; q0 += kBlockThreads * kUnroll) {
         f4 xv[kUnroll], gv[kUnroll], mv[kUnroll], vv[kUnroll];
@@ -231,15 +231,14 @@ __device__ __forceinline__ void sgdm4(f4& x, f4 g, f4& m, const SgdScalars& s) {
 
 __global__ __launch_bounds__(kBlockThreads) void k_local_sgdm(
     const Chunk* __restrict__ chunks, float* x_rep, RepLayout rl, const float* x_src,
-    RepLayout sl, const float* __restrict__ g_rep, float* __restrict__ s1, int64_t stride,
+    RepLayout sl, const float* __restrict__ g_rep, float* __restrict__ s1, StateLayout ml,
     int worker0, SgdScalars sc) {
     const Piece pc = piece_of<kMapLocal>(chunks);
     const int64_t w = worker0 + static_cast<int>(blockIdx.y);
-    const int64_t wo = w * stride + pc.e0;
     f4* xp = reinterpret_cast<f4*>(x_rep + rep_index(rl, w, pc.e0));
     const f4* xs = reinterpret_cast<const f4*>(x_src + rep_index(sl, w, pc.e0));
-    const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + wo);
-    f4* __restrict__ mp = reinterpret_cast<f4*>(s1 + wo);
+    const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + rep_index(ml.g, w, pc.e0));
+    f4* __restrict__ mp = reinterpret_cast<f4*>(s1 + rep_index(ml.s1, w, pc.e0));
     for (int q0 = threadIdx.x; q0 < pc.nq; q0 += kBlockThreads * kUnroll) {
         f4 xv[kUnroll], gv[kUnroll], mv[kUnroll];
 #pragma unroll
@@ -603,7 +602,7 @@ template <int N, int BASE>
 __global__ __launch_bounds__(kBlockThreads) void k_local_from_x(
     const Chunk* __restrict__ chunks, const float* __restrict__ x, float* __restrict__ x_rep,
     RepLayout rl, const float* __restrict__ g_rep, float* __restrict__ s1,
-    float* __restrict__ s2, int64_t stride, int n_rt, AdamScalars as, SgdScalars ss) {
+    float* __restrict__ s2, StateLayout ml, int n_rt, AdamScalars as, SgdScalars ss) {
     const Piece pc = piece_of<kMapFromX>(chunks);
     const int n = N > 0 ? N : n_rt;
     const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + pc.e0);
@@ -623,11 +622,10 @@ __global__ __launch_bounds__(kBlockThreads) void k_local_from_x(
 #pragma unroll 2
 #endif
         for (int i = 0; i < (N > 0 ? N : n); ++i) {
-            const int64_t wo = i * stride + pc.e0;
             f4* __restrict__ xr = reinterpret_cast<f4*>(x_rep + rep_index(rl, i, pc.e0));
-            const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + wo);
-            f4* __restrict__ s1p = reinterpret_cast<f4*>(s1 + wo);
-            f4* __restrict__ s2p = reinterpret_cast<f4*>(s2 + wo);
+            const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + rep_index(ml.g, i, pc.e0));
+            f4* __restrict__ s1p = reinterpret_cast<f4*>(s1 + rep_index(ml.s1, i, pc.e0));
+            f4* __restrict__ s2p = reinterpret_cast<f4*>(s2 + rep_index(ml.s2, i, pc.e0));
             f4 gi[kUnroll], mi[kUnroll], vi[kUnroll];
 #pragma unroll
             for (int k = 0; k < kUnroll; ++k) {
@@ -674,7 +672,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_round_end(
     const Chunk* __restrict__ chunks, float* x, float* __restrict__ m, float* x_rep,
     RepLayout rl, const float* x_src, RepLayout sl, const float* __restrict__ g_rep,
     float* __restrict__ s1, float* __restrict__ s2, float* __restrict__ u_out,
-    uint32_t* __restrict__ piece_max, int64_t stride, AdamScalars as, SgdScalars ss,
+    uint32_t* __restrict__ piece_max, StateLayout ml, AdamScalars as, SgdScalars ss,
     GlobalScalars gs) {
     // x_src is the replicas or, when they are stale, x itself: it may alias
     // x and x_rep, so none of the three is __restrict__.  Every load of a
@@ -709,11 +707,10 @@ __global__ __launch_bounds__(kBlockThreads) void k_round_end(
 #pragma unroll 2
 #endif
         for (int i = 0; i < (N > 0 ? N : n); ++i) {
-            const int64_t wo = i * stride + pc.e0;
             const f4* xs = reinterpret_cast<const f4*>(x_src + rep_index(sl, i, pc.e0));
-            const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + wo);
-            f4* __restrict__ s1p = reinterpret_cast<f4*>(s1 + wo);
-            f4* __restrict__ s2p = reinterpret_cast<f4*>(s2 + wo);
+            const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + rep_index(ml.g, i, pc.e0));
+            f4* __restrict__ s1p = reinterpret_cast<f4*>(s1 + rep_index(ml.s1, i, pc.e0));
+            f4* __restrict__ s2p = reinterpret_cast<f4*>(s2 + rep_index(ml.s2, i, pc.e0));
             f4 xi[kUnroll], gi[kUnroll], mi[kUnroll], vi[kUnroll];
 #pragma unroll
             for (int k = 0; k < kUnroll; ++k) {
@@ -797,7 +794,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_broadcast(
 __global__ __launch_bounds__(kBlockThreads) void k_init(
     const Chunk* __restrict__ chunks, const float* __restrict__ x, float* __restrict__ m,
     float* __restrict__ v, float* __restrict__ x_rep, RepLayout rl, float* __restrict__ s1,
-    float* __restrict__ s2, int64_t stride, int n) {
+    float* __restrict__ s2, StateLayout ml, int n) {
     const Piece pc = piece_of(chunks);
     const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + pc.e0);
     const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -807,10 +804,10 @@ __global__ __launch_bounds__(kBlockThreads) void k_init(
         store_vec(zero, reinterpret_cast<f4*>(m + pc.e0) + q, valid);
         if (v != nullptr) store_vec(zero, reinterpret_cast<f4*>(v + pc.e0) + q, valid);
         for (int i = 0; i < n; ++i) {
-            const int64_t o = i * stride + pc.e0;
             store_vec(xv, reinterpret_cast<f4*>(x_rep + rep_index(rl, i, pc.e0)) + q, valid);
-            store_vec(zero, reinterpret_cast<f4*>(s1 + o) + q, valid);
-            if (s2 != nullptr) store_vec(zero, reinterpret_cast<f4*>(s2 + o) + q, valid);
+            store_vec(zero, reinterpret_cast<f4*>(s1 + rep_index(ml.s1, i, pc.e0)) + q, valid);
+            if (s2 != nullptr)
+                store_vec(zero, reinterpret_cast<f4*>(s2 + rep_index(ml.s2, i, pc.e0)) + q, valid);
         }
     }
 }
@@ -838,31 +835,31 @@ dim3 chunk_grid(int64_t n_chunks, int n_workers) {
 // ---------------------------------------------------------------- launchers
 
 hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float* m, float* v,
-                       float* x_rep, RepLayout rl, float* s1, float* s2, int64_t stride, int n,
+                       float* x_rep, RepLayout rl, float* s1, float* s2, StateLayout ml, int n,
                        hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_init, chunk_grid(n_chunks, 1), dim3(kBlockThreads), 0, st, chunks, x, m,
-                       v, x_rep, rl, s1, s2, stride, n);
+                       v, x_rep, rl, s1, s2, ml, n);
     return hipGetLastError();
 }
 
 hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_rep, RepLayout rl,
                               const float* x_src, RepLayout sl, const float* g_rep, float* s1,
-                              float* s2, int64_t stride, int worker0, int n_workers,
+                              float* s2, StateLayout ml, int worker0, int n_workers,
                               const AdamScalars& sc, hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_local_adamw, chunk_grid(n_chunks, n_workers), dim3(kBlockThreads), 0, st,
-                       chunks, x_rep, rl, x_src, sl, g_rep, s1, s2, stride, worker0, sc);
+                       chunks, x_rep, rl, x_src, sl, g_rep, s1, s2, ml, worker0, sc);
     return hipGetLastError();
 }
 
 hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep, RepLayout rl,
                              const float* x_src, RepLayout sl, const float* g_rep, float* s1,
-                             int64_t stride, int worker0, int n_workers, const SgdScalars& sc,
+                             StateLayout ml, int worker0, int n_workers, const SgdScalars& sc,
                              hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_local_sgdm, chunk_grid(n_chunks, n_workers), dim3(kBlockThreads), 0, st,
-                       chunks, x_rep, rl, x_src, sl, g_rep, s1, stride, worker0, sc);
+                       chunks, x_rep, rl, x_src, sl, g_rep, s1, ml, worker0, sc);
     return hipGetLastError();
 }
 
@@ -873,7 +870,7 @@ static void launch_round_end_n(const Chunk* chunks, int64_t n_chunks, const Roun
 #define DSM_ROUND_END(NW)                                                                        \
     hipLaunchKernelGGL((k_round_end<NW, BASE, KIND>), grid, block, 0, st, chunks, a.x, a.m,      \
                        a.x_rep, a.rl, a.x_src, a.sl, a.g_rep, a.s1, a.s2, a.u, a.bound.piece_max, \
-                       a.stride, a.as, a.ss, a.gs)
+                       a.ml, a.as, a.ss, a.gs)
     switch (a.gs.n) {
         case 1: DSM_ROUND_END(1); break;
         case 2: DSM_ROUND_END(2); break;
@@ -898,12 +895,12 @@ static void launch_round_end_base(const Chunk* chunks, int64_t n_chunks, const R
 template <int BASE>
 static void launch_local_from_x_n(const Chunk* chunks, int64_t n_chunks, const float* x,
                                   float* x_rep, RepLayout rl, const float* g_rep, float* s1,
-                                  float* s2, int64_t stride, int n, const AdamScalars& as,
+                                  float* s2, StateLayout ml, int n, const AdamScalars& as,
                                   const SgdScalars& ss, hipStream_t st) {
     const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
 #define DSM_LOCAL_FROM_X(NW)                                                                   \
     hipLaunchKernelGGL((k_local_from_x<NW, BASE>), grid, block, 0, st, chunks, x, x_rep, rl,    \
-                       g_rep, s1, s2, stride, n, as, ss)
+                       g_rep, s1, s2, ml, n, as, ss)
     switch (n) {
         case 1: DSM_LOCAL_FROM_X(1); break;
         case 2: DSM_LOCAL_FROM_X(2); break;
@@ -916,15 +913,15 @@ static void launch_local_from_x_n(const Chunk* chunks, int64_t n_chunks, const f
 
 hipError_t launch_local_from_x(const Chunk* chunks, int64_t n_chunks, const float* x,
                                float* x_rep, RepLayout rl, const float* g_rep, float* s1,
-                               float* s2, int64_t stride, int n, bool adamw,
+                               float* s2, StateLayout ml, int n, bool adamw,
                                const AdamScalars& as, const SgdScalars& ss, hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
     if (adamw)
-        launch_local_from_x_n<kBaseAdamW>(chunks, n_chunks, x, x_rep, rl, g_rep, s1, s2, stride,
-                                          n, as, ss, st);
+        launch_local_from_x_n<kBaseAdamW>(chunks, n_chunks, x, x_rep, rl, g_rep, s1, s2, ml, n,
+                                          as, ss, st);
     else
-        launch_local_from_x_n<kBaseSgd>(chunks, n_chunks, x, x_rep, rl, g_rep, s1, s2, stride, n,
-                                        as, ss, st);
+        launch_local_from_x_n<kBaseSgd>(chunks, n_chunks, x, x_rep, rl, g_rep, s1, s2, ml, n, as,
+                                        ss, st);
     return hipGetLastError();
 }
 

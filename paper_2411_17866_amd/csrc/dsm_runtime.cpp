@@ -22,6 +22,7 @@ struct dsm_ctx {
     int64_t arena_elems = 0;
     std::vector<dsm::Chunk> chunks;  // host copy; the device copy lives in the workspace
     dsm::RepLayout rep{};            // how x_rep holds the n replicas
+    dsm::StateLayout ml{};           // how g_rep, s1_rep and s2_rep hold theirs
     std::vector<int32_t> chunk0;     // first chunk of each tensor, then n_chunks (host copy)
     dsm_buffers buf{};
     dsm::Chunk* d_chunks = nullptr;
@@ -91,7 +92,8 @@ dsm_status check_problem(const dsm_problem* p) {
         return fail(nullptr, DSM_ERR_INVALID_ARG, "n_tensors must be >= 0, got %d", p->n_tensors);
     if (p->base != DSM_BASE_ADAMW && p->base != DSM_BASE_SGD_MOMENTUM)
         return fail(nullptr, DSM_ERR_INVALID_ARG, "unknown base optimizer %d", p->base);
-    if (p->replica_layout != DSM_REPLICAS_CONTIGUOUS && p->replica_layout != DSM_REPLICAS_BLOCKED)
+    if (p->replica_layout != DSM_REPLICAS_CONTIGUOUS && p->replica_layout != DSM_REPLICAS_BLOCKED &&
+        p->replica_layout != DSM_REPLICAS_STATE_BLOCKED)
         return fail(nullptr, DSM_ERR_INVALID_ARG, "unknown replica layout %d", p->replica_layout);
     if (p->n_tensors > 0 && !p->numel)
         return fail(nullptr, DSM_ERR_INVALID_ARG, "numel is NULL");
@@ -104,16 +106,18 @@ dsm_status check_problem(const dsm_problem* p) {
 }
 
 // Tensors back to back, each starting at a multiple of 64 elements (of the
-// blocked alignment, with the arena a whole number of 64 KiB blocks, when the
-// replicas are blocked).  The workspace holds, each part at a 256-byte boundary: the chunk table
+// blocked alignment, with the arena a whole number of the layout's blocks,
+// when the replicas are blocked).  The workspace holds, each part at a 256-byte boundary: the chunk table
 // (kChunkElems elements per chunk, never crossing a tensor); the per-tensor
 // bound words; the first chunk of each tensor (n_tensors + 1 words); and one
 // piece-maximum word per work-group piece (n_chunks * kSplit), level one of
 // the bound.
 dsm_status make_layout(const dsm_problem* p, Layout* L, std::vector<dsm::Chunk>* chunks,
                        std::vector<int32_t>* chunk0 = nullptr) {
-    const bool blocked = p->replica_layout == DSM_REPLICAS_BLOCKED;
+    const bool blocked = p->replica_layout != DSM_REPLICAS_CONTIGUOUS;
     const int64_t align = blocked ? dsm::kBlockedTensorAlign : dsm::kTensorAlign;
+    const int64_t block = p->replica_layout == DSM_REPLICAS_BLOCKED ? dsm::kRepBlockElems
+                                                                     : dsm::kStateBlockElems;
     L->offsets.resize(p->n_tensors);
     int64_t off = 0, n_chunks = 0;
     for (int i = 0; i < p->n_tensors; ++i) {
@@ -121,7 +125,7 @@ dsm_status make_layout(const dsm_problem* p, Layout* L, std::vector<dsm::Chunk>*
         off += round_up(p->numel[i], align);
         n_chunks += (p->numel[i] + dsm::kChunkElems - 1) / dsm::kChunkElems;
     }
-    if (blocked) off = round_up(off, dsm::kRepBlockElems);
+    if (blocked) off = round_up(off, block);
     if (n_chunks > kMaxChunks)
         return fail(nullptr, DSM_ERR_UNSUPPORTED, "problem needs %lld chunks, limit %lld",
                     static_cast<long long>(n_chunks), static_cast<long long>(kMaxChunks));
@@ -292,9 +296,9 @@ hipError_t launch_local(dsm_ctx* ctx, const LocalCoefs& lc, const float* src, ds
     if (ctx->base == DSM_BASE_ADAMW)
         return dsm::launch_local_adamw(ctx->d_chunks, n_chunks, ctx->buf.x_rep, ctx->rep, src, sl,
                                        ctx->buf.g_rep, ctx->buf.s1_rep, ctx->buf.s2_rep,
-                                       ctx->arena_elems, w0, nw, lc.adam, ctx->stream);
+                                       ctx->ml, w0, nw, lc.adam, ctx->stream);
     return dsm::launch_local_sgdm(ctx->d_chunks, n_chunks, ctx->buf.x_rep, ctx->rep, src, sl,
-                                  ctx->buf.g_rep, ctx->buf.s1_rep, ctx->arena_elems, w0, nw, lc.sgd,
+                                  ctx->buf.g_rep, ctx->buf.s1_rep, ctx->ml, w0, nw, lc.sgd,
                                   ctx->stream);
 }
 
@@ -395,6 +399,27 @@ dsm_status init_context(const dsm_problem* problem, const dsm_buffers* caller, d
                 return fail(nullptr, DSM_ERR_INVALID_ARG, "buffer %s is not 256-byte aligned", q.name);
         }
     }
+    // How the per-worker buffers hold their n copies.
+    dsm::RepLayout rep = dsm::contiguous_copies(L.arena_elems);
+    dsm::StateLayout ml{rep, rep, rep};
+    if (problem->replica_layout == DSM_REPLICAS_BLOCKED) {
+        rep = dsm::blocked_copies(problem->n_workers);
+    } else if (problem->replica_layout == DSM_REPLICAS_STATE_BLOCKED) {
+        const int nb = adamw ? 4 : 3;
+        rep = dsm::state_blocked_copies(problem->n_workers, nb);
+        ml = dsm::StateLayout{rep, rep, rep};
+        // One allocation: g_rep, s1_rep (and s2_rep) start 1, 2 (and 3) times
+        // n blocks after x_rep.
+        const int64_t gap = int64_t(problem->n_workers) * dsm::kStateBlockElems;
+        if (L.arena_elems > 0 &&
+            (b->g_rep != b->x_rep + gap || b->s1_rep != b->x_rep + 2 * gap ||
+             (adamw && b->s2_rep != b->x_rep + 3 * gap)))
+            return fail(nullptr, DSM_ERR_INVALID_ARG,
+                        "state-blocked layout: g_rep, s1_rep%s must start %lld, %lld%s floats "
+                        "after x_rep, in one allocation of %d * n * d_pad floats",
+                        adamw ? " and s2_rep" : "", static_cast<long long>(gap),
+                        static_cast<long long>(2 * gap), adamw ? " and 3x that" : "", nb);
+    }
     if (L.workspace_bytes > 0) {
         if (!b->workspace) return fail(nullptr, DSM_ERR_INVALID_ARG, "workspace is NULL");
         if (!aligned256(b->workspace))
@@ -419,9 +444,8 @@ dsm_status init_context(const dsm_problem* problem, const dsm_buffers* caller, d
         ctx->decay[i] = problem->decay ? (problem->decay[i] ? 1 : 0) : 1;
     ctx->offsets = L.offsets;
     ctx->arena_elems = L.arena_elems;
-    ctx->rep = problem->replica_layout == DSM_REPLICAS_BLOCKED
-                   ? dsm::blocked_copies(problem->n_workers)
-                   : dsm::contiguous_copies(L.arena_elems);
+    ctx->rep = rep;
+    ctx->ml = ml;
     ctx->chunks = std::move(chunks);
     ctx->chunk0 = std::move(chunk0);
     ctx->buf = *b;
@@ -455,7 +479,7 @@ dsm_status init_context(const dsm_problem* problem, const dsm_buffers* caller, d
         }
         e = dsm::launch_init(ctx->d_chunks, static_cast<int64_t>(ctx->chunks.size()), b->x, b->m,
                              b->v, b->x_rep, ctx->rep, b->s1_rep, adamw ? b->s2_rep : nullptr,
-                             ctx->arena_elems, ctx->n, ctx->stream);
+                             ctx->ml, ctx->n, ctx->stream);
         if (e != hipSuccess) {
             dsm_status r = hip_fail(nullptr, "launching the initialisation kernel", e);
             delete ctx;
@@ -509,7 +533,7 @@ dsm_status dsm_local_step(dsm_ctx* ctx, int32_t worker, int64_t step, const dsm_
     if (all_stale) {
         hipError_t e = dsm::launch_local_from_x(
             ctx->d_chunks, static_cast<int64_t>(ctx->chunks.size()), ctx->buf.x, ctx->buf.x_rep,
-            ctx->rep, ctx->buf.g_rep, ctx->buf.s1_rep, ctx->buf.s2_rep, ctx->arena_elems, ctx->n,
+            ctx->rep, ctx->buf.g_rep, ctx->buf.s1_rep, ctx->buf.s2_rep, ctx->ml, ctx->n,
             ctx->base == DSM_BASE_ADAMW, lc.adam, lc.sgd, ctx->stream);
         if (e != hipSuccess) return hip_fail(ctx, "launching the local step", e);
     }
@@ -594,7 +618,7 @@ dsm_status dsm_round_end(dsm_ctx* ctx, int64_t step, const dsm_local_hparams* lo
     a.s2 = ctx->buf.s2_rep;
     a.u = ctx->buf.u_scratch;
     a.bound = ctx->bound;
-    a.stride = ctx->arena_elems;
+    a.ml = ctx->ml;
     a.as = lc.adam;
     a.ss = lc.sgd;
     a.gs = gs;

@@ -35,7 +35,9 @@ DSM_RULE_GLOBAL_ADAMW = 3
 
 DSM_REPLICAS_CONTIGUOUS = 0
 DSM_REPLICAS_BLOCKED = 1
+DSM_REPLICAS_STATE_BLOCKED = 2
 DSM_REPLICA_BLOCK_ELEMS = 16384
+DSM_STATE_BLOCK_ELEMS = 4096
 
 EXPORTED = ("dsm_layout", "dsm_init", "dsm_init_static", "dsm_local_step", "dsm_global_step",
             "dsm_round_end", "dsm_sync",

@@ -65,7 +65,7 @@ struct Launch {
     const uint32_t* piece_max = nullptr;
     const int32_t* chunk0 = nullptr;
     int worker0 = -1, n_workers = -1, n_tensors = -1;
-    int64_t stride = -1;
+    dsm::StateLayout ml{{-1, -1, -1, 0}, {-1, -1, -1, 0}, {-1, -1, -1, 0}};
     bool broadcast = false, adamw = false;
     dsm::AdamScalars as{};
     dsm::SgdScalars ss{};
@@ -103,7 +103,7 @@ hipError_t hipGetDevice(int* device) {
 
 namespace dsm {
 hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float*, float* v,
-                       float* x_rep, RepLayout rl, float*, float* s2, int64_t stride, int n,
+                       float* x_rep, RepLayout rl, float*, float* s2, StateLayout ml, int n,
                        hipStream_t) {
     Launch l;
     l.kind = "init";
@@ -114,13 +114,13 @@ hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float*, 
     l.rl = rl;
     l.v = v;
     l.s2 = s2;
-    l.stride = stride;
+    l.ml = ml;
     l.n_workers = n;
     return record(l);
 }
 hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_rep, RepLayout rl,
                               const float* x_src, RepLayout sl, const float*, float*, float* s2,
-                              int64_t stride, int worker0, int n_workers, const AdamScalars& sc,
+                              StateLayout ml, int worker0, int n_workers, const AdamScalars& sc,
                               hipStream_t) {
     Launch l;
     l.kind = "local_adamw";
@@ -131,7 +131,7 @@ hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_re
     l.x_src = x_src;
     l.sl = sl;
     l.s2 = s2;
-    l.stride = stride;
+    l.ml = ml;
     l.worker0 = worker0;
     l.n_workers = n_workers;
     l.as = sc;
@@ -139,7 +139,7 @@ hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_re
 }
 hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep, RepLayout rl,
                              const float* x_src, RepLayout sl, const float*, float*,
-                             int64_t stride, int worker0, int n_workers, const SgdScalars& sc,
+                             StateLayout ml, int worker0, int n_workers, const SgdScalars& sc,
                              hipStream_t) {
     Launch l;
     l.kind = "local_sgdm";
@@ -149,7 +149,7 @@ hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep
     l.rl = rl;
     l.x_src = x_src;
     l.sl = sl;
-    l.stride = stride;
+    l.ml = ml;
     l.worker0 = worker0;
     l.n_workers = n_workers;
     l.ss = sc;
@@ -157,7 +157,7 @@ hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep
 }
 hipError_t launch_local_from_x(const Chunk* chunks, int64_t n_chunks, const float* x,
                                float* x_rep, RepLayout rl, const float*, float*, float* s2,
-                               int64_t stride, int n, bool adamw, const AdamScalars& as,
+                               StateLayout ml, int n, bool adamw, const AdamScalars& as,
                                const SgdScalars& ss, hipStream_t) {
     Launch l;
     l.kind = "local_from_x";
@@ -167,7 +167,7 @@ hipError_t launch_local_from_x(const Chunk* chunks, int64_t n_chunks, const floa
     l.x_rep = x_rep;
     l.rl = rl;
     l.s2 = s2;
-    l.stride = stride;
+    l.ml = ml;
     l.n_workers = n;
     l.adamw = adamw;
     l.as = as;
@@ -192,7 +192,7 @@ hipError_t launch_round_end(const Chunk* chunks, int64_t n_chunks, int n_tensors
     l.bounds = a.bound.bits;
     l.piece_max = a.bound.piece_max;
     l.chunk0 = a.bound.chunk0;
-    l.stride = a.stride;
+    l.ml = a.ml;
     l.broadcast = broadcast;
     l.as = a.as;
     l.ss = a.ss;
@@ -274,10 +274,17 @@ bool same_layout(const dsm::RepLayout& a, const dsm::RepLayout& b) {
 }
 
 // The replica layout a launch must use, written out from dsm.h: contiguous
-// copies at i * d_pad, or 64 KiB blocks at ((e / 16384) * n + i) * 16384.
-dsm::RepLayout expected_layout(int replica_layout, int n, int64_t arena) {
+// copies at i * d_pad, 64 KiB blocks at ((e / 16384) * n + i) * 16384, or
+// state blocks at ((e / 4096) * B * n + i) * 4096 from each buffer's start.
+dsm::RepLayout expected_layout(int replica_layout, int n, int64_t arena, int buffers) {
     if (replica_layout == DSM_REPLICAS_BLOCKED) return dsm::RepLayout{int64_t(n) * 16384, 16384, 14, 0};
+    if (replica_layout == DSM_REPLICAS_STATE_BLOCKED)
+        return dsm::RepLayout{int64_t(buffers) * n * 4096, 4096, 12, 0};
     return dsm::RepLayout{0, arena, 62, 0};
+}
+
+bool same_state(const dsm::StateLayout& a, const dsm::RepLayout& g) {
+    return same_layout(a.g, g) && same_layout(a.s1, g) && same_layout(a.s2, g);
 }
 
 // The element index a RepLayout gives copy i of element e.
@@ -287,7 +294,12 @@ int64_t rep_element(const dsm::RepLayout& L, int64_t i, int64_t e) {
 }
 
 int64_t tensor_align(int replica_layout) {
-    return replica_layout == DSM_REPLICAS_BLOCKED ? std::max<int64_t>(1024, dsm::kPieceElems) : 64;
+    return replica_layout != DSM_REPLICAS_CONTIGUOUS ? std::max<int64_t>(1024, dsm::kPieceElems) : 64;
+}
+
+int64_t arena_block(int replica_layout) {
+    return replica_layout == DSM_REPLICAS_BLOCKED ? 16384
+           : replica_layout == DSM_REPLICAS_STATE_BLOCKED ? 4096 : 1;
 }
 
 struct Problem {
@@ -313,6 +325,7 @@ struct Buffers {
     dsm_buffers b{};
     int64_t arena = 0;
     dsm::RepLayout rep{};  // the replica layout every launch must pass
+    dsm::RepLayout state{};  // and the layout of g_rep, s1_rep and s2_rep
     float* alloc(int64_t floats) {
         const size_t bytes = static_cast<size_t>(round_up(std::max<int64_t>(floats, 1) * 4, 256));
         void* p = std::aligned_alloc(256, bytes);
@@ -326,13 +339,25 @@ struct Buffers {
         dsm_status st = dsm_layout(&P.p, &arena, off.data(), &ws);
         CHECK(st == DSM_OK, "layout of a valid problem");
         const int n = P.p.n_workers;
-        rep = expected_layout(P.p.replica_layout, n, arena);
+        const bool adamw = P.p.base == DSM_BASE_ADAMW;
+        const int nb = adamw ? 4 : 3;
+        rep = expected_layout(P.p.replica_layout, n, arena, nb);
         b.x = alloc(arena);
         b.m = alloc(arena);
-        b.x_rep = alloc(n * arena);
-        b.g_rep = alloc(n * arena);
-        b.s1_rep = alloc(n * arena);
-        b.s2_rep = P.p.base == DSM_BASE_ADAMW ? alloc(n * arena) : nullptr;
+        if (P.p.replica_layout == DSM_REPLICAS_STATE_BLOCKED) {
+            // One allocation; each buffer starts j * n blocks in.
+            state = rep;
+            b.x_rep = alloc(nb * n * arena);
+            b.g_rep = b.x_rep + n * 4096;
+            b.s1_rep = b.x_rep + 2 * n * 4096;
+            b.s2_rep = adamw ? b.x_rep + 3 * n * 4096 : nullptr;
+        } else {
+            state = dsm::RepLayout{0, arena, 62, 0};
+            b.x_rep = alloc(n * arena);
+            b.g_rep = alloc(n * arena);
+            b.s1_rep = alloc(n * arena);
+            b.s2_rep = adamw ? alloc(n * arena) : nullptr;
+        }
         b.u_scratch = randomized ? alloc(arena) : nullptr;
         b.v = global_adamw ? alloc(arena) : nullptr;
         b.workspace = alloc(ws / 4 + 64);
@@ -383,7 +408,7 @@ void check_layout_fuzz() {
             v = (rng() % 3) ? special[rng() % 12] : static_cast<int64_t>(rng() % 300000);
         int n = 1 + static_cast<int>(rng() % 64), H = 1 + static_cast<int>(rng() % 30);
         int base = static_cast<int>(rng() % 2);
-        int layout = static_cast<int>(rng() % 2);
+        int layout = static_cast<int>(rng() % 3);
         std::vector<uint8_t> dec;
         if (rng() % 2) {
             dec.resize(nt);
@@ -396,7 +421,7 @@ void check_layout_fuzz() {
         if (bad == 3) base = 2 + static_cast<int>(rng() % 5);
         if (bad == 4 && nt > 0) ne[rng() % nt] = -1 - static_cast<int64_t>(rng() % 5);
         if (bad == 5 && nt > 0) ne[rng() % nt] = (int64_t(1) << 34) + static_cast<int64_t>(rng() % 7);
-        if (bad == 6) layout = (rng() % 2) ? -1 : 2 + static_cast<int>(rng() % 5);
+        if (bad == 6) layout = (rng() % 2) ? -1 : 3 + static_cast<int>(rng() % 5);
         const bool invalid =
             bad == 1 || bad == 2 || bad == 3 || bad == 6 || ((bad == 4 || bad == 5) && nt > 0);
         Problem P(ne, n, H, base, dec, layout);
@@ -418,7 +443,7 @@ void check_layout_fuzz() {
             o += round_up(ne[i], tensor_align(layout));
             chunks += (ne[i] + dsm::kChunkElems - 1) / dsm::kChunkElems;
         }
-        if (layout == DSM_REPLICAS_BLOCKED) o = round_up(o, 16384);
+        o = round_up(o, arena_block(layout));
         CHECK(arena == o, "iter %d: arena %lld, expected %lld", iter, static_cast<long long>(arena),
               static_cast<long long>(o));
         CHECK(ws == round_up(chunks * 32, 256) + round_up(int64_t(nt) * 4, 256) +
@@ -498,8 +523,8 @@ void check_init_and_chunks() {
     for (size_t s = 0; s < shapes.size(); ++s) {
         std::vector<uint8_t> dec(shapes[s].size());
         for (size_t i = 0; i < dec.size(); ++i) dec[i] = (i % 3 != 1);
-        for (int with_decay = 0; with_decay < 4; ++with_decay) {
-            const int layout = with_decay / 2 ? DSM_REPLICAS_BLOCKED : DSM_REPLICAS_CONTIGUOUS;
+        for (int with_decay = 0; with_decay < 6; ++with_decay) {
+            const int layout = with_decay / 2;   // contiguous, blocked, state-blocked
             Problem P(shapes[s], 3, 2, DSM_BASE_ADAMW,
                       with_decay % 2 ? dec : std::vector<uint8_t>{}, layout);
             Buffers B(P, false, true);
@@ -511,7 +536,7 @@ void check_init_and_chunks() {
             if (!empty && !g_log.empty()) {
                 const Launch& l = g_log[0];
                 CHECK(l.kind == "init" && l.x == B.b.x && l.x_rep == B.b.x_rep && l.v == B.b.v &&
-                          l.s2 == B.b.s2_rep && l.stride == B.arena && l.n_workers == 3 &&
+                          l.s2 == B.b.s2_rep && same_state(l.ml, B.state) && l.n_workers == 3 &&
                           same_layout(l.rl, B.rep),
                       "init arguments");
                 check_chunk_table(P, B, l);
@@ -575,7 +600,7 @@ void check_init_rejections() {
 void expect_local(const Launch& l, const Buffers& B, bool adamw, bool from_x, int w0, int nw,
                   const char* what) {
     CHECK(l.kind == (adamw ? "local_adamw" : "local_sgdm"), "%s: kind %s", what, l.kind.c_str());
-    CHECK(l.x_rep == B.b.x_rep && l.stride == B.arena && same_layout(l.rl, B.rep),
+    CHECK(l.x_rep == B.b.x_rep && same_state(l.ml, B.state) && same_layout(l.rl, B.rep),
           "%s: replica buffer", what);
     CHECK(l.x_src == (from_x ? B.b.x : B.b.x_rep) &&
               same_layout(l.sl, from_x ? dsm::RepLayout{0, 0, 62, 0} : B.rep),
@@ -742,7 +767,7 @@ void check_local_from_x(int layout) {
                 const Launch& l = g_log[0];
                 if (n >= 2) {
                     CHECK(l.kind == "local_from_x" && l.x == B.b.x && l.x_rep == B.b.x_rep &&
-                              l.stride == B.arena && l.n_workers == n && l.adamw == adamw &&
+                              same_state(l.ml, B.state) && l.n_workers == n && l.adamw == adamw &&
                               l.s2 == B.b.s2_rep && l.chunks == B.b.workspace &&
                               same_layout(l.rl, B.rep),
                           "n = %d: all-worker launch from x", n);
@@ -943,20 +968,26 @@ void check_global_rand_args() {
     }
 }
 
-// Blocked replicas: every work-group piece of every chunk lies inside one
-// 64 KiB block, and (copy, element) -> slot covers each tensor element of each
-// copy exactly once inside the n * d_pad buffer, for random problems.
-void check_blocked_addressing() {
-    std::mt19937_64 rng(777);
+// Blocked layouts: every work-group piece of every chunk lies inside one
+// block, and (buffer, copy, element) -> slot covers each tensor element of each
+// copy of each blocked buffer exactly once inside the allocation (n * d_pad
+// for blocked replicas; B * n * d_pad for the replicas and their state), for
+// random problems.
+void check_blocked_addressing(int layout) {
+    std::mt19937_64 rng(777 + layout);
     const int64_t piece = dsm::kPieceElems;
+    const bool state = layout == DSM_REPLICAS_STATE_BLOCKED;
     for (int iter = 0; iter < 200; ++iter) {
         const int nt = 1 + static_cast<int>(rng() % 12);
         std::vector<int64_t> ne(nt);
         for (auto& v : ne) v = (rng() % 4 == 0) ? static_cast<int64_t>(rng() % 70000) : 1 + rng() % 3000;
         const int n = 1 + static_cast<int>(rng() % 9);
-        Problem P(ne, n, 2, DSM_BASE_SGD_MOMENTUM, {}, DSM_REPLICAS_BLOCKED);
+        const int base = state ? static_cast<int>(rng() % 2) : DSM_BASE_SGD_MOMENTUM;
+        Problem P(ne, n, 2, base, {}, layout);
         Buffers B(P, false, false);
-        CHECK(B.arena % 16384 == 0, "iter %d: blocked arena %lld not whole blocks", iter,
+        const int64_t block = state ? 4096 : 16384;
+        const int64_t shift = state ? 12 : 14;
+        CHECK(B.arena % block == 0, "iter %d: blocked arena %lld not whole blocks", iter,
               static_cast<long long>(B.arena));
         dsm_ctx* ctx = nullptr;
         g_log.clear();
@@ -967,32 +998,57 @@ void check_blocked_addressing() {
         }
         const Launch& l = g_log[0];
         CHECK(same_layout(l.rl, B.rep), "iter %d: init layout", iter);
+        // The blocked buffers and their offsets from the first one.
+        std::vector<std::pair<dsm::RepLayout, int64_t>> bufs = {{l.rl, 0}};
+        if (state) {
+            CHECK(same_state(l.ml, B.rep), "iter %d: state layouts", iter);
+            bufs.push_back({l.ml.g, B.b.g_rep - B.b.x_rep});
+            bufs.push_back({l.ml.s1, B.b.s1_rep - B.b.x_rep});
+            if (base == DSM_BASE_ADAMW) bufs.push_back({l.ml.s2, B.b.s2_rep - B.b.x_rep});
+        }
+        const int64_t total = static_cast<int64_t>(bufs.size()) * n * B.arena;
         const auto* c = static_cast<const dsm::Chunk*>(B.b.workspace);
-        std::vector<uint8_t> seen(static_cast<size_t>(n) * B.arena, 0);
+        std::vector<uint8_t> seen(static_cast<size_t>(total), 0);
         bool ok_piece = true, ok_slot = true;
         for (int64_t k = 0; k < l.n_chunks; ++k) {
             for (int64_t e0 = c[k].off; e0 < c[k].off + c[k].len; e0 += piece) {
                 const int64_t e1 = std::min<int64_t>(e0 + piece, c[k].off + c[k].len) - 1;
-                ok_piece &= (e0 >> 14) == (e1 >> 14);
+                ok_piece &= (e0 >> shift) == (e1 >> shift);
             }
-            for (int i = 0; i < n; ++i) {
-                for (int64_t e = c[k].off; e < c[k].off + c[k].len; ++e) {
-                    const int64_t idx = rep_element(l.rl, i, e);
-                    if (idx < 0 || idx >= n * B.arena || seen[idx]) {
-                        ok_slot = false;
-                    } else {
-                        seen[idx] = 1;
-                        // A piece's base plus the in-piece offset is the same slot.
-                        const int64_t base = c[k].off + ((e - c[k].off) / piece) * piece;
-                        ok_slot &= rep_element(l.rl, i, base) + (e - base) == idx;
+            for (const auto& [L, off] : bufs) {
+                for (int i = 0; i < n; ++i) {
+                    for (int64_t e = c[k].off; e < c[k].off + c[k].len; ++e) {
+                        const int64_t idx = off + rep_element(L, i, e);
+                        if (idx < 0 || idx >= total || seen[idx]) {
+                            ok_slot = false;
+                        } else {
+                            seen[idx] = 1;
+                            // A piece's base plus the in-piece offset is the same slot.
+                            const int64_t pb = c[k].off + ((e - c[k].off) / piece) * piece;
+                            ok_slot &= off + rep_element(L, i, pb) + (e - pb) == idx;
+                        }
                     }
                 }
             }
         }
-        CHECK(ok_piece, "iter %d: a piece crosses a 64 KiB block", iter);
-        CHECK(ok_slot, "iter %d: replica slots overlap, leave the buffer or break within a piece",
-              iter);
+        CHECK(ok_piece, "iter %d: a piece crosses a block", iter);
+        CHECK(ok_slot, "iter %d: slots overlap, leave the allocation or break within a piece", iter);
         CHECK(dsm_destroy(ctx) == DSM_OK, "destroy");
+    }
+    // The state-blocked layout refuses buffers that are not one allocation in
+    // its order.
+    if (state) {
+        Problem P({5000, 7}, 3, 2, DSM_BASE_ADAMW, {}, layout);
+        Buffers B(P, false, false);
+        dsm_ctx* ctx = nullptr;
+        float* keep = B.b.s2_rep;
+        B.b.s2_rep = B.b.s1_rep;
+        CHECK(dsm_init(&P.p, &B.b, &ctx) == DSM_ERR_INVALID_ARG && ctx == nullptr,
+              "state-blocked buffers out of order");
+        CHECK(std::strstr(dsm_last_error(nullptr), "state-blocked") != nullptr, "order message");
+        B.b.s2_rep = keep;
+        CHECK(dsm_init(&P.p, &B.b, &ctx) == DSM_OK, "state-blocked in order");
+        dsm_destroy(ctx);
     }
 }
 
@@ -1076,8 +1132,9 @@ int main() {
     check_init_and_chunks();
     check_init_rejections();
     check_init_static();
-    check_blocked_addressing();
-    for (int layout : {DSM_REPLICAS_CONTIGUOUS, DSM_REPLICAS_BLOCKED}) {
+    check_blocked_addressing(DSM_REPLICAS_BLOCKED);
+    check_blocked_addressing(DSM_REPLICAS_STATE_BLOCKED);
+    for (int layout : {DSM_REPLICAS_CONTIGUOUS, DSM_REPLICAS_BLOCKED, DSM_REPLICAS_STATE_BLOCKED}) {
         check_state_machine_adamw(layout);
         check_state_machine_sgd_h1(layout);
         check_local_from_x(layout);

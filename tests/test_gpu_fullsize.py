@@ -6,7 +6,8 @@ configuration the benchmark times:
   large   774M, n = 8, H = 24, AdamW, heavy-tailed gradients, deterministic
   xl      1.56B, n = 4, H = 12, AdamW, deterministic and randomized sign
 
-each with contiguous and with 64 KiB-blocked replicas.
+each with contiguous and with 64 KiB-blocked replicas, and medium and xl with the
+replicas and their state in 16 KiB blocks.
 Every update is elementwise given the per-tensor bound, so outputs are
 checked on sampled elements the oracle computes one by one (random elements,
 the first and last elements of every tensor, chunk seams of the largest
@@ -92,8 +93,11 @@ class Run:
         return dict(gamma=self.w.local["lr"], seed=self.w.philox_seed, **self.w.glob)
 
 
-LAYOUT_NAMES = {dsm.DSM_REPLICAS_CONTIGUOUS: "contiguous", dsm.DSM_REPLICAS_BLOCKED: "blocked"}
-CASES = [(wl, lay) for lay in LAYOUT_NAMES for wl in ("small", "medium", "large", "xl")]
+LAYOUT_NAMES = {dsm.DSM_REPLICAS_CONTIGUOUS: "contiguous", dsm.DSM_REPLICAS_BLOCKED: "blocked",
+                dsm.DSM_REPLICAS_STATE_BLOCKED: "state-blocked"}
+CASES = [(wl, lay) for lay in (dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_BLOCKED)
+         for wl in ("small", "medium", "large", "xl")]
+CASES += [("medium", dsm.DSM_REPLICAS_STATE_BLOCKED), ("xl", dsm.DSM_REPLICAS_STATE_BLOCKED)]
 
 
 @pytest.fixture(scope="module", params=CASES,

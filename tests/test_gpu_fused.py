@@ -37,7 +37,7 @@ def _grads(ar, t, k):
     ar.g_rep.normal_(0.0, 0.01, generator=gen)
 
 
-LAYOUTS = [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_BLOCKED]
+LAYOUTS = [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_BLOCKED, dsm.DSM_REPLICAS_STATE_BLOCKED]
 
 
 def run(base, mode, broadcast, n, H, fused, rounds=3, record_grads=False,
@@ -54,7 +54,7 @@ def run(base, mode, broadcast, n, H, fused, rounds=3, record_grads=False,
             _grads(ar, t, k)
             if record_grads:
                 for i in range(n):
-                    grads[(t, i, k)] = tensors(ar, ar.g_rep[i])
+                    grads[(t, i, k)] = tensors(ar, ar.worker("g_rep", i))
             s = t * H + k + 1
             if fused and k == H - 1:
                 dsm.dsm_round_end(ar.ctx, s, local, t, gamma=local["lr"], mode=mode, seed=9,
@@ -64,9 +64,9 @@ def run(base, mode, broadcast, n, H, fused, rounds=3, record_grads=False,
         if not fused:
             dsm.dsm_global_step(ar.ctx, t, gamma=local["lr"], mode=mode, seed=9,
                                 broadcast=broadcast, **GLOB)
-    out = {"x": host(ar.x), "m": host(ar.m), "s1": host(ar.s1_rep)}
+    out = {"x": host(ar.x), "m": host(ar.m), "s1": host(ar.workers("s1_rep"))}
     if ar.s2_rep is not None:
-        out["s2"] = host(ar.s2_rep)
+        out["s2"] = host(ar.workers("s2_rep"))
     if broadcast:
         out["x_rep"] = host(ar.replicas())
     if mode != dsm.DSM_SIGN_DET:
@@ -144,7 +144,7 @@ def test_mixed_stale_and_fresh_workers(layout):
     st = O.init_state(tensors(ar, ar.x), n, "sgd")
     for t in range(2):
         ar.g_rep.normal_(0.0, 0.01, generator=gen)
-        g = [tensors(ar, ar.g_rep[i]) for i in range(n)]
+        g = [tensors(ar, ar.worker("g_rep", i)) for i in range(n)]
         if t == 0:
             dsm.dsm_local_step(ar.ctx, -1, 1, **SGD)
             dsm.dsm_local_step(ar.ctx, -1, 2, **SGD)
@@ -206,9 +206,9 @@ def test_all_worker_step_from_x_equals_per_worker_steps(base, n, layout):
                 dsm.dsm_local_step(ar.ctx, i, H + 1, **local)
         else:
             dsm.dsm_local_step(ar.ctx, -1, H + 1, **local)
-        first = {"x_rep": host(ar.replicas()), "s1": host(ar.s1_rep)}
+        first = {"x_rep": host(ar.replicas()), "s1": host(ar.workers("s1_rep"))}
         if ar.s2_rep is not None:
-            first["s2"] = host(ar.s2_rep)
+            first["s2"] = host(ar.workers("s2_rep"))
         _grads(ar, 1, 1)
         dsm.dsm_local_step(ar.ctx, -1, H + 2, **local)
         dsm.dsm_global_step(ar.ctx, 1, gamma=local["lr"], broadcast=True, **GLOB)

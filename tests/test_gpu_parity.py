@@ -21,8 +21,8 @@ pytestmark = pytest.mark.gpu
 
 RAGGED = [1, 3, 4, 5, 63, 64, 65, 0, 1000, 16383, 16384, 16385, 40003]
 DECAY = [i % 3 != 1 for i in range(len(RAGGED))]
-# Both replica layouts of dsm_problem.replica_layout.
-LAYOUTS = [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_BLOCKED]
+# The layouts of dsm_problem.replica_layout.
+LAYOUTS = [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_BLOCKED, dsm.DSM_REPLICAS_STATE_BLOCKED]
 
 
 def host(t):
@@ -201,8 +201,8 @@ def test_global_det_parity(n, broadcast, layout):
         # Replicas are left stale; the next local step reads the new x.
         np.testing.assert_array_equal(rep_after, rep_before)
         gx_now = per_tensor(ar, ar.x)
-        m1 = [per_tensor(ar, ar.s1_rep[i]) for i in range(n)]
-        g1 = [per_tensor(ar, ar.g_rep[i]) for i in range(n)]
+        m1 = [per_tensor(ar, ar.worker("s1_rep", i)) for i in range(n)]
+        g1 = [per_tensor(ar, ar.worker("g_rep", i)) for i in range(n)]
         dsm.dsm_local_step(ar.ctx, -1, 1, lr=0.05, beta1=0.5)
         for i in range(n):
             xi = per_tensor(ar, ar.replica(i))
@@ -328,7 +328,7 @@ def test_tiny_rounds_free_running_bit_identical():
         for k in range(w.local_steps):
             for i in range(w.n_workers):
                 W.fill_grads_(ar.g_rep[i], w, i, t * w.local_steps + k)
-                grads[(i, k)] = per_tensor(ar, ar.g_rep[i])
+                grads[(i, k)] = per_tensor(ar, ar.worker("g_rep", i))
             dsm.dsm_local_step(ar.ctx, -1, t * w.local_steps + k + 1, **w.local)
         dsm.dsm_global_step(ar.ctx, t, gamma=w.local["lr"], mode=dsm.DSM_SIGN_DET,
                             broadcast=True, **w.glob)
@@ -339,8 +339,8 @@ def test_tiny_rounds_free_running_bit_identical():
                                    ("m", per_tensor(ar, ar.m)[p], st["m"][p])):
                 assert np.array_equal(gpu.view(np.uint32), ora.view(np.uint32)), (t, name, p)
             for i in range(w.n_workers):
-                assert np.array_equal(per_tensor(ar, ar.s1_rep[i])[p], st["s1"][i][p])
-                assert np.array_equal(per_tensor(ar, ar.s2_rep[i])[p], st["s2"][i][p])
+                assert np.array_equal(per_tensor(ar, ar.worker("s1_rep", i))[p], st["s1"][i][p])
+                assert np.array_equal(per_tensor(ar, ar.worker("s2_rep", i))[p], st["s2"][i][p])
                 assert np.array_equal(per_tensor(ar, ar.replica(i))[p], st["replicas"][i][p])
     ar.destroy()
 
@@ -367,7 +367,7 @@ def test_tiny_long_free_run_all_signs_and_paths(layout):
         for k in range(H):
             for i in range(w.n_workers):
                 W.fill_grads_(ar.g_rep[i], w, i, t * H + k)
-                grads[(i, k)] = per_tensor(ar, ar.g_rep[i])
+                grads[(i, k)] = per_tensor(ar, ar.worker("g_rep", i))
             s = t * H + k + 1
             if fused and k == H - 1:
                 dsm.dsm_round_end(ar.ctx, s, w.local, t, gamma=w.local["lr"], mode=mode,
@@ -385,7 +385,7 @@ def test_tiny_long_free_run_all_signs_and_paths(layout):
             assert np.array_equal(gx[p].view(np.uint32), st["x"][p].view(np.uint32)), (t, "x", p)
             assert np.array_equal(gm[p].view(np.uint32), st["m"][p].view(np.uint32)), (t, "m", p)
         for i in range(w.n_workers):
-            g1, g2 = per_tensor(ar, ar.s1_rep[i]), per_tensor(ar, ar.s2_rep[i])
+            g1, g2 = per_tensor(ar, ar.worker("s1_rep", i)), per_tensor(ar, ar.worker("s2_rep", i))
             for p in range(len(w.numel)):
                 assert np.array_equal(g1[p].view(np.uint32), st["s1"][i][p].view(np.uint32))
                 assert np.array_equal(g2[p].view(np.uint32), st["s2"][i][p].view(np.uint32))
@@ -402,7 +402,7 @@ def test_rerun_is_bitwise_deterministic():
             dsm.dsm_local_step(ar.ctx, -1, k + 1, lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8,
                                weight_decay=0.1)
         dsm.dsm_global_step(ar.ctx, 3, mode=dsm.DSM_SIGN_RAND_FLIP, seed=42, **GLOB)
-        outs.append([host(t) for t in (ar.x, ar.m, ar.replicas(), ar.s1_rep, ar.s2_rep, ar.u)])
+        outs.append([host(t) for t in (ar.x, ar.m, ar.replicas(), ar.workers("s1_rep"), ar.workers("s2_rep"), ar.u)])
         ar.destroy()
     for a, b in zip(*outs):
         assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
@@ -491,7 +491,7 @@ def test_max_workers_every_entry_point(layout):
         for k in range(H):
             ar.g_rep.normal_(0.0, 0.01, generator=gen)
             for i in range(n):
-                grads[(i, k)] = per_tensor(ar, ar.g_rep[i])
+                grads[(i, k)] = per_tensor(ar, ar.worker("g_rep", i))
             s = t * H + k + 1
             if fused and k == H - 1:
                 dsm.dsm_round_end(ar.ctx, s, local, t, mode=mode, seed=3, broadcast=False, **GLOB)

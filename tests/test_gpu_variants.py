@@ -85,7 +85,8 @@ def _run_variant(rule, n, broadcast, rounds, seed, layout=dsm.DSM_REPLICAS_CONTI
 @pytest.mark.parametrize("rule", [dsm.DSM_RULE_LOOKAHEAD, dsm.DSM_RULE_SIGNED_SLOWMO,
                                   dsm.DSM_RULE_GLOBAL_ADAMW])
 @pytest.mark.parametrize("n,broadcast", [(1, True), (3, True), (4, False), (5, True)])
-@pytest.mark.parametrize("layout", [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_BLOCKED])
+@pytest.mark.parametrize("layout", [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_BLOCKED,
+                                    dsm.DSM_REPLICAS_STATE_BLOCKED])
 def test_global_variant_parity(rule, n, broadcast, layout):
     nonbit = _run_variant(rule, n, broadcast, rounds=3, seed=31 * n + rule, layout=layout)
     print(f"rule {rule} n={n}: {nonbit} elements not bit-identical to the fp32 oracle")

@@ -25,11 +25,20 @@ MUTATIONS = [
      "const dsm::RepLayout sl = ctx->rep;", "stale workers read their own replica"),
     ("const int64_t align = blocked ? dsm::kBlockedTensorAlign : dsm::kTensorAlign;",
      "const int64_t align = dsm::kTensorAlign;", "blocked replicas without the piece alignment"),
-    ("    if (blocked) off = round_up(off, dsm::kRepBlockElems);\n", "",
+    ("    if (blocked) off = round_up(off, block);\n", "",
      "blocked arena not a whole number of blocks"),
-    ("                   ? dsm::blocked_copies(problem->n_workers)\n",
-     "                   ? dsm::contiguous_copies(L.arena_elems)\n",
+    ("        rep = dsm::blocked_copies(problem->n_workers);",
+     "        rep = dsm::contiguous_copies(L.arena_elems);",
      "blocked replicas addressed as contiguous copies"),
+    ("        ml = dsm::StateLayout{rep, rep, rep};",
+     "        ml = dsm::StateLayout{rep, rep, dsm::contiguous_copies(L.arena_elems)};",
+     "state-blocked second moments addressed as contiguous copies"),
+    ("        rep = dsm::state_blocked_copies(problem->n_workers, nb);",
+     "        rep = dsm::state_blocked_copies(problem->n_workers, 4);",
+     "state blocks sized for four buffers with the SGD base"),
+    ("             (adamw && b->s2_rep != b->x_rep + 3 * gap)))",
+     "             (adamw && b->s2_rep != b->x_rep + 2 * gap)))",
+     "state-blocked buffer order not checked"),
     ("    a.sl = from_x ? dsm::single_copy() : ctx->rep;", "    a.sl = ctx->rep;",
      "round end after a lazy broadcast reads the stale replicas"),
     ("        g_static_busy[ctx->static_device] = false;\n", "",

@@ -1,6 +1,6 @@
 """dsm_init_static, the entry point that allocates nothing, against dsm_init.
 
-Two problems in a row, the second smaller, so the second context starts from
+Three problems in a row, each smaller than the one before, so the second context starts from
 the static scratch the first one left behind.  Each is run twice from the same
 seeded start: once on a context from dsm_init (caller workspace and u
 staging) and once on a context from dsm_init_static, whose buffers carry no
@@ -21,6 +21,7 @@ pytestmark = pytest.mark.gpu
 
 CASES = [  # (numel, n, H, base, layout): the second one smaller
     ([16385, 40003, 5, 100000, 0, 63], 3, 2, dsm.DSM_BASE_ADAMW, dsm.DSM_REPLICAS_BLOCKED),
+    ([40000, 1000], 2, 2, dsm.DSM_BASE_ADAMW, dsm.DSM_REPLICAS_STATE_BLOCKED),
     ([1000, 7], 2, 1, dsm.DSM_BASE_SGD_MOMENTUM, dsm.DSM_REPLICAS_CONTIGUOUS),
 ]
 LOCAL = {dsm.DSM_BASE_ADAMW: dict(lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1),
@@ -32,9 +33,9 @@ ROUNDS = [(dsm.DSM_SIGN_DET, False, True), (dsm.DSM_SIGN_RAND_FLIP, False, True)
 
 def _state(ar):
     torch.cuda.synchronize()
-    out = {"x": ar.x, "m": ar.m, "x_rep": ar.replicas(), "s1": ar.s1_rep}
+    out = {"x": ar.x, "m": ar.m, "x_rep": ar.replicas(), "s1": ar.workers("s1_rep")}
     if ar.s2_rep is not None:
-        out["s2"] = ar.s2_rep
+        out["s2"] = ar.workers("s2_rep")
     return {k: v.detach().cpu().numpy().view(np.uint32).copy() for k, v in out.items()}
 
 
