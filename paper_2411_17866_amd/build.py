@@ -58,8 +58,9 @@ def build(verbose=False, out=LIBPATH, defines=()):
     """Compiles the kernels and the host runtime and links libdsm.so.
 
     defines: extra -D settings of the build-time tuning knobs (DSM_BLOCK_THREADS,
-    DSM_UNROLL, DSM_ITERS, DSM_NT, DSM_CHUNK_ELEMS, DSM_XCD_MAP,
-    DSM_XCD_MAP_LOCAL, DSM_XCD_MAP_ROUND_END); the defaults are the tuned
+    DSM_UNROLL, DSM_ITERS, DSM_NT, DSM_CHUNK_ELEMS, and the XCD maps of each
+    replica layout DSM_MAPS_CONTIGUOUS, DSM_MAPS_BLOCKED, DSM_MAPS_STATE_BLOCKED
+    as "local, round_end, from_x, global, copy"); the defaults are the tuned
     values.
     """
     os.makedirs(os.path.dirname(out), exist_ok=True)

@@ -131,30 +131,53 @@ struct GlobalScalars {
     float eta, eps;
 };
 
+// How a launch's work-group index maps to its piece (the XCD map): 0, the
+// index itself (XCD k takes piece k mod 8 of every chunk); 1, XCD k takes the
+// k-th eighth of the grid row, in order; 2, XCD k takes whole chunks.  The
+// best map of each kernel kind depends on the replica layout (measured), so
+// the runtime keeps one set per layout; build-time -D settings override them.
+// global: the global steps and the randomized second pass of the round end;
+// copy: the broadcast of dsm_sync and the initial copy of dsm_init.
+struct XcdMaps {
+    int local, round_end, from_x, global, copy;
+};
+#ifndef DSM_MAPS_CONTIGUOUS
+#define DSM_MAPS_CONTIGUOUS 1, 2, 2, 0, 0
+#endif
+#ifndef DSM_MAPS_BLOCKED
+#define DSM_MAPS_BLOCKED 1, 2, 1, 0, 1
+#endif
+#ifndef DSM_MAPS_STATE_BLOCKED
+#define DSM_MAPS_STATE_BLOCKED 1, 1, 1, 1, 1
+#endif
+constexpr XcdMaps kMapsByLayout[3] = {{DSM_MAPS_CONTIGUOUS}, {DSM_MAPS_BLOCKED},
+                                      {DSM_MAPS_STATE_BLOCKED}};
+
 // Kernel launchers (dsm_kernels.hip).  All return the launch status.  The
 // replica buffer x_rep is addressed through its RepLayout rl, and g_rep, s1
-// and s2 through the layouts of ml.
+// and s2 through the layouts of ml; map is the launch's XCD map.
 hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float* m, float* v,
                        float* x_rep, RepLayout rl, float* s1, float* s2, StateLayout ml, int n,
-                       hipStream_t st);
+                       int map, hipStream_t st);
 // Local steps: worker w reads its starting point from x_src through sl (its
 // replica, or the shared global model with single_copy()) and writes its
 // replica through rl.
 hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_rep, RepLayout rl,
                               const float* x_src, RepLayout sl, const float* g_rep, float* s1,
                               float* s2, StateLayout ml, int worker0, int n_workers,
-                              const AdamScalars& sc, hipStream_t st);
+                              const AdamScalars& sc, int map, hipStream_t st);
 hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep, RepLayout rl,
                              const float* x_src, RepLayout sl, const float* g_rep, float* s1,
                              StateLayout ml, int worker0, int n_workers, const SgdScalars& sc,
-                             hipStream_t st);
+                             int map, hipStream_t st);
 
 // Local step of all n workers from the global model x (every replica stale):
 // x is read once per element and each worker's result goes to its replica.
 hipError_t launch_local_from_x(const Chunk* chunks, int64_t n_chunks, const float* x,
                                float* x_rep, RepLayout rl, const float* g_rep, float* s1,
                                float* s2, StateLayout ml, int n, bool adamw,
-                               const AdamScalars& as, const SgdScalars& ss, hipStream_t st);
+                               const AdamScalars& as, const SgdScalars& ss, int map,
+                               hipStream_t st);
 
 // Workspace words of the randomized sign's per-tensor bound B_p = max |u|,
 // reduced in two levels without atomics.
@@ -177,19 +200,21 @@ struct RoundEndArgs {
     AdamScalars as;
     SgdScalars ss;
     GlobalScalars gs;
+    int map;        // XCD map of the round-end kernel
+    int map_pass2;  // and of the randomized sign's second pass
 };
 hipError_t launch_round_end(const Chunk* chunks, int64_t n_chunks, int n_tensors, bool adamw,
                             const RoundEndArgs& a, bool broadcast, hipStream_t st);
 // Deterministic global step of any rule; v is the Global AdamW second moment.
 hipError_t launch_global_det(const Chunk* chunks, int64_t n_chunks, float* x, float* m,
                              float* v, float* x_rep, RepLayout rl, const GlobalScalars& sc,
-                             bool broadcast, hipStream_t st);
+                             bool broadcast, int map, hipStream_t st);
 hipError_t launch_global_rand(const Chunk* chunks, int64_t n_chunks, int n_tensors, float* x,
                               float* m, float* x_rep, RepLayout rl, float* u,
                               const BoundWords& bw, const GlobalScalars& sc, bool broadcast,
-                              hipStream_t st);
+                              int map, hipStream_t st);
 hipError_t launch_broadcast(const Chunk* chunks, int64_t n_chunks, const float* x, float* x_rep,
-                            RepLayout rl, int n, hipStream_t st);
+                            RepLayout rl, int n, int map, hipStream_t st);
 hipError_t launch_test_philox(uint32_t key0, uint32_t key1, uint32_t tensor, uint32_t t,
                               uint32_t q0, int64_t count, uint32_t* out, hipStream_t st);
 

@@ -92,23 +92,7 @@ struct Piece {
     uint32_t j4;     // in-tensor index of the first group, divided by 4
 };
 
-#ifndef DSM_XCD_MAP
-#define DSM_XCD_MAP 0
-#endif
-#ifndef DSM_XCD_MAP_LOCAL
-#define DSM_XCD_MAP_LOCAL 1
-#endif
-#ifndef DSM_XCD_MAP_ROUND_END
-#define DSM_XCD_MAP_ROUND_END 2
-#endif
 constexpr uint32_t kXcds = 8;  // MI355X: work-groups go to its 8 XCDs round-robin
-constexpr int kMapLocal = DSM_XCD_MAP_LOCAL;         // local-step kernels
-constexpr int kMapRoundEnd = DSM_XCD_MAP_ROUND_END;  // fused round end
-#ifndef DSM_XCD_MAP_FROM_X
-#define DSM_XCD_MAP_FROM_X DSM_XCD_MAP_ROUND_END
-#endif
-constexpr int kMapFromX = DSM_XCD_MAP_FROM_X;        // all-worker local step from x
-constexpr int kMapOther = DSM_XCD_MAP;               // every other chunk kernel
 
 // Work item of this work-group.  MAP 0: the work-group index itself (XCD k
 // takes piece k mod 8 of every chunk).  1: XCD k takes the k-th eighth of the
@@ -132,10 +116,17 @@ __device__ __forceinline__ uint32_t work_index() {
     }
 }
 
-template <int MAP = kMapOther>
-__device__ __forceinline__ Piece piece_of(const Chunk* __restrict__ chunks) {
+// The map is a launch argument (the runtime picks it per kernel kind and
+// replica layout) and uniform over the grid, so the branch is scalar.
+__device__ __forceinline__ uint32_t work_index(int map) {
+    if (map == 1) return work_index<1>();
+    if (map == 2) return work_index<2>();
+    return work_index<0>();
+}
+
+__device__ __forceinline__ Piece piece_of(const Chunk* __restrict__ chunks, int map) {
     Piece pc;
-    const uint32_t wi = work_index<MAP>();
+    const uint32_t wi = work_index(map);
     pc.wi = wi;
     pc.c = chunks[wi / kSplit];
     const int nvec = (pc.c.len + 3) >> 2;
@@ -182,10 +173,10 @@ __device__ __forceinline__ void adamw4(f4& x, f4 g, f4& m, f4& v, float lam, con
 // same memory, so neither pointer is __restrict__; each thread loads every
 // stream of its group before it stores.
 __global__ __launch_bounds__(kBlockThreads) void k_local_adamw(
-    const Chunk* __restrict__ chunks, float* x_rep, RepLayout rl, const float* x_src,
+    const Chunk* __restrict__ chunks, int map, float* x_rep, RepLayout rl, const float* x_src,
     RepLayout sl, const float* __restrict__ g_rep, float* __restrict__ s1,
     float* __restrict__ s2, StateLayout ml, int worker0, AdamScalars sc) {
-    const Piece pc = piece_of<kMapLocal>(chunks);
+    const Piece pc = piece_of(chunks, map);
     const int64_t w = worker0 + static_cast<int>(blockIdx.y);
     f4* xp = reinterpret_cast<f4*>(x_rep + rep_index(rl, w, pc.e0));
     const f4* xs = reinterpret_cast<const f4*>(x_src + rep_index(sl, w, pc.e0));
@@ -230,10 +221,10 @@ __device__ __forceinline__ void sgdm4(f4& x, f4 g, f4& m, const SgdScalars& s) {
 }
 
 __global__ __launch_bounds__(kBlockThreads) void k_local_sgdm(
-    const Chunk* __restrict__ chunks, float* x_rep, RepLayout rl, const float* x_src,
+    const Chunk* __restrict__ chunks, int map, float* x_rep, RepLayout rl, const float* x_src,
     RepLayout sl, const float* __restrict__ g_rep, float* __restrict__ s1, StateLayout ml,
     int worker0, SgdScalars sc) {
-    const Piece pc = piece_of<kMapLocal>(chunks);
+    const Piece pc = piece_of(chunks, map);
     const int64_t w = worker0 + static_cast<int>(blockIdx.y);
     f4* xp = reinterpret_cast<f4*>(x_rep + rep_index(rl, w, pc.e0));
     const f4* xs = reinterpret_cast<const f4*>(x_src + rep_index(sl, w, pc.e0));
@@ -349,9 +340,9 @@ __device__ __forceinline__ f4 global_adamw4(f4 x, f4 delta, f4& m, f4& v, float 
 
 template <int N, int RULE, bool BCAST>
 __global__ __launch_bounds__(kBlockThreads) void k_global_det(
-    const Chunk* __restrict__ chunks, float* __restrict__ x, float* __restrict__ m,
+    const Chunk* __restrict__ chunks, int map, float* __restrict__ x, float* __restrict__ m,
     float* __restrict__ v, float* __restrict__ x_rep, RepLayout rl, GlobalScalars sc) {
-    const Piece pc = piece_of(chunks);
+    const Piece pc = piece_of(chunks, map);
     const int n = N > 0 ? N : sc.n;
     f4* __restrict__ xp = reinterpret_cast<f4*>(x + pc.e0);
     f4* __restrict__ mp = reinterpret_cast<f4*>(m + pc.e0);
@@ -446,10 +437,10 @@ __device__ __forceinline__ void store_piece_max(uint32_t bits, uint32_t* wave_ma
 // and m_{t+1} (Eqs. (6), (8)), and the tensor bound B_p = max |u|.
 template <int N>
 __global__ __launch_bounds__(kBlockThreads) void k_global_rand_pass1(
-    const Chunk* __restrict__ chunks, const float* __restrict__ x, float* __restrict__ m,
+    const Chunk* __restrict__ chunks, int map, const float* __restrict__ x, float* __restrict__ m,
     const float* __restrict__ x_rep, RepLayout rl, float* __restrict__ u_out,
     uint32_t* __restrict__ piece_max, GlobalScalars sc) {
-    const Piece pc = piece_of(chunks);
+    const Piece pc = piece_of(chunks, map);
     const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + pc.e0);
     f4* __restrict__ mp = reinterpret_cast<f4*>(m + pc.e0);
     f4* __restrict__ up = reinterpret_cast<f4*>(u_out + pc.e0);
@@ -542,10 +533,10 @@ __device__ __forceinline__ float rand_sign(float u, uint32_t w, double B) {
 // so its step is NaN rather than a step of a reversed or zero sign.
 template <int MODE, bool BCAST>
 __global__ __launch_bounds__(kBlockThreads) void k_global_rand_pass2(
-    const Chunk* __restrict__ chunks, float* __restrict__ x, float* __restrict__ x_rep,
+    const Chunk* __restrict__ chunks, int map, float* __restrict__ x, float* __restrict__ x_rep,
     RepLayout rl, const float* __restrict__ u_in, const uint32_t* __restrict__ bound_bits,
     GlobalScalars sc) {
-    const Piece pc = piece_of(chunks);
+    const Piece pc = piece_of(chunks, map);
     const Chunk& c = pc.c;
     f4* __restrict__ xp = reinterpret_cast<f4*>(x + pc.e0);
     const f4* __restrict__ up = reinterpret_cast<const f4*>(u_in + pc.e0);
@@ -600,10 +591,10 @@ constexpr int kBaseSgd = 1;
 // per-element arithmetic is adamw4 / sgdm4, as in the per-worker kernels.
 template <int N, int BASE>
 __global__ __launch_bounds__(kBlockThreads) void k_local_from_x(
-    const Chunk* __restrict__ chunks, const float* __restrict__ x, float* __restrict__ x_rep,
+    const Chunk* __restrict__ chunks, int map, const float* __restrict__ x, float* __restrict__ x_rep,
     RepLayout rl, const float* __restrict__ g_rep, float* __restrict__ s1,
     float* __restrict__ s2, StateLayout ml, int n_rt, AdamScalars as, SgdScalars ss) {
-    const Piece pc = piece_of<kMapFromX>(chunks);
+    const Piece pc = piece_of(chunks, map);
     const int n = N > 0 ? N : n_rt;
     const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + pc.e0);
     const float lam = pc.c.decay ? as.wd : 0.0f;
@@ -669,7 +660,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_local_from_x(
 
 template <int N, int BASE, int KIND>
 __global__ __launch_bounds__(kBlockThreads) void k_round_end(
-    const Chunk* __restrict__ chunks, float* x, float* __restrict__ m, float* x_rep,
+    const Chunk* __restrict__ chunks, int map, float* x, float* __restrict__ m, float* x_rep,
     RepLayout rl, const float* x_src, RepLayout sl, const float* __restrict__ g_rep,
     float* __restrict__ s1, float* __restrict__ s2, float* __restrict__ u_out,
     uint32_t* __restrict__ piece_max, StateLayout ml, AdamScalars as, SgdScalars ss,
@@ -678,7 +669,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_round_end(
     // x and x_rep, so none of the three is __restrict__.  Every load of a
     // group precedes its stores.
     __shared__ uint32_t wave_max[kBlockThreads / 64];
-    const Piece pc = piece_of<kMapRoundEnd>(chunks);
+    const Piece pc = piece_of(chunks, map);
     const int n = N > 0 ? N : gs.n;
     f4* xp = reinterpret_cast<f4*>(x + pc.e0);
     f4* __restrict__ mp = reinterpret_cast<f4*>(m + pc.e0);
@@ -778,9 +769,9 @@ __global__ __launch_bounds__(kBlockThreads) void k_round_end(
 
 // Synchronisation step: x_rep[i] <- x for every replica.
 __global__ __launch_bounds__(kBlockThreads) void k_broadcast(
-    const Chunk* __restrict__ chunks, const float* __restrict__ x, float* __restrict__ x_rep,
+    const Chunk* __restrict__ chunks, int map, const float* __restrict__ x, float* __restrict__ x_rep,
     RepLayout rl, int n) {
-    const Piece pc = piece_of(chunks);
+    const Piece pc = piece_of(chunks, map);
     const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + pc.e0);
     for (int q = threadIdx.x; q < pc.nq; q += kBlockThreads) {
         const f4 v = ntload(xp + q);
@@ -792,10 +783,10 @@ __global__ __launch_bounds__(kBlockThreads) void k_broadcast(
 
 // Algorithm 1 initialisation: m = 0, replicas = x, base state = 0.
 __global__ __launch_bounds__(kBlockThreads) void k_init(
-    const Chunk* __restrict__ chunks, const float* __restrict__ x, float* __restrict__ m,
+    const Chunk* __restrict__ chunks, int map, const float* __restrict__ x, float* __restrict__ m,
     float* __restrict__ v, float* __restrict__ x_rep, RepLayout rl, float* __restrict__ s1,
     float* __restrict__ s2, StateLayout ml, int n) {
-    const Piece pc = piece_of(chunks);
+    const Piece pc = piece_of(chunks, map);
     const f4* __restrict__ xp = reinterpret_cast<const f4*>(x + pc.e0);
     const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
     for (int q = threadIdx.x; q < pc.nq; q += kBlockThreads) {
@@ -836,30 +827,30 @@ dim3 chunk_grid(int64_t n_chunks, int n_workers) {
 
 hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float* m, float* v,
                        float* x_rep, RepLayout rl, float* s1, float* s2, StateLayout ml, int n,
-                       hipStream_t st) {
+                       int map, hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_init, chunk_grid(n_chunks, 1), dim3(kBlockThreads), 0, st, chunks, x, m,
-                       v, x_rep, rl, s1, s2, ml, n);
+    hipLaunchKernelGGL(k_init, chunk_grid(n_chunks, 1), dim3(kBlockThreads), 0, st, chunks, map, x,
+                       m, v, x_rep, rl, s1, s2, ml, n);
     return hipGetLastError();
 }
 
 hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_rep, RepLayout rl,
                               const float* x_src, RepLayout sl, const float* g_rep, float* s1,
                               float* s2, StateLayout ml, int worker0, int n_workers,
-                              const AdamScalars& sc, hipStream_t st) {
+                              const AdamScalars& sc, int map, hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_local_adamw, chunk_grid(n_chunks, n_workers), dim3(kBlockThreads), 0, st,
-                       chunks, x_rep, rl, x_src, sl, g_rep, s1, s2, ml, worker0, sc);
+                       chunks, map, x_rep, rl, x_src, sl, g_rep, s1, s2, ml, worker0, sc);
     return hipGetLastError();
 }
 
 hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep, RepLayout rl,
                              const float* x_src, RepLayout sl, const float* g_rep, float* s1,
                              StateLayout ml, int worker0, int n_workers, const SgdScalars& sc,
-                             hipStream_t st) {
+                             int map, hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_local_sgdm, chunk_grid(n_chunks, n_workers), dim3(kBlockThreads), 0, st,
-                       chunks, x_rep, rl, x_src, sl, g_rep, s1, ml, worker0, sc);
+                       chunks, map, x_rep, rl, x_src, sl, g_rep, s1, ml, worker0, sc);
     return hipGetLastError();
 }
 
@@ -868,7 +859,7 @@ static void launch_round_end_n(const Chunk* chunks, int64_t n_chunks, const Roun
                                hipStream_t st) {
     const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
 #define DSM_ROUND_END(NW)                                                                        \
-    hipLaunchKernelGGL((k_round_end<NW, BASE, KIND>), grid, block, 0, st, chunks, a.x, a.m,      \
+    hipLaunchKernelGGL((k_round_end<NW, BASE, KIND>), grid, block, 0, st, chunks, a.map, a.x, a.m,\
                        a.x_rep, a.rl, a.x_src, a.sl, a.g_rep, a.s1, a.s2, a.u, a.bound.piece_max, \
                        a.ml, a.as, a.ss, a.gs)
     switch (a.gs.n) {
@@ -896,10 +887,10 @@ template <int BASE>
 static void launch_local_from_x_n(const Chunk* chunks, int64_t n_chunks, const float* x,
                                   float* x_rep, RepLayout rl, const float* g_rep, float* s1,
                                   float* s2, StateLayout ml, int n, const AdamScalars& as,
-                                  const SgdScalars& ss, hipStream_t st) {
+                                  const SgdScalars& ss, int map, hipStream_t st) {
     const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
 #define DSM_LOCAL_FROM_X(NW)                                                                   \
-    hipLaunchKernelGGL((k_local_from_x<NW, BASE>), grid, block, 0, st, chunks, x, x_rep, rl,    \
+    hipLaunchKernelGGL((k_local_from_x<NW, BASE>), grid, block, 0, st, chunks, map, x, x_rep, rl,\
                        g_rep, s1, s2, ml, n, as, ss)
     switch (n) {
         case 1: DSM_LOCAL_FROM_X(1); break;
@@ -914,14 +905,15 @@ static void launch_local_from_x_n(const Chunk* chunks, int64_t n_chunks, const f
 hipError_t launch_local_from_x(const Chunk* chunks, int64_t n_chunks, const float* x,
                                float* x_rep, RepLayout rl, const float* g_rep, float* s1,
                                float* s2, StateLayout ml, int n, bool adamw,
-                               const AdamScalars& as, const SgdScalars& ss, hipStream_t st) {
+                               const AdamScalars& as, const SgdScalars& ss, int map,
+                               hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
     if (adamw)
         launch_local_from_x_n<kBaseAdamW>(chunks, n_chunks, x, x_rep, rl, g_rep, s1, s2, ml, n,
-                                          as, ss, st);
+                                          as, ss, map, st);
     else
         launch_local_from_x_n<kBaseSgd>(chunks, n_chunks, x, x_rep, rl, g_rep, s1, s2, ml, n, as,
-                                        ss, st);
+                                        ss, map, st);
     return hipGetLastError();
 }
 
@@ -934,10 +926,10 @@ static void launch_bound_reduce(const BoundWords& bw, int n_tensors, hipStream_t
 
 static void launch_rand_pass2(const Chunk* chunks, int64_t n_chunks, float* x, float* x_rep,
                               RepLayout rl, const float* u, const uint32_t* bits,
-                              const GlobalScalars& sc, bool broadcast, hipStream_t st) {
+                              const GlobalScalars& sc, bool broadcast, int map, hipStream_t st) {
     const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
 #define DSM_PASS2(MODE, B) \
-    hipLaunchKernelGGL((k_global_rand_pass2<MODE, B>), grid, block, 0, st, chunks, x, x_rep, rl, u, bits, sc)
+    hipLaunchKernelGGL((k_global_rand_pass2<MODE, B>), grid, block, 0, st, chunks, map, x, x_rep, rl, u, bits, sc)
     if (sc.mode == 1) {
         if (broadcast) DSM_PASS2(1, true); else DSM_PASS2(1, false);
     } else {
@@ -959,18 +951,18 @@ hipError_t launch_round_end(const Chunk* chunks, int64_t n_chunks, int n_tensors
     if (randomized && n_tensors > 0) launch_bound_reduce(a.bound, n_tensors, st);
     if (randomized && n_chunks > 0)
         launch_rand_pass2(chunks, n_chunks, a.x, a.x_rep, a.rl, a.u, a.bound.bits, a.gs,
-                          broadcast, st);
+                          broadcast, a.map_pass2, st);
     return hipGetLastError();
 }
 
 template <int RULE, bool BCAST>
 static void launch_global_det_n(const Chunk* chunks, int64_t n_chunks, float* x, float* m,
                                 float* v, float* x_rep, RepLayout rl, const GlobalScalars& sc,
-                                hipStream_t st) {
+                                int map, hipStream_t st) {
     const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
 #define DSM_GLOBAL_DET(NW)                                                                     \
-    hipLaunchKernelGGL((k_global_det<NW, RULE, BCAST>), grid, block, 0, st, chunks, x, m, v,   \
-                       x_rep, rl, sc)
+    hipLaunchKernelGGL((k_global_det<NW, RULE, BCAST>), grid, block, 0, st, chunks, map, x, m, \
+                       v, x_rep, rl, sc)
     switch (sc.n) {
         case 1: DSM_GLOBAL_DET(1); break;
         case 2: DSM_GLOBAL_DET(2); break;
@@ -984,33 +976,33 @@ static void launch_global_det_n(const Chunk* chunks, int64_t n_chunks, float* x,
 template <int RULE>
 static void launch_global_det_rule(const Chunk* chunks, int64_t n_chunks, float* x, float* m,
                                    float* v, float* x_rep, RepLayout rl, const GlobalScalars& sc,
-                                   bool broadcast, hipStream_t st) {
+                                   bool broadcast, int map, hipStream_t st) {
     if (broadcast)
-        launch_global_det_n<RULE, true>(chunks, n_chunks, x, m, v, x_rep, rl, sc, st);
+        launch_global_det_n<RULE, true>(chunks, n_chunks, x, m, v, x_rep, rl, sc, map, st);
     else
-        launch_global_det_n<RULE, false>(chunks, n_chunks, x, m, v, x_rep, rl, sc, st);
+        launch_global_det_n<RULE, false>(chunks, n_chunks, x, m, v, x_rep, rl, sc, map, st);
 }
 
 hipError_t launch_global_det(const Chunk* chunks, int64_t n_chunks, float* x, float* m,
                              float* v, float* x_rep, RepLayout rl, const GlobalScalars& sc,
-                             bool broadcast, hipStream_t st) {
+                             bool broadcast, int map, hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
     switch (sc.rule) {
         case kRuleLookahead:
             launch_global_det_rule<kRuleLookahead>(chunks, n_chunks, x, m, v, x_rep, rl, sc,
-                                                   broadcast, st);
+                                                   broadcast, map, st);
             break;
         case kRuleSignedSlowMo:
             launch_global_det_rule<kRuleSignedSlowMo>(chunks, n_chunks, x, m, v, x_rep, rl, sc,
-                                                      broadcast, st);
+                                                      broadcast, map, st);
             break;
         case kRuleGlobalAdamW:
             launch_global_det_rule<kRuleGlobalAdamW>(chunks, n_chunks, x, m, v, x_rep, rl, sc,
-                                                     broadcast, st);
+                                                     broadcast, map, st);
             break;
         default:
             launch_global_det_rule<kRuleSignMomentum>(chunks, n_chunks, x, m, v, x_rep, rl, sc,
-                                                      broadcast, st);
+                                                      broadcast, map, st);
             break;
     }
     return hipGetLastError();
@@ -1019,12 +1011,12 @@ hipError_t launch_global_det(const Chunk* chunks, int64_t n_chunks, float* x, fl
 hipError_t launch_global_rand(const Chunk* chunks, int64_t n_chunks, int n_tensors, float* x,
                               float* m, float* x_rep, RepLayout rl, float* u,
                               const BoundWords& bw, const GlobalScalars& sc, bool broadcast,
-                              hipStream_t st) {
+                              int map, hipStream_t st) {
     if (n_chunks > 0) {
         const dim3 grid = chunk_grid(n_chunks, 1), block(kBlockThreads);
         uint32_t* pm = bw.piece_max;
 #define DSM_PASS1(NW) \
-    hipLaunchKernelGGL(k_global_rand_pass1<NW>, grid, block, 0, st, chunks, x, m, x_rep, rl, u, pm, sc)
+    hipLaunchKernelGGL(k_global_rand_pass1<NW>, grid, block, 0, st, chunks, map, x, m, x_rep, rl, u, pm, sc)
         switch (sc.n) {
             case 1: DSM_PASS1(1); break;
             case 2: DSM_PASS1(2); break;
@@ -1035,15 +1027,16 @@ hipError_t launch_global_rand(const Chunk* chunks, int64_t n_chunks, int n_tenso
 #undef DSM_PASS1
     }
     if (n_tensors > 0) launch_bound_reduce(bw, n_tensors, st);
-    if (n_chunks > 0) launch_rand_pass2(chunks, n_chunks, x, x_rep, rl, u, bw.bits, sc, broadcast, st);
+    if (n_chunks > 0)
+        launch_rand_pass2(chunks, n_chunks, x, x_rep, rl, u, bw.bits, sc, broadcast, map, st);
     return hipGetLastError();
 }
 
 hipError_t launch_broadcast(const Chunk* chunks, int64_t n_chunks, const float* x, float* x_rep,
-                            RepLayout rl, int n, hipStream_t st) {
+                            RepLayout rl, int n, int map, hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_broadcast, chunk_grid(n_chunks, 1), dim3(kBlockThreads), 0, st, chunks, x,
-                       x_rep, rl, n);
+    hipLaunchKernelGGL(k_broadcast, chunk_grid(n_chunks, 1), dim3(kBlockThreads), 0, st, chunks,
+                       map, x, x_rep, rl, n);
     return hipGetLastError();
 }
 

@@ -23,6 +23,7 @@ struct dsm_ctx {
     std::vector<dsm::Chunk> chunks;  // host copy; the device copy lives in the workspace
     dsm::RepLayout rep{};            // how x_rep holds the n replicas
     dsm::StateLayout ml{};           // how g_rep, s1_rep and s2_rep hold theirs
+    dsm::XcdMaps maps{};             // XCD map of each kernel kind for this layout
     std::vector<int32_t> chunk0;     // first chunk of each tensor, then n_chunks (host copy)
     dsm_buffers buf{};
     dsm::Chunk* d_chunks = nullptr;
@@ -296,10 +297,10 @@ hipError_t launch_local(dsm_ctx* ctx, const LocalCoefs& lc, const float* src, ds
     if (ctx->base == DSM_BASE_ADAMW)
         return dsm::launch_local_adamw(ctx->d_chunks, n_chunks, ctx->buf.x_rep, ctx->rep, src, sl,
                                        ctx->buf.g_rep, ctx->buf.s1_rep, ctx->buf.s2_rep,
-                                       ctx->ml, w0, nw, lc.adam, ctx->stream);
+                                       ctx->ml, w0, nw, lc.adam, ctx->maps.local, ctx->stream);
     return dsm::launch_local_sgdm(ctx->d_chunks, n_chunks, ctx->buf.x_rep, ctx->rep, src, sl,
                                   ctx->buf.g_rep, ctx->buf.s1_rep, ctx->ml, w0, nw, lc.sgd,
-                                  ctx->stream);
+                                  ctx->maps.local, ctx->stream);
 }
 
 // After a global step: the round's local counts restart; without broadcast
@@ -446,6 +447,7 @@ dsm_status init_context(const dsm_problem* problem, const dsm_buffers* caller, d
     ctx->arena_elems = L.arena_elems;
     ctx->rep = rep;
     ctx->ml = ml;
+    ctx->maps = dsm::kMapsByLayout[problem->replica_layout];
     ctx->chunks = std::move(chunks);
     ctx->chunk0 = std::move(chunk0);
     ctx->buf = *b;
@@ -479,7 +481,7 @@ dsm_status init_context(const dsm_problem* problem, const dsm_buffers* caller, d
         }
         e = dsm::launch_init(ctx->d_chunks, static_cast<int64_t>(ctx->chunks.size()), b->x, b->m,
                              b->v, b->x_rep, ctx->rep, b->s1_rep, adamw ? b->s2_rep : nullptr,
-                             ctx->ml, ctx->n, ctx->stream);
+                             ctx->ml, ctx->n, ctx->maps.copy, ctx->stream);
         if (e != hipSuccess) {
             dsm_status r = hip_fail(nullptr, "launching the initialisation kernel", e);
             delete ctx;
@@ -534,7 +536,7 @@ dsm_status dsm_local_step(dsm_ctx* ctx, int32_t worker, int64_t step, const dsm_
         hipError_t e = dsm::launch_local_from_x(
             ctx->d_chunks, static_cast<int64_t>(ctx->chunks.size()), ctx->buf.x, ctx->buf.x_rep,
             ctx->rep, ctx->buf.g_rep, ctx->buf.s1_rep, ctx->buf.s2_rep, ctx->ml, ctx->n,
-            ctx->base == DSM_BASE_ADAMW, lc.adam, lc.sgd, ctx->stream);
+            ctx->base == DSM_BASE_ADAMW, lc.adam, lc.sgd, ctx->maps.from_x, ctx->stream);
         if (e != hipSuccess) return hip_fail(ctx, "launching the local step", e);
     }
     for (int a = w0; a < w0 + nw && !all_stale;) {
@@ -571,11 +573,12 @@ dsm_status dsm_global_step(dsm_ctx* ctx, int64_t t, const dsm_global_hparams* hp
     hipError_t e;
     if (!randomized) {
         e = dsm::launch_global_det(ctx->d_chunks, n_chunks, ctx->buf.x, ctx->buf.m, ctx->buf.v,
-                                   ctx->buf.x_rep, ctx->rep, sc, broadcast != 0, ctx->stream);
+                                   ctx->buf.x_rep, ctx->rep, sc, broadcast != 0, ctx->maps.global,
+                                   ctx->stream);
     } else {
         e = dsm::launch_global_rand(ctx->d_chunks, n_chunks, ctx->n_tensors, ctx->buf.x, ctx->buf.m,
                                     ctx->buf.x_rep, ctx->rep, ctx->buf.u_scratch, ctx->bound, sc,
-                                    broadcast != 0, ctx->stream);
+                                    broadcast != 0, ctx->maps.global, ctx->stream);
     }
     if (e != hipSuccess) return hip_fail(ctx, "launching the global step", e);
     end_round(ctx, broadcast != 0, randomized);
@@ -619,6 +622,8 @@ dsm_status dsm_round_end(dsm_ctx* ctx, int64_t step, const dsm_local_hparams* lo
     a.u = ctx->buf.u_scratch;
     a.bound = ctx->bound;
     a.ml = ctx->ml;
+    a.map = ctx->maps.round_end;
+    a.map_pass2 = ctx->maps.global;
     a.as = lc.adam;
     a.ss = lc.sgd;
     a.gs = gs;
@@ -636,7 +641,7 @@ dsm_status dsm_sync(dsm_ctx* ctx) {
     if (st != DSM_OK) return st;
     hipError_t e = dsm::launch_broadcast(ctx->d_chunks, static_cast<int64_t>(ctx->chunks.size()),
                                          ctx->buf.x, ctx->buf.x_rep, ctx->rep, ctx->n,
-                                         ctx->stream);
+                                         ctx->maps.copy, ctx->stream);
     if (e != hipSuccess) return hip_fail(ctx, "launching the synchronisation", e);
     for (int i = 0; i < ctx->n; ++i) {
         ctx->local_count[i] = 0;

@@ -53,6 +53,7 @@ struct Launch {
     std::string kind;
     const dsm::Chunk* chunks = nullptr;
     int64_t n_chunks = -1;
+    int map = -1, map2 = -1;
     const float* x = nullptr;
     const float* x_rep = nullptr;
     const float* x_src = nullptr;
@@ -104,9 +105,10 @@ hipError_t hipGetDevice(int* device) {
 namespace dsm {
 hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float*, float* v,
                        float* x_rep, RepLayout rl, float*, float* s2, StateLayout ml, int n,
-                       hipStream_t) {
+                       int map, hipStream_t) {
     Launch l;
     l.kind = "init";
+    l.map = map;
     l.chunks = chunks;
     l.n_chunks = n_chunks;
     l.x = x;
@@ -121,9 +123,10 @@ hipError_t launch_init(const Chunk* chunks, int64_t n_chunks, float* x, float*, 
 hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_rep, RepLayout rl,
                               const float* x_src, RepLayout sl, const float*, float*, float* s2,
                               StateLayout ml, int worker0, int n_workers, const AdamScalars& sc,
-                              hipStream_t) {
+                              int map, hipStream_t) {
     Launch l;
     l.kind = "local_adamw";
+    l.map = map;
     l.chunks = chunks;
     l.n_chunks = n_chunks;
     l.x_rep = x_rep;
@@ -140,9 +143,10 @@ hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_re
 hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep, RepLayout rl,
                              const float* x_src, RepLayout sl, const float*, float*,
                              StateLayout ml, int worker0, int n_workers, const SgdScalars& sc,
-                             hipStream_t) {
+                             int map, hipStream_t) {
     Launch l;
     l.kind = "local_sgdm";
+    l.map = map;
     l.chunks = chunks;
     l.n_chunks = n_chunks;
     l.x_rep = x_rep;
@@ -158,9 +162,10 @@ hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep
 hipError_t launch_local_from_x(const Chunk* chunks, int64_t n_chunks, const float* x,
                                float* x_rep, RepLayout rl, const float*, float*, float* s2,
                                StateLayout ml, int n, bool adamw, const AdamScalars& as,
-                               const SgdScalars& ss, hipStream_t) {
+                               const SgdScalars& ss, int map, hipStream_t) {
     Launch l;
     l.kind = "local_from_x";
+    l.map = map;
     l.chunks = chunks;
     l.n_chunks = n_chunks;
     l.x = x;
@@ -178,6 +183,8 @@ hipError_t launch_round_end(const Chunk* chunks, int64_t n_chunks, int n_tensors
                             const RoundEndArgs& a, bool broadcast, hipStream_t) {
     Launch l;
     l.kind = "round_end";
+    l.map = a.map;
+    l.map2 = a.map_pass2;
     l.chunks = chunks;
     l.n_chunks = n_chunks;
     l.n_tensors = n_tensors;
@@ -201,9 +208,10 @@ hipError_t launch_round_end(const Chunk* chunks, int64_t n_chunks, int n_tensors
 }
 hipError_t launch_global_det(const Chunk* chunks, int64_t n_chunks, float* x, float*, float* v,
                              float* x_rep, RepLayout rl, const GlobalScalars& sc, bool broadcast,
-                             hipStream_t) {
+                             int map, hipStream_t) {
     Launch l;
     l.kind = "global_det";
+    l.map = map;
     l.chunks = chunks;
     l.n_chunks = n_chunks;
     l.x = x;
@@ -216,9 +224,10 @@ hipError_t launch_global_det(const Chunk* chunks, int64_t n_chunks, float* x, fl
 }
 hipError_t launch_global_rand(const Chunk* chunks, int64_t n_chunks, int n_tensors, float* x,
                               float*, float* x_rep, RepLayout rl, float* u, const BoundWords& bw,
-                              const GlobalScalars& sc, bool broadcast, hipStream_t) {
+                              const GlobalScalars& sc, bool broadcast, int map, hipStream_t) {
     Launch l;
     l.kind = "global_rand";
+    l.map = map;
     l.chunks = chunks;
     l.n_chunks = n_chunks;
     l.n_tensors = n_tensors;
@@ -234,9 +243,10 @@ hipError_t launch_global_rand(const Chunk* chunks, int64_t n_chunks, int n_tenso
     return record(l);
 }
 hipError_t launch_broadcast(const Chunk* chunks, int64_t n_chunks, const float* x, float* x_rep,
-                            RepLayout rl, int n, hipStream_t) {
+                            RepLayout rl, int n, int map, hipStream_t) {
     Launch l;
     l.kind = "broadcast";
+    l.map = map;
     l.chunks = chunks;
     l.n_chunks = n_chunks;
     l.x = x;
@@ -326,6 +336,7 @@ struct Buffers {
     int64_t arena = 0;
     dsm::RepLayout rep{};  // the replica layout every launch must pass
     dsm::RepLayout state{};  // and the layout of g_rep, s1_rep and s2_rep
+    dsm::XcdMaps maps{};     // the XCD maps of the problem's layout
     float* alloc(int64_t floats) {
         const size_t bytes = static_cast<size_t>(round_up(std::max<int64_t>(floats, 1) * 4, 256));
         void* p = std::aligned_alloc(256, bytes);
@@ -342,6 +353,8 @@ struct Buffers {
         const bool adamw = P.p.base == DSM_BASE_ADAMW;
         const int nb = adamw ? 4 : 3;
         rep = expected_layout(P.p.replica_layout, n, arena, nb);
+        if (P.p.replica_layout >= 0 && P.p.replica_layout <= 2)
+            maps = dsm::kMapsByLayout[P.p.replica_layout];
         b.x = alloc(arena);
         b.m = alloc(arena);
         if (P.p.replica_layout == DSM_REPLICAS_STATE_BLOCKED) {
@@ -537,7 +550,7 @@ void check_init_and_chunks() {
                 const Launch& l = g_log[0];
                 CHECK(l.kind == "init" && l.x == B.b.x && l.x_rep == B.b.x_rep && l.v == B.b.v &&
                           l.s2 == B.b.s2_rep && same_state(l.ml, B.state) && l.n_workers == 3 &&
-                          same_layout(l.rl, B.rep),
+                          same_layout(l.rl, B.rep) && l.map == B.maps.copy,
                       "init arguments");
                 check_chunk_table(P, B, l);
             }
@@ -600,7 +613,8 @@ void check_init_rejections() {
 void expect_local(const Launch& l, const Buffers& B, bool adamw, bool from_x, int w0, int nw,
                   const char* what) {
     CHECK(l.kind == (adamw ? "local_adamw" : "local_sgdm"), "%s: kind %s", what, l.kind.c_str());
-    CHECK(l.x_rep == B.b.x_rep && same_state(l.ml, B.state) && same_layout(l.rl, B.rep),
+    CHECK(l.x_rep == B.b.x_rep && same_state(l.ml, B.state) && same_layout(l.rl, B.rep) &&
+              l.map == B.maps.local,
           "%s: replica buffer", what);
     CHECK(l.x_src == (from_x ? B.b.x : B.b.x_rep) &&
               same_layout(l.sl, from_x ? dsm::RepLayout{0, 0, 62, 0} : B.rep),
@@ -640,7 +654,8 @@ void check_state_machine_adamw(int layout) {
     g_log.clear();
     CHECK(dsm_global_step(ctx, 0, &gh, 0) == DSM_OK, "global, no broadcast");
     CHECK(g_log.size() == 1 && g_log[0].kind == "global_det" && !g_log[0].broadcast &&
-              g_log[0].x == B.b.x && g_log[0].x_rep == B.b.x_rep && same_layout(g_log[0].rl, B.rep),
+              g_log[0].x == B.b.x && g_log[0].x_rep == B.b.x_rep && same_layout(g_log[0].rl, B.rep) &&
+              g_log[0].map == B.maps.global,
           "global launch");
     // Round t = 1: worker 1 first (reads x), then all: runs [0], [1], [2, 5) with
     // sources x, x_rep, x.
@@ -667,6 +682,7 @@ void check_state_machine_adamw(int layout) {
         CHECK(l.kind == "round_end" && l.adamw && l.broadcast && l.n_tensors == 3, "round end");
         CHECK(l.x_src == B.b.x_rep && same_layout(l.sl, B.rep) && same_layout(l.rl, B.rep),
               "round end reads the replicas");
+        CHECK(l.map == B.maps.round_end && l.map2 == B.maps.global, "round end XCD maps");
         CHECK(l.u == B.b.u_scratch && l.s2 == B.b.s2_rep, "round end buffers");
         check_bound_words(P, B, l.bounds, l.chunk0, l.piece_max, "round end");
         CHECK(l.gs.mode == DSM_SIGN_RAND_FLIP && l.gs.t == 1 && l.gs.key0 == 0x89ABCDEFu &&
@@ -698,7 +714,8 @@ void check_state_machine_adamw(int layout) {
     g_log.clear();
     CHECK(dsm_sync(ctx) == DSM_OK, "sync");
     CHECK(g_log.size() == 1 && g_log[0].kind == "broadcast" && g_log[0].n_workers == 5 &&
-              g_log[0].x == B.b.x && g_log[0].x_rep == B.b.x_rep && same_layout(g_log[0].rl, B.rep),
+              g_log[0].x == B.b.x && g_log[0].x_rep == B.b.x_rep && same_layout(g_log[0].rl, B.rep) &&
+              g_log[0].map == B.maps.copy,
           "broadcast launch");
     for (int k = 0; k < 3; ++k) CHECK(dsm_local_step(ctx, -1, 11 + k, &lh) == DSM_OK, "after sync");
     CHECK(dsm_local_step(ctx, -1, 14, &lh) == DSM_ERR_STATE, "H after sync");
@@ -769,7 +786,7 @@ void check_local_from_x(int layout) {
                     CHECK(l.kind == "local_from_x" && l.x == B.b.x && l.x_rep == B.b.x_rep &&
                               same_state(l.ml, B.state) && l.n_workers == n && l.adamw == adamw &&
                               l.s2 == B.b.s2_rep && l.chunks == B.b.workspace &&
-                              same_layout(l.rl, B.rep),
+                              same_layout(l.rl, B.rep) && l.map == B.maps.from_x,
                           "n = %d: all-worker launch from x", n);
                 } else {
                     expect_local(l, B, adamw, true, 0, 1, "n = 1 from x");

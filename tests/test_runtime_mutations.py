@@ -41,6 +41,16 @@ MUTATIONS = [
      "state-blocked buffer order not checked"),
     ("    a.sl = from_x ? dsm::single_copy() : ctx->rep;", "    a.sl = ctx->rep;",
      "round end after a lazy broadcast reads the stale replicas"),
+    ("    ctx->maps = dsm::kMapsByLayout[problem->replica_layout];",
+     "    ctx->maps = dsm::kMapsByLayout[0];", "XCD maps of the contiguous layout for every layout"),
+    ("    a.map_pass2 = ctx->maps.global;", "    a.map_pass2 = ctx->maps.round_end;",
+     "randomized second pass launched with the round-end map"),
+    ("ctx->base == DSM_BASE_ADAMW, lc.adam, lc.sgd, ctx->maps.from_x, ctx->stream);",
+     "ctx->base == DSM_BASE_ADAMW, lc.adam, lc.sgd, ctx->maps.local, ctx->stream);",
+     "step from x launched with the local-step map"),
+    ("ctx->buf.x, ctx->buf.x_rep, ctx->rep, ctx->n,\n                                         ctx->maps.copy,",
+     "ctx->buf.x, ctx->buf.x_rep, ctx->rep, ctx->n,\n                                         ctx->maps.global,",
+     "synchronisation launched with the global-step map"),
     ("        g_static_busy[ctx->static_device] = false;\n", "",
      "a static-scratch context never releases its device"),
     ("        if (need > dsm::kStaticScratchBytes)", "        if (need > 2 * dsm::kStaticScratchBytes)",
