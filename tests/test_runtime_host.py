@@ -1,14 +1,19 @@
 """The library's host runtime under AddressSanitizer and UBSan, on the CPU.
 
 tests/native/runtime_host_check.cpp compiles the runtime source
-(paper_2411_17866_amd/csrc/dsm_runtime.cpp) with g++ against stubs of the four
-HIP calls the runtime makes and of the kernel launchers, so the whole C ABI
-runs without a GPU.  Its checks are:
-  * dsm_layout on 3000 random valid and invalid problems;
+(paper_2411_17866_amd/csrc/dsm_runtime.cpp) with g++ against stubs of the HIP
+calls the runtime makes (device count and current device, copy, stream sync,
+error string), of the static-scratch lookup and of the kernel launchers, so
+the whole C ABI runs without a GPU.  Its checks are:
+  * dsm_layout on 3000 random valid and invalid problems, in the three
+    replica layouts;
   * the uploaded chunk table;
+  * the blocked layouts' addressing: every piece inside one block, and every
+    element of every copy at its own slot of the allocation;
   * the randomized sign's bound words in the workspace;
-  * the Algorithm 1 state machine;
+  * the Algorithm 1 state machine, with the layouts and XCD map of each launch;
   * the replica source of each local launch, fresh or stale;
+  * dsm_init_static: the static scratch, its limit, one context per device;
   * the fp32 host coefficients against long double;
   * every error path.
 """
