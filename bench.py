@@ -252,9 +252,8 @@ def main():
     ap.add_argument("--replica-layout", choices=("auto", "state-blocked", "blocked", "contiguous"),
                     default="auto",
                     help="how the per-worker buffers hold their n copies (dsm_replica_layout); "
-                         "auto: state-blocked for n <= 4 when one copy of the parameters "
-                         "exceeds the 256 MB last-level cache, contiguous for smaller n <= 4 "
-                         "problems, blocked replicas for n > 4")
+                         "auto: state-blocked when one copy of the parameters exceeds the "
+                         "256 MB last-level cache, contiguous otherwise")
     ap.add_argument("--no-parity", action="store_true",
                     help="skip the oracle check of one untimed round after the timed region")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -281,16 +280,12 @@ def main():
     print(f"[bench] workload {w.name}: d={w.d} tensors={len(w.tensors)} n={n} H={H}",
           file=sys.stderr, flush=True)
     if args.replica_layout == "auto":
-        # Measured on MI355X: the blocked layouts pin down where the streams
-        # of a kernel sit in HBM, which pays once the arenas stream from HBM;
-        # arenas that stay in the 256 MB MALL between calls run faster
-        # contiguous (tiny workload: local AdamW 20.8-21.0 us against 22.6).
-        if n > 4:
-            args.replica_layout = "blocked"
-        elif 4 * w.d > 256 << 20:
-            args.replica_layout = "state-blocked"
-        else:
-            args.replica_layout = "contiguous"
+        # Measured on MI355X: blocking the replicas with their optimizer state
+        # pins down where a kernel's streams sit in HBM, which pays once the
+        # arenas stream from HBM (GPT-2 small to xl, n = 4 and 8); arenas that
+        # stay in the 256 MB MALL between calls run faster contiguous (tiny
+        # workload: local AdamW 20.8-21.0 us against 22.6 us).
+        args.replica_layout = "state-blocked" if 4 * w.d > 256 << 20 else "contiguous"
     layout = {"state-blocked": dsm.DSM_REPLICAS_STATE_BLOCKED, "blocked": dsm.DSM_REPLICAS_BLOCKED,
               "contiguous": dsm.DSM_REPLICAS_CONTIGUOUS}[args.replica_layout]
     ar = A.Arenas(w.numel, n, H, w.base, decay=w.decay, randomized=True, global_adamw=True,

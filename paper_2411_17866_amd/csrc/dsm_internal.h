@@ -138,6 +138,12 @@ struct GlobalScalars {
 // the runtime keeps one set per layout; build-time -D settings override them.
 // global: the global steps and the randomized second pass of the round end;
 // copy: the broadcast of dsm_sync and the initial copy of dsm_init.
+//
+// A local step's map may add kInterleaveWorkers: its grid is then one row of
+// pieces x workers, worker fastest, so consecutive work-groups take the same
+// piece of successive workers (with the state blocked, one block at a time)
+// instead of running worker by worker.
+constexpr int kInterleaveWorkers = 4;
 struct XcdMaps {
     int local, round_end, from_x, global, copy;
 };
@@ -148,10 +154,20 @@ struct XcdMaps {
 #define DSM_MAPS_BLOCKED 1, 2, 1, 0, 1
 #endif
 #ifndef DSM_MAPS_STATE_BLOCKED
-#define DSM_MAPS_STATE_BLOCKED 1, 1, 1, 1, 1
+#define DSM_MAPS_STATE_BLOCKED 1 + kInterleaveWorkers, 1, 1, 1, 1
 #endif
 constexpr XcdMaps kMapsByLayout[3] = {{DSM_MAPS_CONTIGUOUS}, {DSM_MAPS_BLOCKED},
                                       {DSM_MAPS_STATE_BLOCKED}};
+
+// The map a local step over n_workers workers launches with: the interleaved
+// order needs the whole pieces x workers row in one grid dimension, which
+// holds fewer than 2^32 threads; past that the step runs worker by worker.
+inline int local_map(int64_t n_chunks, int n_workers, int map) {
+    const int64_t row = n_chunks * kSplit * n_workers;
+    if ((map & kInterleaveWorkers) && row * kBlockThreads >= (int64_t(1) << 32))
+        return map & ~kInterleaveWorkers;
+    return map;
+}
 
 // Kernel launchers (dsm_kernels.hip).  All return the launch status.  The
 // replica buffer x_rep is addressed through its RepLayout rl, and g_rep, s1

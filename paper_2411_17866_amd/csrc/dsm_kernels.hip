@@ -124,9 +124,8 @@ __device__ __forceinline__ uint32_t work_index(int map) {
     return work_index<0>();
 }
 
-__device__ __forceinline__ Piece piece_of(const Chunk* __restrict__ chunks, int map) {
+__device__ __forceinline__ Piece piece_at(const Chunk* __restrict__ chunks, uint32_t wi) {
     Piece pc;
-    const uint32_t wi = work_index(map);
     pc.wi = wi;
     pc.c = chunks[wi / kSplit];
     const int nvec = (pc.c.len + 3) >> 2;
@@ -136,6 +135,25 @@ __device__ __forceinline__ Piece piece_of(const Chunk* __restrict__ chunks, int 
     pc.e0 = pc.c.off + 4 * static_cast<int64_t>(q_lo);
     pc.j4 = static_cast<uint32_t>(pc.c.j0 >> 2) + static_cast<uint32_t>(q_lo);
     return pc;
+}
+
+__device__ __forceinline__ Piece piece_of(const Chunk* __restrict__ chunks, int map) {
+    return piece_at(chunks, work_index(map & 3));
+}
+
+// The piece and worker of a local-step work-group.  Without kInterleaveWorkers
+// in the map the grid is (pieces, workers) and runs worker by worker; with it
+// the grid is one row of pieces x workers, worker fastest, so consecutive
+// work-groups take the same piece of successive workers.
+__device__ __forceinline__ Piece local_piece(const Chunk* __restrict__ chunks, int map, int worker0,
+                                             int n_workers, int64_t& w) {
+    if (map & kInterleaveWorkers) {
+        const uint32_t f = work_index(map & 3);
+        w = worker0 + static_cast<int64_t>(f % static_cast<uint32_t>(n_workers));
+        return piece_at(chunks, f / static_cast<uint32_t>(n_workers));
+    }
+    w = worker0 + static_cast<int64_t>(blockIdx.y);
+    return piece_at(chunks, work_index(map & 3));
 }
 
 // ---------------------------------------------------------------- AdamW
@@ -175,9 +193,9 @@ __device__ __forceinline__ void adamw4(f4& x, f4 g, f4& m, f4& v, float lam, con
 __global__ __launch_bounds__(kBlockThreads) void k_local_adamw(
     const Chunk* __restrict__ chunks, int map, float* x_rep, RepLayout rl, const float* x_src,
     RepLayout sl, const float* __restrict__ g_rep, float* __restrict__ s1,
-    float* __restrict__ s2, StateLayout ml, int worker0, AdamScalars sc) {
-    const Piece pc = piece_of(chunks, map);
-    const int64_t w = worker0 + static_cast<int>(blockIdx.y);
+    float* __restrict__ s2, StateLayout ml, int worker0, int n_workers, AdamScalars sc) {
+    int64_t w;
+    const Piece pc = local_piece(chunks, map, worker0, n_workers, w);
     f4* xp = reinterpret_cast<f4*>(x_rep + rep_index(rl, w, pc.e0));
     const f4* xs = reinterpret_cast<const f4*>(x_src + rep_index(sl, w, pc.e0));
     const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + rep_index(ml.g, w, pc.e0));
@@ -223,9 +241,9 @@ __device__ __forceinline__ void sgdm4(f4& x, f4 g, f4& m, const SgdScalars& s) {
 __global__ __launch_bounds__(kBlockThreads) void k_local_sgdm(
     const Chunk* __restrict__ chunks, int map, float* x_rep, RepLayout rl, const float* x_src,
     RepLayout sl, const float* __restrict__ g_rep, float* __restrict__ s1, StateLayout ml,
-    int worker0, SgdScalars sc) {
-    const Piece pc = piece_of(chunks, map);
-    const int64_t w = worker0 + static_cast<int>(blockIdx.y);
+    int worker0, int n_workers, SgdScalars sc) {
+    int64_t w;
+    const Piece pc = local_piece(chunks, map, worker0, n_workers, w);
     f4* xp = reinterpret_cast<f4*>(x_rep + rep_index(rl, w, pc.e0));
     const f4* xs = reinterpret_cast<const f4*>(x_src + rep_index(sl, w, pc.e0));
     const f4* __restrict__ gp = reinterpret_cast<const f4*>(g_rep + rep_index(ml.g, w, pc.e0));
@@ -821,6 +839,14 @@ dim3 chunk_grid(int64_t n_chunks, int n_workers) {
     return dim3(static_cast<unsigned>(n_chunks * kSplit), static_cast<unsigned>(n_workers), 1);
 }
 
+// Grid of a local step: one row of pieces x workers when the map interleaves
+// the workers, else (pieces, workers).
+dim3 local_grid(int64_t n_chunks, int n_workers, int map) {
+    if (map & kInterleaveWorkers)
+        return dim3(static_cast<unsigned>(n_chunks * kSplit * n_workers), 1, 1);
+    return chunk_grid(n_chunks, n_workers);
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------- launchers
@@ -839,8 +865,10 @@ hipError_t launch_local_adamw(const Chunk* chunks, int64_t n_chunks, float* x_re
                               float* s2, StateLayout ml, int worker0, int n_workers,
                               const AdamScalars& sc, int map, hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_local_adamw, chunk_grid(n_chunks, n_workers), dim3(kBlockThreads), 0, st,
-                       chunks, map, x_rep, rl, x_src, sl, g_rep, s1, s2, ml, worker0, sc);
+    map = local_map(n_chunks, n_workers, map);
+    hipLaunchKernelGGL(k_local_adamw, local_grid(n_chunks, n_workers, map), dim3(kBlockThreads), 0,
+                       st, chunks, map, x_rep, rl, x_src, sl, g_rep, s1, s2, ml, worker0, n_workers,
+                       sc);
     return hipGetLastError();
 }
 
@@ -849,8 +877,9 @@ hipError_t launch_local_sgdm(const Chunk* chunks, int64_t n_chunks, float* x_rep
                              StateLayout ml, int worker0, int n_workers, const SgdScalars& sc,
                              int map, hipStream_t st) {
     if (n_chunks == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_local_sgdm, chunk_grid(n_chunks, n_workers), dim3(kBlockThreads), 0, st,
-                       chunks, map, x_rep, rl, x_src, sl, g_rep, s1, ml, worker0, sc);
+    map = local_map(n_chunks, n_workers, map);
+    hipLaunchKernelGGL(k_local_sgdm, local_grid(n_chunks, n_workers, map), dim3(kBlockThreads), 0,
+                       st, chunks, map, x_rep, rl, x_src, sl, g_rep, s1, ml, worker0, n_workers, sc);
     return hipGetLastError();
 }
 

@@ -1144,7 +1144,37 @@ void check_init_static() {
     g_scratch = nullptr;
 }
 
+// The worker-interleaved local-step order keeps the whole pieces x workers row
+// in one grid dimension of fewer than 2^32 threads, or falls back to the
+// worker-by-worker grid.
+void check_local_map() {
+    using dsm::kBlockThreads;
+    using dsm::kInterleaveWorkers;
+    using dsm::kSplit;
+    const int64_t limit = (int64_t(1) << 32) / kBlockThreads;  // work-groups per row
+    for (int base : {0, 1, 2}) {
+        const int il = base | kInterleaveWorkers;
+        for (int n : {1, 2, 3, 8, 64}) {
+            // The largest chunk count whose row fits, and one more.
+            const int64_t fit = (limit - 1) / (int64_t(kSplit) * n);
+            CHECK(dsm::local_map(fit, n, il) == il, "row of %lld chunks x %d workers fits",
+                  static_cast<long long>(fit), n);
+            CHECK(fit * kSplit * n * kBlockThreads < (int64_t(1) << 32), "fit really fits");
+            const int64_t over = fit + 1;
+            CHECK(over * kSplit * n * kBlockThreads >= (int64_t(1) << 32) ?
+                      dsm::local_map(over, n, il) == base : dsm::local_map(over, n, il) == il,
+                  "row of %lld chunks x %d workers", static_cast<long long>(over), n);
+            CHECK(dsm::local_map(over, n, base) == base, "no interleave bit, no change");
+            CHECK(dsm::local_map(1LL << 40, n, il) == base, "huge row falls back");
+        }
+    }
+    // The state-blocked layout's default local map interleaves the workers.
+    CHECK(dsm::kMapsByLayout[DSM_REPLICAS_STATE_BLOCKED].local & kInterleaveWorkers,
+          "state-blocked local steps interleave workers");
+}
+
 int main() {
+    check_local_map();
     check_layout_fuzz();
     check_init_and_chunks();
     check_init_rejections();
