@@ -106,9 +106,11 @@ typedef enum dsm_replica_layout {
                                     allocation, g_rep = x_rep + n * 4096, s1_rep = x_rep
                                     + 2 n * 4096, s2_rep = x_rep + 3 n * 4096.  The
                                     streams a work-group touches then share one
-                                    B * n * 16 KiB span; the local step measured faster
-                                    at n = 4.  d_pad is a multiple of 4096, tensors start
-                                    on multiples of 1024 elements. */
+                                    B * n * 16 KiB span, and the local steps take the
+                                    same piece of every worker in turn, so they sweep
+                                    whole blocks; local steps measured faster at n = 4
+                                    and n = 8.  d_pad is a multiple of 4096, tensors
+                                    start on multiples of 1024 elements. */
 } dsm_replica_layout;
 #define DSM_REPLICA_BLOCK_ELEMS 16384
 #define DSM_STATE_BLOCK_ELEMS 4096
