@@ -7,7 +7,8 @@ import torch
 
 from . import dsm
 
-# Each buffer's base is moved by a different multiple of this many floats
+# With contiguous or blocked replicas every buffer is its own allocation, and
+# each buffer's base is moved by a different multiple of this many floats
 # (1 MiB + 1 KiB).  Large allocations start on 2 MiB boundaries, so without it
 # the same element of x, m and the replicas shares its low address bits across
 # buffers.  Measured on MI355X at GPT-2 xl over alternating allocations, the
@@ -29,8 +30,9 @@ class Arenas:
     x_rep is an (n, d_pad) view with contiguous replicas, and an (n, blocks,
     16384) strided view of the same memory with blocked replicas.  With the
     replicas and their state blocked, x_rep, g_rep, s1_rep and s2_rep are
-    (n, blocks, 4096) strided views of one allocation.  worker(), workers(),
-    gather(), replica() and replicas() read every layout the same way.
+    (n, blocks, 4096) strided views of one allocation, which also holds x, m,
+    u and v.  worker(), workers(), gather(), replica() and replicas() read
+    every layout the same way.
     """
 
     def __init__(self, numel, n_workers, local_steps, base, decay=None, randomized=True,
@@ -60,20 +62,41 @@ class Arenas:
             self._storage.append(flat)
             return flat[pad:].view(*shape)
 
-        self.x = alloc(a)
-        self.m = alloc(a)
         adamw = self.base == dsm.DSM_BASE_ADAMW
         self.n_state_buffers = 4 if adamw else 3
         if self.state_blocked and self.arena_elems > 0:
-            # One allocation; block b holds the n copies of x_rep, g_rep,
-            # s1_rep (and s2_rep) of elements [4096 b, 4096 b + 4096).
+            # One allocation for everything: x, m, u, v, then the blocks, each
+            # part on a 2 MiB boundary; block b of the last part holds the n
+            # copies of x_rep, g_rep, s1_rep (and s2_rep) of elements
+            # [4096 b, 4096 b + 4096).  One allocation fixes where x and m sit
+            # relative to the blocks.  Measured on MI355X over re-allocations,
+            # the kernels that read x and m next to the blocks ran at 77-80%
+            # of 8 TB/s at GPT-2 xl and large this way, against 70-78% with
+            # separate allocations (the local steps are unaffected).
             K = dsm.DSM_STATE_BLOCK_ELEMS
-            # Unstaggered, so the blocks keep their place in the 2 MiB pages.
-            self.x_rep_flat = alloc(self.n_state_buffers * self.n * a, stagger=False)
+            page = 1 << 19                      # 2 MiB in floats
+            parts = [("x", a), ("m", a)]
+            parts += [("u", a)] if randomized else []
+            parts += [("v", a)] if global_adamw else []
+            parts += [("x_rep_flat", self.n_state_buffers * self.n * a)]
+            start, o = {}, 0
+            for name, count in parts:
+                start[name] = o
+                o = -(-(o + count) // page) * page
+            flat = torch.zeros(o, dtype=torch.float32, device=device)
+            self._storage.append(flat)
+            for name, count in parts:
+                setattr(self, name, flat[start[name]:start[name] + count])
+            if not randomized:
+                self.u = None
+            if not global_adamw:
+                self.v = None
             sup = self.x_rep_flat.view(a // K, self.n_state_buffers, self.n, K)
             self.x_rep, self.g_rep, self.s1_rep = (sup[:, j].permute(1, 0, 2) for j in range(3))
             self.s2_rep = sup[:, 3].permute(1, 0, 2) if adamw else None
         else:
+            self.x = alloc(a)
+            self.m = alloc(a)
             self.x_rep_flat = alloc(self.n * a)
             if self.blocked and self.arena_elems > 0:
                 B = dsm.DSM_REPLICA_BLOCK_ELEMS
@@ -83,8 +106,8 @@ class Arenas:
             self.g_rep = alloc(self.n, a)
             self.s1_rep = alloc(self.n, a)
             self.s2_rep = alloc(self.n, a) if adamw else None
-        self.u = alloc(a) if randomized else None
-        self.v = alloc(a) if global_adamw else None
+            self.u = alloc(a) if randomized else None
+            self.v = alloc(a) if global_adamw else None
         self.workspace = torch.zeros(max(self.workspace_bytes, 256), dtype=torch.uint8,
                                      device=device)
         self.ctx = None
