@@ -6,8 +6,9 @@ configuration the benchmark times:
   large   774M, n = 8, H = 24, AdamW, heavy-tailed gradients, deterministic
   xl      1.56B, n = 4, H = 12, AdamW, deterministic and randomized sign
 
-each with contiguous and with 64 KiB-blocked replicas, and medium and xl with the
-replicas and their state in 16 KiB blocks.
+each with contiguous replicas, with 64 KiB-blocked replicas, and with the
+replicas and their state in 16 KiB blocks of one allocation (the benchmark's
+layout).
 Every update is elementwise given the per-tensor bound, so outputs are
 checked on sampled elements the oracle computes one by one (random elements,
 the first and last elements of every tensor, chunk seams of the largest
@@ -97,7 +98,8 @@ LAYOUT_NAMES = {dsm.DSM_REPLICAS_CONTIGUOUS: "contiguous", dsm.DSM_REPLICAS_BLOC
                 dsm.DSM_REPLICAS_STATE_BLOCKED: "state-blocked"}
 CASES = [(wl, lay) for lay in (dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_BLOCKED)
          for wl in ("small", "medium", "large", "xl")]
-CASES += [("medium", dsm.DSM_REPLICAS_STATE_BLOCKED), ("xl", dsm.DSM_REPLICAS_STATE_BLOCKED)]
+# The bench's layout for every GPT-2 size: the replicas and their state blocked.
+CASES += [(wl, dsm.DSM_REPLICAS_STATE_BLOCKED) for wl in ("small", "medium", "large", "xl")]
 
 
 @pytest.fixture(scope="module", params=CASES,
