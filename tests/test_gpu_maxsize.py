@@ -17,7 +17,8 @@ and for the small tensors, against the oracle's own max.
 
 AdamW runs with one worker (7 buffers, 120 GB); SGD with momentum runs with
 two workers (9 buffers, 155 GB), whose second replica starts 2^32 elements
-past the first.
+past the first; AdamW runs again with two workers and the replicas and their
+state in 16 KiB blocks of one allocation (11 buffers, 189 GB).
 """
 import gc
 
@@ -46,6 +47,12 @@ CASES = {
     "sgdm_n2_blocked": dict(base=dsm.DSM_BASE_SGD_MOMENTUM, n=2,
                             modes=(dsm.DSM_SIGN_RAND_ZERO, dsm.DSM_SIGN_RAND_FLIP),
                             local=dict(lr=0.1, beta1=0.9), layout=dsm.DSM_REPLICAS_BLOCKED),
+    # Replicas and their state in 16 KiB blocks: the block addressing and the
+    # worker-interleaved local steps past 2^32 elements.
+    "adamw_n2_state": dict(base=dsm.DSM_BASE_ADAMW, n=2,
+                           modes=(dsm.DSM_SIGN_RAND_FLIP, dsm.DSM_SIGN_DET),
+                           local=dict(lr=2e-4, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1),
+                           layout=dsm.DSM_REPLICAS_STATE_BLOCKED),
 }
 
 
