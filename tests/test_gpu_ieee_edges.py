@@ -56,10 +56,19 @@ def same(gpu, ora, what):
     assert not bad.any(), f"{what}: {bad.sum()} finite-or-inf values differ"
 
 
+def _set_grad(ar, i, e, val):
+    """Element e (arena index) of worker i's gradient, in any layout."""
+    if ar.state_blocked:
+        ar.x_rep_flat[ar.state_index("g_rep", i, e)] = val
+    else:
+        ar.g_rep[i, e] = val
+
+
 @pytest.mark.parametrize("mode", [dsm.DSM_SIGN_DET, dsm.DSM_SIGN_RAND_FLIP,
                                   dsm.DSM_SIGN_RAND_ZERO])
 @pytest.mark.parametrize("base", [dsm.DSM_BASE_ADAMW, dsm.DSM_BASE_SGD_MOMENTUM])
-@pytest.mark.parametrize("layout", [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_BLOCKED])
+@pytest.mark.parametrize("layout", [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_BLOCKED,
+                                    dsm.DSM_REPLICAS_STATE_BLOCKED])
 def test_nonfinite_gradients_match_oracle(base, mode, layout):
     adamw = base == dsm.DSM_BASE_ADAMW
     local = ADAM if adamw else SGD
@@ -77,7 +86,7 @@ def test_nonfinite_gradients_match_oracle(base, mode, layout):
                 ar.g_rep.normal_(0.0, 1e-3, generator=gen)
                 for w, p, j, val in PLANTS[(t, k)]:
                     for i in (range(N) if w is None else (w,)):
-                        ar.g_rep[i, ar.offsets[p] + j] = float(val)
+                        _set_grad(ar, i, ar.offsets[p] + j, float(val))
                 before = {name: [tensors(ar, ar.worker(name, i)) for i in range(N)]
                           for name in keys + ("g_rep",)}
                 dsm.dsm_local_step(ar.ctx, -1, s, **local)
