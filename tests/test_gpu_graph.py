@@ -37,10 +37,13 @@ def bits(t):
 
 
 @pytest.mark.parametrize("fused", [False, True])
-def test_captured_round_replays_like_eager(fused):
+@pytest.mark.parametrize("layout", [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_STATE_BLOCKED])
+def test_captured_round_replays_like_eager(fused, layout):
     side = torch.cuda.Stream()
-    eager = A.Arenas(NUMEL, N, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, randomized=False)
-    graph = A.Arenas(NUMEL, N, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, randomized=False)
+    eager = A.Arenas(NUMEL, N, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, randomized=False,
+                     replica_layout=layout)
+    graph = A.Arenas(NUMEL, N, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, randomized=False,
+                     replica_layout=layout)
     gen = torch.Generator(device="cuda").manual_seed(17)
     eager.x.normal_(0.0, 0.02, generator=gen)
     eager.g_rep.normal_(0.0, 1e-3, generator=gen)

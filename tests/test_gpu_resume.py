@@ -50,8 +50,13 @@ def run_round(ar, t):
         dsm.dsm_global_step(ar.ctx, t, mode=mode, broadcast=True, **GLOB)
 
 
-def fresh(seed):
-    ar = A.Arenas(NUMEL, N, H, dsm.DSM_BASE_ADAMW, decay=DECAY, randomized=True)
+# The ABI default and the bench's layout (replicas and their state blocked).
+LAYOUTS = [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_STATE_BLOCKED]
+
+
+def fresh(seed, layout):
+    ar = A.Arenas(NUMEL, N, H, dsm.DSM_BASE_ADAMW, decay=DECAY, randomized=True,
+                  replica_layout=layout)
     gen = torch.Generator(device="cuda").manual_seed(seed)
     ar.x.normal_(0.0, 0.02, generator=gen)
     return ar
@@ -72,9 +77,10 @@ def final_state(ar):
     return out
 
 
-def test_resume_at_round_boundary_is_bitwise_exact():
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_resume_at_round_boundary_is_bitwise_exact(layout):
     # Uninterrupted run, with the checkpoint taken on the way.
-    ar = fresh(11)
+    ar = fresh(11, layout)
     ar.init()
     ckpt = None
     for t in range(len(ROUNDS)):
@@ -88,7 +94,7 @@ def test_resume_at_round_boundary_is_bitwise_exact():
     del ar
     # Resume in a fresh allocation (different addresses and placement).
     filler = torch.empty(12345, device="cuda")  # shifts the allocator
-    ar = fresh(999)
+    ar = fresh(999, layout)
     ar.x.copy_(ckpt["x"].to("cuda"))
     ar.init()
     for name in ("m", "s1_rep", "s2_rep"):
@@ -102,12 +108,13 @@ def test_resume_at_round_boundary_is_bitwise_exact():
         assert np.array_equal(got[key], want[key]), f"{key} differs after resume"
 
 
-def test_resume_after_lazy_round_end():
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_resume_after_lazy_round_end(layout):
     """The cut falls right after a fused round end without broadcast, where
     the replicas on the device still hold the previous round's values."""
     cut = 1  # round 0 is fused and lazy
     assert ROUNDS[cut - 1][1]
-    ar = fresh(3)
+    ar = fresh(3, layout)
     ar.init()
     run_round(ar, 0)
     torch.cuda.synchronize()
@@ -118,7 +125,7 @@ def test_resume_after_lazy_round_end():
         run_round(ar, t)
     want = final_state(ar)
     ar.destroy()
-    ar = fresh(4)
+    ar = fresh(4, layout)
     ar.x.copy_(ckpt["x"])
     ar.init()
     for name in ("m", "s1_rep", "s2_rep"):
