@@ -254,6 +254,10 @@ def main():
                     help="how the per-worker buffers hold their n copies (dsm_replica_layout); "
                          "auto: state-blocked when one copy of the parameters exceeds the "
                          "256 MB last-level cache, contiguous otherwise")
+    ap.add_argument("--placement", choices=("auto", "probe", "none"), default="auto",
+                    help="with the state-blocked layout, place the buffers at the fastest of the "
+                         "offsets of a 64 GiB larger allocation, timed at set-up (Arenas "
+                         "placement_span); auto: for working sets under 64 GB")
     ap.add_argument("--no-parity", action="store_true",
                     help="skip the oracle check of one untimed round after the timed region")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -288,8 +292,20 @@ def main():
         args.replica_layout = "state-blocked" if 4 * w.d > 256 << 20 else "contiguous"
     layout = {"state-blocked": dsm.DSM_REPLICAS_STATE_BLOCKED, "blocked": dsm.DSM_REPLICAS_BLOCKED,
               "contiguous": dsm.DSM_REPLICAS_CONTIGUOUS}[args.replica_layout]
+    # Where in physical memory a working set of a few tens of GB lands sets its
+    # kernels' rate on MI355X (a pattern repeating every 32 GiB); larger ones
+    # land fast.  So smaller state-blocked problems get the placement probe.
+    working_set = 4 * w.d * (4 + (4 if adamw else 3) * n)
+    probe = layout == dsm.DSM_REPLICAS_STATE_BLOCKED and (
+        args.placement == "probe" or (args.placement == "auto" and working_set < 64e9))
     ar = A.Arenas(w.numel, n, H, w.base, decay=w.decay, randomized=True, global_adamw=True,
-                  replica_layout=layout)
+                  replica_layout=layout,
+                  placement_span=A.PROBE_SPAN_BYTES if probe else 0)
+    if ar.placement is not None:
+        print("[bench] placement: offset %.1f GB, %.3f ms (slowest candidate %.3f ms) over %d "
+              "candidates" % (ar.placement["offset_bytes"] / 1e9, ar.placement["best_ms"],
+                              ar.placement["worst_ms"], ar.placement["candidates"]),
+              file=sys.stderr, flush=True)
     gen = torch.Generator(device="cuda").manual_seed(w.seed)
     W.fill_params_(ar.x, w, gen)
     for i in range(n):
@@ -551,6 +567,11 @@ def main():
             "d": d, "n_workers": n, "local_steps": H, "base": "adamw" if adamw else "sgd_momentum",
             "sign": args.sign, "path": args.path, "updates_per_step": updates_per_step,
             "replica_layout": args.replica_layout,
+            "placement": None if ar.placement is None else {
+                "offset_GB": round(ar.placement["offset_bytes"] / 1e9, 2),
+                "candidates": ar.placement["candidates"],
+                "probe_ms_best": round(ar.placement["best_ms"], 3),
+                "probe_ms_worst": round(ar.placement["worst_ms"], 3)},
         },
         "roofline": {
             "bound": "hbm",

@@ -16,6 +16,16 @@ from . import dsm
 # 27.5-28.4 ms); the local and global steps are unaffected.
 STAGGER_FLOATS = (1 << 18) + 256
 
+# 2 MiB in floats: the parts of the state-blocked allocation start on it.
+PAGE_FLOATS = 1 << 19
+# Spacing of the candidate offsets of the placement probe (Arenas(...,
+# placement_span=...)).
+PROBE_STEP_BYTES = 2 << 30
+# A span that holds a fast placement of a working set on MI355X: the pattern
+# repeats every 32 GiB, and a sweep through one 250 GB allocation found a
+# period without a fast window, so the probe covers two periods.
+PROBE_SPAN_BYTES = 64 << 30
+
 
 class Arenas:
     """The arenas and workspace of one problem, allocated with torch, plus the
@@ -25,7 +35,11 @@ class Arenas:
     problem (dsm_problem); decay: per-tensor weight-decay flags or None;
     randomized: allocate u_scratch for the randomized sign; global_adamw:
     allocate the global second moment v of the Global AdamW rule;
-    replica_layout: how x_rep holds the replicas (dsm_replica_layout).
+    replica_layout: how x_rep holds the replicas (dsm_replica_layout);
+    placement_span (bytes, state-blocked layout only): allocate this much more
+    and place the buffers at the offset in it where the problem's kernels run
+    fastest (placement_step apart; see _probe_placement); 0 places them at
+    the start.
 
     x_rep is an (n, d_pad) view with contiguous replicas, and an (n, blocks,
     16384) strided view of the same memory with blocked replicas.  With the
@@ -36,7 +50,8 @@ class Arenas:
     """
 
     def __init__(self, numel, n_workers, local_steps, base, decay=None, randomized=True,
-                 global_adamw=False, device="cuda", replica_layout=dsm.DSM_REPLICAS_CONTIGUOUS):
+                 global_adamw=False, device="cuda", replica_layout=dsm.DSM_REPLICAS_CONTIGUOUS,
+                 placement_span=0, placement_step=PROBE_STEP_BYTES):
         self.numel = [int(v) for v in numel]
         self.n = int(n_workers)
         self.H = int(local_steps)
@@ -73,27 +88,29 @@ class Arenas:
             # the kernels that read x and m next to the blocks ran at 77-80%
             # of 8 TB/s at GPT-2 xl and large this way, against 70-78% with
             # separate allocations (the local steps are unaffected).
-            K = dsm.DSM_STATE_BLOCK_ELEMS
-            page = 1 << 19                      # 2 MiB in floats
             parts = [("x", a), ("m", a)]
             parts += [("u", a)] if randomized else []
             parts += [("v", a)] if global_adamw else []
             parts += [("x_rep_flat", self.n_state_buffers * self.n * a)]
-            start, o = {}, 0
+            self._parts, o = [], 0
             for name, count in parts:
-                start[name] = o
-                o = -(-(o + count) // page) * page
-            flat = torch.zeros(o, dtype=torch.float32, device=device)
+                self._parts.append((name, o, count))
+                o = -(-(o + count) // PAGE_FLOATS) * PAGE_FLOATS
+            span = -(-int(placement_span) // (4 * PAGE_FLOATS)) * PAGE_FLOATS
+            flat = torch.zeros(o + span, dtype=torch.float32, device=device)
             self._storage.append(flat)
-            for name, count in parts:
-                setattr(self, name, flat[start[name]:start[name] + count])
+            self.workspace = torch.zeros(max(self.workspace_bytes, 256), dtype=torch.uint8,
+                                         device=device)
+            self.placement = None
+            self.u = self.v = None
+            if span > 0:
+                self.placement = self._probe_placement(flat, span, placement_step)
+                flat[self.placement["offset_floats"]:][:o].zero_()
+            self._carve(flat, 0 if span == 0 else self.placement["offset_floats"])
             if not randomized:
                 self.u = None
             if not global_adamw:
                 self.v = None
-            sup = self.x_rep_flat.view(a // K, self.n_state_buffers, self.n, K)
-            self.x_rep, self.g_rep, self.s1_rep = (sup[:, j].permute(1, 0, 2) for j in range(3))
-            self.s2_rep = sup[:, 3].permute(1, 0, 2) if adamw else None
         else:
             self.x = alloc(a)
             self.m = alloc(a)
@@ -108,9 +125,62 @@ class Arenas:
             self.s2_rep = alloc(self.n, a) if adamw else None
             self.u = alloc(a) if randomized else None
             self.v = alloc(a) if global_adamw else None
-        self.workspace = torch.zeros(max(self.workspace_bytes, 256), dtype=torch.uint8,
-                                     device=device)
+            self.workspace = torch.zeros(max(self.workspace_bytes, 256), dtype=torch.uint8,
+                                         device=device)
+            self.placement = None
         self.ctx = None
+
+    def _carve(self, flat, offset):
+        """Points x, m, u, v and the per-worker blocks at their parts of flat,
+        offset floats in (the state-blocked layout)."""
+        a = max(self.arena_elems, 64)
+        K = dsm.DSM_STATE_BLOCK_ELEMS
+        for name, start, count in self._parts:
+            setattr(self, name, flat[offset + start:offset + start + count])
+        sup = self.x_rep_flat.view(a // K, self.n_state_buffers, self.n, K)
+        self.x_rep, self.g_rep, self.s1_rep = (sup[:, j].permute(1, 0, 2) for j in range(3))
+        self.s2_rep = sup[:, 3].permute(1, 0, 2) if self.n_state_buffers == 4 else None
+
+    def _probe_placement(self, flat, span, step_bytes):
+        """Times the problem's kernels with its buffers carved at each 2 MiB-
+        aligned offset in [0, span] floats of flat, step_bytes apart, and
+        returns the fastest offset.  On MI355X the rate of a working set of a
+        few tens of GB depends on where in physical memory it lands, in a
+        pattern that repeats every 32 GiB (measured: small GPT-2-sized arenas
+        ran their local steps at 76% or 82% of 8 TB/s, and the kernels that
+        read x and m at 66% or 78%, by offset), so a span of two periods
+        holds a fast placement.  Each candidate runs, on zeroed buffers, one fused
+        round end and one local step of the problem with H = 1; the contents
+        do not matter, and the chosen part is zeroed again afterwards."""
+        step = max(PAGE_FLOATS, (int(step_bytes) // 4) // PAGE_FLOATS * PAGE_FLOATS)
+        offsets = list(range(0, span + 1, step))
+        probe = dsm.make_problem(self.numel, self.n, 1, self.base, self.decay, self.replica_layout)
+        if self.base == dsm.DSM_BASE_ADAMW:
+            local = dict(lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.0)
+        else:
+            local = dict(lr=1e-3, beta1=0.9)
+        glob = dict(gamma=1e-3, eta=0.8, beta1=0.95, beta2=0.98, lam=0.0)
+        stream = torch.cuda.current_stream()
+        events = []
+        for k, off in enumerate([offsets[0]] + offsets):   # the first run warms up
+            self._carve(flat, off)
+            ctx = dsm.dsm_init(probe, self.buffers(stream))
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+            ev[0].record(stream)
+            dsm.dsm_round_end(ctx, 1, local, 0, broadcast=False, **glob)
+            ev[1].record(stream)
+            dsm.dsm_sync(ctx)
+            ev[2].record(stream)
+            dsm.dsm_local_step(ctx, -1, 2, **local)
+            ev[3].record(stream)
+            stream.synchronize()
+            dsm.dsm_destroy(ctx)
+            if k > 0:
+                events.append((off, ev[0].elapsed_time(ev[1]) + ev[2].elapsed_time(ev[3])))
+        best = min(events, key=lambda e: e[1])
+        return {"offset_floats": best[0], "offset_bytes": 4 * best[0],
+                "candidates": len(events), "best_ms": best[1],
+                "worst_ms": max(t for _, t in events)}
 
     def buffers(self, stream=None):
         if stream is None:
