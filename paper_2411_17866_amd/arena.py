@@ -165,16 +165,18 @@ class Arenas:
         for k, off in enumerate([offsets[0]] + offsets):   # the first run warms up
             self._carve(flat, off)
             ctx = dsm.dsm_init(probe, self.buffers(stream))
-            ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
-            ev[0].record(stream)
-            dsm.dsm_round_end(ctx, 1, local, 0, broadcast=False, **glob)
-            ev[1].record(stream)
-            dsm.dsm_sync(ctx)
-            ev[2].record(stream)
-            dsm.dsm_local_step(ctx, -1, 2, **local)
-            ev[3].record(stream)
-            stream.synchronize()
-            dsm.dsm_destroy(ctx)
+            try:
+                ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+                ev[0].record(stream)
+                dsm.dsm_round_end(ctx, 1, local, 0, broadcast=False, **glob)
+                ev[1].record(stream)
+                dsm.dsm_sync(ctx)
+                ev[2].record(stream)
+                dsm.dsm_local_step(ctx, -1, 2, **local)
+                ev[3].record(stream)
+                stream.synchronize()
+            finally:
+                dsm.dsm_destroy(ctx)
             if k > 0:
                 events.append((off, ev[0].elapsed_time(ev[1]) + ev[2].elapsed_time(ev[3])))
         best = min(events, key=lambda e: e[1])
