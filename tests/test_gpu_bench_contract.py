@@ -16,7 +16,8 @@ REQUIRED = ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step
 
 
 @pytest.mark.parametrize("extra", [[], ["--sign", "rand", "--path", "split",
-                                          "--replica-layout", "contiguous"]])
+                                          "--replica-layout", "contiguous"],
+                                   ["--replica-layout", "state-blocked", "--placement", "probe"]])
 def test_bench_prints_one_consistent_json_line(extra):
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--workload", "tiny",
                         "--steps", "3", "--warmup", "1", "--extra-steps", "2", *extra],
@@ -45,3 +46,10 @@ def test_bench_prints_one_consistent_json_line(extra):
     assert par["non_bit_identical"] == 0 and par["flips_outside_margin"] == 0
     for name, entry in out["breakdown"].items():
         assert entry is not None and entry["launches"] >= 2, name
+    # The placement probe, when asked for, reports what it chose.
+    pl = cfg.get("placement")
+    if "probe" in extra:
+        assert pl["candidates"] == 33 and 0 <= pl["offset_GB"] <= 68.8
+        assert pl["probe_ms_best"] <= pl["probe_ms_worst"]
+    else:
+        assert pl is None
