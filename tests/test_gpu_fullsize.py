@@ -356,3 +356,64 @@ def test_fullsize_first_step_after_lazy_round_end(run):
     print(f"{w.name} first step after a lazy round end: {r.p.size} sampled elements x "
           f"{w.n_workers} workers, {nonbit} not bit-identical")
     assert nonbit == 0
+
+
+VARIANT_RULES = {dsm.DSM_RULE_LOOKAHEAD: O.RULE_LOOKAHEAD,
+                 dsm.DSM_RULE_SIGNED_SLOWMO: O.RULE_SIGNED_SLOWMO}
+
+
+XL_CASES = [c for c in CASES if c[0] == "xl"]
+
+
+@pytest.mark.parametrize("run", XL_CASES, indirect=True,
+                         ids=[f"xl-{LAYOUT_NAMES[lay]}" for _, lay in XL_CASES])
+def test_fullsize_global_variants_sampled(run):
+    """Lookahead and signed SlowMo (Section 4.1) at the xl size, each after H
+    local steps, against the oracle on the sampled elements: x and m bit for bit
+    against fp32; x against fp64 within the error bound, signed SlowMo's sign
+    decisions allowed to differ only where the averaged difference is below
+    1e-6 of its rms."""
+    r = run
+    w, ar = r.w, r.ar
+    H = w.local_steps
+    nonbit = 0
+    for k_rule, (rule, orule) in enumerate(VARIANT_RULES.items()):
+        t = 5 + k_rule
+        dsm.dsm_sync(ar.ctx)
+        for k in range(H):
+            r.grads(t * H + k + 1)
+            r.local(t * H + k + 1)
+        torch.cuda.synchronize()
+        x0, m0 = _gather(ar.x, r.idx), _gather(ar.m, r.idx)
+        reps = [ar.gather("x_rep", i, r.idx).cpu().numpy().copy() for i in range(w.n_workers)]
+        dsm.dsm_global_step(ar.ctx, t, rule=rule, **r.glob_kw())
+        torch.cuda.synchronize()
+        gx, gm = _gather(ar.x, r.idx), _gather(ar.m, r.idx)
+        kw = dict(gamma=w.local["lr"], t=t, rule=orule, **w.glob)
+        for dec in (True, False):
+            s_ = r.decay == dec
+            if not s_.any():
+                continue
+            args = ([x0[s_]], [m0[s_]], [[rp[s_]] for rp in reps])
+            o32 = O.global_step(*args, decay=[dec], prec="fp32", **kw)
+            o64 = O.global_step(*args, decay=[dec], prec="fp64", **kw)
+            nonbit += rel_check(gx[s_], o32["x"][0], f"{w.name} rule {rule} x")
+            nonbit += rel_check(gm[s_], o32["m"][0], f"{w.name} rule {rule} m")
+            ok = np.ones(int(s_.sum()), dtype=bool)
+            if rule == dsm.DSM_RULE_SIGNED_SLOWMO:
+                flip = np.sign(o32["delta"][0]) != np.sign(o64["delta"][0])
+                if flip.any():
+                    assert np.all(np.abs(o64["delta"][0][flip]) < 1e-6 * rms(o64["delta"][0]))
+                ok &= ~flip
+            err = np.abs(gx[s_].astype(np.float64) - o64["x"][0])
+            bound = 64 * 2.0 ** -24 * (np.abs(o64["x"][0]) + np.abs(x0[s_]) +
+                                       O.f32(w.glob["eta"]) * O.f32(w.local["lr"]) *
+                                       (np.abs(o64["u"][0]) + np.abs(o64["m"][0]) + 1.0))
+            assert np.all(err[ok] <= bound[ok]), f"{w.name} rule {rule} x vs fp64"
+        for i in range(w.n_workers):
+            for a, b in zip(ar.views(ar.replica(i)), ar.views(ar.x)):
+                assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+    print(f"{w.name} Lookahead and signed SlowMo: {r.p.size} sampled elements, "
+          f"{nonbit} not bit-identical")
+    assert nonbit == 0
+
