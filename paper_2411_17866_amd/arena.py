@@ -21,9 +21,9 @@ PAGE_FLOATS = 1 << 19
 # Spacing of the candidate offsets of the placement probe (Arenas(...,
 # placement_span=...)).
 PROBE_STEP_BYTES = 2 << 30
-# A span that holds a fast placement of a working set on MI355X: the pattern
-# repeats every 32 GiB, and a sweep through one 250 GB allocation found a
-# period without a fast window, so the probe covers two periods.
+# The probe's span: two periods of the 32 GiB pattern on MI355X, since a sweep
+# through one 250 GB allocation found a period without a fast window.  It
+# raises the odds of a fast placement; it does not guarantee one.
 PROBE_SPAN_BYTES = 64 << 30
 
 
@@ -149,7 +149,7 @@ class Arenas:
         pattern that repeats every 32 GiB (measured: small GPT-2-sized arenas
         ran their local steps at 76% or 82% of 8 TB/s, and the kernels that
         read x and m at 66% or 78%, by offset), so a span of two periods
-        holds a fast placement.  Each candidate runs, on zeroed buffers, one fused
+        usually holds a fast placement.  Each candidate runs, on zeroed buffers, one fused
         round end and one local step of the problem with H = 1; the contents
         do not matter, and the chosen part is zeroed again afterwards."""
         step = max(PAGE_FLOATS, (int(step_bytes) // 4) // PAGE_FLOATS * PAGE_FLOATS)
