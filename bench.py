@@ -489,12 +489,26 @@ def main():
     torch.cuda.synchronize()
     dsm.dsm_destroy(ctx2)
 
-    # Practical ceiling of this device: a plain 4 GiB copy and fill (torch).
+    # Practical ceiling of this device over 4 GiB buffers: torch's copy and
+    # fill, and the library's pure-read and pure-write stream kernels (the
+    # optimizer kernels' access shape without their arithmetic).
     src = torch.empty(1 << 30, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
+    words = torch.empty(src.numel() // dsm.DSM_PIECE_ELEMS, dtype=torch.int32, device="cuda")
+    sp = stream.cuda_stream
+
+    def stream_read():
+        dsm.dsm_test_stream(dsm.DSM_STREAM_READ, src.data_ptr(), src.numel(), words.data_ptr(),
+                            0.0, sp)
+
+    def stream_write():
+        dsm.dsm_test_stream(dsm.DSM_STREAM_WRITE, dst.data_ptr(), dst.numel(), None, 3.0, sp)
+
     dst.copy_(src)
     dst.fill_(1.0)
-    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    stream_read()
+    stream_write()
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
     e[0].record(stream)
     for _ in range(3):
         dst.copy_(src)
@@ -502,10 +516,57 @@ def main():
     for _ in range(3):
         dst.fill_(2.0)
     e[2].record(stream)
+    for _ in range(3):
+        stream_read()
+    e[3].record(stream)
+    for _ in range(3):
+        stream_write()
+    e[4].record(stream)
     torch.cuda.synchronize()
-    copy_gbs = 3 * 8 * (1 << 30) / (e[0].elapsed_time(e[1]) / 1e3) / 1e9
-    fill_gbs = 3 * 4 * (1 << 30) / (e[1].elapsed_time(e[2]) / 1e3) / 1e9
-    del src, dst
+    gib = 1 << 30
+    copy_gbs = 3 * 8 * gib / (e[0].elapsed_time(e[1]) / 1e3) / 1e9
+    fill_gbs = 3 * 4 * gib / (e[1].elapsed_time(e[2]) / 1e3) / 1e9
+    sread_gbs = 3 * 4 * gib / (e[2].elapsed_time(e[3]) / 1e3) / 1e9
+    swrite_gbs = 3 * 4 * gib / (e[3].elapsed_time(e[4]) / 1e3) / 1e9
+    del src, dst, words
+
+    # The same two stream kernels over the replica storage the local step
+    # reads (its physical pages, which set the rate): the one block allocation
+    # of the state-blocked layout, else x_rep, g_rep, s1_rep (and s2_rep).
+    # Every context over the arenas is destroyed by now, so overwriting them
+    # is harmless.
+    rep_bufs = [ar.x_rep_flat] if ar.state_blocked else \
+        [t for t in (ar.x_rep_flat, ar.g_rep, ar.s1_rep, ar.s2_rep) if t is not None]
+    rep_span = 1 << 33  # elements per call, within one grid dimension
+    rep_pieces = []
+    for t in rep_bufs:
+        flat = t.reshape(-1)
+        usable = flat.numel() // dsm.DSM_PIECE_ELEMS * dsm.DSM_PIECE_ELEMS
+        for o in range(0, usable, rep_span):
+            rep_pieces.append((flat.data_ptr() + 4 * o, min(rep_span, usable - o)))
+    rep_bytes = 4 * sum(c for _, c in rep_pieces)
+    rep_read_gbs = rep_write_gbs = None
+    if rep_bytes > 0:
+        words = torch.empty(min(rep_span, max(c for _, c in rep_pieces)) // dsm.DSM_PIECE_ELEMS,
+                            dtype=torch.int32, device="cuda")
+
+        def rep_pass(kind):
+            for ptr, c in rep_pieces:
+                dsm.dsm_test_stream(kind, ptr, c, words.data_ptr(), 0.0, sp)
+
+        rep_pass(dsm.DSM_STREAM_READ)
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record(stream)
+        for _ in range(3):
+            rep_pass(dsm.DSM_STREAM_READ)
+        e[1].record(stream)
+        for _ in range(3):
+            rep_pass(dsm.DSM_STREAM_WRITE)
+        e[2].record(stream)
+        torch.cuda.synchronize()
+        rep_read_gbs = 3 * rep_bytes / (e[0].elapsed_time(e[1]) / 1e3) / 1e9
+        rep_write_gbs = 3 * rep_bytes / (e[1].elapsed_time(e[2]) / 1e3) / 1e9
+        del words
 
     def avg_ms(entries):
         """Average launch duration over (start, end, launches) event entries."""
@@ -611,7 +672,14 @@ def main():
             "global_det": kern(ev_flushed["split_det"], bytes_global(n, False) * d, d),
         },
         "device_ceiling": {"torch_copy_GB_per_s": round(copy_gbs, 1),
-                           "torch_fill_GB_per_s": round(fill_gbs, 1)},
+                           "torch_fill_GB_per_s": round(fill_gbs, 1),
+                           "stream_read_GB_per_s": round(sread_gbs, 1),
+                           "stream_write_GB_per_s": round(swrite_gbs, 1),
+                           "replica_stream_read_GB_per_s":
+                               None if rep_read_gbs is None else round(rep_read_gbs, 1),
+                           "replica_stream_write_GB_per_s":
+                               None if rep_write_gbs is None else round(rep_write_gbs, 1),
+                           "replica_stream_GB": round(rep_bytes / 1e9, 3)},
         "kernel_source_hash": khash,
     }
     out["parity"] = parity

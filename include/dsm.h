@@ -332,6 +332,27 @@ DSM_API dsm_status dsm_test_philox(uint64_t seed, uint32_t tensor, int64_t t, in
                            int64_t count, uint32_t* dev_out, void* stream);
 
 /*
+ * dsm_test_stream - diagnostic: streams n_elems fp32 elements of the device
+ * buffer dev_buf (caller-owned, 256-byte aligned) with the access shape of the
+ * library's kernels: one piece of DSM_PIECE_ELEMS elements per 256-thread
+ * work-group, 16-byte nontemporal loads or stores, consecutive lanes on
+ * consecutive 16-byte groups.  It measures the device's pure read and pure
+ * write rates, and calibrates byte counters against the library's own access
+ * shape.
+ *   DSM_STREAM_READ:  reads every element and writes, for piece k, the XOR of
+ *                     its elements' 32-bit patterns to dev_words[k]
+ *                     (caller-owned, n_elems / DSM_PIECE_ELEMS words);
+ *   DSM_STREAM_WRITE: writes value to every element (dev_words unused).
+ * Enqueued on `stream`.  Errors: DSM_ERR_INVALID_ARG (unknown kind, n_elems
+ * not a non-negative multiple of DSM_PIECE_ELEMS or beyond one grid
+ * dimension, NULL or misaligned buffers); DSM_ERR_HIP.
+ */
+#define DSM_PIECE_ELEMS 1024
+typedef enum dsm_stream_kind { DSM_STREAM_READ = 0, DSM_STREAM_WRITE = 1 } dsm_stream_kind;
+DSM_API dsm_status dsm_test_stream(int32_t kind, float* dev_buf, int64_t n_elems,
+                                   uint32_t* dev_words, float value, void* stream);
+
+/*
  * dsm_destroy - synchronises the context's stream and frees the context's
  * host memory.  The caller's device buffers are untouched.  NULL is a no-op.
  */

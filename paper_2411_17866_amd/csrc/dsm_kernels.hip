@@ -835,6 +835,40 @@ __global__ __launch_bounds__(kBlockThreads) void k_test_philox(uint32_t key0, ui
     out[4 * b + 3] = w3;
 }
 
+// Streaming diagnostics with the access shape of the kernels above: one
+// piece of kPieceVec float4 groups per work-group, XCD map 1, 16-byte
+// nontemporal accesses, consecutive lanes on consecutive groups.  The read
+// kernel folds its piece into one word (the XOR of its 32-bit patterns) so
+// that nothing is dropped; the write kernel stores one value everywhere.
+__global__ __launch_bounds__(kBlockThreads) void k_stream_read(const float* __restrict__ buf,
+                                                              uint32_t* __restrict__ words) {
+    __shared__ uint32_t wave_acc[kBlockThreads / 64];
+    const uint32_t wi = work_index<1>();
+    const f4* __restrict__ p = reinterpret_cast<const f4*>(buf) + static_cast<int64_t>(wi) * kPieceVec;
+    uint32_t acc = 0;
+    for (int q = threadIdx.x; q < kPieceVec; q += kBlockThreads) {
+        const f4 v = ntload(p + q);
+        acc ^= __float_as_uint(v.x) ^ __float_as_uint(v.y) ^ __float_as_uint(v.z) ^
+               __float_as_uint(v.w);
+    }
+    for (int off = 32; off > 0; off >>= 1) acc ^= __shfl_xor(acc, off, 64);
+    if ((threadIdx.x & 63) == 0) wave_acc[threadIdx.x >> 6] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t total = 0;
+        for (int k = 0; k < kBlockThreads / 64; ++k) total ^= wave_acc[k];
+        words[wi] = total;
+    }
+}
+
+__global__ __launch_bounds__(kBlockThreads) void k_stream_write(float* __restrict__ buf,
+                                                               float value) {
+    const uint32_t wi = work_index<1>();
+    f4* __restrict__ p = reinterpret_cast<f4*>(buf) + static_cast<int64_t>(wi) * kPieceVec;
+    const f4 v = {value, value, value, value};
+    for (int q = threadIdx.x; q < kPieceVec; q += kBlockThreads) ntstore(v, p + q);
+}
+
 dim3 chunk_grid(int64_t n_chunks, int n_workers) {
     return dim3(static_cast<unsigned>(n_chunks * kSplit), static_cast<unsigned>(n_workers), 1);
 }
@@ -1093,6 +1127,17 @@ hipError_t static_scratch(void** ptr) {
     }
     *ptr = addr[dev];
     return hipSuccess;
+}
+
+hipError_t launch_test_stream(int kind, float* buf, int64_t n_pieces, uint32_t* words,
+                              float value, hipStream_t st) {
+    if (n_pieces == 0) return hipSuccess;
+    const dim3 grid(static_cast<unsigned>(n_pieces)), block(kBlockThreads);
+    if (kind == 0)
+        hipLaunchKernelGGL(k_stream_read, grid, block, 0, st, buf, words);
+    else
+        hipLaunchKernelGGL(k_stream_write, grid, block, 0, st, buf, value);
+    return hipGetLastError();
 }
 
 hipError_t launch_test_philox(uint32_t key0, uint32_t key1, uint32_t tensor, uint32_t t,

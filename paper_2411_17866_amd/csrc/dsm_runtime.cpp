@@ -688,6 +688,34 @@ dsm_status dsm_test_philox(uint64_t seed, uint32_t tensor, int64_t t, int64_t q0
     return DSM_OK;
 }
 
+#if DSM_UNROLL == 1 && DSM_ITERS == 1 && DSM_BLOCK_THREADS == 256
+static_assert(dsm::kPieceElems == DSM_PIECE_ELEMS, "dsm.h's piece size is the default build's");
+#endif
+
+dsm_status dsm_test_stream(int32_t kind, float* dev_buf, int64_t n_elems, uint32_t* dev_words,
+                           float value, void* stream) {
+    if (kind != DSM_STREAM_READ && kind != DSM_STREAM_WRITE)
+        return fail(nullptr, DSM_ERR_INVALID_ARG, "kind must be DSM_STREAM_READ or DSM_STREAM_WRITE");
+    if (n_elems < 0 || n_elems % dsm::kPieceElems != 0)
+        return fail(nullptr, DSM_ERR_INVALID_ARG, "n_elems must be a non-negative multiple of %lld",
+                    static_cast<long long>(dsm::kPieceElems));
+    const int64_t n_pieces = n_elems / dsm::kPieceElems;
+    if (n_pieces * dsm::kBlockThreads >= (int64_t(1) << 32))
+        return fail(nullptr, DSM_ERR_INVALID_ARG, "n_elems exceeds one grid dimension (%lld pieces)",
+                    static_cast<long long>(n_pieces));
+    if (n_elems > 0 && (!dev_buf || !aligned256(dev_buf)))
+        return fail(nullptr, DSM_ERR_INVALID_ARG, "dev_buf is NULL or not 256-byte aligned");
+    if (kind == DSM_STREAM_READ && n_elems > 0 &&
+        (!dev_words || (reinterpret_cast<uintptr_t>(dev_words) & 3u) != 0))
+        return fail(nullptr, DSM_ERR_INVALID_ARG, "dev_words is NULL or not 4-byte aligned");
+    dsm_status st = check_device(nullptr);
+    if (st != DSM_OK) return st;
+    hipError_t e = dsm::launch_test_stream(kind, dev_buf, n_pieces, dev_words, value,
+                                           static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(nullptr, "launching the streaming test kernel", e);
+    return DSM_OK;
+}
+
 dsm_status dsm_destroy(dsm_ctx* ctx) {
     if (!ctx) return DSM_OK;
     hipError_t e = hipStreamSynchronize(ctx->stream);

@@ -38,10 +38,13 @@ DSM_REPLICAS_BLOCKED = 1
 DSM_REPLICAS_STATE_BLOCKED = 2
 DSM_REPLICA_BLOCK_ELEMS = 16384
 DSM_STATE_BLOCK_ELEMS = 4096
+DSM_PIECE_ELEMS = 1024
+DSM_STREAM_READ, DSM_STREAM_WRITE = 0, 1
 
 EXPORTED = ("dsm_layout", "dsm_init", "dsm_init_static", "dsm_local_step", "dsm_global_step",
             "dsm_round_end", "dsm_sync",
-            "dsm_read_bounds", "dsm_test_philox", "dsm_destroy", "dsm_last_error")
+            "dsm_read_bounds", "dsm_test_philox", "dsm_test_stream", "dsm_destroy",
+            "dsm_last_error")
 
 
 class DsmError(RuntimeError):
@@ -109,6 +112,8 @@ def load_library(path=LIBPATH):
     lib.dsm_test_philox.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int64,
                                     ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p,
                                     ctypes.c_void_p]
+    lib.dsm_test_stream.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
+                                    ctypes.c_void_p, ctypes.c_float, ctypes.c_void_p]
     lib.dsm_destroy.argtypes = [ctypes.c_void_p]
     lib.dsm_last_error.argtypes = [ctypes.c_void_p]
     lib.dsm_last_error.restype = ctypes.c_char_p
@@ -208,6 +213,11 @@ def dsm_read_bounds(ctx, n_tensors):
 
 def dsm_test_philox(seed, tensor, t, q0, count, dev_out_ptr, stream_ptr=None):
     _check(load_library().dsm_test_philox(seed, tensor, t, q0, count, dev_out_ptr, stream_ptr))
+
+
+def dsm_test_stream(kind, dev_buf_ptr, n_elems, dev_words_ptr=None, value=0.0, stream_ptr=None):
+    _check(load_library().dsm_test_stream(kind, dev_buf_ptr, n_elems, dev_words_ptr, value,
+                                          stream_ptr))
 
 
 def dsm_destroy(ctx):

@@ -155,6 +155,21 @@ def test_test_philox_rejects_bad_arguments(lib, args):
     assert st == dsm.DSM_ERR_INVALID_ARG
 
 
+@needs_no_gpu
+@pytest.mark.parametrize("args", [
+    (2, 1 << 40, 1024, 1 << 40),          # unknown kind
+    (1, 1 << 40, 1000, None),             # not whole pieces
+    (1, 1 << 40, -1024, None),            # negative size
+    (1, 1 << 40, (1 << 24) * 1024, None),  # beyond one grid dimension
+    (0, 1 << 40, 1024, None),             # read without the word array
+    (1, (1 << 40) + 16, 1024, None),      # misaligned buffer
+    (1, None, 1024, None),                # NULL buffer
+])
+def test_test_stream_rejects_bad_arguments(lib, args):
+    kind, buf, n, words = args
+    assert lib.dsm_test_stream(kind, buf, n, words, 0.0, None) == dsm.DSM_ERR_INVALID_ARG
+
+
 def test_struct_layouts_match_header(lib):
     """ctypes mirrors of the header structs have the C sizes and offsets."""
     assert ctypes.sizeof(dsm.dsm_problem) == 40
