@@ -149,7 +149,7 @@ class Arenas:
         pattern that repeats every 32 GiB (measured: small GPT-2-sized arenas
         ran their local steps at 76% or 82% of 8 TB/s, and the kernels that
         read x and m at 66% or 78%, by offset); a span of two periods found
-        a fast placement for 4 of 7 medium-sized and 1 of 8 small-sized
+        a fast placement for 7 of 11 medium-sized and 2 of 12 small-sized
         problems measured.  Each candidate runs, on zeroed buffers, one fused
         round end and one local step of the problem with H = 1; the contents
         do not matter, and the chosen part is zeroed again afterwards."""
