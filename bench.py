@@ -491,18 +491,23 @@ def main():
 
     # Practical ceiling of this device over 4 GiB buffers: torch's copy and
     # fill, and the library's pure-read and pure-write stream kernels (the
-    # optimizer kernels' access shape without their arithmetic).
-    src = torch.empty(1 << 30, dtype=torch.float32, device="cuda")
+    # optimizer kernels' access shape without their arithmetic).  The read
+    # kernel writes a word only for a piece whose XOR matches its pattern; a
+    # piece of equal floats XORs to 0, so a non-zero pattern keeps the read
+    # free of writes.
+    no_match = 0x5A5A5A5A
+    src = torch.zeros(1 << 30, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
-    words = torch.empty(src.numel() // dsm.DSM_PIECE_ELEMS, dtype=torch.int32, device="cuda")
+    words = torch.zeros(src.numel() // dsm.DSM_PIECE_ELEMS, dtype=torch.int32, device="cuda")
     sp = stream.cuda_stream
 
     def stream_read():
         dsm.dsm_test_stream(dsm.DSM_STREAM_READ, src.data_ptr(), src.numel(), words.data_ptr(),
-                            0.0, sp)
+                            no_match, sp)
 
     def stream_write():
-        dsm.dsm_test_stream(dsm.DSM_STREAM_WRITE, dst.data_ptr(), dst.numel(), None, 3.0, sp)
+        dsm.dsm_test_stream(dsm.DSM_STREAM_WRITE, dst.data_ptr(), dst.numel(), None, 0x40400000,
+                            sp)
 
     dst.copy_(src)
     dst.fill_(1.0)
@@ -550,22 +555,23 @@ def main():
         words = torch.empty(min(rep_span, max(c for _, c in rep_pieces)) // dsm.DSM_PIECE_ELEMS,
                             dtype=torch.int32, device="cuda")
 
-        def rep_pass(kind):
+        def rep_pass(kind, pattern):
             for ptr, c in rep_pieces:
-                dsm.dsm_test_stream(kind, ptr, c, words.data_ptr(), 0.0, sp)
+                dsm.dsm_test_stream(kind, ptr, c, words.data_ptr(), pattern, sp)
 
-        rep_pass(dsm.DSM_STREAM_READ)
+        # The writes come first and store zeros, so the reads find no match.
+        rep_pass(dsm.DSM_STREAM_WRITE, 0)
         e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
         e[0].record(stream)
         for _ in range(3):
-            rep_pass(dsm.DSM_STREAM_READ)
+            rep_pass(dsm.DSM_STREAM_WRITE, 0)
         e[1].record(stream)
         for _ in range(3):
-            rep_pass(dsm.DSM_STREAM_WRITE)
+            rep_pass(dsm.DSM_STREAM_READ, no_match)
         e[2].record(stream)
         torch.cuda.synchronize()
-        rep_read_gbs = 3 * rep_bytes / (e[0].elapsed_time(e[1]) / 1e3) / 1e9
-        rep_write_gbs = 3 * rep_bytes / (e[1].elapsed_time(e[2]) / 1e3) / 1e9
+        rep_write_gbs = 3 * rep_bytes / (e[0].elapsed_time(e[1]) / 1e3) / 1e9
+        rep_read_gbs = 3 * rep_bytes / (e[1].elapsed_time(e[2]) / 1e3) / 1e9
         del words
 
     def avg_ms(entries):

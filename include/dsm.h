@@ -339,10 +339,13 @@ DSM_API dsm_status dsm_test_philox(uint64_t seed, uint32_t tensor, int64_t t, in
  * consecutive 16-byte groups.  It measures the device's pure read and pure
  * write rates, and calibrates byte counters against the library's own access
  * shape.
- *   DSM_STREAM_READ:  reads every element and writes, for piece k, the XOR of
- *                     its elements' 32-bit patterns to dev_words[k]
- *                     (caller-owned, n_elems / DSM_PIECE_ELEMS words);
- *   DSM_STREAM_WRITE: writes value to every element (dev_words unused).
+ *   DSM_STREAM_READ:  reads every element; for each piece k whose elements'
+ *                     32-bit patterns XOR to `pattern`, writes 1 to
+ *                     dev_words[k] (caller-owned, n_elems / DSM_PIECE_ELEMS
+ *                     words); no other word is written.  With a pattern that
+ *                     no piece matches, the kernel only reads;
+ *   DSM_STREAM_WRITE: writes the float whose bit pattern is `pattern` to
+ *                     every element (dev_words unused).
  * Enqueued on `stream`.  Errors: DSM_ERR_INVALID_ARG (unknown kind, n_elems
  * not a non-negative multiple of DSM_PIECE_ELEMS or beyond one grid
  * dimension, NULL or misaligned buffers); DSM_ERR_HIP.
@@ -350,7 +353,7 @@ DSM_API dsm_status dsm_test_philox(uint64_t seed, uint32_t tensor, int64_t t, in
 #define DSM_PIECE_ELEMS 1024
 typedef enum dsm_stream_kind { DSM_STREAM_READ = 0, DSM_STREAM_WRITE = 1 } dsm_stream_kind;
 DSM_API dsm_status dsm_test_stream(int32_t kind, float* dev_buf, int64_t n_elems,
-                                   uint32_t* dev_words, float value, void* stream);
+                                   uint32_t* dev_words, uint32_t pattern, void* stream);
 
 /*
  * dsm_destroy - synchronises the context's stream and frees the context's

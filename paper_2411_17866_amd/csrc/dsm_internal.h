@@ -232,9 +232,10 @@ hipError_t launch_global_rand(const Chunk* chunks, int64_t n_chunks, int n_tenso
 hipError_t launch_broadcast(const Chunk* chunks, int64_t n_chunks, const float* x, float* x_rep,
                             RepLayout rl, int n, int map, hipStream_t st);
 // Streaming diagnostic over n_pieces pieces of kPieceElems floats: kind 0
-// reads buf and writes one word per piece to words, kind 1 writes value.
+// reads buf and writes 1 to words[k] for each piece k whose 32-bit patterns
+// XOR to pattern; kind 1 writes the float with bit pattern `pattern`.
 hipError_t launch_test_stream(int kind, float* buf, int64_t n_pieces, uint32_t* words,
-                              float value, hipStream_t st);
+                              uint32_t pattern, hipStream_t st);
 hipError_t launch_test_philox(uint32_t key0, uint32_t key1, uint32_t tensor, uint32_t t,
                               uint32_t q0, int64_t count, uint32_t* out, hipStream_t st);
 

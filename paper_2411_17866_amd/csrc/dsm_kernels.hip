@@ -838,10 +838,14 @@ __global__ __launch_bounds__(kBlockThreads) void k_test_philox(uint32_t key0, ui
 // Streaming diagnostics with the access shape of the kernels above: one
 // piece of kPieceVec float4 groups per work-group, XCD map 1, 16-byte
 // nontemporal accesses, consecutive lanes on consecutive groups.  The read
-// kernel folds its piece into one word (the XOR of its 32-bit patterns) so
-// that nothing is dropped; the write kernel stores one value everywhere.
+// kernel folds its piece into one word (the XOR of its 32-bit patterns) and
+// writes only where that word equals `pattern`, so with a pattern no piece
+// matches it issues no write at all: even one 4-byte store per piece,
+// interleaved with the loads, costs the read stream a measurable share of
+// its rate.  The write kernel stores the float with bit pattern `pattern`.
 __global__ __launch_bounds__(kBlockThreads) void k_stream_read(const float* __restrict__ buf,
-                                                              uint32_t* __restrict__ words) {
+                                                              uint32_t* __restrict__ words,
+                                                              uint32_t pattern) {
     __shared__ uint32_t wave_acc[kBlockThreads / 64];
     const uint32_t wi = work_index<1>();
     const f4* __restrict__ p = reinterpret_cast<const f4*>(buf) + static_cast<int64_t>(wi) * kPieceVec;
@@ -857,14 +861,15 @@ __global__ __launch_bounds__(kBlockThreads) void k_stream_read(const float* __re
     if (threadIdx.x == 0) {
         uint32_t total = 0;
         for (int k = 0; k < kBlockThreads / 64; ++k) total ^= wave_acc[k];
-        words[wi] = total;
+        if (total == pattern) words[wi] = 1u;
     }
 }
 
 __global__ __launch_bounds__(kBlockThreads) void k_stream_write(float* __restrict__ buf,
-                                                               float value) {
+                                                               uint32_t pattern) {
     const uint32_t wi = work_index<1>();
     f4* __restrict__ p = reinterpret_cast<f4*>(buf) + static_cast<int64_t>(wi) * kPieceVec;
+    const float value = __uint_as_float(pattern);
     const f4 v = {value, value, value, value};
     for (int q = threadIdx.x; q < kPieceVec; q += kBlockThreads) ntstore(v, p + q);
 }
@@ -1130,13 +1135,13 @@ hipError_t static_scratch(void** ptr) {
 }
 
 hipError_t launch_test_stream(int kind, float* buf, int64_t n_pieces, uint32_t* words,
-                              float value, hipStream_t st) {
+                              uint32_t pattern, hipStream_t st) {
     if (n_pieces == 0) return hipSuccess;
     const dim3 grid(static_cast<unsigned>(n_pieces)), block(kBlockThreads);
     if (kind == 0)
-        hipLaunchKernelGGL(k_stream_read, grid, block, 0, st, buf, words);
+        hipLaunchKernelGGL(k_stream_read, grid, block, 0, st, buf, words, pattern);
     else
-        hipLaunchKernelGGL(k_stream_write, grid, block, 0, st, buf, value);
+        hipLaunchKernelGGL(k_stream_write, grid, block, 0, st, buf, pattern);
     return hipGetLastError();
 }
 

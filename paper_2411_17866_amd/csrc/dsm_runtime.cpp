@@ -693,7 +693,7 @@ static_assert(dsm::kPieceElems == DSM_PIECE_ELEMS, "dsm.h's piece size is the de
 #endif
 
 dsm_status dsm_test_stream(int32_t kind, float* dev_buf, int64_t n_elems, uint32_t* dev_words,
-                           float value, void* stream) {
+                           uint32_t pattern, void* stream) {
     if (kind != DSM_STREAM_READ && kind != DSM_STREAM_WRITE)
         return fail(nullptr, DSM_ERR_INVALID_ARG, "kind must be DSM_STREAM_READ or DSM_STREAM_WRITE");
     if (n_elems < 0 || n_elems % dsm::kPieceElems != 0)
@@ -710,7 +710,7 @@ dsm_status dsm_test_stream(int32_t kind, float* dev_buf, int64_t n_elems, uint32
         return fail(nullptr, DSM_ERR_INVALID_ARG, "dev_words is NULL or not 4-byte aligned");
     dsm_status st = check_device(nullptr);
     if (st != DSM_OK) return st;
-    hipError_t e = dsm::launch_test_stream(kind, dev_buf, n_pieces, dev_words, value,
+    hipError_t e = dsm::launch_test_stream(kind, dev_buf, n_pieces, dev_words, pattern,
                                            static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(nullptr, "launching the streaming test kernel", e);
     return DSM_OK;

@@ -113,7 +113,7 @@ def load_library(path=LIBPATH):
                                     ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p,
                                     ctypes.c_void_p]
     lib.dsm_test_stream.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
-                                    ctypes.c_void_p, ctypes.c_float, ctypes.c_void_p]
+                                    ctypes.c_void_p, ctypes.c_uint32, ctypes.c_void_p]
     lib.dsm_destroy.argtypes = [ctypes.c_void_p]
     lib.dsm_last_error.argtypes = [ctypes.c_void_p]
     lib.dsm_last_error.restype = ctypes.c_char_p
@@ -215,8 +215,8 @@ def dsm_test_philox(seed, tensor, t, q0, count, dev_out_ptr, stream_ptr=None):
     _check(load_library().dsm_test_philox(seed, tensor, t, q0, count, dev_out_ptr, stream_ptr))
 
 
-def dsm_test_stream(kind, dev_buf_ptr, n_elems, dev_words_ptr=None, value=0.0, stream_ptr=None):
-    _check(load_library().dsm_test_stream(kind, dev_buf_ptr, n_elems, dev_words_ptr, value,
+def dsm_test_stream(kind, dev_buf_ptr, n_elems, dev_words_ptr=None, pattern=0, stream_ptr=None):
+    _check(load_library().dsm_test_stream(kind, dev_buf_ptr, n_elems, dev_words_ptr, pattern,
                                           stream_ptr))
 
 

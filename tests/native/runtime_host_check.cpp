@@ -265,7 +265,7 @@ hipError_t static_scratch(void** ptr) {
     return hipSuccess;
 }
 hipError_t launch_test_stream(int kind, float* buf, int64_t n_pieces, uint32_t* words,
-                              float, hipStream_t) {
+                              uint32_t, hipStream_t) {
     Launch l;
     l.kind = kind == 0 ? "stream_read" : "stream_write";
     l.x = buf;
@@ -972,41 +972,41 @@ void check_test_stream_args() {
     float* buf = static_cast<float*>(std::aligned_alloc(256, 4096 * 4));
     uint32_t* words = static_cast<uint32_t*>(std::aligned_alloc(256, 256));
     g_log.clear();
-    CHECK(dsm_test_stream(DSM_STREAM_READ, buf, 4096, words, 0.f, nullptr) == DSM_OK, "read");
+    CHECK(dsm_test_stream(DSM_STREAM_READ, buf, 4096, words, 0u, nullptr) == DSM_OK, "read");
     CHECK(g_log.size() == 1 && g_log[0].kind == "stream_read" && g_log[0].x == buf &&
               g_log[0].n_chunks == 4 && g_log[0].bounds == words,
           "read launch arguments");
-    CHECK(dsm_test_stream(DSM_STREAM_WRITE, buf, 2048, nullptr, 1.f, nullptr) == DSM_OK, "write");
+    CHECK(dsm_test_stream(DSM_STREAM_WRITE, buf, 2048, nullptr, 0x3F800000u, nullptr) == DSM_OK, "write");
     CHECK(g_log.size() == 2 && g_log[1].kind == "stream_write" && g_log[1].n_chunks == 2,
           "write launch arguments");
-    CHECK(dsm_test_stream(DSM_STREAM_READ, buf, 0, nullptr, 0.f, nullptr) == DSM_OK, "empty");
+    CHECK(dsm_test_stream(DSM_STREAM_READ, buf, 0, nullptr, 0u, nullptr) == DSM_OK, "empty");
     const int32_t bad_kind = 2;
-    CHECK(dsm_test_stream(bad_kind, buf, 1024, words, 0.f, nullptr) == DSM_ERR_INVALID_ARG,
+    CHECK(dsm_test_stream(bad_kind, buf, 1024, words, 0u, nullptr) == DSM_ERR_INVALID_ARG,
           "unknown kind");
-    CHECK(dsm_test_stream(DSM_STREAM_WRITE, buf, 1000, nullptr, 0.f, nullptr) ==
+    CHECK(dsm_test_stream(DSM_STREAM_WRITE, buf, 1000, nullptr, 0u, nullptr) ==
               DSM_ERR_INVALID_ARG,
           "partial piece");
-    CHECK(dsm_test_stream(DSM_STREAM_WRITE, buf, -1024, nullptr, 0.f, nullptr) ==
+    CHECK(dsm_test_stream(DSM_STREAM_WRITE, buf, -1024, nullptr, 0u, nullptr) ==
               DSM_ERR_INVALID_ARG,
           "negative size");
     CHECK(dsm_test_stream(DSM_STREAM_WRITE, buf, (int64_t(1) << 24) * DSM_PIECE_ELEMS, nullptr,
                           0.f, nullptr) == DSM_ERR_INVALID_ARG,
           "beyond one grid dimension");
-    CHECK(dsm_test_stream(DSM_STREAM_READ, buf, 1024, nullptr, 0.f, nullptr) == DSM_ERR_INVALID_ARG,
+    CHECK(dsm_test_stream(DSM_STREAM_READ, buf, 1024, nullptr, 0u, nullptr) == DSM_ERR_INVALID_ARG,
           "read without words");
-    CHECK(dsm_test_stream(DSM_STREAM_WRITE, buf + 1, 1024, nullptr, 0.f, nullptr) ==
+    CHECK(dsm_test_stream(DSM_STREAM_WRITE, buf + 1, 1024, nullptr, 0u, nullptr) ==
               DSM_ERR_INVALID_ARG,
           "misaligned buffer");
-    CHECK(dsm_test_stream(DSM_STREAM_WRITE, nullptr, 1024, nullptr, 0.f, nullptr) ==
+    CHECK(dsm_test_stream(DSM_STREAM_WRITE, nullptr, 1024, nullptr, 0u, nullptr) ==
               DSM_ERR_INVALID_ARG,
           "NULL buffer");
     CHECK(dsm_test_stream(DSM_STREAM_READ, buf, 1024,
-                          reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(words) + 2), 0.f,
+                          reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(words) + 2), 0u,
                           nullptr) == DSM_ERR_INVALID_ARG,
           "misaligned words");
     CHECK(g_log.size() == 3, "three accepted calls launched, got %zu", g_log.size());
     g_devices = 0;
-    CHECK(dsm_test_stream(DSM_STREAM_WRITE, buf, 1024, nullptr, 0.f, nullptr) == DSM_ERR_HIP,
+    CHECK(dsm_test_stream(DSM_STREAM_WRITE, buf, 1024, nullptr, 0u, nullptr) == DSM_ERR_HIP,
           "no device");
     g_devices = 1;
     std::free(buf);

@@ -167,7 +167,7 @@ def test_test_philox_rejects_bad_arguments(lib, args):
 ])
 def test_test_stream_rejects_bad_arguments(lib, args):
     kind, buf, n, words = args
-    assert lib.dsm_test_stream(kind, buf, n, words, 0.0, None) == dsm.DSM_ERR_INVALID_ARG
+    assert lib.dsm_test_stream(kind, buf, n, words, 0, None) == dsm.DSM_ERR_INVALID_ARG
 
 
 def test_struct_layouts_match_header(lib):
