@@ -256,7 +256,7 @@ def main():
                          "256 MB last-level cache, contiguous otherwise")
     ap.add_argument("--placement", choices=("auto", "probe", "none"), default="auto",
                     help="with the state-blocked layout, place the buffers at the fastest of the "
-                         "offsets of a 64 GiB larger allocation, timed at set-up (Arenas "
+                         "offsets of a 128 GiB larger allocation, timed at set-up (Arenas "
                          "placement_span); auto: for working sets under 64 GB")
     ap.add_argument("--no-parity", action="store_true",
                     help="skip the oracle check of one untimed round after the timed region")

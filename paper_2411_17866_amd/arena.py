@@ -21,10 +21,11 @@ PAGE_FLOATS = 1 << 19
 # Spacing of the candidate offsets of the placement probe (Arenas(...,
 # placement_span=...)).
 PROBE_STEP_BYTES = 2 << 30
-# The probe's span: two periods of the 32 GiB pattern on MI355X, since a sweep
-# through one 250 GB allocation found a period without a fast window.  It
-# raises the odds of a fast placement; it does not guarantee one.
-PROBE_SPAN_BYTES = 64 << 30
+# The probe's span.  Measured on MI355X with GPT-2-small-sized arenas
+# (17 GB), fast placements start inside windows ~12 GB wide that recur
+# irregularly, 32-100 GB apart, so a span of 64 GiB often holds none.  The
+# span raises the odds of a fast placement; it does not guarantee one.
+PROBE_SPAN_BYTES = 128 << 30
 
 
 class Arenas:

@@ -8,6 +8,8 @@ import sys
 
 import pytest
 
+from paper_2411_17866_amd import arena as A
+
 pytestmark = pytest.mark.gpu
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -49,7 +51,8 @@ def test_bench_prints_one_consistent_json_line(extra):
     # The placement probe, when asked for, reports what it chose.
     pl = cfg.get("placement")
     if "probe" in extra:
-        assert pl["candidates"] == 33 and 0 <= pl["offset_GB"] <= 68.8
+        assert pl["candidates"] == A.PROBE_SPAN_BYTES // A.PROBE_STEP_BYTES + 1
+        assert 0 <= pl["offset_GB"] <= A.PROBE_SPAN_BYTES / 1e9 + 0.01
         assert pl["probe_ms_best"] <= pl["probe_ms_worst"]
     else:
         assert pl is None
