@@ -257,7 +257,7 @@ def main():
     ap.add_argument("--placement", choices=("auto", "probe", "none"), default="auto",
                     help="with the state-blocked layout, place the buffers at the fastest of the "
                          "offsets of a 128 GiB larger allocation, timed at set-up (Arenas "
-                         "placement_span); auto: for working sets under 64 GB")
+                         "placement_span); auto: for working sets under 120 GB")
     ap.add_argument("--no-parity", action="store_true",
                     help="skip the oracle check of one untimed round after the timed region")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -292,12 +292,13 @@ def main():
         args.replica_layout = "state-blocked" if 4 * w.d > 256 << 20 else "contiguous"
     layout = {"state-blocked": dsm.DSM_REPLICAS_STATE_BLOCKED, "blocked": dsm.DSM_REPLICAS_BLOCKED,
               "contiguous": dsm.DSM_REPLICAS_CONTIGUOUS}[args.replica_layout]
-    # Where in physical memory a working set of a few tens of GB lands sets its
-    # kernels' rate on MI355X (a pattern repeating every 32 GiB); larger ones
-    # land fast.  So smaller state-blocked problems get the placement probe.
+    # Where in physical memory a working set lands sets its kernels' rate on
+    # MI355X; the xl working set (125 GB) has always landed fast, smaller ones
+    # often do not.  So state-blocked problems under 120 GB get the placement
+    # probe, whose span (128 GiB) still fits beside them in 288 GB.
     working_set = 4 * w.d * (4 + (4 if adamw else 3) * n)
     probe = layout == dsm.DSM_REPLICAS_STATE_BLOCKED and (
-        args.placement == "probe" or (args.placement == "auto" and working_set < 64e9))
+        args.placement == "probe" or (args.placement == "auto" and working_set < 120e9))
     ar = A.Arenas(w.numel, n, H, w.base, decay=w.decay, randomized=True, global_adamw=True,
                   replica_layout=layout,
                   placement_span=A.PROBE_SPAN_BYTES if probe else 0)

@@ -146,12 +146,13 @@ class Arenas:
         """Times the problem's kernels with its buffers carved at each 2 MiB-
         aligned offset in [0, span] floats of flat, step_bytes apart, and
         returns the fastest offset.  On MI355X the rate of a working set of a
-        few tens of GB depends on where in physical memory it lands, in a
-        pattern that repeats every 32 GiB (measured: small GPT-2-sized arenas
-        ran their local steps at 76% or 82% of 8 TB/s, and the kernels that
-        read x and m at 66% or 78%, by offset); a span of two periods found
-        a fast placement for 7 of 11 medium-sized and 2 of 12 small-sized
-        problems measured.  Each candidate runs, on zeroed buffers, one fused
+        few tens of GB depends on where in physical memory it lands
+        (measured: small GPT-2-sized arenas ran their local steps at 76% or
+        82% of 8 TB/s, and the kernels that read x and m at 66% or 78%, by
+        offset, fast only inside windows ~12 GB wide and 32-100 GB apart); a
+        span of 128 GiB found a fast placement for every small-, medium- and
+        large-sized problem measured (23 processes), one of 64 GiB for 3 of
+        15 small-sized ones.  Each candidate runs, on zeroed buffers, one fused
         round end and one local step of the problem with H = 1; the contents
         do not matter, and the chosen part is zeroed again afterwards."""
         step = max(PAGE_FLOATS, (int(step_bytes) // 4) // PAGE_FLOATS * PAGE_FLOATS)
