@@ -348,7 +348,8 @@ DSM_API dsm_status dsm_test_philox(uint64_t seed, uint32_t tensor, int64_t t, in
  *                     every element (dev_words unused).
  * Enqueued on `stream`.  Errors: DSM_ERR_INVALID_ARG (unknown kind, n_elems
  * not a non-negative multiple of DSM_PIECE_ELEMS or beyond one grid
- * dimension, NULL or misaligned buffers); DSM_ERR_HIP.
+ * dimension, NULL or misaligned buffers); DSM_ERR_UNSUPPORTED (a build whose
+ * work-group shape knobs give another piece size); DSM_ERR_HIP.
  */
 #define DSM_PIECE_ELEMS 1024
 typedef enum dsm_stream_kind { DSM_STREAM_READ = 0, DSM_STREAM_WRITE = 1 } dsm_stream_kind;

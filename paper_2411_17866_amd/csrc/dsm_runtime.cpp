@@ -696,6 +696,11 @@ dsm_status dsm_test_stream(int32_t kind, float* dev_buf, int64_t n_elems, uint32
                            uint32_t pattern, void* stream) {
     if (kind != DSM_STREAM_READ && kind != DSM_STREAM_WRITE)
         return fail(nullptr, DSM_ERR_INVALID_ARG, "kind must be DSM_STREAM_READ or DSM_STREAM_WRITE");
+    // A build with other work-group shape knobs has another piece size than
+    // the one dsm.h promises for the word array.
+    if (dsm::kPieceElems != DSM_PIECE_ELEMS)
+        return fail(nullptr, DSM_ERR_UNSUPPORTED, "this build's piece is %lld elements, not %d",
+                    static_cast<long long>(dsm::kPieceElems), DSM_PIECE_ELEMS);
     if (n_elems < 0 || n_elems % dsm::kPieceElems != 0)
         return fail(nullptr, DSM_ERR_INVALID_ARG, "n_elems must be a non-negative multiple of %lld",
                     static_cast<long long>(dsm::kPieceElems));
