@@ -85,6 +85,12 @@ MUTATIONS = [
     ("ctx->bound.piece_max = reinterpret_cast<uint32_t*>(ws + L.piece_max_off);",
      "ctx->bound.piece_max = reinterpret_cast<uint32_t*>(ws + L.chunk0_off);",
      "piece maxima over the tensor chunk index"),
+    ("    if (n_pieces * dsm::kBlockThreads >= (int64_t(1) << 32))",
+     "    if (n_pieces * dsm::kBlockThreads >= (int64_t(1) << 40))",
+     "streaming diagnostic grid past one dimension"),
+    ("    if (kind == DSM_STREAM_READ && n_elems > 0 &&",
+     "    if (kind == DSM_STREAM_WRITE && n_elems > 0 &&",
+     "streaming read without its word array"),
 ]
 
 
