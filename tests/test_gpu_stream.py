@@ -84,3 +84,25 @@ def test_stream_read_after_write_round_trips():
                         stream())
     torch.cuda.synchronize()
     assert (words == 1).all()
+
+
+def test_stream_at_the_largest_grid():
+    """2^24 - 1 pieces (64 GiB), the most one grid dimension takes: 64-bit
+    addressing to the last piece, written then read back."""
+    n_pieces = (1 << 24) - 1
+    buf = torch.empty(n_pieces * P + 64, device="cuda")
+    buf[-64:] = 9.0
+    words = torch.zeros(n_pieces + 1, dtype=torch.int32, device="cuda")
+    try:
+        dsm.dsm_test_stream(dsm.DSM_STREAM_WRITE, buf.data_ptr(), n_pieces * P, None, 0x3FC00000,
+                            stream())
+        # 1024 equal floats XOR to 0: pattern 0 marks every piece.
+        dsm.dsm_test_stream(dsm.DSM_STREAM_READ, buf.data_ptr(), n_pieces * P, words.data_ptr(), 0,
+                            stream())
+        torch.cuda.synchronize()
+        assert int(words[:n_pieces].sum()) == n_pieces and int(words[n_pieces]) == 0
+        assert float(buf[0]) == 1.5 and float(buf[n_pieces * P - 1]) == 1.5
+        assert (buf[-64:] == 9.0).all(), "wrote past the last piece"
+    finally:
+        del buf, words
+        torch.cuda.empty_cache()
