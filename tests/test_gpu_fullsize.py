@@ -67,8 +67,14 @@ class Run:
         w = self.w
         self.adamw = w.base == W.BASE_ADAMW
         self.mode = dsm.DSM_SIGN_RAND_FLIP if 1 in w.sign_modes else dsm.DSM_SIGN_DET
+        # As the bench places them: state-blocked arenas under 120 GB at the
+        # probed offset of a 128 GiB larger allocation.
+        working_set = 4 * w.d * (4 + (4 if self.adamw else 3) * w.n_workers)
+        probe = layout == dsm.DSM_REPLICAS_STATE_BLOCKED and working_set < 120e9
         self.ar = A.Arenas(w.numel, w.n_workers, w.local_steps, w.base, decay=w.decay,
-                           randomized=True, global_adamw=True, replica_layout=layout)
+                           randomized=True, global_adamw=True, replica_layout=layout,
+                           placement_span=A.PROBE_SPAN_BYTES if probe else 0)
+        assert (self.ar.placement is not None) == probe
         gen = torch.Generator(device="cuda").manual_seed(w.seed)
         W.fill_params_(self.ar.x, w, gen)
         self.ar.init()
@@ -98,7 +104,8 @@ LAYOUT_NAMES = {dsm.DSM_REPLICAS_CONTIGUOUS: "contiguous", dsm.DSM_REPLICAS_BLOC
                 dsm.DSM_REPLICAS_STATE_BLOCKED: "state-blocked"}
 CASES = [(wl, lay) for lay in (dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_BLOCKED)
          for wl in ("small", "medium", "large", "xl")]
-# The bench's layout for every GPT-2 size: the replicas and their state blocked.
+# The bench's layout and placement for every GPT-2 size: the replicas and
+# their state blocked, and below xl carved at the probed offset.
 CASES += [(wl, dsm.DSM_REPLICAS_STATE_BLOCKED) for wl in ("small", "medium", "large", "xl")]
 
 
