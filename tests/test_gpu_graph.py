@@ -9,7 +9,10 @@ Such a round is captured once and replayed; between replays the same round
 runs eagerly on a second set of buffers, with other GPU work and
 synchronisations in between, and after every replay both sets must agree bit
 for bit.  (Captured scalars are fixed at capture: a round with AdamW's s, the
-randomized sign's t or a lazy broadcast is not replayable this way.)
+randomized sign's t or a lazy broadcast is not replayable this way.)  The
+randomized sign is also replayed, with the same t on both sides: its two
+passes and the bound reduction between them rewrite their workspace words on
+every run, so nothing has to be cleared between replays.
 """
 import pytest
 import torch
@@ -26,23 +29,26 @@ LOCAL = dict(lr=0.05, beta1=0.9)
 GLOB = dict(gamma=0.05, eta=0.8, beta1=0.95, beta2=0.98, lam=0.1)
 
 
-def run_round(ctx):
+def run_round(ctx, mode):
     for k in range(H):
         dsm.dsm_local_step(ctx, -1, k + 1, **LOCAL)
-    dsm.dsm_global_step(ctx, 0, broadcast=True, **GLOB)
+    dsm.dsm_global_step(ctx, 0, broadcast=True, mode=mode, seed=0x5EED, **GLOB)
 
 
 def bits(t):
     return t.view(torch.int32).clone()
 
 
+@pytest.mark.parametrize("mode", [dsm.DSM_SIGN_DET, dsm.DSM_SIGN_RAND_FLIP],
+                         ids=["det", "rand"])
 @pytest.mark.parametrize("fused", [False, True])
 @pytest.mark.parametrize("layout", [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_STATE_BLOCKED])
-def test_captured_round_replays_like_eager(fused, layout):
+def test_captured_round_replays_like_eager(fused, layout, mode):
     side = torch.cuda.Stream()
-    eager = A.Arenas(NUMEL, N, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, randomized=False,
+    rand = mode != dsm.DSM_SIGN_DET
+    eager = A.Arenas(NUMEL, N, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, randomized=rand,
                      replica_layout=layout)
-    graph = A.Arenas(NUMEL, N, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, randomized=False,
+    graph = A.Arenas(NUMEL, N, H, dsm.DSM_BASE_SGD_MOMENTUM, decay=DECAY, randomized=rand,
                      replica_layout=layout)
     gen = torch.Generator(device="cuda").manual_seed(17)
     eager.x.normal_(0.0, 0.02, generator=gen)
@@ -58,9 +64,10 @@ def test_captured_round_replays_like_eager(fused, layout):
         if fused:
             for k in range(H - 1):
                 dsm.dsm_local_step(ctx, -1, k + 1, **LOCAL)
-            dsm.dsm_round_end(ctx, H, dict(LOCAL), 0, broadcast=True, **GLOB)
+            dsm.dsm_round_end(ctx, H, dict(LOCAL), 0, broadcast=True, mode=mode, seed=0x5EED,
+                              **GLOB)
         else:
-            run_round(ctx)
+            run_round(ctx, mode)
 
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=side):
@@ -80,6 +87,10 @@ def test_captured_round_replays_like_eager(fused, layout):
         for name in ("x", "m", "x_rep", "s1_rep"):
             a, b = getattr(eager, name), getattr(graph, name)
             assert torch.equal(bits(a), bits(b)), f"replay {r}: {name} differs from the eager round"
+        if rand:
+            be = dsm.dsm_read_bounds(eager.ctx, len(NUMEL))
+            bg = dsm.dsm_read_bounds(graph.ctx, len(NUMEL))
+            assert list(be) == list(bg), f"replay {r}: tensor bounds differ"
         assert not torch.equal(bits(graph.x), x0), "the replayed round did not move the model"
         x0 = bits(graph.x)
     del g
