@@ -95,3 +95,50 @@ def test_static_scratch_refuses_a_problem_beyond_it():
         dsm.dsm_init_static(prob, dsm.dsm_buffers())
     assert e.value.status == dsm.DSM_ERR_INVALID_ARG
     assert "static scratch" in e.value.message
+
+
+@pytest.mark.parametrize("mode", [dsm.DSM_SIGN_DET, dsm.DSM_SIGN_RAND_FLIP], ids=["det", "rand"])
+def test_static_context_round_replays_from_a_graph(mode):
+    """The callers it is for include code under graph capture: a round of a
+    static-scratch context (SGD base, broadcast, the same t every round)
+    records into a HIP graph and each replay matches an eager dsm_init round."""
+    numel, n, H = [5, 16385, 40003, 64], 3, 2
+    local = LOCAL[dsm.DSM_BASE_SGD_MOMENTUM]
+    side = torch.cuda.Stream()
+    eager = A.Arenas(numel, n, H, dsm.DSM_BASE_SGD_MOMENTUM, randomized=True)
+    graph = A.Arenas(numel, n, H, dsm.DSM_BASE_SGD_MOMENTUM, randomized=True)
+    gen = torch.Generator(device="cuda").manual_seed(5)
+    eager.x.normal_(0.0, 0.02, generator=gen)
+    eager.g_rep.normal_(0.0, 1e-3, generator=gen)
+    graph.x.copy_(eager.x)
+    graph.g_rep.copy_(eager.g_rep)
+    torch.cuda.synchronize()
+    eager.ctx = dsm.dsm_init(eager.problem, eager.buffers(side))
+    bufs = graph.buffers(side)
+    bufs.workspace, bufs.workspace_bytes, bufs.u_scratch = None, 0, None
+    graph.ctx = dsm.dsm_init_static(graph.problem, bufs)
+    side.synchronize()
+
+    def round_(ctx):
+        for k in range(H):
+            dsm.dsm_local_step(ctx, -1, k + 1, **local)
+        dsm.dsm_global_step(ctx, 0, gamma=local["lr"], mode=mode, seed=7, broadcast=True, **GLOB)
+
+    try:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            round_(graph.ctx)
+        torch.cuda.synchronize()
+        for r in range(3):
+            with torch.cuda.stream(side):
+                round_(eager.ctx)
+            side.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            a, b = _state(eager), _state(graph)
+            for key in a:
+                assert np.array_equal(a[key], b[key]), (r, key)
+        del g
+    finally:
+        graph.destroy()
+        eager.destroy()
