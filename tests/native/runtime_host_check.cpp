@@ -13,16 +13,21 @@
 //     (the replica, or x after a global step without broadcast), with the
 //     replica addressing of both replica layouts;
 //   * the fp32 coefficients formed on the host, against long double;
-//   * error paths: no device, failed launches, bad hyperparameters, NULLs.
+//   * error paths: no device, failed launches, bad hyperparameters, NULLs;
+//   * contexts driven from several threads at once (also built with the
+//     thread sanitizer, where `threads` as the only argument runs just that).
 // Prints "all checks passed" and exits 0, or lists the failures and exits 1.
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <random>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "dsm.h"
@@ -35,8 +40,8 @@ int g_device = 0;            // hipGetDevice's answer
 void* g_scratch = nullptr;   // host stand-in for the static device scratch
 int g_scratch_lookups = 0;
 hipError_t g_launch_status = hipSuccess;
-int g_failures = 0;
-int g_checks = 0;
+std::atomic<int> g_failures{0};
+std::atomic<int> g_checks{0};
 
 #define CHECK(cond, ...)                                                          \
     do {                                                                          \
@@ -73,8 +78,10 @@ struct Launch {
     dsm::GlobalScalars gs{};
 };
 std::vector<Launch> g_log;
+std::mutex g_log_mu;  // launches may come from several threads (check_threads)
 
 hipError_t record(const Launch& l) {
+    std::lock_guard<std::mutex> lock(g_log_mu);
     g_log.push_back(l);
     return g_launch_status;
 }
@@ -1229,7 +1236,86 @@ void check_local_map() {
           "state-blocked local steps interleave workers");
 }
 
-int main() {
+// Contexts share no state but the static-scratch slot of each device and the
+// per-thread last error.  Four threads each drive their own context through
+// rounds of Algorithm 1 at once (both bases, all three replica layouts), each
+// provoking an error whose text must come back to it and not to another
+// thread; three more take turns on the device's one static-scratch slot, which
+// must never hold two live contexts.
+void check_threads() {
+    std::atomic<int> static_alive{0}, static_max{0}, static_wins{0};
+    auto own_context = [&](int seed) {
+        const int base = seed % 2 ? DSM_BASE_SGD_MOMENTUM : DSM_BASE_ADAMW;
+        Problem P({1000 + 17 * seed, 3000, 64}, 2, 3, base, {}, seed % 3);
+        Buffers B(P, true, false);
+        dsm_ctx* ctx = nullptr;
+        CHECK(dsm_init(&P.p, &B.b, &ctx) == DSM_OK, "thread %d: init", seed);
+        if (!ctx) return;
+        const dsm_local_hparams lh = base == DSM_BASE_ADAMW ? adam_hp() : sgd_hp();
+        for (int t = 0; t < 4; ++t) {
+            const dsm_global_hparams gh = glob_hp(t % 2 ? DSM_SIGN_RAND_FLIP : DSM_SIGN_DET);
+            for (int k = 0; k < 3; ++k)
+                CHECK(dsm_local_step(ctx, -1, 3 * t + k + 1, &lh) == DSM_OK, "thread %d: local",
+                      seed);
+            CHECK(dsm_global_step(ctx, t, &gh, 1) == DSM_OK, "thread %d: global", seed);
+        }
+        const int bad = 50 + seed;
+        CHECK(dsm_local_step(ctx, bad, 1, &lh) == DSM_ERR_INVALID_ARG, "thread %d: bad worker",
+              seed);
+        char want[32];
+        std::snprintf(want, sizeof want, "got %d", bad);
+        const std::string mine = dsm_last_error(nullptr);
+        CHECK(mine.find(want) != std::string::npos, "thread %d: its own error text, got '%s'", seed,
+              mine.c_str());
+        CHECK(std::string(dsm_last_error(ctx)).find(want) != std::string::npos,
+              "thread %d: the context's error text", seed);
+        CHECK(dsm_destroy(ctx) == DSM_OK, "thread %d: destroy", seed);
+    };
+    auto static_turns = [&](int seed) {
+        Problem P({2000 + seed, 40}, 2, 1, DSM_BASE_SGD_MOMENTUM);
+        Buffers B(P, false, false);
+        dsm_buffers b = B.b;
+        b.workspace = nullptr;
+        b.workspace_bytes = 0;
+        b.u_scratch = nullptr;
+        const dsm_local_hparams lh = sgd_hp();
+        for (int it = 0; it < 200; ++it) {
+            dsm_ctx* ctx = nullptr;
+            const dsm_status st = dsm_init_static(&P.p, &b, &ctx);
+            if (st == DSM_ERR_STATE) {
+                std::this_thread::yield();
+                continue;
+            }
+            CHECK(st == DSM_OK, "static thread %d: init (%d)", seed, static_cast<int>(st));
+            if (st != DSM_OK) return;
+            const int alive = ++static_alive;
+            int prev = static_max.load();
+            while (alive > prev && !static_max.compare_exchange_weak(prev, alive)) {
+            }
+            ++static_wins;
+            CHECK(dsm_local_step(ctx, -1, 1, &lh) == DSM_OK, "static thread %d: local", seed);
+            --static_alive;  // before the slot is released, so no later owner overlaps it
+            CHECK(dsm_destroy(ctx) == DSM_OK, "static thread %d: destroy", seed);
+        }
+    };
+    std::vector<std::thread> threads;
+    for (int i = 0; i < 4; ++i) threads.emplace_back(own_context, i);
+    for (int i = 0; i < 3; ++i) threads.emplace_back(static_turns, i);
+    for (auto& t : threads) t.join();
+    CHECK(static_max.load() == 1, "static contexts alive at once: %d", static_max.load());
+    CHECK(static_wins.load() > 0, "no thread got the static scratch");
+}
+
+int main(int argc, char** argv) {
+    if (argc == 2 && std::strcmp(argv[1], "threads") == 0) {
+        check_threads();
+        if (g_failures) {
+            std::fprintf(stderr, "%d of %d checks failed\n", g_failures.load(), g_checks.load());
+            return 1;
+        }
+        std::printf("all checks passed (%d)\n", g_checks.load());
+        return 0;
+    }
     check_local_map();
     check_layout_fuzz();
     check_init_and_chunks();
@@ -1247,10 +1333,11 @@ int main() {
     check_hyperparameter_errors();
     check_test_philox_args();
     check_test_stream_args();
+    check_threads();
     if (g_failures) {
-        std::fprintf(stderr, "%d of %d checks failed\n", g_failures, g_checks);
+        std::fprintf(stderr, "%d of %d checks failed\n", g_failures.load(), g_checks.load());
         return 1;
     }
-    std::printf("all checks passed (%d)\n", g_checks);
+    std::printf("all checks passed (%d)\n", g_checks.load());
     return 0;
 }
