@@ -4,7 +4,9 @@ thread, give bit for bit the results they give one after the other.
 A context keeps all of its state in its own host object and the caller's
 buffers (the error text of a failed call is per thread), so contexts do not
 interact.  ctypes releases the interpreter lock during each call, so the two
-threads are inside the library at the same time.
+threads are inside the library at the same time.  The first context is also
+run from dsm_init_static, whose workspace is the library's static scratch,
+beside an ordinary one.
 """
 import threading
 
@@ -36,10 +38,15 @@ def setup(spec, seed):
     return ar, grads
 
 
-def drive(ar, spec, grads, stream):
+def drive(ar, spec, grads, stream, static=False):
     """ROUNDS rounds: fused lazy and split rounds, both signs, on `stream`."""
     with torch.cuda.stream(stream):
-        ar.init(stream)
+        if static:
+            bufs = ar.buffers(stream)
+            bufs.workspace, bufs.workspace_bytes, bufs.u_scratch = None, 0, None
+            ar.ctx = dsm.dsm_init_static(ar.problem, bufs)
+        else:
+            ar.init(stream)
         H = spec["H"]
         for t in range(ROUNDS):
             mode = (dsm.DSM_SIGN_DET, dsm.DSM_SIGN_RAND_FLIP, dsm.DSM_SIGN_RAND_ZERO)[t % 3]
@@ -61,13 +68,15 @@ def state(ar):
             for name in ("x", "m", "x_rep", "s1_rep")}
 
 
-def test_two_contexts_on_two_streams_from_two_threads():
+@pytest.mark.parametrize("static_first", [False, True], ids=["init", "init_static"])
+def test_two_contexts_on_two_streams_from_two_threads(static_first):
     streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    static = [static_first, False]
     # One after the other.
     want = []
     for i, spec in enumerate(PROBLEMS):
         ar, grads = setup(spec, 100 + i)
-        drive(ar, spec, grads, streams[i])
+        drive(ar, spec, grads, streams[i], static[i])
         want.append(state(ar))
         ar.destroy()
     # At the same time, from two threads.
@@ -76,7 +85,7 @@ def test_two_contexts_on_two_streams_from_two_threads():
 
     def work(i):
         try:
-            drive(runs[i][0], PROBLEMS[i], runs[i][1], streams[i])
+            drive(runs[i][0], PROBLEMS[i], runs[i][1], streams[i], static[i])
         except Exception as e:          # reported below, in the main thread
             errors.append(repr(e))
     threads = [threading.Thread(target=work, args=(i,)) for i in range(2)]
