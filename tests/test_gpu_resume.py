@@ -50,8 +50,9 @@ def run_round(ar, t):
         dsm.dsm_global_step(ar.ctx, t, mode=mode, broadcast=True, **GLOB)
 
 
-# The ABI default and the bench's layout (replicas and their state blocked).
-LAYOUTS = [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_STATE_BLOCKED]
+# All three replica layouts: the ABI default, blocked replicas, and the
+# bench's (replicas and their state blocked).
+LAYOUTS = [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_BLOCKED, dsm.DSM_REPLICAS_STATE_BLOCKED]
 
 
 def fresh(seed, layout):
