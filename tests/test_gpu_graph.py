@@ -42,7 +42,8 @@ def bits(t):
 @pytest.mark.parametrize("mode", [dsm.DSM_SIGN_DET, dsm.DSM_SIGN_RAND_FLIP],
                          ids=["det", "rand"])
 @pytest.mark.parametrize("fused", [False, True])
-@pytest.mark.parametrize("layout", [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_STATE_BLOCKED])
+@pytest.mark.parametrize("layout", [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_BLOCKED,
+                                    dsm.DSM_REPLICAS_STATE_BLOCKED])
 def test_captured_round_replays_like_eager(fused, layout, mode):
     side = torch.cuda.Stream()
     rand = mode != dsm.DSM_SIGN_DET
