@@ -338,7 +338,7 @@ DSM_API dsm_status dsm_test_philox(uint64_t seed, uint32_t tensor, int64_t t, in
  * work-group, 16-byte nontemporal loads or stores, consecutive lanes on
  * consecutive 16-byte groups.  It measures the device's pure read and pure
  * write rates, and calibrates byte counters against the library's own access
- * shape.
+ * shape.  It is a measurement aid, not a step of the method.
  *   DSM_STREAM_READ:  reads every element; for each piece k whose elements'
  *                     32-bit patterns XOR to `pattern`, writes 1 to
  *                     dev_words[k] (caller-owned, n_elems / DSM_PIECE_ELEMS
