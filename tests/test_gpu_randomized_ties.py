@@ -10,7 +10,8 @@ gets its own tie |u| = k_j 2^-24 (Eq. (10)) or (2k_j - 2^24) 2^-24 (Eq. (9)),
 or the fp32 value one ulp above or below it, with k_j from the generator's
 published stream (the oracle's Philox).  At the tie and below, the sign is
 not kept; one ulp above, it is.  The expected S follows from the two
-comparisons above, not from the oracle's decision function.
+comparisons above, not from the oracle's decision function.  Both the split
+global step and the fused round end decide, in each replica layout.
 """
 import numpy as np
 import pytest
@@ -26,8 +27,21 @@ N = 3 * 16384 + 5
 SEED, T = 0x0DDBA11, 9
 
 
+def _set_grad(ar, g):
+    """Worker 0's gradient, element by element, in any replica layout."""
+    v = torch.from_numpy(g).cuda()
+    if ar.state_blocked:
+        idx = torch.arange(g.size, device="cuda")
+        ar.x_rep_flat[ar.state_index("g_rep", 0, idx)] = v
+    else:
+        ar.g_rep[0, :g.size] = v
+
+
+@pytest.mark.parametrize("layout", [dsm.DSM_REPLICAS_CONTIGUOUS, dsm.DSM_REPLICAS_BLOCKED,
+                                    dsm.DSM_REPLICAS_STATE_BLOCKED])
+@pytest.mark.parametrize("fused", [False, True], ids=["split", "fused"])
 @pytest.mark.parametrize("mode", [dsm.DSM_SIGN_RAND_ZERO, dsm.DSM_SIGN_RAND_FLIP])
-def test_randomized_decision_at_and_around_its_ties(mode):
+def test_randomized_decision_at_and_around_its_ties(mode, fused, layout):
     k = O.randomized_sign_uniforms(N, 0, T, SEED)              # U_j = k_j 2^-24
     rng = np.random.default_rng(mode)
     side = rng.integers(0, 3, N)                               # 0 tie, 1 one ulp up, 2 one ulp down
@@ -51,13 +65,18 @@ def test_randomized_decision_at_and_around_its_ties(mode):
     lost = 0.0 if mode == dsm.DSM_SIGN_RAND_ZERO else -1.0
     want = np.where(keep, sgn, lost * sgn).astype(np.float32)
 
-    ar = A.Arenas([N], 1, 1, dsm.DSM_BASE_SGD_MOMENTUM, decay=[False], randomized=True)
+    ar = A.Arenas([N], 1, 1, dsm.DSM_BASE_SGD_MOMENTUM, decay=[False], randomized=True,
+                  replica_layout=layout)
     ar.x.zero_()
     ar.init()
-    ar.g_rep[0, :N] = torch.from_numpy(g).cuda()
-    dsm.dsm_local_step(ar.ctx, -1, 1, lr=1.0, beta1=0.0)
-    dsm.dsm_global_step(ar.ctx, T, gamma=1.0, eta=1.0, beta1=0.0, beta2=0.5, lam=0.0,
-                        mode=mode, seed=SEED, broadcast=True)
+    _set_grad(ar, g)
+    glob = dict(gamma=1.0, eta=1.0, beta1=0.0, beta2=0.5, lam=0.0, mode=mode, seed=SEED,
+                broadcast=True)
+    if fused:       # H = 1: the round end takes the local step and the global step
+        dsm.dsm_round_end(ar.ctx, 1, dict(lr=1.0, beta1=0.0), T, **glob)
+    else:
+        dsm.dsm_local_step(ar.ctx, -1, 1, lr=1.0, beta1=0.0)
+        dsm.dsm_global_step(ar.ctx, T, **glob)
     torch.cuda.synchronize()
     u = ar.u[:N].cpu().numpy()
     S = -ar.x[:N].cpu().numpy()
