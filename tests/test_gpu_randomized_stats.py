@@ -12,7 +12,7 @@ The gradient plants 2^21 elements in each of eight classes u/B in
 {1, 0.75, 0.5, 0.25, 0.1, 0, -0.5, -1}.  Per class, the mean of S must lie
 within 5 standard errors of u/B, and the sample variance near its expected
 value.  The limits are exact: |u| = B always keeps sign(u), and u = 0 gives
-S = 0.
+S = 0.  The split global step and the fused round end (H = 1) both draw.
 """
 import numpy as np
 import pytest
@@ -27,18 +27,23 @@ CLASSES = np.array([1.0, 0.75, 0.5, 0.25, 0.1, 0.0, -0.5, -1.0], dtype=np.float3
 N = 1 << 24
 
 
+@pytest.mark.parametrize("fused", [False, True], ids=["split", "fused"])
 @pytest.mark.parametrize("mode", [dsm.DSM_SIGN_RAND_FLIP, dsm.DSM_SIGN_RAND_ZERO])
 @pytest.mark.parametrize("seed", [1, 0xDEADBEEFCAFE])
-def test_randomized_sign_is_unbiased_at_scale(mode, seed):
+def test_randomized_sign_is_unbiased_at_scale(mode, seed, fused):
     ar = A.Arenas([N], 1, 1, dsm.DSM_BASE_SGD_MOMENTUM, decay=[False], randomized=True)
     ar.x.zero_()
     ar.init()
     cls = torch.arange(N, device="cuda") % len(CLASSES)
     g = torch.as_tensor(CLASSES, device="cuda")[cls]
     ar.g_rep[0, :N] = g
-    dsm.dsm_local_step(ar.ctx, -1, 1, lr=1.0, beta1=0.0)
-    dsm.dsm_global_step(ar.ctx, 5, gamma=1.0, eta=1.0, beta1=0.0, beta2=0.5, lam=0.0,
-                        mode=mode, seed=seed, broadcast=True)
+    glob = dict(gamma=1.0, eta=1.0, beta1=0.0, beta2=0.5, lam=0.0, mode=mode, seed=seed,
+                broadcast=True)
+    if fused:
+        dsm.dsm_round_end(ar.ctx, 1, dict(lr=1.0, beta1=0.0), 5, **glob)
+    else:
+        dsm.dsm_local_step(ar.ctx, -1, 1, lr=1.0, beta1=0.0)
+        dsm.dsm_global_step(ar.ctx, 5, **glob)
     torch.cuda.synchronize()
     u = ar.u[:N].cpu().numpy()
     S = -ar.x[:N].cpu().numpy()
