@@ -3,7 +3,8 @@ with gcc against libdsm.so, allocates with hipMalloc and runs a fused lazy
 round and a split round with broadcast, then checks the synchronisation
 step, the size of the sign step (Eq. (7) with lambda = 0), a round with the
 randomized sign of Eq. (10) (its per-tensor bounds against max |u|, its steps
-0 or along sign(u)) and error paths."""
+0 or along sign(u)) and error paths; with contiguous replicas and again with
+the replicas and their state blocked in one allocation."""
 import os
 import subprocess
 import sys
