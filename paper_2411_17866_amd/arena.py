@@ -244,6 +244,13 @@ class Arenas:
         contiguous, else a copy)."""
         return getattr(self, name).reshape(self.n, -1)
 
+    def write_workers(self, name, src):
+        """Copies an (n, d_pad) tensor (worker i's copy in row i, arena order)
+        into a per-worker buffer, in place, in any replica layout: the caller's
+        gradients before a local step, or restored optimizer state."""
+        dst = getattr(self, name)
+        dst.copy_(src.reshape(dst.shape))
+
     def gather(self, name, i, idx):
         """Elements idx (arena indices, a device tensor) of worker i's copy of a
         per-worker buffer, without materialising a blocked copy."""
