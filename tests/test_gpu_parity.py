@@ -471,6 +471,24 @@ def test_empty_problem_is_a_no_op():
     ar.destroy()
 
 
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_only_empty_tensors_give_zero_bounds(layout):
+    """Tensors that all have zero elements: no chunk to launch over, yet every
+    tensor's bound is written (0), through the split and the fused paths."""
+    ar = A.Arenas([0, 0, 0], 2, 2, dsm.DSM_BASE_SGD_MOMENTUM, replica_layout=layout)
+    ar.init()
+    dsm.dsm_local_step(ar.ctx, -1, 1, lr=0.05, beta1=0.9)
+    dsm.dsm_local_step(ar.ctx, -1, 2, lr=0.05, beta1=0.9)
+    dsm.dsm_global_step(ar.ctx, 0, mode=dsm.DSM_SIGN_RAND_FLIP, **GLOB)
+    assert np.array_equal(dsm.dsm_read_bounds(ar.ctx, 3), np.zeros(3, np.float32))
+    dsm.dsm_local_step(ar.ctx, -1, 3, lr=0.05, beta1=0.9)
+    dsm.dsm_round_end(ar.ctx, 4, dict(lr=0.05, beta1=0.9), 1, mode=dsm.DSM_SIGN_RAND_ZERO,
+                      broadcast=False, **GLOB)
+    assert np.array_equal(dsm.dsm_read_bounds(ar.ctx, 3), np.zeros(3, np.float32))
+    dsm.dsm_sync(ar.ctx)
+    ar.destroy()
+
+
 # ---------------------------------------------------------------- limits, degenerate cases
 
 @pytest.mark.parametrize("layout", LAYOUTS)
